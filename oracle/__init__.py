@@ -1,0 +1,209 @@
+"""ctypes driver of the plain C oracle (oracle.c).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's CPU
+baseline leg may import this package; the product path never does.  It shares
+no code with the GPU library.  `build()` compiles liboracle.so with gcc.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build() -> str:
+    """Compile the oracle (plain C, fp64, OpenMP over output frames)."""
+    tmp = _LIB + ".tmp"
+    subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-std=gnu11",
+                    "-o", tmp, _SRC, "-lm"], check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Arch(ctypes.Structure):
+    _fields_ = [
+        ("vocab", ctypes.c_int), ("embed", ctypes.c_int), ("frames_per_token", ctypes.c_int),
+        ("n_pre", ctypes.c_int), ("pre_kernel", ctypes.c_int),
+        ("n_stages", ctypes.c_int), ("up_rate", ctypes.c_int * 8), ("channels", ctypes.c_int * 9),
+        ("n_rb", ctypes.c_int), ("rb_kernel", ctypes.c_int * 8),
+        ("n_dil", ctypes.c_int), ("dil", ctypes.c_int * 8),
+        ("head_kernel", ctypes.c_int), ("n_fft", ctypes.c_int), ("hop", ctypes.c_int),
+        ("slope", ctypes.c_double),
+    ]
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        D = ctypes.POINTER(ctypes.c_double)
+        F = ctypes.POINTER(ctypes.c_float)
+        I = ctypes.POINTER(ctypes.c_int32)
+        lib.oc_cconv.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_long,
+                                 D, D, D, D]
+        lib.oc_convt.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_long, D, D, D, D]
+        lib.oc_irfft.argtypes = [ctypes.c_int, D, D, D]
+        lib.oc_istft.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_long, D, D, D]
+        lib.oc_hann.argtypes = [ctypes.c_int, ctypes.c_int]
+        lib.oc_hann.restype = ctypes.c_double
+        lib.oc_ola_norm.argtypes = [ctypes.c_int, ctypes.c_int]
+        lib.oc_ola_norm.restype = ctypes.c_double
+        lib.oc_round_bf16.argtypes = [ctypes.c_float]
+        lib.oc_round_bf16.restype = ctypes.c_float
+        lib.oc_num_threads.restype = ctypes.c_int
+        lib.oc_blob_floats.argtypes = [ctypes.POINTER(_Arch)]
+        lib.oc_blob_floats.restype = ctypes.c_long
+        lib.oc_samples_per_token.argtypes = [ctypes.POINTER(_Arch)]
+        lib.oc_samples_per_token.restype = ctypes.c_long
+        lib.oc_decode.argtypes = [ctypes.POINTER(_Arch), ctypes.c_int, F, ctypes.c_long, I, ctypes.c_long,
+                                  D, ctypes.c_char_p, D]
+        lib.oc_decode.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _p(a: np.ndarray, ct):
+    return a.ctypes.data_as(ctypes.POINTER(ct))
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def arch_struct(arch: dict) -> _Arch:
+    s = _Arch()
+    s.vocab, s.embed, s.frames_per_token = arch["vocab"], arch["embed"], arch["frames_per_token"]
+    s.n_pre, s.pre_kernel = arch["n_pre"], arch["pre_kernel"]
+    s.n_stages = len(arch["up_rate"])
+    for i, u in enumerate(arch["up_rate"]):
+        s.up_rate[i] = u
+    for i, c in enumerate(arch["channels"]):
+        s.channels[i] = c
+    s.n_rb = len(arch["rb_kernel"])
+    for i, k in enumerate(arch["rb_kernel"]):
+        s.rb_kernel[i] = k
+    s.n_dil = len(arch["dil"])
+    for i, d in enumerate(arch["dil"]):
+        s.dil[i] = d
+    s.head_kernel, s.n_fft, s.hop = arch["head_kernel"], arch["n_fft"], arch["hop"]
+    s.slope = arch["lrelu_slope"]
+    return s
+
+
+# ---------------------------------------------------------------- single ops
+
+def cconv(W, b, v, d: int = 1) -> np.ndarray:
+    """Causal dilated conv: W [Co][Ci][k], b [Co], v [T][Ci] -> [T][Co]."""
+    W, b, v = _f64(W), _f64(b), _f64(v)
+    co, ci, k = W.shape
+    T = v.shape[0]
+    out = np.empty((T, co), dtype=np.float64)
+    _load().oc_cconv(ci, co, k, d, T, _p(W, ctypes.c_double), _p(b, ctypes.c_double),
+                     _p(v, ctypes.c_double), _p(out, ctypes.c_double))
+    return out
+
+
+def convt(W, b, v) -> np.ndarray:
+    """Causal transposed conv, kernel 2u stride u: W [Ci][Co][2u], v [F][Ci] -> [F*u][Co]."""
+    W, b, v = _f64(W), _f64(b), _f64(v)
+    ci, co, k2 = W.shape
+    u = k2 // 2
+    F = v.shape[0]
+    out = np.empty((F * u, co), dtype=np.float64)
+    _load().oc_convt(ci, co, u, F, _p(W, ctypes.c_double), _p(b, ctypes.c_double),
+                     _p(v, ctypes.c_double), _p(out, ctypes.c_double))
+    return out
+
+
+def irfft(re, im) -> np.ndarray:
+    re, im = _f64(re), _f64(im)
+    N = 2 * (re.size - 1)
+    out = np.empty(N, dtype=np.float64)
+    _load().oc_irfft(N, _p(re, ctypes.c_double), _p(im, ctypes.c_double), _p(out, ctypes.c_double))
+    return out
+
+
+def istft(logmag, phase, n_fft: int = 16, hop: int = 4) -> np.ndarray:
+    """[M][n_fft/2+1] log-magnitude and phase -> hop*M samples."""
+    lm, ph = _f64(logmag), _f64(phase)
+    M = lm.shape[0]
+    out = np.empty(M * hop, dtype=np.float64)
+    _load().oc_istft(n_fft, hop, M, _p(lm, ctypes.c_double), _p(ph, ctypes.c_double),
+                     _p(out, ctypes.c_double))
+    return out
+
+
+def hann(N: int) -> np.ndarray:
+    lib = _load()
+    return np.array([lib.oc_hann(N, n) for n in range(N)])
+
+
+def ola_norm(N: int, hop: int) -> float:
+    return _load().oc_ola_norm(N, hop)
+
+
+def round_bf16(x) -> np.ndarray:
+    lib = _load()
+    x = np.asarray(x, dtype=np.float32)
+    return np.array([lib.oc_round_bf16(float(v)) for v in x.ravel()], dtype=np.float32).reshape(x.shape)
+
+
+def num_threads() -> int:
+    return _load().oc_num_threads()
+
+
+def samples_per_token(arch: dict) -> int:
+    s = arch_struct(arch)
+    return int(_load().oc_samples_per_token(ctypes.byref(s)))
+
+
+# ---------------------------------------------------------------- the decoder
+
+def decode(arch: dict, dtype: str, blob: np.ndarray, ids, tap: str | None = None):
+    """Offline decode of one stream from the zero state.
+
+    Returns the fp64 PCM (len(ids) * samples_per_token samples), or
+    (pcm, tap_values) when `tap` names an intermediate.  dtype "bf16" rounds
+    every parameter to bfloat16 first.
+    """
+    lib = _load()
+    s = arch_struct(arch)
+    blob = np.ascontiguousarray(blob, dtype=np.float32)
+    ids = np.ascontiguousarray(ids, dtype=np.int32).ravel()
+    T = ids.size
+    spt = int(lib.oc_samples_per_token(ctypes.byref(s)))
+    pcm = np.empty(T * spt, dtype=np.float64)
+    tap_buf = None
+    if tap is not None:
+        frames, ch = _tap_shape(arch, tap, T)
+        tap_buf = np.empty((frames, ch), dtype=np.float64)
+    rc = lib.oc_decode(ctypes.byref(s), 1 if dtype == "bf16" else 0, _p(blob, ctypes.c_float), blob.size,
+                       _p(ids, ctypes.c_int32), T, _p(pcm, ctypes.c_double),
+                       tap.encode() if tap else None,
+                       _p(tap_buf, ctypes.c_double) if tap_buf is not None else None)
+    if rc != 0:
+        raise ValueError(f"oracle decode failed (rc={rc})")
+    return pcm if tap is None else (pcm, tap_buf)
+
+
+def _tap_shape(arch: dict, tap: str, T: int):
+    F = T * arch["frames_per_token"]
+    if tap == "embed" or tap.startswith("pre"):
+        return F, arch["channels"][0]
+    if tap == "head":
+        for u in arch["up_rate"]:
+            F *= u
+        return F, 2 * (arch["n_fft"] // 2 + 1)
+    s = int(tap[1:tap.index(".")])
+    for u in arch["up_rate"][:s + 1]:
+        F *= u
+    return F, arch["channels"][s + 1]

@@ -1,0 +1,143 @@
+"""Seeded synthetic workloads: decoder architectures, random weights and token ids.
+
+This module holds no arithmetic of the decode step.  It only describes the
+shapes of the streaming Token2Wav vocoder workloads and draws the random
+numbers they are fed with, so that the GPU library and the CPU oracle can be
+driven with identical inputs.
+
+Workload shapes follow the paper's shared streaming decoder (Evaluation,
+"Setup"): 25 Hz speech tokens, 2 frames per token, 25-token chunks that each
+become one second of 24 kHz PCM, and several independent sessions sharing one
+set of weights (Design, "Why the two rules are inseparable", multi-session
+paragraph).  The paper publishes no layer shapes and no weights, so the
+architectures below are synthetic random-weight decoders of that shape.
+
+Weight blob format (little-endian float32, tensors back to back, PyTorch
+layouts):
+
+    emb              [vocab][embed]
+    per pre layer:   W [C0][C0][pre_kernel], b [C0]
+    per stage s:     convT W [C_{s-1}][C_s][2*u_s], b [C_s]
+                     per resblock kernel k_j, per dilation d:
+                         W1 [C_s][C_s][k_j], b1 [C_s], W2 [C_s][C_s][k_j], b2 [C_s]
+    head:            W [2*(n_fft/2+1)][C_last][head_kernel], b [2*(n_fft/2+1)]
+
+Weights are N(0, 1/fan_in) with fan_in = C_in*k for a Conv1d and 2*C_in for a
+ConvTranspose1d with kernel 2u and stride u (each output reads two input
+frames); biases are N(0, 1/fan_in) of their layer; the embedding is N(0, 1).
+All draws come from numpy's PCG64 seeded by SeedSequence([seed, 0]) in blob
+order, in float64, then rounded to float32.  Token ids of stream b come from
+SeedSequence([seed, 1, b]), uniform over the vocabulary.
+"""
+from __future__ import annotations
+
+import copy
+import math
+
+import numpy as np
+
+TINY_ARCH = dict(
+    vocab=256, embed=64, frames_per_token=1,
+    n_pre=4, pre_kernel=3,
+    up_rate=[2, 2, 4], channels=[64, 32, 16, 8],
+    rb_kernel=[3], dil=[1, 3],
+    head_kernel=7, n_fft=16, hop=4, lrelu_slope=0.1,
+)
+
+REAL_ARCH = dict(
+    vocab=6561, embed=512, frames_per_token=2,
+    n_pre=8, pre_kernel=3,
+    up_rate=[8, 5, 3], channels=[512, 256, 128, 64],
+    rb_kernel=[3, 7, 11], dil=[1, 3, 5],
+    head_kernel=7, n_fft=16, hop=4, lrelu_slope=0.1,
+)
+
+# Workloads: architecture, arithmetic type, independent streams, tokens per
+# chunk and chunks per measured pass.
+WORKLOADS = {
+    "tiny_f32_b1_n8": dict(arch=TINY_ARCH, dtype="f32", batch=1, chunk_tokens=8, chunks=8),
+    "real_f32_b1_n25": dict(arch=REAL_ARCH, dtype="f32", batch=1, chunk_tokens=25, chunks=20),
+    "real_bf16_b16_n25": dict(arch=REAL_ARCH, dtype="bf16", batch=16, chunk_tokens=25, chunks=20),
+    "real_bf16_b1_n4": dict(arch=REAL_ARCH, dtype="bf16", batch=1, chunk_tokens=4, chunks=200),
+    "real_bf16_b128_n25": dict(arch=REAL_ARCH, dtype="bf16", batch=128, chunk_tokens=25, chunks=40),
+}
+
+SAMPLE_RATE = 24000  # output rate of the real architecture (960 samples / 25 Hz token)
+
+
+def workload(name: str) -> dict:
+    """Deep copy of a named workload description."""
+    return copy.deepcopy(WORKLOADS[name])
+
+
+def head_channels(arch: dict) -> int:
+    return 2 * (arch["n_fft"] // 2 + 1)
+
+
+def samples_per_token(arch: dict) -> int:
+    return arch["frames_per_token"] * math.prod(arch["up_rate"]) * arch["hop"]
+
+
+def tensor_list(arch: dict):
+    """(name, shape, fan_in) for every tensor of the blob, in blob order."""
+    out = []
+    c0 = arch["channels"][0]
+    out.append(("emb", (arch["vocab"], arch["embed"]), None))
+    assert arch["embed"] == c0, "the pre-stack runs at the embedding width"
+    k = arch["pre_kernel"]
+    for l in range(arch["n_pre"]):
+        out.append((f"pre{l}.W", (c0, c0, k), c0 * k))
+        out.append((f"pre{l}.b", (c0,), c0 * k))
+    for s, u in enumerate(arch["up_rate"]):
+        ci, co = arch["channels"][s], arch["channels"][s + 1]
+        out.append((f"s{s}.up.W", (ci, co, 2 * u), 2 * ci))
+        out.append((f"s{s}.up.b", (co,), 2 * ci))
+        for j, kj in enumerate(arch["rb_kernel"]):
+            for i, _d in enumerate(arch["dil"]):
+                for half in (1, 2):
+                    out.append((f"s{s}.rb{j}.d{i}.W{half}", (co, co, kj), co * kj))
+                    out.append((f"s{s}.rb{j}.d{i}.b{half}", (co,), co * kj))
+    cl = arch["channels"][-1]
+    hc = head_channels(arch)
+    kh = arch["head_kernel"]
+    out.append(("head.W", (hc, cl, kh), cl * kh))
+    out.append(("head.b", (hc,), cl * kh))
+    return out
+
+
+def blob_floats(arch: dict) -> int:
+    return sum(math.prod(shape) for _, shape, _ in tensor_list(arch))
+
+
+def make_weights(arch: dict, seed: int = 0) -> np.ndarray:
+    """The float32 weight blob of `arch` drawn from `seed`."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 0]))
+    parts = []
+    for _name, shape, fan_in in tensor_list(arch):
+        x = rng.standard_normal(math.prod(shape))
+        if fan_in is not None:
+            x = x / math.sqrt(fan_in)
+        parts.append(x.astype(np.float32))
+    return np.concatenate(parts)
+
+
+def split_weights(arch: dict, blob: np.ndarray) -> dict:
+    """Views of the blob by tensor name (for tests that plant special weights)."""
+    out, off = {}, 0
+    for name, shape, _ in tensor_list(arch):
+        n = math.prod(shape)
+        out[name] = blob[off:off + n].reshape(shape)
+        off += n
+    assert off == blob.size
+    return out
+
+
+def make_tokens(arch: dict, batch: int, total_tokens: int, seed: int = 0,
+                first_stream: int = 0) -> np.ndarray:
+    """int32 [batch][total_tokens] uniform ids; stream b uses SeedSequence([seed, 1, b])."""
+    out = np.empty((batch, total_tokens), dtype=np.int32)
+    for r in range(batch):
+        b = first_stream + r
+        rng = np.random.default_rng(np.random.SeedSequence([seed, 1, b]))
+        out[r] = rng.integers(0, arch["vocab"], size=total_tokens, dtype=np.int32)
+    return out

@@ -1,0 +1,198 @@
+/*
+ * dc.h — C ABI of the MI355X streaming Token2Wav decode step.
+ *
+ * One call to dc_decode_chunk turns a chunk of n speech tokens per stream into
+ * fp32 PCM: token embedding repeated to the frame clock, a causal Conv1d
+ * pre-stack, ConvTranspose1d upsampling stages each followed by a
+ * multi-receptive-field residual block, a head conv to log-magnitude and phase,
+ * and an inverse STFT with overlap-add.  Every causal layer reads its left
+ * context from a ring buffer kept at a fixed device address (the carry of the
+ * paper's state rule: Design, "State rule: demand sizing and the carry",
+ * Eq. carry), written in place by the kernel that produces it; the whole step
+ * for the declared chunk shape is replayed as one HIP graph (the compute rule:
+ * Design, "Compute rule: exact-shape replay", clauses (i)-(ii), Eq. granularity).
+ *
+ * Correctness contract (Design, Definition 2, strict trace equivalence): for
+ * every stream, decoding a token sequence chunk by chunk yields bit-for-bit the
+ * PCM of decoding the concatenation in one call, and graph replay yields
+ * bit-for-bit the PCM of direct launches.  Results never depend on the batch
+ * size, the chunk size or the tile shapes chosen for the hardware.
+ *
+ * Conventions for every function:
+ *   - the return value is a dc_status (0 on success, negative on error); no
+ *     exception or abort crosses the ABI; dc_last_error() explains the last one;
+ *   - a dc_state is not thread-safe; distinct states are independent;
+ *   - the state owns all device memory it allocates (one arena at dc_init); its
+ *     addresses are fixed until dc_free.
+ */
+#ifndef DC_H
+#define DC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DC_ABI_VERSION 1
+#define DC_MAX_STAGES 4
+#define DC_MAX_RB 4
+#define DC_MAX_DIL 4
+
+typedef enum {
+    DC_OK = 0,
+    DC_EINVAL = -1,   /* bad argument or configuration; nothing launched, state unchanged */
+    DC_ERANGE = -2,   /* token id outside [0, vocab) or n > max_tokens                      */
+    DC_ENOMEM = -3,   /* device allocation failed at dc_init                                 */
+    DC_EDEVICE = -4,  /* a HIP call failed; the state is poisoned until dc_reset             */
+    DC_ESTATE = -5,   /* the state is poisoned (earlier device or id error); call dc_reset   */
+    DC_EVERSION = -6  /* cfg->abi_version != DC_ABI_VERSION                                  */
+} dc_status;
+
+typedef enum { DC_F32 = 0, DC_BF16 = 1 } dc_dtype;
+
+enum {
+    DC_HOST_PTRS = 1u << 0, /* tokens/audio are host pointers; each call is synchronous          */
+    DC_NO_GRAPH = 1u << 1   /* never capture or replay a graph; always launch kernels directly   */
+};
+
+/*
+ * Decoder architecture and serving shape.  The architecture fields describe
+ * the weight blob (see dc_init); the serving fields size the state.
+ * Constraints checked by dc_init (DC_EINVAL otherwise): 1 <= n_stages <= 4,
+ * channels multiples of 8, channels[0] == embed, 1 <= n_rb <= 4,
+ * 1 <= n_dil <= 4, odd or even kernels >= 1, n_fft == 16 and hop == 4,
+ * batch >= 1, 1 <= chunk_tokens <= max_tokens.
+ */
+typedef struct dc_cfg {
+    int32_t abi_version;                 /* DC_ABI_VERSION                                        */
+    int32_t vocab, embed;                /* token vocabulary, embedding width                     */
+    int32_t frames_per_token;            /* embedding repeat to the frame clock                  */
+    int32_t n_pre, pre_kernel;           /* causal Conv1d pre-stack (dilation 1)                  */
+    int32_t n_stages;                    /* upsampling stages                                     */
+    int32_t up_rate[DC_MAX_STAGES];      /* stride u of each ConvTranspose1d (kernel 2u)          */
+    int32_t channels[DC_MAX_STAGES + 1]; /* channels[0] pre-stack width, channels[s+1] stage s    */
+    int32_t n_rb, rb_kernel[DC_MAX_RB];  /* resblock kernel sizes (one branch each)               */
+    int32_t n_dil, dil[DC_MAX_DIL];      /* dilations of every branch                             */
+    int32_t head_kernel, n_fft, hop;     /* head conv width, iSTFT size and hop                   */
+    float lrelu_slope;                   /* LeakyReLU negative slope                              */
+    int32_t dtype;                       /* dc_dtype: arithmetic of the conv operands             */
+    int32_t batch;                       /* B independent streams sharing the weights             */
+    int32_t chunk_tokens;                /* the chunk shape captured as a graph                   */
+    int32_t max_tokens;                  /* largest n accepted by dc_decode_chunk                 */
+    uint32_t flags;                      /* DC_HOST_PTRS | DC_NO_GRAPH                            */
+    int32_t tile_variant;                /* 0: automatic; v > 0 forces tile shape v-1 everywhere
+                                            it fits (results are identical by construction)      */
+    void* hip_stream;                    /* hipStream_t all work is ordered on; NULL: own stream  */
+} dc_cfg;
+
+typedef struct dc_stats {
+    int64_t calls;            /* dc_decode_chunk calls that launched work                       */
+    int64_t replays;          /* ... of which replayed the captured graph                       */
+    int64_t direct_shape;     /* direct launches because n != chunk_tokens                      */
+    int64_t direct_nograph;   /* direct launches because no graph exists (DC_NO_GRAPH)          */
+    int64_t staged_tokens;    /* token copies into the fixed token buffer (caller not aliased)  */
+    int64_t staged_audio;     /* PCM copies out of the fixed audio buffer (caller not aliased)  */
+    int64_t rejected;         /* calls refused before any launch                                */
+    int64_t clock_tokens;     /* tokens decoded per stream since the last dc_reset              */
+    int64_t arena_bytes;      /* the one device allocation                                      */
+    int64_t weight_bytes;     /* packed weights and device-resident constants                   */
+    int64_t carry_bytes;      /* left-context part of every ring (the state kept across chunks) */
+    int64_t ring_bytes;       /* all ring buffers (carry plus the frames of one call)           */
+    int32_t kernels_per_step; /* kernel launches of one chunk step                              */
+    int32_t graph_nodes;      /* nodes of the captured graph (0 if none)                        */
+    double capture_ms;        /* wall time of warm-up, capture and instantiation at dc_init     */
+} dc_stats;
+
+typedef struct dc_state dc_state;
+
+/*
+ * Create a decoder.  weights_blob: host pointer to blob_bytes of little-endian
+ * float32, the tensors back to back in this order and PyTorch layouts:
+ *   emb [vocab][embed];
+ *   per pre layer: W [C0][C0][pre_kernel], b [C0];
+ *   per stage s: ConvTranspose1d W [C_s][C_{s+1}][2*u_s], b [C_{s+1}], then per
+ *     resblock kernel k_j, per dilation d: W1 [C][C][k_j], b1 [C], W2 [C][C][k_j], b2 [C];
+ *   head: W [2*(n_fft/2+1)][C_last][head_kernel], b [2*(n_fft/2+1)].
+ * The blob is copied (rounded to bfloat16, nearest-even, when dtype is
+ * DC_BF16; the head stays fp32 arithmetic on those rounded values) and may be
+ * freed on return.  On success *out owns the state, reset to the start of
+ * every stream, with the chunk graph captured unless DC_NO_GRAPH.
+ * Errors: DC_EVERSION, DC_EINVAL (cfg or blob size), DC_ENOMEM, DC_EDEVICE;
+ * *out is NULL then.
+ */
+dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg, dc_state** out);
+
+/*
+ * Decode the next n tokens of every stream.
+ *   tokens:    int32 [batch][n], row-major.
+ *   audio_out: float32 [batch][n * dc_samples_per_token(cfg)], row-major; the
+ *              samples continue each stream where the previous call ended.
+ * Pointers are device pointers ordered on the state's stream (asynchronous)
+ * unless the state was created with DC_HOST_PTRS (synchronous, host memory).
+ * Passing dc_token_buffer(s) / dc_audio_buffer(s) aliases the fixed buffers and
+ * avoids the staging copy of that side.
+ * Admission (Design, compute rule clauses (i)-(ii), fail-closed): n ==
+ * chunk_tokens replays the captured graph; any other 0 < n <= max_tokens runs
+ * the same kernels directly (bit-identical output, counted as direct_shape).
+ * n <= 0 or NULL pointers: DC_EINVAL; n > max_tokens: DC_ERANGE; both leave
+ * the state unchanged.  Token ids outside [0, vocab): with DC_HOST_PTRS,
+ * DC_ERANGE before any launch, state unchanged; with device pointers the
+ * embedding kernel raises a device flag, and this call (host mode) or the
+ * next dc_sync returns DC_ERANGE and poisons the state until dc_reset.
+ */
+dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* audio_out);
+
+/* Return every stream to its start: zero every ring in place (addresses are
+ * unchanged) and set the clock to 0.  Clears a poisoned state. */
+dc_status dc_reset(dc_state* s);
+
+/* Return stream b (0 <= b < batch) to its start in place; other streams keep
+ * their carry.  DC_EINVAL for a bad b. */
+dc_status dc_reset_stream(dc_state* s, int32_t b);
+
+/* Wait for all work of the state; report DC_ERANGE for a bad token id seen on
+ * the device, DC_EDEVICE for a HIP error (both poison the state). */
+dc_status dc_sync(dc_state* s);
+
+/* frames_per_token * prod(up_rate) * hop for cfg (0 for a NULL cfg). */
+int64_t dc_samples_per_token(const dc_cfg* cfg);
+
+/* Number of float32 values the weight blob of cfg must hold (0 for NULL). */
+int64_t dc_blob_floats(const dc_cfg* cfg);
+
+/* The fixed device buffers that dc_decode_chunk stages through:
+ * int32 [batch][max_tokens] and float32 [batch][max_tokens * samples_per_token]
+ * (read as [batch][n] and [batch][n * spt] for a call with n tokens). */
+int32_t* dc_token_buffer(dc_state* s);
+float* dc_audio_buffer(dc_state* s);
+
+/* Copy the counters into *out. */
+dc_status dc_get_stats(const dc_state* s, dc_stats* out);
+
+/*
+ * Inspection of the carried state and intermediates (tests, shadow checks).
+ * dc_tap_find returns the index of a named intermediate ("embed", "pre<l>",
+ * "s<s>.y", "s<s>.rb<j>.h<i>" (stored as LeakyReLU of h), "s<s>.rb<j>.z<i>",
+ * "s<s>.x", "head"), or -1.  dc_tap_read copies, for stream b, the frames
+ * with absolute index [frame0, frame0 + nframes) of that ring into host
+ * memory as float32 [nframes][C]; *channels receives C.  Only frames still held
+ * by the ring (the last call's frames and the carried left context) are
+ * readable; others give DC_ERANGE.  Synchronous.
+ */
+int32_t dc_tap_find(const dc_state* s, const char* name);
+dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32_t nframes,
+                      float* host_out, int32_t* channels);
+
+/* Human-readable reason for the last error on s (or on dc_init when s is NULL). */
+const char* dc_last_error(const dc_state* s);
+
+/* Release the state and all its device memory (NULL is a no-op). */
+void dc_free(dc_state* s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DC_H */

@@ -1,0 +1,309 @@
+"""MI355X streaming Token2Wav decode step: Python binding of libdc.so.
+
+The functions below carry the C-ABI names of include/dc.h and only marshal
+arguments (torch tensors or numpy arrays to pointers); every step of the
+decode runs in the gfx950 kernels of libdc.so.  Importing this package never
+falls back to anything else: if libdc.so is missing, `lib()` raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import synth  # noqa: F401  (workload shapes and seeded inputs)
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdc.so")
+
+DC_ABI_VERSION = 1
+DC_OK, DC_EINVAL, DC_ERANGE, DC_ENOMEM, DC_EDEVICE, DC_ESTATE, DC_EVERSION = 0, -1, -2, -3, -4, -5, -6
+DC_F32, DC_BF16 = 0, 1
+DC_HOST_PTRS, DC_NO_GRAPH = 1, 2
+STATUS_NAMES = {0: "DC_OK", -1: "DC_EINVAL", -2: "DC_ERANGE", -3: "DC_ENOMEM", -4: "DC_EDEVICE",
+                -5: "DC_ESTATE", -6: "DC_EVERSION"}
+
+
+class DcError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class DcCfg(ctypes.Structure):
+    _fields_ = [
+        ("abi_version", ctypes.c_int32),
+        ("vocab", ctypes.c_int32), ("embed", ctypes.c_int32),
+        ("frames_per_token", ctypes.c_int32),
+        ("n_pre", ctypes.c_int32), ("pre_kernel", ctypes.c_int32),
+        ("n_stages", ctypes.c_int32),
+        ("up_rate", ctypes.c_int32 * 4),
+        ("channels", ctypes.c_int32 * 5),
+        ("n_rb", ctypes.c_int32), ("rb_kernel", ctypes.c_int32 * 4),
+        ("n_dil", ctypes.c_int32), ("dil", ctypes.c_int32 * 4),
+        ("head_kernel", ctypes.c_int32), ("n_fft", ctypes.c_int32), ("hop", ctypes.c_int32),
+        ("lrelu_slope", ctypes.c_float),
+        ("dtype", ctypes.c_int32),
+        ("batch", ctypes.c_int32),
+        ("chunk_tokens", ctypes.c_int32),
+        ("max_tokens", ctypes.c_int32),
+        ("flags", ctypes.c_uint32),
+        ("tile_variant", ctypes.c_int32),
+        ("hip_stream", ctypes.c_void_p),
+    ]
+
+
+class DcStats(ctypes.Structure):
+    _fields_ = [
+        ("calls", ctypes.c_int64), ("replays", ctypes.c_int64), ("direct_shape", ctypes.c_int64),
+        ("direct_nograph", ctypes.c_int64), ("staged_tokens", ctypes.c_int64),
+        ("staged_audio", ctypes.c_int64), ("rejected", ctypes.c_int64), ("clock_tokens", ctypes.c_int64),
+        ("arena_bytes", ctypes.c_int64), ("weight_bytes", ctypes.c_int64), ("carry_bytes", ctypes.c_int64),
+        ("ring_bytes", ctypes.c_int64), ("kernels_per_step", ctypes.c_int32), ("graph_nodes", ctypes.c_int32),
+        ("capture_ms", ctypes.c_double),
+    ]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+# Every symbol include/dc.h declares, with its ctypes signature.
+_P = ctypes.c_void_p
+SIGNATURES = {
+    "dc_init": ([_P, ctypes.c_size_t, ctypes.POINTER(DcCfg), ctypes.POINTER(_P)], ctypes.c_int),
+    "dc_decode_chunk": ([_P, _P, ctypes.c_int32, _P], ctypes.c_int),
+    "dc_reset": ([_P], ctypes.c_int),
+    "dc_reset_stream": ([_P, ctypes.c_int32], ctypes.c_int),
+    "dc_sync": ([_P], ctypes.c_int),
+    "dc_samples_per_token": ([ctypes.POINTER(DcCfg)], ctypes.c_int64),
+    "dc_blob_floats": ([ctypes.POINTER(DcCfg)], ctypes.c_int64),
+    "dc_token_buffer": ([_P], _P),
+    "dc_audio_buffer": ([_P], _P),
+    "dc_get_stats": ([_P, ctypes.POINTER(DcStats)], ctypes.c_int),
+    "dc_tap_find": ([_P, ctypes.c_char_p], ctypes.c_int32),
+    "dc_tap_read": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _P,
+                     ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+    "dc_last_error": ([_P], ctypes.c_char_p),
+    "dc_free": ([_P], None),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libdc.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(hipcc --offload-arch=gfx950); there is no fallback path")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def make_cfg(arch: dict, dtype: str, batch: int, chunk_tokens: int, max_tokens: int | None = None,
+             flags: int = 0, tile_variant: int = 0, stream: int | None = None) -> DcCfg:
+    c = DcCfg()
+    c.abi_version = DC_ABI_VERSION
+    c.vocab, c.embed, c.frames_per_token = arch["vocab"], arch["embed"], arch["frames_per_token"]
+    c.n_pre, c.pre_kernel = arch["n_pre"], arch["pre_kernel"]
+    c.n_stages = len(arch["up_rate"])
+    for i, u in enumerate(arch["up_rate"]):
+        c.up_rate[i] = u
+    for i, ch in enumerate(arch["channels"]):
+        c.channels[i] = ch
+    c.n_rb = len(arch["rb_kernel"])
+    for i, k in enumerate(arch["rb_kernel"]):
+        c.rb_kernel[i] = k
+    c.n_dil = len(arch["dil"])
+    for i, d in enumerate(arch["dil"]):
+        c.dil[i] = d
+    c.head_kernel, c.n_fft, c.hop = arch["head_kernel"], arch["n_fft"], arch["hop"]
+    c.lrelu_slope = arch["lrelu_slope"]
+    c.dtype = DC_BF16 if dtype == "bf16" else DC_F32
+    c.batch = batch
+    c.chunk_tokens = chunk_tokens
+    c.max_tokens = max_tokens if max_tokens is not None else chunk_tokens
+    c.flags = flags
+    c.tile_variant = tile_variant
+    c.hip_stream = stream
+    return c
+
+
+def _ptr(x) -> int:
+    """Address of a torch tensor (device or host) or a numpy array."""
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    return x.data_ptr()
+
+
+def _check(status: int, handle) -> int:
+    if status != DC_OK:
+        raise DcError(status, dc_last_error(handle))
+    return status
+
+
+# ------------------------------------------------------------ the C-ABI calls
+
+def dc_init(blob: np.ndarray, cfg: DcCfg):
+    blob = np.ascontiguousarray(blob, dtype=np.float32)
+    h = ctypes.c_void_p()
+    st = lib().dc_init(blob.ctypes.data, blob.nbytes, ctypes.byref(cfg), ctypes.byref(h))
+    if st != DC_OK:
+        raise DcError(st, dc_last_error(None))
+    return h
+
+
+def dc_decode_chunk(h, tokens, n: int, audio_out) -> int:
+    """Raw call: returns the status (no exception)."""
+    return lib().dc_decode_chunk(h, _ptr(tokens) if tokens is not None else None, n,
+                                 _ptr(audio_out) if audio_out is not None else None)
+
+
+def dc_reset(h) -> int:
+    return lib().dc_reset(h)
+
+
+def dc_reset_stream(h, b: int) -> int:
+    return lib().dc_reset_stream(h, b)
+
+
+def dc_sync(h) -> int:
+    return lib().dc_sync(h)
+
+
+def dc_samples_per_token(cfg: DcCfg) -> int:
+    return lib().dc_samples_per_token(ctypes.byref(cfg))
+
+
+def dc_blob_floats(cfg: DcCfg) -> int:
+    return lib().dc_blob_floats(ctypes.byref(cfg))
+
+
+def dc_token_buffer(h) -> int:
+    return lib().dc_token_buffer(h)
+
+
+def dc_audio_buffer(h) -> int:
+    return lib().dc_audio_buffer(h)
+
+
+def dc_get_stats(h) -> dict:
+    s = DcStats()
+    _check(lib().dc_get_stats(h, ctypes.byref(s)), h)
+    return s.as_dict()
+
+
+def dc_tap_find(h, name: str) -> int:
+    return lib().dc_tap_find(h, name.encode())
+
+
+def dc_tap_read(h, tap: int, b: int, frame0: int, nframes: int, channels: int) -> np.ndarray:
+    out = np.empty((nframes, channels), dtype=np.float32)
+    c = ctypes.c_int32()
+    _check(lib().dc_tap_read(h, tap, b, frame0, nframes, out.ctypes.data, ctypes.byref(c)), h)
+    assert c.value == channels, (c.value, channels)
+    return out
+
+
+def dc_last_error(h) -> str:
+    r = lib().dc_last_error(h)
+    return r.decode() if r else ""
+
+
+def dc_free(h) -> None:
+    lib().dc_free(h)
+
+
+# --------------------------------------------------------------- convenience
+
+class Decoder:
+    """One dc_state on the current GPU, with torch-ROCm tensors for device memory
+    and a dedicated torch stream that every call is ordered on."""
+
+    def __init__(self, arch: dict, dtype: str, blob: np.ndarray, batch: int, chunk_tokens: int,
+                 max_tokens: int | None = None, flags: int = 0, tile_variant: int = 0):
+        import torch
+        self.torch = torch
+        self.arch, self.dtype, self.batch = arch, dtype, batch
+        self.host = bool(flags & DC_HOST_PTRS)
+        self.stream = torch.cuda.Stream()
+        self.cfg = make_cfg(arch, dtype, batch, chunk_tokens, max_tokens, flags, tile_variant,
+                            self.stream.cuda_stream)
+        self.spt = dc_samples_per_token(self.cfg)
+        self.chunk_tokens = chunk_tokens
+        self.max_tokens = self.cfg.max_tokens
+        self.h = dc_init(blob, self.cfg)
+
+    def close(self):
+        if self.h is not None:
+            dc_free(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def decode(self, tokens, check: bool = True):
+        """tokens [batch][n] int32 (numpy in host mode, else a device tensor or
+        numpy copied to the device) -> PCM [batch][n*spt] (numpy in host mode,
+        else a device tensor)."""
+        torch = self.torch
+        n = tokens.shape[1]
+        if self.host:
+            tok = np.ascontiguousarray(tokens, dtype=np.int32)
+            out = np.empty((self.batch, n * self.spt), dtype=np.float32)
+            st = dc_decode_chunk(self.h, tok, n, out)
+        else:
+            with torch.cuda.stream(self.stream):
+                if isinstance(tokens, np.ndarray):
+                    tok = torch.from_numpy(np.ascontiguousarray(tokens, dtype=np.int32)).to("cuda")
+                else:
+                    tok = tokens.contiguous()
+                out = torch.empty((self.batch, n * self.spt), dtype=torch.float32, device="cuda")
+            self.stream.wait_stream(torch.cuda.current_stream())
+            st = dc_decode_chunk(self.h, tok, n, out)
+            tok.record_stream(self.stream)
+            out.record_stream(self.stream)
+            torch.cuda.current_stream().wait_stream(self.stream)
+        if check:
+            _check(st, self.h)
+        return out
+
+    def sync(self):
+        return _check(dc_sync(self.h), self.h)
+
+    def reset(self):
+        return _check(dc_reset(self.h), self.h)
+
+    def reset_stream(self, b: int):
+        return _check(dc_reset_stream(self.h, b), self.h)
+
+    def stats(self) -> dict:
+        return dc_get_stats(self.h)
+
+    def tap(self, name: str, b: int, frame0: int, nframes: int) -> np.ndarray:
+        t = dc_tap_find(self.h, name)
+        if t < 0:
+            raise KeyError(name)
+        ch = _tap_channels(self.arch, name)
+        return dc_tap_read(self.h, t, b, frame0, nframes, ch)
+
+
+def _tap_channels(arch: dict, name: str) -> int:
+    if name == "embed" or name.startswith("pre"):
+        return arch["channels"][0]
+    if name == "head":
+        return 2 * (arch["n_fft"] // 2 + 1)
+    if name == "G":
+        return arch["n_fft"]
+    s = int(name[1:name.index(".")])
+    return arch["channels"][s + 1]

@@ -1,0 +1,90 @@
+// Internal interface between the host runtime (dc_runtime.hip) and the gfx950
+// kernels (dc_kernels.hip).  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dc {
+
+// Element type of a ring buffer or of a conv operand.
+enum Elem : int { kF32 = 0, kBF16 = 1 };
+
+// A ring of frames for B streams: frame with absolute index tau of stream b
+// lives at ptr + ((b * R) + (tau mod R)) * C elements.  R >= ctx + frames of
+// the largest call, so a call's frames never overwrite the left context
+// (ctx frames) its consumers read.
+struct Ring {
+    void* ptr = nullptr;
+    int C = 0;
+    int elem = kF32;
+    int64_t R = 0;
+    int ctx = 0;
+    int level = 0;          // clock level: 0 = pre-stack frames, s+1 = after stage s
+};
+
+// One implicit-GEMM causal convolution launch.
+//   rows   (b, t): stream b, frame t in [0, F) of this call (input clock)
+//   cols   n in [0, N)
+//   K      (channel block cb, tap j, channel c): fixed order, independent of
+//          every launch parameter except the layer's own geometry
+//   out    conv:  frame t, channel n
+//          convT: frame t*u + n / Co, channel n % Co  (polyphase transposed conv)
+struct ConvParams {
+    const void* in;
+    int64_t in_R;
+    int in_C;
+    int in_elem;
+    int in_act;           // apply LeakyReLU to the operand at load
+    const void* wp;       // packed weights, operand element type
+    const float* bias;    // [N]
+    int CB;               // channels per block (multiple of the MFMA K quantum)
+    int n_cb;             // channel blocks (CB * n_cb >= in_C, zero padded)
+    int k, d;             // taps, dilation
+    int N;                // real columns
+    int NB16;             // packed column blocks of 16
+    void* out;
+    int64_t out_R;
+    int out_C;
+    int out_elem;
+    int out_act;          // apply LeakyReLU before the store
+    int u;                // 1 for a conv, stride u for a transposed conv
+    const float* res;     // residual ring (fp32, out geometry) or null
+    int64_t res_R;
+    const float* mean[3]; // earlier branch results (fp32 rings, out geometry)
+    int64_t mean_R;
+    int n_mean;           // >0: out = (mean[0] + ... + mean[n_mean-1] + z) / (n_mean + 1)
+    int B, F;             // streams, input frames of this call
+    int tiles_t;          // ceil(F / BM)
+    const int64_t* clock; // tokens decoded before this call
+    int64_t in_fpt;       // input-clock frames per token
+    float slope;
+};
+
+struct TileShape {
+    int BM, BN, WGM;      // rows, cols, waves along rows (4 waves per block)
+};
+
+// The tile shapes compiled for each operand type.
+int num_tile_variants();
+TileShape tile_variant(int v);
+
+// LDS bytes a conv launch needs with tile shape v.
+size_t conv_lds_bytes(int v, bool bf16, const ConvParams& p);
+
+hipError_t launch_conv(int v, bool bf16, const ConvParams& p, hipStream_t st);
+
+hipError_t launch_embed(const int32_t* tokens, int n, int B, const void* table, int vocab, int C,
+                        int elem, int fpt, Ring out, const int64_t* clock, int* err, hipStream_t st);
+
+// Head output [B][F][2*(N/2+1)] -> windowed inverse-DFT frames in the G ring.
+hipError_t launch_spectrum(const float* head, int64_t head_R, int B, int F, const float* table,
+                           Ring g, const int64_t* clock, int64_t fpt, hipStream_t st);
+
+// G ring -> PCM [B][F*hop] (row stride F*hop), overlap-added in ascending frame order.
+hipError_t launch_ola(Ring g, int B, int F, int hop, int n_fft, float* pcm, const int64_t* clock,
+                      int64_t fpt, hipStream_t st);
+
+hipError_t launch_clock(int64_t* clock, int n, hipStream_t st);
+
+}  // namespace dc

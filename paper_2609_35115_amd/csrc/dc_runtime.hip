@@ -1,0 +1,767 @@
+// Host runtime of the streaming Token2Wav decode step: configuration checks,
+// weight packing, the one device arena, the carried ring buffers, the device
+// clock, fail-closed admission, HIP-graph capture and replay, counters.
+//
+// State rule (Design, "State rule: demand sizing and the carry", Eq. carry):
+// every intermediate a causal layer reads is a ring of ctx + F_max frames per
+// stream at a fixed address, where ctx is exactly the left context its
+// consumers read ((k-1)*d for a conv, 1 frame for a transposed conv, n_fft/hop
+// - 1 windowed frames for the overlap-add) and F_max the frames of the largest
+// call.  The producing kernel writes a call's frames at slots tau mod R, so
+// the left context of the next call is already in place: no staging copy, no
+// pointer change, and a reset zeroes the rings where they are.
+//
+// Compute rule (Design, "Compute rule: exact-shape replay", Eq. granularity):
+// the whole chunk step for n == chunk_tokens is captured once as one HIP
+// graph and replayed; kernels take the time offset of a call from a device
+// clock that the last node advances, so the frozen kernel arguments stay
+// valid.  Any other admissible n launches the same kernels directly.
+#include <chrono>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/dc.h"
+#include "dc_internal.h"
+
+using namespace dc;
+
+namespace {
+
+struct ConvOp {
+    std::string name;
+    int in = -1, out = -1, res = -1;
+    int mean[3] = {-1, -1, -1};
+    int n_mean = 0;
+    int Ci = 0, N = 0, out_C = 0, k = 1, d = 1, u = 1;
+    int in_act = 0, out_act = 0;
+    bool bf16 = false;   // operand type
+    bool transposed = false;
+    size_t w_off = 0, b_off = 0, w_bytes = 0;
+    size_t blob_w = 0, blob_b = 0;  // float offsets into the blob
+    int CB = 0, n_cb = 0, NB16 = 0;
+    int variant = 0;
+    int level_in = 0;
+};
+
+thread_local std::string g_init_error;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+uint16_t host_f2bf(float f)
+{
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0x007fffffu) ? 0x40u : 0u));
+    return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
+float host_bf2f(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+float round_param(float x, bool bf16) { return bf16 ? host_bf2f(host_f2bf(x)) : x; }
+
+}  // namespace
+
+struct dc_state {
+    dc_cfg cfg{};
+    hipStream_t stream = nullptr;
+    bool own_stream = false;
+    char* arena = nullptr;
+    size_t arena_bytes = 0;
+    std::vector<Ring> rings;
+    std::vector<std::string> ring_names;
+    std::vector<int> ring_ctx;
+    std::vector<ConvOp> convs;
+    int ring_E = -1, ring_S = -1, ring_G = -1;
+    int levels = 0;
+    int64_t fpt[DC_MAX_STAGES + 2] = {};
+    int64_t spt = 0;
+    size_t emb_off = 0, table_off = 0, tok_off = 0, audio_off = 0, clock_off = 0, err_off = 0;
+    size_t ring_begin = 0, ring_end = 0;
+    int32_t* tok = nullptr;
+    float* audio = nullptr;
+    int64_t* clock = nullptr;
+    int* err = nullptr;
+    void* emb = nullptr;
+    float* table = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    dc_stats st{};
+    int64_t clock_host = 0;
+    bool poisoned = false;
+    std::string msg;
+};
+
+// ------------------------------------------------------------------ helpers
+
+static dc_status fail(dc_state* s, dc_status code, const std::string& why)
+{
+    if (s) s->msg = why;
+    else g_init_error = why;
+    return code;
+}
+
+static dc_status device_fail(dc_state* s, hipError_t e, const char* where)
+{
+    s->poisoned = true;
+    return fail(s, DC_EDEVICE, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+static int64_t samples_per_token(const dc_cfg* c)
+{
+    int64_t u = 1;
+    for (int i = 0; i < c->n_stages; i++) u *= c->up_rate[i];
+    return (int64_t)c->frames_per_token * u * c->hop;
+}
+
+static int64_t blob_floats(const dc_cfg* c)
+{
+    int64_t n = (int64_t)c->vocab * c->embed;
+    int64_t c0 = c->channels[0];
+    n += (int64_t)c->n_pre * (c0 * c0 * c->pre_kernel + c0);
+    for (int s = 0; s < c->n_stages; s++) {
+        int64_t ci = c->channels[s], co = c->channels[s + 1];
+        n += ci * co * 2 * c->up_rate[s] + co;
+        for (int j = 0; j < c->n_rb; j++) n += (int64_t)c->n_dil * 2 * (co * co * c->rb_kernel[j] + co);
+    }
+    int64_t hc = 2 * (c->n_fft / 2 + 1);
+    n += hc * c->channels[c->n_stages] * c->head_kernel + hc;
+    return n;
+}
+
+static std::string validate(const dc_cfg* c)
+{
+    if (c->vocab <= 0 || c->embed <= 0) return "vocab and embed must be positive";
+    if (c->frames_per_token < 1 || c->frames_per_token > 64) return "frames_per_token must be in [1, 64]";
+    if (c->n_pre < 0 || c->n_pre > 64 || c->pre_kernel < 1 || c->pre_kernel > 64) return "bad pre-stack";
+    if (c->n_stages < 1 || c->n_stages > DC_MAX_STAGES) return "n_stages must be in [1, 4]";
+    for (int i = 0; i < c->n_stages; i++)
+        if (c->up_rate[i] < 1 || c->up_rate[i] > 64) return "up_rate must be in [1, 64]";
+    for (int i = 0; i <= c->n_stages; i++)
+        if (c->channels[i] < 8 || c->channels[i] % 8 || c->channels[i] > 4096)
+            return "channels must be positive multiples of 8 (<= 4096)";
+    if (c->channels[0] != c->embed) return "channels[0] must equal embed";
+    if (c->n_rb < 1 || c->n_rb > DC_MAX_RB) return "n_rb must be in [1, 4]";
+    for (int i = 0; i < c->n_rb; i++)
+        if (c->rb_kernel[i] < 1 || c->rb_kernel[i] > 64) return "rb_kernel must be in [1, 64]";
+    if (c->n_dil < 1 || c->n_dil > DC_MAX_DIL) return "n_dil must be in [1, 4]";
+    for (int i = 0; i < c->n_dil; i++)
+        if (c->dil[i] < 1 || c->dil[i] > 64) return "dil must be in [1, 64]";
+    if (c->head_kernel < 1 || c->head_kernel > 64) return "head_kernel must be in [1, 64]";
+    if (c->n_fft != 16 || c->hop != 4) return "only n_fft = 16, hop = 4 is supported";
+    if (!(c->lrelu_slope >= 0.0f && c->lrelu_slope <= 1.0f)) return "lrelu_slope must be in [0, 1]";
+    if (c->dtype != DC_F32 && c->dtype != DC_BF16) return "dtype must be DC_F32 or DC_BF16";
+    if (c->batch < 1 || c->batch > 65536) return "batch must be in [1, 65536]";
+    if (c->chunk_tokens < 1 || c->max_tokens < c->chunk_tokens) return "need 1 <= chunk_tokens <= max_tokens";
+    if ((int64_t)c->max_tokens * samples_per_token(c) > (int64_t)1 << 30) return "max_tokens too large";
+    if (c->flags & ~(uint32_t)(DC_HOST_PTRS | DC_NO_GRAPH)) return "unknown flag bits";
+    if (c->tile_variant < 0 || c->tile_variant > num_tile_variants()) return "tile_variant out of range";
+    return "";
+}
+
+// Geometry of the packed weights of one conv (operand type decides the K quantum).
+static void set_blocks(ConvOp& op)
+{
+    const int kq = op.bf16 ? 32 : 16;
+    const int cmax = op.bf16 ? 128 : 64;
+    const int cpad = (op.Ci + kq - 1) / kq * kq;
+    op.CB = cpad < cmax ? cpad : cmax;
+    op.n_cb = (cpad + op.CB - 1) / op.CB;
+    op.NB16 = (op.N + 15) / 16;
+    op.w_bytes = (size_t)op.n_cb * op.k * (op.CB / kq) * op.NB16 * 64 * 16;
+}
+
+// Weight value of column n, input channel ch, tap j (0 outside the layer).
+static float weight_at(const ConvOp& op, const float* blob, int n, int ch, int j)
+{
+    if (n >= op.N || ch >= op.Ci) return 0.0f;
+    if (!op.transposed) return blob[op.blob_w + ((size_t)n * op.Ci + ch) * op.k + j];
+    // transposed conv [Ci][Co][2u]: column n = r*Co + o; tap 0 reads the
+    // previous input frame (kernel index r + u), tap 1 the current one (r).
+    const int r = n / op.out_C, o = n % op.out_C;
+    return blob[op.blob_w + ((size_t)ch * op.out_C + o) * (2 * op.u) + r + (1 - j) * op.u];
+}
+
+// Pack into MFMA fragment order: [cb][tap][chunk][col block][lane][values].
+static void pack_weights(const ConvOp& op, const float* blob, bool round_bf16, char* dst)
+{
+    const int kq = op.bf16 ? 32 : 16;
+    const int chunks = op.CB / kq;
+    size_t idx = 0;
+    for (int cb = 0; cb < op.n_cb; cb++)
+        for (int j = 0; j < op.k; j++)
+            for (int kc = 0; kc < chunks; kc++)
+                for (int nb = 0; nb < op.NB16; nb++)
+                    for (int lane = 0; lane < 64; lane++) {
+                        const int n = nb * 16 + (lane & 15);
+                        if (op.bf16) {
+                            uint16_t* o = (uint16_t*)dst + idx * 8;
+                            for (int e = 0; e < 8; e++) {
+                                const int ch = cb * op.CB + kc * 32 + (lane >> 4) * 8 + e;
+                                o[e] = host_f2bf(weight_at(op, blob, n, ch, j));
+                            }
+                        } else {
+                            float* o = (float*)dst + idx * 4;
+                            for (int q = 0; q < 4; q++) {
+                                const int ch = cb * op.CB + kc * 16 + (lane >> 4) * 4 + q;
+                                o[q] = round_param(weight_at(op, blob, n, ch, j), round_bf16);
+                            }
+                        }
+                        idx++;
+                    }
+}
+
+static int pick_variant(const dc_state* s, const ConvOp& op)
+{
+    const int B = s->cfg.batch;
+    const int64_t F = (int64_t)s->cfg.chunk_tokens * s->fpt[op.level_in];
+    ConvParams p{};
+    p.k = op.k;
+    p.d = op.d;
+    p.CB = op.CB;
+    const size_t lds_max = 64 * 1024;
+    if (s->cfg.tile_variant > 0) {
+        const int v = s->cfg.tile_variant - 1;
+        if (conv_lds_bytes(v, op.bf16, p) <= lds_max) return v;
+    }
+    const int npad = (op.N + 15) / 16 * 16;
+    static const int order[] = {6, 5, 4, 3, 2, 1, 0};
+    int best = -1;
+    double best_score = -1.0;
+    for (int v : order) {
+        const TileShape t = tile_variant(v);
+        if (conv_lds_bytes(v, op.bf16, p) > lds_max) continue;
+        if (t.BN > (npad > 32 ? npad : 32)) continue;
+        const int64_t tiles_t = (F + t.BM - 1) / t.BM;
+        const int64_t blocks = (int64_t)B * tiles_t * ((op.N + t.BN - 1) / t.BN);
+        const double eff = (double)F / (double)(tiles_t * t.BM);
+        if (blocks >= 512 && eff >= 0.75) return v;
+        const double score = (double)(blocks < 512 ? blocks : 512) * eff;
+        if (score > best_score) {
+            best_score = score;
+            best = v;
+        }
+    }
+    return best < 0 ? 0 : best;
+}
+
+// ------------------------------------------------------------ the network
+
+static int add_ring(dc_state* s, const std::string& name, int C, int elem, int level)
+{
+    Ring r;
+    r.C = C;
+    r.elem = elem;
+    r.level = level;
+    s->rings.push_back(r);
+    s->ring_names.push_back(name);
+    s->ring_ctx.push_back(0);
+    return (int)s->rings.size() - 1;
+}
+
+static void need_ctx(dc_state* s, int ring, int ctx)
+{
+    if (ctx > s->ring_ctx[ring]) s->ring_ctx[ring] = ctx;
+}
+
+static void build_network(dc_state* s)
+{
+    const dc_cfg& c = s->cfg;
+    const bool bf = c.dtype == DC_BF16;
+    const int opE = bf ? kBF16 : kF32;
+    size_t off = (size_t)c.vocab * c.embed;  // blob float offset after the embedding
+    auto conv = [&](const std::string& name, int in, int out, int Ci, int N, int k, int d, int level) -> ConvOp& {
+        ConvOp op;
+        op.name = name;
+        op.in = in;
+        op.out = out;
+        op.Ci = Ci;
+        op.N = N;
+        op.out_C = N;
+        op.k = k;
+        op.d = d;
+        op.bf16 = bf;
+        op.level_in = level;
+        op.blob_w = off;
+        off += (size_t)N * Ci * k;
+        op.blob_b = off;
+        off += (size_t)N;
+        s->convs.push_back(op);
+        return s->convs.back();
+    };
+
+    const int C0 = c.channels[0];
+    s->ring_E = add_ring(s, "embed", C0, opE, 0);
+    int cur = s->ring_E;
+    for (int l = 0; l < c.n_pre; l++) {
+        const int P = add_ring(s, "pre" + std::to_string(l), C0, opE, 0);
+        ConvOp& op = conv("pre" + std::to_string(l), cur, P, C0, C0, c.pre_kernel, 1, 0);
+        op.out_act = 1;
+        need_ctx(s, cur, c.pre_kernel - 1);
+        cur = P;
+    }
+    for (int st = 0; st < c.n_stages; st++) {
+        const int ci = c.channels[st], co = c.channels[st + 1], u = c.up_rate[st];
+        const std::string sn = "s" + std::to_string(st);
+        const int Y = add_ring(s, sn + ".y", co, kF32, st + 1);
+        {
+            ConvOp op;
+            op.name = sn + ".up";
+            op.in = cur;
+            op.out = Y;
+            op.Ci = ci;
+            op.N = u * co;
+            op.out_C = co;
+            op.k = 2;
+            op.d = 1;
+            op.u = u;
+            op.transposed = true;
+            op.in_act = 1;
+            op.bf16 = bf;
+            op.level_in = st;
+            op.blob_w = off;
+            off += (size_t)ci * co * 2 * u;
+            op.blob_b = off;
+            off += (size_t)co;
+            s->convs.push_back(op);
+            need_ctx(s, cur, 1);
+        }
+        std::vector<int> zlast;
+        int X = -1;
+        for (int j = 0; j < c.n_rb; j++) {
+            const int kj = c.rb_kernel[j];
+            int zin = Y;
+            for (int i = 0; i < c.n_dil; i++) {
+                const std::string pn = sn + ".rb" + std::to_string(j);
+                const int H = add_ring(s, pn + ".h" + std::to_string(i), co, opE, st + 1);
+                {
+                    ConvOp& op = conv(pn + ".d" + std::to_string(i) + ".c1", zin, H, co, co, kj, c.dil[i], st + 1);
+                    op.in_act = 1;
+                    op.out_act = 1;
+                    need_ctx(s, zin, (kj - 1) * c.dil[i]);
+                }
+                const bool last = i == c.n_dil - 1;
+                int Z;
+                if (last && j == c.n_rb - 1)
+                    Z = X = add_ring(s, sn + ".x", co, kF32, st + 1);
+                else
+                    Z = add_ring(s, pn + ".z" + std::to_string(i), co, kF32, st + 1);
+                ConvOp& op = conv(pn + ".d" + std::to_string(i) + ".c2", H, Z, co, co, kj, 1, st + 1);
+                op.res = zin;
+                need_ctx(s, H, kj - 1);
+                if (Z == X) {
+                    op.n_mean = (int)zlast.size();
+                    for (int m = 0; m < op.n_mean; m++) op.mean[m] = zlast[m];
+                }
+                zin = Z;
+            }
+            zlast.push_back(zin);
+        }
+        cur = X;
+    }
+    const int L = c.n_stages;
+    const int hc = 2 * (c.n_fft / 2 + 1);
+    s->ring_S = add_ring(s, "head", hc, kF32, L);
+    {
+        ConvOp& op = conv("head", cur, s->ring_S, c.channels[L], hc, c.head_kernel, 1, L);
+        op.in_act = 1;
+        op.bf16 = false;  // head arithmetic is fp32 on (possibly bf16-rounded) weights
+        need_ctx(s, cur, c.head_kernel - 1);
+    }
+    s->ring_G = add_ring(s, "G", c.n_fft, kF32, L);
+    need_ctx(s, s->ring_G, c.n_fft / c.hop - 1);
+    for (auto& op : s->convs) set_blocks(op);
+}
+
+// ------------------------------------------------------------ one chunk step
+
+static hipError_t enqueue_step(dc_state* s, int n, hipStream_t st)
+{
+    const dc_cfg& c = s->cfg;
+    hipError_t e = launch_embed(s->tok, n, c.batch, s->emb, c.vocab, c.embed, s->rings[s->ring_E].elem,
+                                c.frames_per_token, s->rings[s->ring_E], s->clock, s->err, st);
+    if (e != hipSuccess) return e;
+    for (const ConvOp& op : s->convs) {
+        const Ring& in = s->rings[op.in];
+        const Ring& out = s->rings[op.out];
+        ConvParams p{};
+        p.in = in.ptr;
+        p.in_R = in.R;
+        p.in_C = in.C;
+        p.in_elem = in.elem;
+        p.in_act = op.in_act;
+        p.wp = s->arena + op.w_off;
+        p.bias = (const float*)(s->arena + op.b_off);
+        p.CB = op.CB;
+        p.n_cb = op.n_cb;
+        p.k = op.k;
+        p.d = op.d;
+        p.N = op.N;
+        p.NB16 = op.NB16;
+        p.out = out.ptr;
+        p.out_R = out.R;
+        p.out_C = out.C;
+        p.out_elem = out.elem;
+        p.out_act = op.out_act;
+        p.u = op.u;
+        if (op.res >= 0) {
+            p.res = (const float*)s->rings[op.res].ptr;
+            p.res_R = s->rings[op.res].R;
+        }
+        p.n_mean = op.n_mean;
+        for (int m = 0; m < op.n_mean; m++) {
+            p.mean[m] = (const float*)s->rings[op.mean[m]].ptr;
+            p.mean_R = s->rings[op.mean[m]].R;
+        }
+        p.B = c.batch;
+        p.F = (int)(n * s->fpt[op.level_in]);
+        p.tiles_t = (p.F + tile_variant(op.variant).BM - 1) / tile_variant(op.variant).BM;
+        p.clock = s->clock;
+        p.in_fpt = s->fpt[op.level_in];
+        p.slope = c.lrelu_slope;
+        e = launch_conv(op.variant, op.bf16, p, st);
+        if (e != hipSuccess) return e;
+    }
+    const int L = c.n_stages;
+    const int FL = (int)(n * s->fpt[L]);
+    e = launch_spectrum((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL, s->table,
+                        s->rings[s->ring_G], s->clock, s->fpt[L], st);
+    if (e != hipSuccess) return e;
+    e = launch_ola(s->rings[s->ring_G], c.batch, FL, c.hop, c.n_fft, s->audio, s->clock, s->fpt[L], st);
+    if (e != hipSuccess) return e;
+    return launch_clock(s->clock, n, st);
+}
+
+static hipError_t zero_state(dc_state* s)
+{
+    hipError_t e = hipMemsetAsync(s->arena + s->ring_begin, 0, s->ring_end - s->ring_begin, s->stream);
+    if (e != hipSuccess) return e;
+    e = hipMemsetAsync(s->clock, 0, sizeof(int64_t), s->stream);
+    if (e != hipSuccess) return e;
+    return hipMemsetAsync(s->err, 0, sizeof(int), s->stream);
+}
+
+// ------------------------------------------------------------------ the ABI
+
+extern "C" {
+
+int64_t dc_samples_per_token(const dc_cfg* cfg) { return cfg ? samples_per_token(cfg) : 0; }
+
+int64_t dc_blob_floats(const dc_cfg* cfg) { return cfg ? blob_floats(cfg) : 0; }
+
+dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg, dc_state** out)
+{
+    if (!out) return fail(nullptr, DC_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!cfg || !weights_blob) return fail(nullptr, DC_EINVAL, "cfg or weights is NULL");
+    if (cfg->abi_version != DC_ABI_VERSION) return fail(nullptr, DC_EVERSION, "abi_version mismatch");
+    const std::string why = validate(cfg);
+    if (!why.empty()) return fail(nullptr, DC_EINVAL, why);
+    if (blob_bytes != (size_t)blob_floats(cfg) * sizeof(float))
+        return fail(nullptr, DC_EINVAL, "blob size does not match the architecture");
+
+    const auto t_start = std::chrono::steady_clock::now();
+    dc_state* s = new dc_state();
+    s->cfg = *cfg;
+    const dc_cfg& c = s->cfg;
+    const bool bf = c.dtype == DC_BF16;
+    s->fpt[0] = c.frames_per_token;
+    for (int i = 0; i < c.n_stages; i++) s->fpt[i + 1] = s->fpt[i] * c.up_rate[i];
+    s->spt = samples_per_token(&c);
+    build_network(s);
+    for (auto& op : s->convs) op.variant = pick_variant(s, op);
+
+    // ---- arena layout: constants and weights, then rings, then I/O buffers
+    const float* blob = (const float*)weights_blob;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    s->emb_off = take((size_t)c.vocab * c.embed * (bf ? 2 : 4));
+    s->table_off = take(2 * 16 * 9 * sizeof(float));
+    for (auto& op : s->convs) {
+        op.w_off = take(op.w_bytes);
+        op.b_off = take((size_t)op.N * sizeof(float));
+    }
+    const size_t weights_end = off;
+    s->ring_begin = off;
+    int64_t carry = 0;
+    for (size_t i = 0; i < s->rings.size(); i++) {
+        Ring& r = s->rings[i];
+        r.ctx = s->ring_ctx[i];
+        r.R = r.ctx + (int64_t)c.max_tokens * s->fpt[r.level];
+        const size_t es = r.elem == kBF16 ? 2 : 4;
+        r.ptr = (void*)take((size_t)c.batch * r.R * r.C * es);  // offset for now
+        carry += (int64_t)c.batch * r.ctx * r.C * es;
+    }
+    s->ring_end = off;
+    s->tok_off = take((size_t)c.batch * c.max_tokens * sizeof(int32_t));
+    s->audio_off = take((size_t)c.batch * c.max_tokens * s->spt * sizeof(float));
+    s->clock_off = take(sizeof(int64_t));
+    s->err_off = take(sizeof(int));
+    s->arena_bytes = off;
+
+    hipError_t e = hipMalloc((void**)&s->arena, s->arena_bytes);
+    if (e != hipSuccess) {
+        delete s;
+        return fail(nullptr, DC_ENOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    for (auto& r : s->rings) r.ptr = s->arena + (size_t)r.ptr;
+    s->emb = s->arena + s->emb_off;
+    s->table = (float*)(s->arena + s->table_off);
+    s->tok = (int32_t*)(s->arena + s->tok_off);
+    s->audio = (float*)(s->arena + s->audio_off);
+    s->clock = (int64_t*)(s->arena + s->clock_off);
+    s->err = (int*)(s->arena + s->err_off);
+
+    if (c.hip_stream) {
+        s->stream = (hipStream_t)c.hip_stream;
+    } else {
+        e = hipStreamCreateWithFlags(&s->stream, hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            (void)hipFree(s->arena);
+            delete s;
+            return fail(nullptr, DC_EDEVICE, std::string("hipStreamCreate: ") + hipGetErrorString(e));
+        }
+        s->own_stream = true;
+    }
+
+    // ---- host-side packing of weights and device-resident constants
+    std::vector<char> host(weights_end, 0);
+    if (bf) {
+        uint16_t* et = (uint16_t*)(host.data() + s->emb_off);
+        for (size_t i = 0; i < (size_t)c.vocab * c.embed; i++) et[i] = host_f2bf(blob[i]);
+    } else {
+        std::memcpy(host.data() + s->emb_off, blob, (size_t)c.vocab * c.embed * sizeof(float));
+    }
+    {
+        // Real inverse DFT x[n] = (1/N)[X0 + (-1)^n X_{N/2} + 2 sum Re X cos - Im X sin],
+        // times the periodic Hann window w[n], divided by the overlap-add
+        // normaliser sum_m w^2[n - hop m]; all in double, rounded once.
+        const int N = c.n_fft, nb = N / 2 + 1;
+        double w[64];
+        for (int n = 0; n < N; n++) w[n] = 0.5 - 0.5 * std::cos(2.0 * M_PI * n / N);
+        double norm = 0.0;
+        for (int n = N - 1; n >= 0; n -= c.hop) norm += w[n] * w[n];
+        float* tr = (float*)(host.data() + s->table_off);
+        float* ti = tr + N * nb;
+        for (int n = 0; n < N; n++)
+            for (int kk = 0; kk < nb; kk++) {
+                const double a = 2.0 * M_PI * kk * n / N;
+                const double f = (kk == 0 || kk == N / 2) ? 1.0 : 2.0;
+                tr[n * nb + kk] = (float)(w[n] * f * std::cos(a) / N / norm);
+                ti[n * nb + kk] = (kk == 0 || kk == N / 2) ? 0.0f : (float)(-w[n] * 2.0 * std::sin(a) / N / norm);
+            }
+    }
+    for (auto& op : s->convs) {
+        pack_weights(op, blob, bf, host.data() + op.w_off);
+        float* bias = (float*)(host.data() + op.b_off);
+        for (int n = 0; n < op.N; n++) bias[n] = round_param(blob[op.blob_b + (op.transposed ? n % op.out_C : n)], bf);
+    }
+    s->st.weight_bytes = (int64_t)weights_end;
+    s->st.arena_bytes = (int64_t)s->arena_bytes;
+    s->st.carry_bytes = carry;
+    s->st.ring_bytes = (int64_t)(s->ring_end - s->ring_begin);
+    s->st.kernels_per_step = (int32_t)s->convs.size() + 4;
+
+    e = hipMemcpy(s->arena, host.data(), weights_end, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemsetAsync(s->arena + weights_end, 0, s->arena_bytes - weights_end, s->stream);
+    // Warm-up: one direct step on zero tokens loads every code object before capture.
+    if (e == hipSuccess) e = enqueue_step(s, c.chunk_tokens, s->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+    if (e == hipSuccess && !(c.flags & DC_NO_GRAPH)) {
+        hipStream_t cs = nullptr;
+        e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+        if (e == hipSuccess) {
+            const hipError_t le = enqueue_step(s, c.chunk_tokens, cs);
+            e = hipStreamEndCapture(cs, &s->graph);
+            if (le != hipSuccess) e = le;
+        }
+        if (e == hipSuccess) e = hipGraphInstantiate(&s->exec, s->graph, nullptr, nullptr, 0);
+        if (e == hipSuccess) {
+            size_t nodes = 0;
+            if (hipGraphGetNodes(s->graph, nullptr, &nodes) == hipSuccess) s->st.graph_nodes = (int32_t)nodes;
+        }
+        if (cs) (void)hipStreamDestroy(cs);
+    }
+    if (e == hipSuccess) e = zero_state(s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) {
+        const std::string m = std::string("dc_init: ") + hipGetErrorString(e);
+        dc_free(s);
+        return fail(nullptr, DC_EDEVICE, m);
+    }
+    s->st.capture_ms =
+        std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+    *out = s;
+    return DC_OK;
+}
+
+dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* audio_out)
+{
+    if (!s) return DC_EINVAL;
+    if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned; call dc_reset");
+    const dc_cfg& c = s->cfg;
+    if (!tokens || !audio_out) {
+        s->st.rejected++;
+        return fail(s, DC_EINVAL, "tokens or audio_out is NULL");
+    }
+    if (n <= 0) {
+        s->st.rejected++;
+        return fail(s, DC_EINVAL, "n must be positive");
+    }
+    if (n > c.max_tokens) {
+        s->st.rejected++;
+        return fail(s, DC_ERANGE, "n exceeds max_tokens");
+    }
+    const bool host = (c.flags & DC_HOST_PTRS) != 0;
+    const size_t tok_bytes = (size_t)c.batch * n * sizeof(int32_t);
+    const size_t pcm_bytes = (size_t)c.batch * n * s->spt * sizeof(float);
+    if (host) {
+        for (size_t i = 0; i < (size_t)c.batch * n; i++)
+            if (tokens[i] < 0 || tokens[i] >= c.vocab) {
+                s->st.rejected++;
+                return fail(s, DC_ERANGE, "token id outside [0, vocab)");
+            }
+    }
+    hipError_t e = hipSuccess;
+    if (tokens != s->tok) {
+        e = hipMemcpyAsync(s->tok, tokens, tok_bytes, host ? hipMemcpyHostToDevice : hipMemcpyDeviceToDevice,
+                           s->stream);
+        if (e != hipSuccess) return device_fail(s, e, "token staging");
+        s->st.staged_tokens++;
+    }
+    if (n == c.chunk_tokens && s->exec) {
+        e = hipGraphLaunch(s->exec, s->stream);
+        if (e != hipSuccess) return device_fail(s, e, "hipGraphLaunch");
+        s->st.replays++;
+    } else {
+        e = enqueue_step(s, n, s->stream);
+        if (e != hipSuccess) return device_fail(s, e, "direct launch");
+        if (n != c.chunk_tokens) s->st.direct_shape++;
+        else s->st.direct_nograph++;
+    }
+    s->st.calls++;
+    s->clock_host += n;
+    if (audio_out != s->audio) {
+        e = hipMemcpyAsync(audio_out, s->audio, pcm_bytes, host ? hipMemcpyDeviceToHost : hipMemcpyDeviceToDevice,
+                           s->stream);
+        if (e != hipSuccess) return device_fail(s, e, "audio staging");
+        s->st.staged_audio++;
+    }
+    if (host) return dc_sync(s);
+    return DC_OK;
+}
+
+dc_status dc_sync(dc_state* s)
+{
+    if (!s) return DC_EINVAL;
+    hipError_t e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) return device_fail(s, e, "hipStreamSynchronize");
+    int flag = 0;
+    e = hipMemcpy(&flag, s->err, sizeof(int), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return device_fail(s, e, "error flag read");
+    if (flag) {
+        s->poisoned = true;
+        return fail(s, DC_ERANGE, "token id outside [0, vocab) reached the device; call dc_reset");
+    }
+    if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned; call dc_reset");
+    return DC_OK;
+}
+
+dc_status dc_reset(dc_state* s)
+{
+    if (!s) return DC_EINVAL;
+    hipError_t e = zero_state(s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) return device_fail(s, e, "dc_reset");
+    s->poisoned = false;
+    s->clock_host = 0;
+    return DC_OK;
+}
+
+dc_status dc_reset_stream(dc_state* s, int32_t b)
+{
+    if (!s) return DC_EINVAL;
+    if (b < 0 || b >= s->cfg.batch) return fail(s, DC_EINVAL, "stream index out of range");
+    for (const Ring& r : s->rings) {
+        const size_t es = r.elem == kBF16 ? 2 : 4;
+        const size_t per = (size_t)r.R * r.C * es;
+        hipError_t e = hipMemsetAsync((char*)r.ptr + (size_t)b * per, 0, per, s->stream);
+        if (e != hipSuccess) return device_fail(s, e, "dc_reset_stream");
+    }
+    return DC_OK;
+}
+
+int32_t* dc_token_buffer(dc_state* s) { return s ? s->tok : nullptr; }
+
+float* dc_audio_buffer(dc_state* s) { return s ? s->audio : nullptr; }
+
+dc_status dc_get_stats(const dc_state* s, dc_stats* out)
+{
+    if (!s || !out) return DC_EINVAL;
+    *out = s->st;
+    out->clock_tokens = s->clock_host;
+    return DC_OK;
+}
+
+int32_t dc_tap_find(const dc_state* s, const char* name)
+{
+    if (!s || !name) return -1;
+    for (size_t i = 0; i < s->ring_names.size(); i++)
+        if (s->ring_names[i] == name) return (int32_t)i;
+    return -1;
+}
+
+dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32_t nframes, float* host_out,
+                      int32_t* channels)
+{
+    if (!s || !host_out || tap < 0 || tap >= (int32_t)s->rings.size() || b < 0 || b >= s->cfg.batch ||
+        nframes < 0)
+        return fail(s, DC_EINVAL, "bad tap arguments");
+    const Ring& r = s->rings[tap];
+    if (channels) *channels = r.C;
+    const int64_t end = s->clock_host * s->fpt[r.level];
+    if (frame0 < end - r.R || frame0 + nframes > end) return fail(s, DC_ERANGE, "frames not held by the ring");
+    hipError_t e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) return device_fail(s, e, "dc_tap_read");
+    const size_t es = r.elem == kBF16 ? 2 : 4;
+    std::vector<char> row((size_t)r.C * es);
+    for (int32_t f = 0; f < nframes; f++) {
+        int64_t slot = (frame0 + f) % r.R;
+        if (slot < 0) slot += r.R;
+        e = hipMemcpy(row.data(), (char*)r.ptr + ((size_t)b * r.R + slot) * r.C * es, row.size(),
+                      hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return device_fail(s, e, "dc_tap_read copy");
+        for (int ch = 0; ch < r.C; ch++)
+            host_out[(size_t)f * r.C + ch] =
+                r.elem == kBF16 ? host_bf2f(((uint16_t*)row.data())[ch]) : ((float*)row.data())[ch];
+    }
+    return DC_OK;
+}
+
+const char* dc_last_error(const dc_state* s) { return s ? s->msg.c_str() : g_init_error.c_str(); }
+
+void dc_free(dc_state* s)
+{
+    if (!s) return;
+    if (s->stream) (void)hipStreamSynchronize(s->stream);
+    if (s->exec) (void)hipGraphExecDestroy(s->exec);
+    if (s->graph) (void)hipGraphDestroy(s->graph);
+    if (s->arena) (void)hipFree(s->arena);
+    if (s->own_stream && s->stream) (void)hipStreamDestroy(s->stream);
+    delete s;
+}
+
+}  // extern "C"

@@ -1,0 +1,88 @@
+"""The C-ABI library on the host: it loads, exports every symbol include/dc.h
+declares, and its host-only logic (sizes, configuration checks) fails closed
+before touching the device.  No GPU needed."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_35115_amd as dc
+from paper_2609_35115_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "dc.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dc_[a-z_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(dc.SIGNATURES)
+
+
+def test_library_exports_every_declared_symbol():
+    L = ctypes.CDLL(dc.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_struct_sizes_match_header_layout():
+    # dc_cfg: 33 int32 fields + float + uint32 -> padded to 8 before the pointer
+    assert ctypes.sizeof(dc.DcCfg) == 152
+    assert ctypes.sizeof(dc.DcStats) == 12 * 8 + 2 * 4 + 8
+
+
+@pytest.mark.parametrize("name", list(synth.WORKLOADS))
+def test_sizes_agree_with_generator(name):
+    w = synth.workload(name)
+    cfg = dc.make_cfg(w["arch"], w["dtype"], w["batch"], w["chunk_tokens"])
+    assert dc.dc_samples_per_token(cfg) == synth.samples_per_token(w["arch"])
+    assert dc.dc_blob_floats(cfg) == synth.blob_floats(w["arch"])
+
+
+def _init_status(cfg, blob):
+    blob = np.ascontiguousarray(blob, dtype=np.float32)
+    h = ctypes.c_void_p()
+    st = dc.lib().dc_init(blob.ctypes.data, blob.nbytes, ctypes.byref(cfg), ctypes.byref(h))
+    return st, h.value
+
+
+def test_init_rejects_bad_configs_before_any_device_call():
+    arch = synth.TINY_ARCH
+    blob = synth.make_weights(arch)
+    good = lambda **kw: dc.make_cfg(arch, "f32", kw.pop("batch", 1), kw.pop("chunk", 8), kw.pop("max", 8))
+    c = good()
+    c.abi_version = 99
+    assert _init_status(c, blob) == (dc.DC_EVERSION, None)
+    c = good()
+    c.n_fft = 32
+    assert _init_status(c, blob)[0] == dc.DC_EINVAL
+    assert "n_fft" in dc.dc_last_error(None)
+    c = good(chunk=9, max=8)
+    assert _init_status(c, blob)[0] == dc.DC_EINVAL
+    c = good()
+    c.channels[2] = 12
+    assert _init_status(c, blob)[0] == dc.DC_EINVAL
+    c = good()
+    c.dtype = 7
+    assert _init_status(c, blob)[0] == dc.DC_EINVAL
+    c = good()
+    c.flags = 1 << 7
+    assert _init_status(c, blob)[0] == dc.DC_EINVAL
+    c = good()
+    assert _init_status(c, blob[:-1])[0] == dc.DC_EINVAL
+    assert "blob size" in dc.dc_last_error(None)
+
+
+def test_null_state_calls_fail_closed():
+    L = dc.lib()
+    assert L.dc_decode_chunk(None, None, 1, None) == dc.DC_EINVAL
+    assert L.dc_reset(None) == dc.DC_EINVAL
+    assert L.dc_sync(None) == dc.DC_EINVAL
+    assert L.dc_token_buffer(None) is None
+    assert L.dc_tap_find(None, b"embed") == -1
+    L.dc_free(None)

@@ -1,0 +1,190 @@
+"""Benchmark of the streaming Token2Wav decode step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one chunk step of the whole decode path (embedding, pre-stack,
+upsampling stages with their resblocks, head, inverse STFT) for every stream
+of the workload, replayed as one HIP graph through the C ABI.  Token chunks
+are resident in HBM before the timed region; each step stages its chunk into
+the state's token buffer (counted in the step) and leaves the PCM in the
+state's audio buffer.  Prints one JSON line:
+
+  value        audio-seconds decoded per wall-second (streams * samples / 24 kHz)
+  ms_per_step  wall milliseconds per chunk step in the timed loop
+  p50/p99      per-chunk latency, host submit to PCM ready on the device
+  roofline     the kernel with the largest share of step time, its algorithmic
+               FLOPs (or bytes) per launch over its mean launch duration, timed
+               with HIP events on the state's stream
+  cpu_baseline the plain fp64 oracle on the host cores, on a bounded sample
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "audio-seconds decoded per wall-second (1 GPU) + p50 per-chunk latency ms"
+DEFAULT_WORKLOAD = "real_f32_b1_n25"
+PEAK = {"hbm": 8000.0, "bf16": 2500.0, "f32": 157.3}   # GB/s, TFLOP/s (MI355X, dense)
+
+
+class _Addr:
+    def __init__(self, addr):
+        self.addr = addr
+
+    def data_ptr(self):
+        return self.addr
+
+
+def cpu_baseline(arch, dtype, blob, tokens, budget_s: float):
+    """Time the oracle (as it stands) decoding a prefix of stream 0, growing the
+    prefix until one run takes budget_s or the workload's tokens run out."""
+    import oracle
+    from paper_2609_35115_amd import synth
+    spt = synth.samples_per_token(arch)
+    T_full = tokens.shape[1]
+    T = min(T_full, 4)
+    while True:
+        t0 = time.perf_counter()
+        oracle.decode(arch, dtype, blob, tokens[0, :T])
+        dt = time.perf_counter() - t0
+        if dt >= budget_s or T >= T_full:
+            break
+        T = min(T_full, max(2 * T, int(T * budget_s / max(dt, 1e-3) * 1.05)))
+    return {"value": T * spt / synth.SAMPLE_RATE / dt, "unit": "audio-s/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"stream 0, tokens [0,{T}) of the workload decoded offline in fp64"
+                      f"{' on bf16-rounded weights' if dtype == 'bf16' else ''}, {dt:.1f} s wall"}
+
+
+def roofline(layers, us, dtype):
+    """Group launches by kernel; the one with the most time per step is reported."""
+    groups = {}
+    for info, t in zip(layers, us):
+        g = groups.setdefault(info["kernel"], {"us": 0.0, "flops": 0.0, "bytes": 0.0, "launches": 0})
+        g["us"] += t
+        g["flops"] += info["flops"]
+        g["bytes"] += info["bytes"]
+        g["launches"] += 1
+    name, g = max(groups.items(), key=lambda kv: kv[1]["us"])
+    step_us = sum(us)
+    conv = name.startswith("dc::conv_kernel")
+    op = "bf16" if "<true" in name else "f32"
+    if conv and g["flops"] / g["bytes"] > PEAK[op] * 1e12 / (PEAK["hbm"] * 1e9):
+        bound, achieved, peak, unit = "mfma", g["flops"] / (g["us"] * 1e-6) / 1e12, PEAK[op], "TFLOP/s"
+    else:
+        bound, achieved, peak, unit = "hbm", g["bytes"] / (g["us"] * 1e-6) / 1e9, PEAK["hbm"], "GB/s"
+    per_kernel = sorted(((k, v["us"] / step_us) for k, v in groups.items()), key=lambda kv: -kv[1])
+    return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "kernel": name, "launches_per_step": g["launches"],
+            "mean_launch_us": round(g["us"] / g["launches"], 3),
+            "flops_per_launch": g["flops"] / g["launches"], "bytes_per_launch": g["bytes"] / g["launches"],
+            "share_of_step": round(g["us"] / step_us, 4),
+            "kernels_by_share": [[k, round(v, 4)] for k, v in per_kernel[:6]]}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--latency-chunks", type=int, default=100)
+    ap.add_argument("--layer-reps", type=int, default=10)
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of one oracle run (0 skips it)")
+    ap.add_argument("--tile-variant", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested). Streams are "
+              "independent, so a multi-GPU deployment runs one state per GPU with no collectives; "
+              "run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_35115_amd as dc
+    from paper_2609_35115_amd import synth
+
+    w = synth.workload(args.workload)
+    arch, dtype, B, n, chunks = w["arch"], w["dtype"], w["batch"], w["chunk_tokens"], w["chunks"]
+    spt = synth.samples_per_token(arch)
+    torch.cuda.set_device(0)
+    blob = synth.make_weights(arch, 0)
+    tokens = synth.make_tokens(arch, B, chunks * n)
+    tok_dev = torch.from_numpy(np.ascontiguousarray(tokens.reshape(B, chunks, n).transpose(1, 0, 2))).cuda()
+    dec = dc.Decoder(arch, dtype, blob, batch=B, chunk_tokens=n, tile_variant=args.tile_variant)
+    audio = _Addr(dc.dc_audio_buffer(dec.h))
+    torch.cuda.synchronize()
+
+    def step(i):
+        st = dc.dc_decode_chunk(dec.h, tok_dev[i % chunks], n, audio)
+        if st != dc.DC_OK:
+            raise dc.DcError(st, dc.dc_last_error(dec.h))
+
+    print(f"# workload {args.workload}: batch {B}, chunk {n} tokens, {dtype}; warmup {args.warmup}, "
+          f"steps {args.steps}", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i)
+    dec.sync()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    dec.stream.synchronize()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dec.sync()
+    ms_per_step = 1000.0 * wall / args.steps
+    audio_s = B * n * spt / synth.SAMPLE_RATE
+    value = audio_s * args.steps / wall
+    print(f"# timed {args.steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
+
+    lat = []
+    for i in range(args.latency_chunks):
+        t = time.perf_counter()
+        step(i)
+        dec.stream.synchronize()
+        lat.append(1000.0 * (time.perf_counter() - t))
+    dec.sync()
+    lat = np.array(lat)
+
+    layers = dec.layers()
+    us = dec.time_layers(args.layer_reps)
+    roof = roofline(layers, us, dtype)
+    stats = dec.stats()
+    dec.close()
+    print(f"# roofline: {roof['kernel']} {roof['achieved']} {roof['unit']} ({roof['frac']:.1%})",
+          file=sys.stderr, flush=True)
+
+    cpu = None
+    if args.cpu_budget > 0:
+        cpu = cpu_baseline(arch, dtype, blob, tokens, args.cpu_budget)
+
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "audio-s/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+        "data": "synthetic (seeded random-weight decoder and uniform token ids)",
+        "config": {"workload": args.workload, "arch": "real" if arch["embed"] == 512 else "tiny",
+                   "batch": B, "chunk_tokens": n, "chunks_cycled": chunks,
+                   "audio_s_per_step": audio_s, "graph_replay": stats["replays"] > 0,
+                   "kernels_per_step": stats["kernels_per_step"],
+                   "flops_per_step": sum(l["flops"] for l in layers)},
+        "p50_chunk_ms": round(float(np.percentile(lat, 50)), 4),
+        "p99_chunk_ms": round(float(np.percentile(lat, 99)), 4),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -185,6 +185,32 @@ int32_t dc_tap_find(const dc_state* s, const char* name);
 dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32_t nframes,
                       float* host_out, int32_t* channels);
 
+/*
+ * Measurement (roofline reporting).  A chunk step is a fixed sequence of
+ * kernel launches ("layers": embed, every conv / transposed conv, head,
+ * spectrum, overlap-add, clock).  dc_layer_info describes layer i at n =
+ * chunk_tokens: its kernel (the demangled name a profiler shows), the GEMM
+ * shape of a conv (rows = batch * frames, cols, depth = taps * input
+ * channels), its algorithmic FLOPs (2 * multiply-adds of the convolution) and
+ * its algorithmic HBM bytes (weights once, operand frames including left
+ * context, residual / branch inputs, output frames).  dc_time_layers launches
+ * every layer reps times in isolation on the state's stream, bracketed by HIP
+ * events, and writes the mean microseconds per launch into us_per_launch
+ * [dc_layer_count].  Re-running a layer rewrites only ring slots of frames the
+ * next call overwrites anyway, so the stream state is unaffected.  Synchronous.
+ */
+typedef struct dc_layer_info {
+    char name[48];
+    char kernel[80];
+    int64_t rows, cols, depth;
+    double flops;
+    double bytes;
+} dc_layer_info;
+
+int32_t dc_layer_count(const dc_state* s);
+dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out);
+dc_status dc_time_layers(dc_state* s, int32_t reps, double* us_per_launch);
+
 /* Human-readable reason for the last error on s (or on dc_init when s is NULL). */
 const char* dc_last_error(const dc_state* s);
 

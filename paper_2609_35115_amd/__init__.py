@@ -68,6 +68,12 @@ class DcStats(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_}
 
 
+class DcLayerInfo(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("kernel", ctypes.c_char * 80),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("depth", ctypes.c_int64),
+                ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
 # Every symbol include/dc.h declares, with its ctypes signature.
 _P = ctypes.c_void_p
 SIGNATURES = {
@@ -84,6 +90,9 @@ SIGNATURES = {
     "dc_tap_find": ([_P, ctypes.c_char_p], ctypes.c_int32),
     "dc_tap_read": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _P,
                      ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+    "dc_layer_count": ([_P], ctypes.c_int32),
+    "dc_layer_info_get": ([_P, ctypes.c_int32, ctypes.POINTER(DcLayerInfo)], ctypes.c_int),
+    "dc_time_layers": ([_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "dc_last_error": ([_P], ctypes.c_char_p),
     "dc_free": ([_P], None),
 }
@@ -212,6 +221,24 @@ def dc_tap_read(h, tap: int, b: int, frame0: int, nframes: int, channels: int) -
     return out
 
 
+def dc_layer_count(h) -> int:
+    return lib().dc_layer_count(h)
+
+
+def dc_layer_info_get(h, i: int) -> dict:
+    info = DcLayerInfo()
+    _check(lib().dc_layer_info_get(h, i, ctypes.byref(info)), h)
+    return {"name": info.name.decode(), "kernel": info.kernel.decode(), "rows": info.rows,
+            "cols": info.cols, "depth": info.depth, "flops": info.flops, "bytes": info.bytes}
+
+
+def dc_time_layers(h, reps: int) -> list:
+    n = dc_layer_count(h)
+    buf = (ctypes.c_double * n)()
+    _check(lib().dc_time_layers(h, reps, buf), h)
+    return list(buf)
+
+
 def dc_last_error(h) -> str:
     r = lib().dc_last_error(h)
     return r.decode() if r else ""
@@ -289,6 +316,12 @@ class Decoder:
 
     def stats(self) -> dict:
         return dc_get_stats(self.h)
+
+    def layers(self) -> list:
+        return [dc_layer_info_get(self.h, i) for i in range(dc_layer_count(self.h))]
+
+    def time_layers(self, reps: int) -> list:
+        return dc_time_layers(self.h, reps)
 
     def tap(self, name: str, b: int, frame0: int, nframes: int) -> np.ndarray:
         t = dc_tap_find(self.h, name)

@@ -382,62 +382,83 @@ static void build_network(dc_state* s)
 }
 
 // ------------------------------------------------------------ one chunk step
+//
+// A step is a fixed list of launches ("layers"): 0 embed, 1..C the convs in
+// network order, then spectrum, overlap-add and clock.
+
+static int layer_count(const dc_state* s) { return (int)s->convs.size() + 4; }
+
+static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
+{
+    const dc_cfg& c = s->cfg;
+    const Ring& in = s->rings[op.in];
+    const Ring& out = s->rings[op.out];
+    ConvParams p{};
+    p.in = in.ptr;
+    p.in_R = in.R;
+    p.in_C = in.C;
+    p.in_elem = in.elem;
+    p.in_act = op.in_act;
+    p.wp = s->arena + op.w_off;
+    p.bias = (const float*)(s->arena + op.b_off);
+    p.CB = op.CB;
+    p.n_cb = op.n_cb;
+    p.k = op.k;
+    p.d = op.d;
+    p.N = op.N;
+    p.NB16 = op.NB16;
+    p.out = out.ptr;
+    p.out_R = out.R;
+    p.out_C = out.C;
+    p.out_elem = out.elem;
+    p.out_act = op.out_act;
+    p.u = op.u;
+    if (op.res >= 0) {
+        p.res = (const float*)s->rings[op.res].ptr;
+        p.res_R = s->rings[op.res].R;
+    }
+    p.n_mean = op.n_mean;
+    for (int m = 0; m < op.n_mean; m++) {
+        p.mean[m] = (const float*)s->rings[op.mean[m]].ptr;
+        p.mean_R = s->rings[op.mean[m]].R;
+    }
+    p.B = c.batch;
+    p.F = (int)(n * s->fpt[op.level_in]);
+    p.tiles_t = (p.F + tile_variant(op.variant).BM - 1) / tile_variant(op.variant).BM;
+    p.clock = s->clock;
+    p.in_fpt = s->fpt[op.level_in];
+    p.slope = c.lrelu_slope;
+    return p;
+}
+
+static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
+{
+    const dc_cfg& c = s->cfg;
+    const int nc = (int)s->convs.size();
+    const int L = c.n_stages;
+    const int FL = (int)(n * s->fpt[L]);
+    if (i == 0)
+        return launch_embed(s->tok, n, c.batch, s->emb, c.vocab, c.embed, s->rings[s->ring_E].elem,
+                            c.frames_per_token, s->rings[s->ring_E], s->clock, s->err, st);
+    if (i <= nc) {
+        const ConvOp& op = s->convs[i - 1];
+        return launch_conv(op.variant, op.bf16, conv_params(s, op, n), st);
+    }
+    if (i == nc + 1)
+        return launch_spectrum((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL,
+                               s->table, s->rings[s->ring_G], s->clock, s->fpt[L], st);
+    if (i == nc + 2)
+        return launch_ola(s->rings[s->ring_G], c.batch, FL, c.hop, c.n_fft, s->audio, s->clock, s->fpt[L], st);
+    return launch_clock(s->clock, n, st);
+}
 
 static hipError_t enqueue_step(dc_state* s, int n, hipStream_t st)
 {
-    const dc_cfg& c = s->cfg;
-    hipError_t e = launch_embed(s->tok, n, c.batch, s->emb, c.vocab, c.embed, s->rings[s->ring_E].elem,
-                                c.frames_per_token, s->rings[s->ring_E], s->clock, s->err, st);
-    if (e != hipSuccess) return e;
-    for (const ConvOp& op : s->convs) {
-        const Ring& in = s->rings[op.in];
-        const Ring& out = s->rings[op.out];
-        ConvParams p{};
-        p.in = in.ptr;
-        p.in_R = in.R;
-        p.in_C = in.C;
-        p.in_elem = in.elem;
-        p.in_act = op.in_act;
-        p.wp = s->arena + op.w_off;
-        p.bias = (const float*)(s->arena + op.b_off);
-        p.CB = op.CB;
-        p.n_cb = op.n_cb;
-        p.k = op.k;
-        p.d = op.d;
-        p.N = op.N;
-        p.NB16 = op.NB16;
-        p.out = out.ptr;
-        p.out_R = out.R;
-        p.out_C = out.C;
-        p.out_elem = out.elem;
-        p.out_act = op.out_act;
-        p.u = op.u;
-        if (op.res >= 0) {
-            p.res = (const float*)s->rings[op.res].ptr;
-            p.res_R = s->rings[op.res].R;
-        }
-        p.n_mean = op.n_mean;
-        for (int m = 0; m < op.n_mean; m++) {
-            p.mean[m] = (const float*)s->rings[op.mean[m]].ptr;
-            p.mean_R = s->rings[op.mean[m]].R;
-        }
-        p.B = c.batch;
-        p.F = (int)(n * s->fpt[op.level_in]);
-        p.tiles_t = (p.F + tile_variant(op.variant).BM - 1) / tile_variant(op.variant).BM;
-        p.clock = s->clock;
-        p.in_fpt = s->fpt[op.level_in];
-        p.slope = c.lrelu_slope;
-        e = launch_conv(op.variant, op.bf16, p, st);
+    for (int i = 0; i < layer_count(s); i++) {
+        const hipError_t e = launch_layer(s, i, n, st);
         if (e != hipSuccess) return e;
     }
-    const int L = c.n_stages;
-    const int FL = (int)(n * s->fpt[L]);
-    e = launch_spectrum((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL, s->table,
-                        s->rings[s->ring_G], s->clock, s->fpt[L], st);
-    if (e != hipSuccess) return e;
-    e = launch_ola(s->rings[s->ring_G], c.batch, FL, c.hop, c.n_fft, s->audio, s->clock, s->fpt[L], st);
-    if (e != hipSuccess) return e;
-    return launch_clock(s->clock, n, st);
+    return hipSuccess;
 }
 
 static hipError_t zero_state(dc_state* s)
@@ -748,6 +769,83 @@ dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32
             host_out[(size_t)f * r.C + ch] =
                 r.elem == kBF16 ? host_bf2f(((uint16_t*)row.data())[ch]) : ((float*)row.data())[ch];
     }
+    return DC_OK;
+}
+
+int32_t dc_layer_count(const dc_state* s) { return s ? layer_count(s) : 0; }
+
+dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
+{
+    if (!s || !out || i < 0 || i >= layer_count(s)) return DC_EINVAL;
+    const dc_cfg& c = s->cfg;
+    std::memset(out, 0, sizeof *out);
+    const int nc = (int)s->convs.size();
+    const int n = c.chunk_tokens;
+    const double B = c.batch;
+    const int L = c.n_stages;
+    const double FL = (double)n * s->fpt[L];
+    auto set = [&](const std::string& name, const std::string& kernel) {
+        std::snprintf(out->name, sizeof out->name, "%s", name.c_str());
+        std::snprintf(out->kernel, sizeof out->kernel, "%s", kernel.c_str());
+    };
+    if (i == 0) {
+        const Ring& E = s->rings[s->ring_E];
+        const double es = E.elem == kBF16 ? 2 : 4;
+        const double F = (double)n * c.frames_per_token;
+        set("embed", "dc::embed_kernel");
+        out->bytes = B * n * 4 + B * n * c.embed * es + B * F * c.embed * es;
+    } else if (i <= nc) {
+        const ConvOp& op = s->convs[i - 1];
+        const TileShape t = tile_variant(op.variant);
+        set(op.name, "dc::conv_kernel<" + std::string(op.bf16 ? "true" : "false") + ", " + std::to_string(t.BM) +
+                         ", " + std::to_string(t.BN) + ", " + std::to_string(t.WGM) + ">");
+        const double F = (double)n * s->fpt[op.level_in];
+        const Ring& in = s->rings[op.in];
+        const Ring& o = s->rings[op.out];
+        out->rows = (int64_t)(B * F);
+        out->cols = op.N;
+        out->depth = (int64_t)op.k * op.Ci;
+        out->flops = 2.0 * B * F * op.N * op.Ci * op.k;
+        const double wes = op.bf16 ? 2 : 4;
+        const double ies = in.elem == kBF16 ? 2 : 4, oes = o.elem == kBF16 ? 2 : 4;
+        const double Fo = F * op.u;
+        out->bytes = (double)op.N * op.Ci * op.k * wes + B * (F + (op.k - 1) * op.d) * op.Ci * ies +
+                     B * Fo * o.C * oes + (op.res >= 0 ? B * Fo * o.C * 4 : 0) + op.n_mean * B * Fo * o.C * 4;
+    } else if (i == nc + 1) {
+        set("spectrum", "dc::spectrum_kernel");
+        out->bytes = B * FL * (2 * (c.n_fft / 2 + 1) + c.n_fft) * 4;
+    } else if (i == nc + 2) {
+        set("ola", "dc::ola_kernel");
+        out->bytes = B * FL * c.n_fft * 4 + B * FL * c.hop * 4;
+    } else {
+        set("clock", "dc::clock_kernel");
+        out->bytes = 16;
+    }
+    return DC_OK;
+}
+
+dc_status dc_time_layers(dc_state* s, int32_t reps, double* us_per_launch)
+{
+    if (!s || !us_per_launch || reps < 1) return fail(s, DC_EINVAL, "bad dc_time_layers arguments");
+    if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned; call dc_reset");
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    hipError_t e = hipEventCreate(&e0);
+    if (e == hipSuccess) e = hipEventCreate(&e1);
+    const int nl = layer_count(s);
+    for (int i = 0; i < nl - 1 && e == hipSuccess; i++) {   // the clock is not re-run
+        e = launch_layer(s, i, s->cfg.chunk_tokens, s->stream);   // warm
+        if (e == hipSuccess) e = hipEventRecord(e0, s->stream);
+        for (int r = 0; r < reps && e == hipSuccess; r++) e = launch_layer(s, i, s->cfg.chunk_tokens, s->stream);
+        if (e == hipSuccess) e = hipEventRecord(e1, s->stream);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float ms = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+        us_per_launch[i] = 1000.0 * ms / reps;
+    }
+    us_per_launch[nl - 1] = 0.0;
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    if (e != hipSuccess) return device_fail(s, e, "dc_time_layers");
     return DC_OK;
 }
 

@@ -36,6 +36,7 @@ struct ConvParams {
     int in_C;
     int in_elem;
     int in_act;           // apply LeakyReLU to the operand at load
+    int split;            // bf16 only: operand as hi + lo bf16 pair (two MFMAs per step)
     const void* wp;       // packed weights, operand element type
     const float* bias;    // [N]
     int CB;               // channels per block (multiple of the MFMA K quantum)
@@ -61,8 +62,15 @@ struct ConvParams {
     float slope;
 };
 
+// Block of 4 waves: WGM x WGN waves tile the output, each wave MB x NB MFMA
+// blocks of 16x16; WGK waves split K; every wave keeps SI accumulation
+// chains.  S = WGK * SI is the number of K partitions (part of the layer's
+// arithmetic: it fixes the order of the fp32 sums).
 struct TileShape {
-    int BM, BN, WGM;      // rows, cols, waves along rows (4 waves per block)
+    int MB, NB, WGM, WGN, WGK, SI;
+    int BM() const { return 16 * MB * WGM; }
+    int BN() const { return 16 * NB * WGN; }
+    int S() const { return WGK * SI; }
 };
 
 // The tile shapes compiled for each operand type.

@@ -12,6 +12,8 @@
 // a frame's value is the same wherever it falls in a tile: chunked and
 // offline decoding agree bit for bit (Design, Definition 2; Proposition 1's
 // premise that replay issues identical kernels over identical shapes).
+#include <type_traits>
+
 #include "dc_internal.h"
 
 namespace dc {
@@ -87,6 +89,20 @@ __device__ __forceinline__ void store8_lds(uint16_t* dst, const float v[8])
     *(u32x4*)dst = w;
 }
 
+// hi = bf16(v), lo = bf16(v - hi): hi + lo carries v to about 2^-16 relative.
+__device__ __forceinline__ void store8_lds_split(uint16_t* hi, uint16_t* lo, const float v[8])
+{
+    u32x4 h, l;
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+        const uint32_t h0 = f2bf(v[2 * e]), h1 = f2bf(v[2 * e + 1]);
+        h[e] = h0 | (h1 << 16);
+        l[e] = f2bf(v[2 * e] - bf2f(h0)) | (f2bf(v[2 * e + 1] - bf2f(h1)) << 16);
+    }
+    *(u32x4*)hi = h;
+    *(u32x4*)lo = l;
+}
+
 __device__ __forceinline__ void store8_lds(float* dst, const float v[8])
 {
     f32x4 a = {v[0], v[1], v[2], v[3]}, b = {v[4], v[5], v[6], v[7]};
@@ -95,142 +111,243 @@ __device__ __forceinline__ void store8_lds(float* dst, const float v[8])
 }
 
 // ------------------------------------------------------------ causal conv
+//
+// Block = 4 waves = WGM x WGN x WGK: WGM x WGN waves tile the output
+// (MB x NB MFMA blocks of 16x16 each), WGK waves share one output tile and
+// split K.  The K steps (channel block cb, tap j, chunk kc) of a layer are
+// numbered q = 0, 1, ...; step q belongs to partition q mod S (S = WGK * SI),
+// each partition is an independent fp32 accumulation chain, and the result
+// is ((P_0 + P_1) + ...) + P_{S-1}.  S divides the steps of a channel block.
 
-template <bool BF16, int BM, int BN, int WGM>
+struct RowSlots {
+    int out, res, mean;   // ring slots of output frame (block row 0, phase 0)
+};
+
+// Slot of a frame `off` frames after a base slot, for 0 <= off < R.
+__device__ __forceinline__ int slot_add(int base, int off, int R)
+{
+    const int s = base + off;
+    return s >= R ? s - R : s;
+}
+
+__device__ __forceinline__ void store_out(const ConvParams& p, int b, const RowSlots& rs, int off, int co,
+                                          float v)
+{
+    // off: output frame offset from the block's base frame; co: output channel
+    if (p.res) v = p.res[((size_t)b * p.res_R + slot_add(rs.res, off, (int)p.res_R)) * p.out_C + co] + v;
+    if (p.n_mean) {
+        const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean, off, (int)p.mean_R)) * p.out_C + co;
+        float x = p.mean[0][mo];
+        for (int i = 1; i < p.n_mean; i++) x = x + p.mean[i][mo];
+        x = x + v;
+        v = x / (float)(p.n_mean + 1);
+    }
+    if (p.out_act) v = lrelu(v, p.slope);
+    const size_t oo = ((size_t)b * p.out_R + slot_add(rs.out, off, (int)p.out_R)) * p.out_C + co;
+    if (p.out_elem == kF32)
+        ((float*)p.out)[oo] = v;
+    else
+        ((uint16_t*)p.out)[oo] = (uint16_t)f2bf(v);
+}
+
+template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int SI>
 __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 {
     using Tr = OpT<BF16>;
     using T = typename Tr::T;
-    constexpr int WGN = 4 / WGM;
-    constexpr int WM = BM / WGM, WN = BN / WGN;
-    constexpr int MB = WM / 16, NB = WN / 16;
-    static_assert(WGM * WGN == 4 && MB >= 1 && NB >= 1, "tile shape");
+    using Frag = typename std::conditional<BF16, u32x4, f32x4>::type;
+    constexpr int BM = 16 * MB * WGM, BN = 16 * NB * WGN, S = WGK * SI;
+    static_assert(WGM * WGN * WGK == 4, "4 waves per block");
 
     extern __shared__ __align__(16) unsigned char smem[];
     T* lds = reinterpret_cast<T*>(smem);
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave % WGM, wn = wave / WGM;
+    const int wk = wave % WGK, wm = (wave / WGK) % WGM, wn = wave / (WGK * WGM);
     const int b = blockIdx.x / p.tiles_t;
-    const int t0 = (blockIdx.x % p.tiles_t) * BM;
+    const int t0 = (blockIdx.x - b * p.tiles_t) * BM;
     const int n0 = blockIdx.y * BN;
-    const int64_t tau0 = p.clock[0] * p.in_fpt;
     const int halo = (p.k - 1) * p.d;
     const int rows = BM + halo;
     const int ldw = p.CB + Tr::PAD;
-    const int vpr = p.CB / 8;               // 8-channel vectors per LDS row
-    const int kchunks = p.CB / Tr::KQ;
+    const int vpr = p.CB / 8;
+    const int kch = p.CB / Tr::KQ;
+    const int qcb = p.k * kch;          // K steps per channel block
+    const int per = qcb / WGK;          // this wave's steps per channel block
+    const int64_t tau0 = p.clock[0] * p.in_fpt;
+    const int in_R = (int)p.in_R;
+    const int base_in = (int)ring_slot(tau0 + t0 - halo, p.in_R);
+    const int nblk0 = n0 / 16 + wn * NB;
+    const Frag* wp = reinterpret_cast<const Frag*>(p.wp);
 
-    f32x4 acc[MB][NB];
+    f32x4 acc[SI][MB][NB];
 #pragma unroll
-    for (int i = 0; i < MB; i++)
+    for (int si = 0; si < SI; si++)
 #pragma unroll
-        for (int j = 0; j < NB; j++) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < MB; i++)
+#pragma unroll
+            for (int j = 0; j < NB; j++) acc[si][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    auto loadB = [&](int cb, int ls, Frag (&w)[NB]) {
+        const size_t wstep = ((size_t)cb * qcb + ls) * p.NB16;
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++) {
+            Frag z = {};
+            if (nblk0 + nb < p.NB16) z = wp[(wstep + nblk0 + nb) * 64 + lane];
+            w[nb] = z;
+        }
+    };
+
+    Frag bnext[NB];
+    loadB(0, wk, bnext);
     for (int cb = 0; cb < p.n_cb; cb++) {
         __syncthreads();
-        // Stage the operand rows [t0 - halo, t0 + BM) of this channel block.
+        // Operand rows [t0 - halo, t0 + BM) of channel block cb, through the ring.
         for (int v = tid; v < rows * vpr; v += 256) {
             const int r = v / vpr, c8 = (v - r * vpr) * 8;
             const int t = t0 - halo + r;
             const int ch = cb * p.CB + c8;
             float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
             if (t < p.F && ch < p.in_C) {
-                const int64_t slot = ring_slot(tau0 + t, p.in_R);
-                load8(p.in, p.in_elem, ((size_t)b * p.in_R + slot) * p.in_C + ch, x);
+                load8(p.in, p.in_elem, ((size_t)b * p.in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x);
                 if (p.in_act) {
 #pragma unroll
                     for (int e = 0; e < 8; e++) x[e] = lrelu(x[e], p.slope);
                 }
             }
-            store8_lds(lds + r * ldw + c8, x);
+            if constexpr (BF16) {
+                if (p.split)
+                    store8_lds_split(lds + r * ldw + c8, lds + (rows + r) * ldw + c8, x);
+                else
+                    store8_lds(lds + r * ldw + c8, x);
+            } else {
+                store8_lds(lds + r * ldw + c8, x);
+            }
         }
         __syncthreads();
 
-        for (int j = 0; j < p.k; j++) {
-            const int roff = j * p.d;
-            for (int kc = 0; kc < kchunks; kc++) {
-                const size_t wbase = ((size_t)(cb * p.k + j) * kchunks + kc) * p.NB16;
+        for (int i = 0; i < per; i += SI) {
+#pragma unroll
+            for (int si = 0; si < SI; si++) {
+                const int ls = (i + si) * WGK + wk;
+                Frag w[NB];
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) w[nb] = bnext[nb];
+                {   // prefetch this wave's next step
+                    int ncb = cb, nls = ls + WGK;
+                    if (nls >= qcb) {
+                        ncb++;
+                        nls -= qcb;
+                    }
+                    if (ncb < p.n_cb) loadB(ncb, nls, bnext);
+                }
+                const int j = ls / kch, kc = ls - j * kch;
+                const int roff = j * p.d + (lane & 15);
                 if constexpr (BF16) {
-                    bf16x8_t a[MB], w[NB];
+                    bf16x8_t a[MB];
 #pragma unroll
-                    for (int mb = 0; mb < MB; mb++) {
-                        const int row = wm * WM + mb * 16 + (lane & 15) + roff;
-                        a[mb] = __builtin_bit_cast(bf16x8_t,
-                                                   *(const u32x4*)(lds + row * ldw + kc * 32 + (lane >> 4) * 8));
-                    }
-#pragma unroll
-                    for (int nb = 0; nb < NB; nb++) {
-                        const int nblk = (n0 + wn * WN) / 16 + nb;
-                        u32x4 wv = {0u, 0u, 0u, 0u};
-                        if (nblk < p.NB16) wv = ((const u32x4*)p.wp)[(wbase + nblk) * 64 + lane];
-                        w[nb] = __builtin_bit_cast(bf16x8_t, wv);
-                    }
+                    for (int mb = 0; mb < MB; mb++)
+                        a[mb] = __builtin_bit_cast(
+                            bf16x8_t, *(const u32x4*)(lds + (wm * 16 * MB + mb * 16 + roff) * ldw + kc * 32 +
+                                                      (lane >> 4) * 8));
 #pragma unroll
                     for (int mb = 0; mb < MB; mb++)
 #pragma unroll
                         for (int nb = 0; nb < NB; nb++)
-                            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mb], w[nb], acc[mb][nb], 0, 0, 0);
+                            acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                a[mb], __builtin_bit_cast(bf16x8_t, w[nb]), acc[si][mb][nb], 0, 0, 0);
+                    if (p.split) {   // the low halves, right after the high halves of the same step
+#pragma unroll
+                        for (int mb = 0; mb < MB; mb++)
+                            a[mb] = __builtin_bit_cast(
+                                bf16x8_t, *(const u32x4*)(lds + (rows + wm * 16 * MB + mb * 16 + roff) * ldw +
+                                                          kc * 32 + (lane >> 4) * 8));
+#pragma unroll
+                        for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                            for (int nb = 0; nb < NB; nb++)
+                                acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    a[mb], __builtin_bit_cast(bf16x8_t, w[nb]), acc[si][mb][nb], 0, 0, 0);
+                    }
                 } else {
-                    f32x4 a[MB], w[NB];
+                    f32x4 a[MB];
 #pragma unroll
-                    for (int mb = 0; mb < MB; mb++) {
-                        const int row = wm * WM + mb * 16 + (lane & 15) + roff;
-                        a[mb] = *(const f32x4*)(lds + row * ldw + kc * 16 + (lane >> 4) * 4);
-                    }
-#pragma unroll
-                    for (int nb = 0; nb < NB; nb++) {
-                        const int nblk = (n0 + wn * WN) / 16 + nb;
-                        f32x4 wv = {0.f, 0.f, 0.f, 0.f};
-                        if (nblk < p.NB16) wv = ((const f32x4*)p.wp)[(wbase + nblk) * 64 + lane];
-                        w[nb] = wv;
-                    }
+                    for (int mb = 0; mb < MB; mb++)
+                        a[mb] = *(const f32x4*)(lds + (wm * 16 * MB + mb * 16 + roff) * ldw + kc * 16 +
+                                                (lane >> 4) * 4);
 #pragma unroll
                     for (int q = 0; q < 4; q++)
 #pragma unroll
                         for (int mb = 0; mb < MB; mb++)
 #pragma unroll
                             for (int nb = 0; nb < NB; nb++)
-                                acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mb][q], w[nb][q], acc[mb][nb], 0, 0, 0);
+                                acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mb][q], w[nb][q],
+                                                                                      acc[si][mb][nb], 0, 0, 0);
                 }
             }
         }
     }
 
-    // Epilogue: bias, residual, branch mean, LeakyReLU, store through the ring.
+    // ---- epilogue: bias, residual, branch mean, LeakyReLU, store through the rings
+    const int64_t tau_out0 = (tau0 + t0) * p.u;   // output frame of block row 0, phase 0
+    RowSlots rs;
+    rs.out = (int)ring_slot(tau_out0, p.out_R);
+    rs.res = p.res ? (int)ring_slot(tau_out0, p.res_R) : 0;
+    rs.mean = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
+
+    if constexpr (WGK == 1) {
+        int rp[NB], co[NB];
+        float bias[NB];
 #pragma unroll
-    for (int mb = 0; mb < MB; mb++) {
+        for (int nb = 0; nb < NB; nb++) {
+            const int n = n0 + (wn * NB + nb) * 16 + (lane & 15);
+            rp[nb] = p.u == 1 ? 0 : n / p.out_C;
+            co[nb] = n - rp[nb] * p.out_C;
+            bias[nb] = n < p.N ? p.bias[n] : 0.f;
+            if (n >= p.N) rp[nb] = -1;
+        }
 #pragma unroll
-        for (int r = 0; r < 4; r++) {
-            const int t = t0 + wm * WM + mb * 16 + (lane >> 4) * 4 + r;
-            if (t >= p.F) continue;
+        for (int mb = 0; mb < MB; mb++)
 #pragma unroll
-            for (int nb = 0; nb < NB; nb++) {
-                const int n = n0 + wn * WN + nb * 16 + (lane & 15);
-                if (n >= p.N) continue;
-                float v = acc[mb][nb][r] + p.bias[n];
-                int64_t fo = t;
-                int co = n;
-                if (p.u != 1) {
-                    fo = (int64_t)t * p.u + n / p.out_C;
-                    co = n % p.out_C;
+            for (int r = 0; r < 4; r++) {
+                const int tl = wm * 16 * MB + mb * 16 + (lane >> 4) * 4 + r;
+                if (t0 + tl >= p.F) continue;
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) {
+                    if (rp[nb] < 0) continue;
+                    float v = acc[0][mb][nb][r];
+#pragma unroll
+                    for (int si = 1; si < SI; si++) v = v + acc[si][mb][nb][r];
+                    store_out(p, b, rs, tl * p.u + rp[nb], co[nb], v + bias[nb]);
                 }
-                const int64_t tau = tau0 * p.u + fo;
-                if (p.res) v = p.res[((size_t)b * p.res_R + ring_slot(tau, p.res_R)) * p.out_C + co] + v;
-                if (p.n_mean) {
-                    const size_t mo = ((size_t)b * p.mean_R + ring_slot(tau, p.mean_R)) * p.out_C + co;
-                    float x = p.mean[0][mo];
-                    for (int i = 1; i < p.n_mean; i++) x = x + p.mean[i][mo];
-                    x = x + v;
-                    v = x / (float)(p.n_mean + 1);
-                }
-                if (p.out_act) v = lrelu(v, p.slope);
-                const size_t oo = ((size_t)b * p.out_R + ring_slot(tau, p.out_R)) * p.out_C + co;
-                if (p.out_elem == kF32)
-                    ((float*)p.out)[oo] = v;
-                else
-                    ((uint16_t*)p.out)[oo] = (uint16_t)f2bf(v);
             }
+    } else {
+        // partial sums of every partition through LDS, added in partition order
+        __syncthreads();
+        float* red = reinterpret_cast<float*>(smem);
+#pragma unroll
+        for (int si = 0; si < SI; si++)
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++)
+#pragma unroll
+                    for (int r = 0; r < 4; r++) {
+                        const int pidx = si * WGK + wk;
+                        const int row = wm * 16 * MB + mb * 16 + (lane >> 4) * 4 + r;
+                        const int col = (wn * NB + nb) * 16 + (lane & 15);
+                        red[(pidx * BM + row) * BN + col] = acc[si][mb][nb][r];
+                    }
+        __syncthreads();
+        for (int idx = tid; idx < BM * BN; idx += 256) {
+            const int tl = idx / BN, nl = idx - tl * BN;
+            const int n = n0 + nl;
+            if (t0 + tl >= p.F || n >= p.N) continue;
+            float v = red[idx];
+#pragma unroll
+            for (int q = 1; q < S; q++) v = v + red[q * BM * BN + idx];
+            const int rpn = p.u == 1 ? 0 : n / p.out_C;
+            store_out(p, b, rs, tl * p.u + rpn, n - rpn * p.out_C, v + p.bias[n]);
         }
     }
 }
@@ -238,7 +355,19 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 // ------------------------------------------------------------- tile table
 
 static const TileShape kTiles[] = {
-    {32, 32, 2}, {32, 64, 2}, {64, 64, 2}, {64, 128, 2}, {128, 64, 4}, {128, 128, 2}, {256, 64, 4},
+    //  MB NB WGM WGN WGK SI
+    {1, 1, 1, 1, 4, 1},   // 0: 16x16, K in 4 partitions across waves
+    {1, 2, 1, 1, 4, 1},   // 1: 16x32, 4 partitions
+    {2, 2, 1, 1, 4, 1},   // 2: 32x32, 4 partitions
+    {1, 1, 2, 2, 1, 1},   // 3: 32x32
+    {1, 2, 2, 2, 1, 1},   // 4: 32x64
+    {2, 2, 2, 2, 1, 1},   // 5: 64x64
+    {2, 4, 2, 2, 1, 1},   // 6: 64x128
+    {2, 4, 4, 1, 1, 1},   // 7: 128x64
+    {4, 4, 2, 2, 1, 1},   // 8: 128x128
+    {4, 4, 4, 1, 1, 1},   // 9: 256x64
+    {2, 2, 2, 1, 2, 1},   // 10: 64x32, 2 partitions across waves
+    {2, 2, 2, 2, 1, 2},   // 11: 64x64, 2 chains per wave
 };
 
 int num_tile_variants() { return (int)(sizeof(kTiles) / sizeof(kTiles[0])); }
@@ -246,39 +375,47 @@ TileShape tile_variant(int v) { return kTiles[v]; }
 
 size_t conv_lds_bytes(int v, bool bf16, const ConvParams& p)
 {
-    const int rows = kTiles[v].BM + (p.k - 1) * p.d;
+    const TileShape& t = kTiles[v];
+    const int rows = t.BM() + (p.k - 1) * p.d;
     const int pad = bf16 ? OpT<true>::PAD : OpT<false>::PAD;
-    return (size_t)rows * (p.CB + pad) * (bf16 ? 2 : 4);
+    const size_t a = (size_t)rows * (p.CB + pad) * (bf16 ? 2 : 4) * (bf16 && p.split ? 2 : 1);
+    const size_t red = t.WGK > 1 ? (size_t)t.S() * t.BM() * t.BN() * 4 : 0;
+    return a > red ? a : red;
 }
 
-template <bool BF16, int BM, int BN, int WGM>
-static hipError_t launch_t(const ConvParams& p, hipStream_t st)
+template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int SI>
+static hipError_t launch_t(const ConvParams& p, size_t lds, hipStream_t st)
 {
+    constexpr int BN = 16 * NB * WGN;
     dim3 grid((unsigned)(p.B * p.tiles_t), (unsigned)((p.N + BN - 1) / BN));
-    const int rows = BM + (p.k - 1) * p.d;
-    const size_t lds = (size_t)rows * (p.CB + OpT<BF16>::PAD) * sizeof(typename OpT<BF16>::T);
-    hipLaunchKernelGGL((conv_kernel<BF16, BM, BN, WGM>), grid, dim3(256), lds, st, p);
+    hipLaunchKernelGGL((conv_kernel<BF16, MB, NB, WGM, WGN, WGK, SI>), grid, dim3(256), lds, st, p);
     return hipGetLastError();
 }
 
 template <bool BF16>
-static hipError_t launch_dt(int v, const ConvParams& p, hipStream_t st)
+static hipError_t launch_dt(int v, const ConvParams& p, size_t lds, hipStream_t st)
 {
     switch (v) {
-    case 0: return launch_t<BF16, 32, 32, 2>(p, st);
-    case 1: return launch_t<BF16, 32, 64, 2>(p, st);
-    case 2: return launch_t<BF16, 64, 64, 2>(p, st);
-    case 3: return launch_t<BF16, 64, 128, 2>(p, st);
-    case 4: return launch_t<BF16, 128, 64, 4>(p, st);
-    case 5: return launch_t<BF16, 128, 128, 2>(p, st);
-    case 6: return launch_t<BF16, 256, 64, 4>(p, st);
+    case 0: return launch_t<BF16, 1, 1, 1, 1, 4, 1>(p, lds, st);
+    case 1: return launch_t<BF16, 1, 2, 1, 1, 4, 1>(p, lds, st);
+    case 2: return launch_t<BF16, 2, 2, 1, 1, 4, 1>(p, lds, st);
+    case 3: return launch_t<BF16, 1, 1, 2, 2, 1, 1>(p, lds, st);
+    case 4: return launch_t<BF16, 1, 2, 2, 2, 1, 1>(p, lds, st);
+    case 5: return launch_t<BF16, 2, 2, 2, 2, 1, 1>(p, lds, st);
+    case 6: return launch_t<BF16, 2, 4, 2, 2, 1, 1>(p, lds, st);
+    case 7: return launch_t<BF16, 2, 4, 4, 1, 1, 1>(p, lds, st);
+    case 8: return launch_t<BF16, 4, 4, 2, 2, 1, 1>(p, lds, st);
+    case 9: return launch_t<BF16, 4, 4, 4, 1, 1, 1>(p, lds, st);
+    case 10: return launch_t<BF16, 2, 2, 2, 1, 2, 1>(p, lds, st);
+    case 11: return launch_t<BF16, 2, 2, 2, 2, 1, 2>(p, lds, st);
     default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_conv(int v, bool bf16, const ConvParams& p, hipStream_t st)
 {
-    return bf16 ? launch_dt<true>(v, p, st) : launch_dt<false>(v, p, st);
+    const size_t lds = conv_lds_bytes(v, bf16, p);
+    return bf16 ? launch_dt<true>(v, p, lds, st) : launch_dt<false>(v, p, lds, st);
 }
 
 // ----------------------------------------------------------- embedding

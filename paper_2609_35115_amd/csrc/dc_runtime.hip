@@ -38,6 +38,7 @@ struct ConvOp {
     int Ci = 0, N = 0, out_C = 0, k = 1, d = 1, u = 1;
     int in_act = 0, out_act = 0;
     bool bf16 = false;   // operand type
+    bool split = false;  // bf16 operand as a hi + lo pair
     bool transposed = false;
     size_t w_off = 0, b_off = 0, w_bytes = 0;
     size_t blob_w = 0, blob_b = 0;  // float offsets into the blob
@@ -219,38 +220,75 @@ static void pack_weights(const ConvOp& op, const float* blob, bool round_bf16, c
                     }
 }
 
-static int pick_variant(const dc_state* s, const ConvOp& op)
+// Tile shape of a conv for this state.  Deterministic: it depends on the
+// layer, the batch and the chunk size only (never on a call's n), so every
+// call of a state -- replayed or direct, chunked or offline -- runs the same
+// arithmetic.  The number of K partitions S is chosen first (4 when even
+// 32x32 output tiles leave fewer than 512 blocks, so waves split K to fill
+// the machine; 1 otherwise), then the largest tile of that S that keeps
+// enough blocks.
+static bool variant_fits(const ConvOp& op, int v)
 {
-    const int B = s->cfg.batch;
-    const int64_t F = (int64_t)s->cfg.chunk_tokens * s->fpt[op.level_in];
     ConvParams p{};
     p.k = op.k;
     p.d = op.d;
     p.CB = op.CB;
-    const size_t lds_max = 64 * 1024;
-    if (s->cfg.tile_variant > 0) {
-        const int v = s->cfg.tile_variant - 1;
-        if (conv_lds_bytes(v, op.bf16, p) <= lds_max) return v;
-    }
+    p.split = op.split;
+    const TileShape t = tile_variant(v);
+    const int kq = op.bf16 ? 32 : 16;
+    const int qcb = op.k * (op.CB / kq);
     const int npad = (op.N + 15) / 16 * 16;
-    static const int order[] = {6, 5, 4, 3, 2, 1, 0};
+    return conv_lds_bytes(v, op.bf16, p) <= 64 * 1024 && qcb % t.S() == 0 && t.BN() <= (npad > 16 ? npad : 16);
+}
+
+static int pick_variant(const dc_state* s, const ConvOp& op)
+{
+    const int64_t B = s->cfg.batch;
+    const int64_t F = (int64_t)s->cfg.chunk_tokens * s->fpt[op.level_in];
+    if (s->cfg.tile_variant > 0) {
+        // a forced shape that does not fit this layer falls back to the largest
+        // fitting shape with the same number of K partitions
+        const int fv = s->cfg.tile_variant - 1;
+        if (variant_fits(op, fv)) return fv;
+        for (int v : {9, 8, 7, 6, 5, 4, 3, 11, 10, 2, 1, 0})
+            if (tile_variant(v).S() == tile_variant(fv).S() && variant_fits(op, v)) return v;
+    }
+    auto blocks = [&](int v) {
+        const TileShape t = tile_variant(v);
+        return B * ((F + t.BM() - 1) / t.BM()) * ((op.N + t.BN() - 1) / t.BN());
+    };
+    auto eff = [&](int v) {
+        const int bm = tile_variant(v).BM();
+        return (double)F / (double)(((F + bm - 1) / bm) * bm);
+    };
+    const bool small = blocks(3) < 512;
+    if (small) {
+        int best = -1;
+        double best_score = -1.0;
+        for (int v : {2, 1, 0}) {
+            if (!variant_fits(op, v)) continue;
+            const TileShape t = tile_variant(v);
+            const double waves = (double)blocks(v) * 4.0;
+            const double score = (waves < 2048.0 ? waves : 2048.0) * eff(v) * (t.MB * t.NB >= 2 ? 1.0 : 0.85);
+            if (score > best_score) {
+                best_score = score;
+                best = v;
+            }
+        }
+        if (best >= 0) return best;
+    }
     int best = -1;
     double best_score = -1.0;
-    for (int v : order) {
-        const TileShape t = tile_variant(v);
-        if (conv_lds_bytes(v, op.bf16, p) > lds_max) continue;
-        if (t.BN > (npad > 32 ? npad : 32)) continue;
-        const int64_t tiles_t = (F + t.BM - 1) / t.BM;
-        const int64_t blocks = (int64_t)B * tiles_t * ((op.N + t.BN - 1) / t.BN);
-        const double eff = (double)F / (double)(tiles_t * t.BM);
-        if (blocks >= 512 && eff >= 0.75) return v;
-        const double score = (double)(blocks < 512 ? blocks : 512) * eff;
+    for (int v : {9, 8, 7, 6, 5, 4, 3}) {
+        if (!variant_fits(op, v)) continue;
+        if (blocks(v) >= 512 && eff(v) >= 0.75) return v;
+        const double score = (double)(blocks(v) < 512 ? blocks(v) : 512) * eff(v);
         if (score > best_score) {
             best_score = score;
             best = v;
         }
     }
-    return best < 0 ? 0 : best;
+    return best < 0 ? 3 : best;
 }
 
 // ------------------------------------------------------------ the network
@@ -302,9 +340,12 @@ static void build_network(dc_state* s)
     s->ring_E = add_ring(s, "embed", C0, opE, 0);
     int cur = s->ring_E;
     for (int l = 0; l < c.n_pre; l++) {
-        const int P = add_ring(s, "pre" + std::to_string(l), C0, opE, 0);
+        // pre-stack outputs stay fp32; a bf16 consumer takes them as hi + lo
+        // operands (these layers carry most of the rounding sensitivity)
+        const int P = add_ring(s, "pre" + std::to_string(l), C0, kF32, 0);
         ConvOp& op = conv("pre" + std::to_string(l), cur, P, C0, C0, c.pre_kernel, 1, 0);
         op.out_act = 1;
+        op.split = bf && l > 0;
         need_ctx(s, cur, c.pre_kernel - 1);
         cur = P;
     }
@@ -326,6 +367,7 @@ static void build_network(dc_state* s)
             op.transposed = true;
             op.in_act = 1;
             op.bf16 = bf;
+            op.split = bf;
             op.level_in = st;
             op.blob_w = off;
             off += (size_t)ci * co * 2 * u;
@@ -399,6 +441,7 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
     p.in_C = in.C;
     p.in_elem = in.elem;
     p.in_act = op.in_act;
+    p.split = op.split;
     p.wp = s->arena + op.w_off;
     p.bias = (const float*)(s->arena + op.b_off);
     p.CB = op.CB;
@@ -424,7 +467,7 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
     }
     p.B = c.batch;
     p.F = (int)(n * s->fpt[op.level_in]);
-    p.tiles_t = (p.F + tile_variant(op.variant).BM - 1) / tile_variant(op.variant).BM;
+    p.tiles_t = (p.F + tile_variant(op.variant).BM() - 1) / tile_variant(op.variant).BM();
     p.clock = s->clock;
     p.in_fpt = s->fpt[op.level_in];
     p.slope = c.lrelu_slope;
@@ -797,8 +840,9 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
     } else if (i <= nc) {
         const ConvOp& op = s->convs[i - 1];
         const TileShape t = tile_variant(op.variant);
-        set(op.name, "dc::conv_kernel<" + std::string(op.bf16 ? "true" : "false") + ", " + std::to_string(t.BM) +
-                         ", " + std::to_string(t.BN) + ", " + std::to_string(t.WGM) + ">");
+        set(op.name, "dc::conv_kernel<" + std::string(op.bf16 ? "true" : "false") + ", " + std::to_string(t.MB) +
+                         ", " + std::to_string(t.NB) + ", " + std::to_string(t.WGM) + ", " + std::to_string(t.WGN) +
+                         ", " + std::to_string(t.WGK) + ", " + std::to_string(t.SI) + ">");
         const double F = (double)n * s->fpt[op.level_in];
         const Ring& in = s->rings[op.in];
         const Ring& o = s->rings[op.out];

@@ -67,7 +67,7 @@ struct ConvParams {
 // chains.  S = WGK * SI is the number of K partitions (part of the layer's
 // arithmetic: it fixes the order of the fp32 sums).
 struct TileShape {
-    int MB, NB, WGM, WGN, WGK, SI;
+    int MB, NB, WGM, WGN, WGK, SI, PD;   // PD: weight fragments in flight per wave
     int BM() const { return 16 * MB * WGM; }
     int BN() const { return 16 * NB * WGN; }
     int S() const { return WGK * SI; }

@@ -16,6 +16,20 @@
 
 #include "dc_internal.h"
 
+#ifndef DC_LOAD_BATCH
+#define DC_LOAD_BATCH 1
+#endif
+// weight fragments in flight per wave, by tile size
+#ifndef DC_PD_SMALL
+#define DC_PD_SMALL 1
+#endif
+#ifndef DC_PD_MED
+#define DC_PD_MED 1
+#endif
+#ifndef DC_PD_BIG
+#define DC_PD_BIG 1
+#endif
+
 namespace dc {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
@@ -150,7 +164,39 @@ __device__ __forceinline__ void store_out(const ConvParams& p, int b, const RowS
         ((uint16_t*)p.out)[oo] = (uint16_t)f2bf(v);
 }
 
-template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int SI>
+// Four consecutive output channels co .. co+3 of one frame (nv < 4 at the
+// edge of an output whose width is not a multiple of 4).
+__device__ __forceinline__ void store_out4(const ConvParams& p, int b, const RowSlots& rs, int off, int co,
+                                           f32x4 v, int nv)
+{
+    if (nv < 4 || (p.out_C & 3)) {
+        for (int e = 0; e < nv; e++) store_out(p, b, rs, off, co + e, v[e]);
+        return;
+    }
+    if (p.res) v = *(const f32x4*)(p.res + ((size_t)b * p.res_R + slot_add(rs.res, off, (int)p.res_R)) * p.out_C + co) + v;
+    if (p.n_mean) {
+        const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean, off, (int)p.mean_R)) * p.out_C + co;
+        f32x4 x = *(const f32x4*)(p.mean[0] + mo);
+        for (int i = 1; i < p.n_mean; i++) x = x + *(const f32x4*)(p.mean[i] + mo);
+        x = x + v;
+        const float J = (float)(p.n_mean + 1);
+        v = f32x4{x[0] / J, x[1] / J, x[2] / J, x[3] / J};
+    }
+    if (p.out_act) {
+#pragma unroll
+        for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
+    }
+    const size_t oo = ((size_t)b * p.out_R + slot_add(rs.out, off, (int)p.out_R)) * p.out_C + co;
+    if (p.out_elem == kF32) {
+        *(f32x4*)((float*)p.out + oo) = v;
+    } else {
+        typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+        u32x2 h = {f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16)};
+        *(u32x2*)((uint16_t*)p.out + oo) = h;
+    }
+}
+
+template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int SI, int PD>
 __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 {
     using Tr = OpT<BF16>;
@@ -198,34 +244,50 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
         }
     };
 
+    constexpr int AU = DC_LOAD_BATCH;          // operand vectors in flight per thread
+
+    // Operand rows [t0 - halo, t0 + BM) of channel block cb, through the ring.
+    auto load_operand = [&](int cb) {
+        for (int v0 = tid; v0 < rows * vpr; v0 += 256 * AU) {
+            float x[AU][8];
+#pragma unroll
+            for (int u = 0; u < AU; u++) {
+                const int v = v0 + u * 256;
+#pragma unroll
+                for (int e = 0; e < 8; e++) x[u][e] = 0.f;
+                const int r = v / vpr, c8 = (v - r * vpr) * 8;
+                const int t = t0 - halo + r;
+                const int ch = cb * p.CB + c8;
+                if (v < rows * vpr && t < p.F && ch < p.in_C)
+                    load8(p.in, p.in_elem, ((size_t)b * p.in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < AU; u++) {
+                const int v = v0 + u * 256;
+                if (v >= rows * vpr) break;
+                const int r = v / vpr, c8 = (v - r * vpr) * 8;
+                if (p.in_act) {
+#pragma unroll
+                    for (int e = 0; e < 8; e++) x[u][e] = lrelu(x[u][e], p.slope);
+                }
+                if constexpr (BF16) {
+                    if (p.split)
+                        store8_lds_split(lds + r * ldw + c8, lds + (rows + r) * ldw + c8, x[u]);
+                    else
+                        store8_lds(lds + r * ldw + c8, x[u]);
+                } else {
+                    store8_lds(lds + r * ldw + c8, x[u]);
+                }
+            }
+        }
+    };
+
     Frag bnext[NB];
     loadB(0, wk, bnext);
     for (int cb = 0; cb < p.n_cb; cb++) {
         __syncthreads();
-        // Operand rows [t0 - halo, t0 + BM) of channel block cb, through the ring.
-        for (int v = tid; v < rows * vpr; v += 256) {
-            const int r = v / vpr, c8 = (v - r * vpr) * 8;
-            const int t = t0 - halo + r;
-            const int ch = cb * p.CB + c8;
-            float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            if (t < p.F && ch < p.in_C) {
-                load8(p.in, p.in_elem, ((size_t)b * p.in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x);
-                if (p.in_act) {
-#pragma unroll
-                    for (int e = 0; e < 8; e++) x[e] = lrelu(x[e], p.slope);
-                }
-            }
-            if constexpr (BF16) {
-                if (p.split)
-                    store8_lds_split(lds + r * ldw + c8, lds + (rows + r) * ldw + c8, x);
-                else
-                    store8_lds(lds + r * ldw + c8, x);
-            } else {
-                store8_lds(lds + r * ldw + c8, x);
-            }
-        }
+        load_operand(cb);
         __syncthreads();
-
         for (int i = 0; i < per; i += SI) {
 #pragma unroll
             for (int si = 0; si < SI; si++) {
@@ -255,7 +317,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 #pragma unroll
                         for (int nb = 0; nb < NB; nb++)
                             acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                a[mb], __builtin_bit_cast(bf16x8_t, w[nb]), acc[si][mb][nb], 0, 0, 0);
+                                __builtin_bit_cast(bf16x8_t, w[nb]), a[mb], acc[si][mb][nb], 0, 0, 0);
                     if (p.split) {   // the low halves, right after the high halves of the same step
 #pragma unroll
                         for (int mb = 0; mb < MB; mb++)
@@ -267,7 +329,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 #pragma unroll
                             for (int nb = 0; nb < NB; nb++)
                                 acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                    a[mb], __builtin_bit_cast(bf16x8_t, w[nb]), acc[si][mb][nb], 0, 0, 0);
+                                    __builtin_bit_cast(bf16x8_t, w[nb]), a[mb], acc[si][mb][nb], 0, 0, 0);
                     }
                 } else {
                     f32x4 a[MB];
@@ -281,7 +343,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
                         for (int mb = 0; mb < MB; mb++)
 #pragma unroll
                             for (int nb = 0; nb < NB; nb++)
-                                acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mb][q], w[nb][q],
+                                acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[nb][q], a[mb][q],
                                                                                       acc[si][mb][nb], 0, 0, 0);
                 }
             }
@@ -295,32 +357,35 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
     rs.res = p.res ? (int)ring_slot(tau_out0, p.res_R) : 0;
     rs.mean = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
 
+    // The weights are the MFMA A operand and the frames the B operand, so lane
+    // l holds output channels 4*(l/16) .. +3 of frame l%16 of each 16x16 block:
+    // four consecutive channels of one frame, stored as one vector.
+    const int fl = lane & 15, cg = (lane >> 4) * 4;
     if constexpr (WGK == 1) {
-        int rp[NB], co[NB];
-        float bias[NB];
+        int rp[NB], co[NB], nv[NB];
+        f32x4 bias[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; nb++) {
-            const int n = n0 + (wn * NB + nb) * 16 + (lane & 15);
-            rp[nb] = p.u == 1 ? 0 : n / p.out_C;
-            co[nb] = n - rp[nb] * p.out_C;
-            bias[nb] = n < p.N ? p.bias[n] : 0.f;
-            if (n >= p.N) rp[nb] = -1;
+            const int n4 = n0 + (wn * NB + nb) * 16 + cg;
+            rp[nb] = p.u == 1 ? 0 : n4 / p.out_C;
+            co[nb] = n4 - rp[nb] * p.out_C;
+            nv[nb] = p.N - n4 < 4 ? p.N - n4 : 4;
+#pragma unroll
+            for (int e = 0; e < 4; e++) bias[nb][e] = e < nv[nb] ? p.bias[n4 + e] : 0.f;
         }
 #pragma unroll
-        for (int mb = 0; mb < MB; mb++)
+        for (int mb = 0; mb < MB; mb++) {
+            const int tl = wm * 16 * MB + mb * 16 + fl;
+            if (t0 + tl >= p.F) continue;
 #pragma unroll
-            for (int r = 0; r < 4; r++) {
-                const int tl = wm * 16 * MB + mb * 16 + (lane >> 4) * 4 + r;
-                if (t0 + tl >= p.F) continue;
+            for (int nb = 0; nb < NB; nb++) {
+                if (nv[nb] <= 0) continue;
+                f32x4 v = acc[0][mb][nb];
 #pragma unroll
-                for (int nb = 0; nb < NB; nb++) {
-                    if (rp[nb] < 0) continue;
-                    float v = acc[0][mb][nb][r];
-#pragma unroll
-                    for (int si = 1; si < SI; si++) v = v + acc[si][mb][nb][r];
-                    store_out(p, b, rs, tl * p.u + rp[nb], co[nb], v + bias[nb]);
-                }
+                for (int si = 1; si < SI; si++) v = v + acc[si][mb][nb];
+                store_out4(p, b, rs, tl * p.u + rp[nb], co[nb], v + bias[nb], nv[nb]);
             }
+        }
     } else {
         // partial sums of every partition through LDS, added in partition order
         __syncthreads();
@@ -330,24 +395,26 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 #pragma unroll
             for (int mb = 0; mb < MB; mb++)
 #pragma unroll
-                for (int nb = 0; nb < NB; nb++)
-#pragma unroll
-                    for (int r = 0; r < 4; r++) {
-                        const int pidx = si * WGK + wk;
-                        const int row = wm * 16 * MB + mb * 16 + (lane >> 4) * 4 + r;
-                        const int col = (wn * NB + nb) * 16 + (lane & 15);
-                        red[(pidx * BM + row) * BN + col] = acc[si][mb][nb][r];
-                    }
+                for (int nb = 0; nb < NB; nb++) {
+                    const int pidx = si * WGK + wk;
+                    const int row = wm * 16 * MB + mb * 16 + fl;
+                    const int col = (wn * NB + nb) * 16 + cg;
+                    *(f32x4*)(red + (pidx * BM + row) * BN + col) = acc[si][mb][nb];
+                }
         __syncthreads();
-        for (int idx = tid; idx < BM * BN; idx += 256) {
+        for (int idx = tid * 4; idx < BM * BN; idx += 256 * 4) {
             const int tl = idx / BN, nl = idx - tl * BN;
-            const int n = n0 + nl;
-            if (t0 + tl >= p.F || n >= p.N) continue;
-            float v = red[idx];
+            const int n4 = n0 + nl;
+            if (t0 + tl >= p.F || n4 >= p.N) continue;
+            f32x4 v = *(const f32x4*)(red + idx);
 #pragma unroll
-            for (int q = 1; q < S; q++) v = v + red[q * BM * BN + idx];
-            const int rpn = p.u == 1 ? 0 : n / p.out_C;
-            store_out(p, b, rs, tl * p.u + rpn, n - rpn * p.out_C, v + p.bias[n]);
+            for (int q = 1; q < S; q++) v = v + *(const f32x4*)(red + q * BM * BN + idx);
+            const int nv = p.N - n4 < 4 ? p.N - n4 : 4;
+            f32x4 bias;
+#pragma unroll
+            for (int e = 0; e < 4; e++) bias[e] = e < nv ? p.bias[n4 + e] : 0.f;
+            const int rpn = p.u == 1 ? 0 : n4 / p.out_C;
+            store_out4(p, b, rs, tl * p.u + rpn, n4 - rpn * p.out_C, v + bias, nv);
         }
     }
 }
@@ -355,19 +422,19 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 // ------------------------------------------------------------- tile table
 
 static const TileShape kTiles[] = {
-    //  MB NB WGM WGN WGK SI
-    {1, 1, 1, 1, 4, 1},   // 0: 16x16, K in 4 partitions across waves
-    {1, 2, 1, 1, 4, 1},   // 1: 16x32, 4 partitions
-    {2, 2, 1, 1, 4, 1},   // 2: 32x32, 4 partitions
-    {1, 1, 2, 2, 1, 1},   // 3: 32x32
-    {1, 2, 2, 2, 1, 1},   // 4: 32x64
-    {2, 2, 2, 2, 1, 1},   // 5: 64x64
-    {2, 4, 2, 2, 1, 1},   // 6: 64x128
-    {2, 4, 4, 1, 1, 1},   // 7: 128x64
-    {4, 4, 2, 2, 1, 1},   // 8: 128x128
-    {4, 4, 4, 1, 1, 1},   // 9: 256x64
-    {2, 2, 2, 1, 2, 1},   // 10: 64x32, 2 partitions across waves
-    {2, 2, 2, 2, 1, 2},   // 11: 64x64, 2 chains per wave
+    //  MB NB WGM WGN WGK SI PD
+    {1, 1, 1, 1, 4, 1, DC_PD_SMALL},   // 0: 16x16, K in 4 partitions across waves
+    {1, 2, 1, 1, 4, 1, DC_PD_SMALL},   // 1: 16x32, 4 partitions
+    {2, 2, 1, 1, 4, 1, DC_PD_MED},   // 2: 32x32, 4 partitions
+    {1, 1, 2, 2, 1, 1, DC_PD_SMALL},   // 3: 32x32
+    {1, 2, 2, 2, 1, 1, DC_PD_SMALL},   // 4: 32x64
+    {2, 2, 2, 2, 1, 1, DC_PD_MED},   // 5: 64x64
+    {2, 4, 2, 2, 1, 1, DC_PD_BIG},   // 6: 64x128
+    {2, 4, 4, 1, 1, 1, DC_PD_BIG},   // 7: 128x64
+    {4, 4, 2, 2, 1, 1, DC_PD_BIG},   // 8: 128x128
+    {4, 4, 4, 1, 1, 1, DC_PD_BIG},   // 9: 256x64
+    {2, 2, 2, 1, 2, 1, DC_PD_MED},   // 10: 64x32, 2 partitions across waves
+    {2, 2, 2, 2, 1, 2, DC_PD_MED},   // 11: 64x64, 2 chains per wave
 };
 
 int num_tile_variants() { return (int)(sizeof(kTiles) / sizeof(kTiles[0])); }
@@ -378,17 +445,25 @@ size_t conv_lds_bytes(int v, bool bf16, const ConvParams& p)
     const TileShape& t = kTiles[v];
     const int rows = t.BM() + (p.k - 1) * p.d;
     const int pad = bf16 ? OpT<true>::PAD : OpT<false>::PAD;
-    const size_t a = (size_t)rows * (p.CB + pad) * (bf16 ? 2 : 4) * (bf16 && p.split ? 2 : 1);
+    size_t a = (size_t)rows * (p.CB + pad) * (bf16 ? 2 : 4) * (bf16 && p.split ? 2 : 1);
     const size_t red = t.WGK > 1 ? (size_t)t.S() * t.BM() * t.BN() * 4 : 0;
     return a > red ? a : red;
 }
 
-template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int SI>
+template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int SI, int PD>
 static hipError_t launch_t(const ConvParams& p, size_t lds, hipStream_t st)
 {
     constexpr int BN = 16 * NB * WGN;
     dim3 grid((unsigned)(p.B * p.tiles_t), (unsigned)((p.N + BN - 1) / BN));
-    hipLaunchKernelGGL((conv_kernel<BF16, MB, NB, WGM, WGN, WGK, SI>), grid, dim3(256), lds, st, p);
+    static size_t lds_set = 64 * 1024;   // the default dynamic LDS limit of a kernel
+    if (lds > lds_set) {
+        const hipError_t e = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&conv_kernel<BF16, MB, NB, WGM, WGN, WGK, SI, PD>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        lds_set = lds;
+    }
+    hipLaunchKernelGGL((conv_kernel<BF16, MB, NB, WGM, WGN, WGK, SI, PD>), grid, dim3(256), lds, st, p);
     return hipGetLastError();
 }
 
@@ -396,18 +471,18 @@ template <bool BF16>
 static hipError_t launch_dt(int v, const ConvParams& p, size_t lds, hipStream_t st)
 {
     switch (v) {
-    case 0: return launch_t<BF16, 1, 1, 1, 1, 4, 1>(p, lds, st);
-    case 1: return launch_t<BF16, 1, 2, 1, 1, 4, 1>(p, lds, st);
-    case 2: return launch_t<BF16, 2, 2, 1, 1, 4, 1>(p, lds, st);
-    case 3: return launch_t<BF16, 1, 1, 2, 2, 1, 1>(p, lds, st);
-    case 4: return launch_t<BF16, 1, 2, 2, 2, 1, 1>(p, lds, st);
-    case 5: return launch_t<BF16, 2, 2, 2, 2, 1, 1>(p, lds, st);
-    case 6: return launch_t<BF16, 2, 4, 2, 2, 1, 1>(p, lds, st);
-    case 7: return launch_t<BF16, 2, 4, 4, 1, 1, 1>(p, lds, st);
-    case 8: return launch_t<BF16, 4, 4, 2, 2, 1, 1>(p, lds, st);
-    case 9: return launch_t<BF16, 4, 4, 4, 1, 1, 1>(p, lds, st);
-    case 10: return launch_t<BF16, 2, 2, 2, 1, 2, 1>(p, lds, st);
-    case 11: return launch_t<BF16, 2, 2, 2, 2, 1, 2>(p, lds, st);
+    case 0: return launch_t<BF16, 1, 1, 1, 1, 4, 1, DC_PD_SMALL>(p, lds, st);
+    case 1: return launch_t<BF16, 1, 2, 1, 1, 4, 1, DC_PD_SMALL>(p, lds, st);
+    case 2: return launch_t<BF16, 2, 2, 1, 1, 4, 1, DC_PD_MED>(p, lds, st);
+    case 3: return launch_t<BF16, 1, 1, 2, 2, 1, 1, DC_PD_SMALL>(p, lds, st);
+    case 4: return launch_t<BF16, 1, 2, 2, 2, 1, 1, DC_PD_SMALL>(p, lds, st);
+    case 5: return launch_t<BF16, 2, 2, 2, 2, 1, 1, DC_PD_MED>(p, lds, st);
+    case 6: return launch_t<BF16, 2, 4, 2, 2, 1, 1, DC_PD_BIG>(p, lds, st);
+    case 7: return launch_t<BF16, 2, 4, 4, 1, 1, 1, DC_PD_BIG>(p, lds, st);
+    case 8: return launch_t<BF16, 4, 4, 2, 2, 1, 1, DC_PD_BIG>(p, lds, st);
+    case 9: return launch_t<BF16, 4, 4, 4, 1, 1, 1, DC_PD_BIG>(p, lds, st);
+    case 10: return launch_t<BF16, 2, 2, 2, 1, 2, 1, DC_PD_MED>(p, lds, st);
+    case 11: return launch_t<BF16, 2, 2, 2, 2, 1, 2, DC_PD_MED>(p, lds, st);
     default: return hipErrorInvalidValue;
     }
 }

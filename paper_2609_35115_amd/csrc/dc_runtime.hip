@@ -168,12 +168,22 @@ static std::string validate(const dc_cfg* c)
     return "";
 }
 
-// Geometry of the packed weights of one conv (operand type decides the K quantum).
+// Geometry of the packed weights of one conv (operand type decides the K
+// quantum).  Channel block CB: bf16 layers take 128 channels per block; fp32
+// layers take as many as keep a 16-row operand tile with its left context
+// within 64 KB of LDS (fewer blocks = fewer dependent load phases for the
+// small-batch shapes fp32 serves).
 static void set_blocks(ConvOp& op)
 {
     const int kq = op.bf16 ? 32 : 16;
-    const int cmax = op.bf16 ? 128 : 64;
     const int cpad = (op.Ci + kq - 1) / kq * kq;
+    int cmax = 128;
+    if (!op.bf16) {
+        cmax = cpad;
+        const int rows = 16 + (op.k - 1) * op.d;
+        while (cmax > kq && (size_t)rows * (cmax + 4) * 4 > 64 * 1024) cmax /= 2;
+        if (cmax % kq) cmax = kq;
+    }
     op.CB = cpad < cmax ? cpad : cmax;
     op.n_cb = (cpad + op.CB - 1) / op.CB;
     op.NB16 = (op.N + 15) / 16;
@@ -227,6 +237,9 @@ static void pack_weights(const ConvOp& op, const float* blob, bool round_bf16, c
 // 32x32 output tiles leave fewer than 512 blocks, so waves split K to fill
 // the machine; 1 otherwise), then the largest tile of that S that keeps
 // enough blocks.
+// LDS budget of one block: at most 80 KB of the CU's 160 KB, so two blocks
+// stay resident.
+
 static bool variant_fits(const ConvOp& op, int v)
 {
     ConvParams p{};
@@ -238,7 +251,7 @@ static bool variant_fits(const ConvOp& op, int v)
     const int kq = op.bf16 ? 32 : 16;
     const int qcb = op.k * (op.CB / kq);
     const int npad = (op.N + 15) / 16 * 16;
-    return conv_lds_bytes(v, op.bf16, p) <= 64 * 1024 && qcb % t.S() == 0 && t.BN() <= (npad > 16 ? npad : 16);
+    return conv_lds_bytes(v, op.bf16, p) <= 80 * 1024 && qcb % t.S() == 0 && t.BN() <= (npad > 16 ? npad : 16);
 }
 
 static int pick_variant(const dc_state* s, const ConvOp& op)
@@ -415,7 +428,9 @@ static void build_network(dc_state* s)
     {
         ConvOp& op = conv("head", cur, s->ring_S, c.channels[L], hc, c.head_kernel, 1, L);
         op.in_act = 1;
-        op.bf16 = false;  // head arithmetic is fp32 on (possibly bf16-rounded) weights
+        // bf16 weights are exact in bf16, and the fp32 operand is carried as a
+        // hi + lo pair: the head keeps (nearly) fp32 products on bf16 MFMA
+        op.split = bf;
         need_ctx(s, cur, c.head_kernel - 1);
     }
     s->ring_G = add_ring(s, "G", c.n_fft, kF32, L);
@@ -842,7 +857,8 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
         const TileShape t = tile_variant(op.variant);
         set(op.name, "dc::conv_kernel<" + std::string(op.bf16 ? "true" : "false") + ", " + std::to_string(t.MB) +
                          ", " + std::to_string(t.NB) + ", " + std::to_string(t.WGM) + ", " + std::to_string(t.WGN) +
-                         ", " + std::to_string(t.WGK) + ", " + std::to_string(t.SI) + ">");
+                         ", " + std::to_string(t.WGK) + ", " + std::to_string(t.SI) + ", " + std::to_string(t.PD) +
+                         ">");
         const double F = (double)n * s->fpt[op.level_in];
         const Ring& in = s->rings[op.in];
         const Ring& o = s->rings[op.out];

@@ -30,6 +30,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "audio-seconds decoded per wall-second (1 GPU) + p50 per-chunk latency ms"
+PROFILES = os.path.join(ROOT, "profiles")
+# rocprofv3 PMC counters against a plain 256 MiB device copy on MI355X: FETCH_SIZE
+# reads half the bytes the copy moves, WRITE_SIZE all of them.
+FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 DEFAULT_WORKLOAD = "real_f32_b1_n25"
 PEAK = {"hbm": 8000.0, "bf16": 2500.0, "f32": 157.3}   # GB/s, TFLOP/s (MI355X, dense)
 
@@ -63,6 +67,32 @@ def cpu_baseline(arch, dtype, blob, tokens, budget_s: float):
                       f"{' on bf16-rounded weights' if dtype == 'bf16' else ''}, {dt:.1f} s wall"}
 
 
+def kernel_source_hash() -> str:
+    """Hash of the kernel sources: a traffic figure taken on other sources is stale."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("dc_kernels.hip", "dc_internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_35115_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` recorded under profiles/ for this workload
+    with the current kernel sources, else None."""
+    path = os.path.join(PROFILES, f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            rec[k.strip()] = v.strip()
+    if rec.get("kernel_source_hash") != kernel_source_hash() or rec.get("kernel") != kernel:
+        return None
+    return float(rec["hbm_bytes_per_launch"])
+
+
 def roofline(layers, us, dtype):
     """Group launches by kernel; the one with the most time per step is reported."""
     groups = {}
@@ -90,7 +120,73 @@ def roofline(layers, us, dtype):
             "kernels_by_share": [[k, round(v, 4)] for k, v in per_kernel[:6]]}
 
 
+def calibrate_copy():
+    """A plain device copy of 256 MiB, three times (the counter calibration run)."""
+    import torch
+    n = 256 << 20
+    a = torch.ones(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(f"copied {n} bytes 3 times", flush=True)
+
+
+def _csv(path):
+    import csv
+    with open(path) as fh:
+        return list(csv.DictReader(fh))
+
+
+def summarize_stats(prof_dir: str, out: str, command: str):
+    """Text summary of a rocprofv3 --kernel-trace --stats --output-format csv run."""
+    import glob
+    rows = _csv(glob.glob(os.path.join(prof_dir, "**", "*kernel_stats.csv"), recursive=True)[0])
+    lines = [f"# rocprofv3 kernel statistics", f"# command: {command}",
+             f"# kernel sources: {kernel_source_hash()}", "",
+             f"{'kernel':64s} {'calls':>7s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'total_ms':>9s} {'pct':>6s}"]
+    for r in rows:
+        name = r["Name"].replace("void ", "")
+        name = name[:name.index("(")] if "(" in name else name
+        lines.append(f"{name[:64]:64s} {int(r['Calls']):7d} {float(r['AverageNs'])/1e3:9.3f} "
+                     f"{float(r['MinNs'])/1e3:9.3f} {float(r['MaxNs'])/1e3:9.3f} "
+                     f"{float(r['TotalDurationNs'])/1e6:9.3f} {float(r['Percentage']):6.2f}")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def summarize_traffic(fetch_dir: str, write_dir: str, workload: str, kernel: str, out: str, command: str):
+    """Mean HBM bytes per dispatch of `kernel` from FETCH_SIZE and WRITE_SIZE runs."""
+    import glob
+    def mean_kib(d, counter):
+        rows = _csv(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0])
+        vals = {}
+        for r in rows:
+            name = r["Kernel_Name"].replace("void ", "")
+            name = name[:name.index("(")] if "(" in name else name
+            if name == kernel and r["Counter_Name"] == counter:
+                vals[r["Dispatch_Id"]] = vals.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+        return sum(vals.values()) / len(vals), len(vals)
+    f, nf = mean_kib(fetch_dir, "FETCH_SIZE")
+    w, nw = mean_kib(write_dir, "WRITE_SIZE")
+    hbm = (f * FETCH_SCALE + w * WRITE_SCALE) * 1024.0
+    lines = ["# HBM traffic per launch from rocprofv3 PMC counters", f"# command: {command}",
+             f"# FETCH_SIZE x {FETCH_SCALE} + WRITE_SIZE x {WRITE_SCALE} (KiB per dispatch; scale factors from a "
+             "plain 256 MiB device copy: python3 bench.py --calibrate-copy)",
+             f"workload: {workload}", f"kernel: {kernel}", f"kernel_source_hash: {kernel_source_hash()}",
+             f"dispatches: {nf} / {nw}", f"fetch_kib_per_dispatch: {f:.1f}", f"write_kib_per_dispatch: {w:.1f}",
+             f"hbm_bytes_per_launch: {hbm:.0f}"]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
+    if len(sys.argv) > 1 and sys.argv[1] == "--calibrate-copy":
+        return calibrate_copy()
+    if len(sys.argv) > 1 and sys.argv[1] == "--summarize-stats":
+        return summarize_stats(sys.argv[2], sys.argv[3], sys.argv[4])
+    if len(sys.argv) > 1 and sys.argv[1] == "--summarize-traffic":
+        return summarize_traffic(*sys.argv[2:8])
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
@@ -159,6 +255,7 @@ def main():
     layers = dec.layers()
     us = dec.time_layers(args.layer_reps)
     roof = roofline(layers, us, dtype)
+    roof["traffic"] = traffic_from_profiles(args.workload, roof["kernel"])
     stats = dec.stats()
     dec.close()
     print(f"# roofline: {roof['kernel']} {roof['achieved']} {roof['unit']} ({roof['frac']:.1%})",

@@ -63,14 +63,15 @@ struct ConvParams {
 };
 
 // Block of 4 waves: WGM x WGN waves tile the output, each wave MB x NB MFMA
-// blocks of 16x16; WGK waves split K; every wave keeps SI accumulation
-// chains.  S = WGK * SI is the number of K partitions (part of the layer's
-// arithmetic: it fixes the order of the fp32 sums).
+// blocks of 16x16; WGK waves split K (each takes every WGK-th K chunk of a
+// tap).  KCH is the channel block in MFMA K chunks.  WGK and KCH are part of
+// a layer's arithmetic (they fix the order of the fp32 sums); MB, NB, WGM
+// and WGN are not.
 struct TileShape {
-    int MB, NB, WGM, WGN, WGK, SI, PD;   // PD: weight fragments in flight per wave
+    int MB, NB, WGM, WGN, WGK, KCH;
     int BM() const { return 16 * MB * WGM; }
     int BN() const { return 16 * NB * WGN; }
-    int S() const { return WGK * SI; }
+    int S() const { return WGK; }
 };
 
 // The tile shapes compiled for each operand type.

@@ -19,16 +19,7 @@
 #ifndef DC_LOAD_BATCH
 #define DC_LOAD_BATCH 1
 #endif
-// weight fragments in flight per wave, by tile size
-#ifndef DC_PD_SMALL
-#define DC_PD_SMALL 1
-#endif
-#ifndef DC_PD_MED
-#define DC_PD_MED 1
-#endif
-#ifndef DC_PD_BIG
-#define DC_PD_BIG 1
-#endif
+
 
 namespace dc {
 
@@ -128,10 +119,10 @@ __device__ __forceinline__ void store8_lds(float* dst, const float v[8])
 //
 // Block = 4 waves = WGM x WGN x WGK: WGM x WGN waves tile the output
 // (MB x NB MFMA blocks of 16x16 each), WGK waves share one output tile and
-// split K.  The K steps (channel block cb, tap j, chunk kc) of a layer are
-// numbered q = 0, 1, ...; step q belongs to partition q mod S (S = WGK * SI),
-// each partition is an independent fp32 accumulation chain, and the result
-// is ((P_0 + P_1) + ...) + P_{S-1}.  S divides the steps of a channel block.
+// split K.  K runs over (channel block cb, tap j, chunk kc) in that order;
+// wave wk of a K-split block takes the chunks kc = wk, wk + WGK, ... of every
+// tap, accumulates them in that order in fp32, and the block adds the WGK
+// partial sums in wave order: ((P_0 + P_1) + ...) + P_{WGK-1}.
 
 struct RowSlots {
     int out, res, mean;   // ring slots of output frame (block row 0, phase 0)
@@ -196,158 +187,145 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Row
     }
 }
 
-template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int SI, int PD>
+template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int KCH>
 __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 {
     using Tr = OpT<BF16>;
     using T = typename Tr::T;
     using Frag = typename std::conditional<BF16, u32x4, f32x4>::type;
-    constexpr int BM = 16 * MB * WGM, BN = 16 * NB * WGN, S = WGK * SI;
-    static_assert(WGM * WGN * WGK == 4, "4 waves per block");
+    constexpr int BM = 16 * MB * WGM, BN = 16 * NB * WGN, S = WGK;
+    constexpr int CB = Tr::KQ * KCH;        // channels per block
+    constexpr int KPW = KCH / WGK;          // this wave's K chunks per tap
+    constexpr int LDW = CB + Tr::PAD;       // LDS row stride (elements)
+    constexpr int VPR = CB / 8;             // 8-channel vectors per LDS row
+    static_assert(WGM * WGN * WGK == 4 && KCH % WGK == 0, "tile shape");
 
     extern __shared__ __align__(16) unsigned char smem[];
     T* lds = reinterpret_cast<T*>(smem);
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar index math
     const int wk = wave % WGK, wm = (wave / WGK) % WGM, wn = wave / (WGK * WGM);
     const int b = blockIdx.x / p.tiles_t;
     const int t0 = (blockIdx.x - b * p.tiles_t) * BM;
     const int n0 = blockIdx.y * BN;
     const int halo = (p.k - 1) * p.d;
     const int rows = BM + halo;
-    const int ldw = p.CB + Tr::PAD;
-    const int vpr = p.CB / 8;
-    const int kch = p.CB / Tr::KQ;
-    const int qcb = p.k * kch;          // K steps per channel block
-    const int per = qcb / WGK;          // this wave's steps per channel block
     const int64_t tau0 = p.clock[0] * p.in_fpt;
     const int in_R = (int)p.in_R;
     const int base_in = (int)ring_slot(tau0 + t0 - halo, p.in_R);
     const int nblk0 = n0 / 16 + wn * NB;
     const Frag* wp = reinterpret_cast<const Frag*>(p.wp);
 
-    f32x4 acc[SI][MB][NB];
+    f32x4 acc[MB][NB];
 #pragma unroll
-    for (int si = 0; si < SI; si++)
+    for (int i = 0; i < MB; i++)
 #pragma unroll
-        for (int i = 0; i < MB; i++)
-#pragma unroll
-            for (int j = 0; j < NB; j++) acc[si][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < NB; j++) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    auto loadB = [&](int cb, int ls, Frag (&w)[NB]) {
-        const size_t wstep = ((size_t)cb * qcb + ls) * p.NB16;
+    // Weight fragments of this wave for tap j of channel block cb.
+    auto load_tap = [&](int cb, int j, Frag (&w)[KPW][NB]) {
+        const size_t base = (size_t)(cb * p.k + j) * KCH * p.NB16;
 #pragma unroll
-        for (int nb = 0; nb < NB; nb++) {
-            Frag z = {};
-            if (nblk0 + nb < p.NB16) z = wp[(wstep + nblk0 + nb) * 64 + lane];
-            w[nb] = z;
-        }
+        for (int ki = 0; ki < KPW; ki++)
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++) {
+                const int kc = ki * WGK + wk;
+                Frag z = {};
+                if (nblk0 + nb < p.NB16) z = wp[(base + (size_t)kc * p.NB16 + nblk0 + nb) * 64 + lane];
+                w[ki][nb] = z;
+            }
     };
 
-    constexpr int AU = DC_LOAD_BATCH;          // operand vectors in flight per thread
-
-    // Operand rows [t0 - halo, t0 + BM) of channel block cb, through the ring.
-    auto load_operand = [&](int cb) {
-        for (int v0 = tid; v0 < rows * vpr; v0 += 256 * AU) {
-            float x[AU][8];
+    // MFMAs of tap j: weights are the A operand, frames the B operand.
+    auto compute_tap = [&](int j, const Frag (&w)[KPW][NB]) {
+        const int roff = j * p.d + (lane & 15);
 #pragma unroll
-            for (int u = 0; u < AU; u++) {
-                const int v = v0 + u * 256;
+        for (int ki = 0; ki < KPW; ki++) {
+            const int kc = ki * WGK + wk;
+            if constexpr (BF16) {
+                bf16x8_t a[MB];
 #pragma unroll
-                for (int e = 0; e < 8; e++) x[u][e] = 0.f;
-                const int r = v / vpr, c8 = (v - r * vpr) * 8;
-                const int t = t0 - halo + r;
-                const int ch = cb * p.CB + c8;
-                if (v < rows * vpr && t < p.F && ch < p.in_C)
-                    load8(p.in, p.in_elem, ((size_t)b * p.in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x[u]);
-            }
+                for (int mb = 0; mb < MB; mb++)
+                    a[mb] = __builtin_bit_cast(
+                        bf16x8_t, *(const u32x4*)(lds + (wm * 16 * MB + mb * 16 + roff) * LDW + kc * 32 + (lane >> 4) * 8));
 #pragma unroll
-            for (int u = 0; u < AU; u++) {
-                const int v = v0 + u * 256;
-                if (v >= rows * vpr) break;
-                const int r = v / vpr, c8 = (v - r * vpr) * 8;
-                if (p.in_act) {
+                for (int mb = 0; mb < MB; mb++)
 #pragma unroll
-                    for (int e = 0; e < 8; e++) x[u][e] = lrelu(x[u][e], p.slope);
-                }
-                if constexpr (BF16) {
-                    if (p.split)
-                        store8_lds_split(lds + r * ldw + c8, lds + (rows + r) * ldw + c8, x[u]);
-                    else
-                        store8_lds(lds + r * ldw + c8, x[u]);
-                } else {
-                    store8_lds(lds + r * ldw + c8, x[u]);
-                }
-            }
-        }
-    };
-
-    Frag bnext[NB];
-    loadB(0, wk, bnext);
-    for (int cb = 0; cb < p.n_cb; cb++) {
-        __syncthreads();
-        load_operand(cb);
-        __syncthreads();
-        for (int i = 0; i < per; i += SI) {
-#pragma unroll
-            for (int si = 0; si < SI; si++) {
-                const int ls = (i + si) * WGK + wk;
-                Frag w[NB];
-#pragma unroll
-                for (int nb = 0; nb < NB; nb++) w[nb] = bnext[nb];
-                {   // prefetch this wave's next step
-                    int ncb = cb, nls = ls + WGK;
-                    if (nls >= qcb) {
-                        ncb++;
-                        nls -= qcb;
-                    }
-                    if (ncb < p.n_cb) loadB(ncb, nls, bnext);
-                }
-                const int j = ls / kch, kc = ls - j * kch;
-                const int roff = j * p.d + (lane & 15);
-                if constexpr (BF16) {
-                    bf16x8_t a[MB];
+                    for (int nb = 0; nb < NB; nb++)
+                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(bf16x8_t, w[ki][nb]), a[mb], acc[mb][nb], 0, 0, 0);
+                if (p.split) {   // the low halves, right after the high halves of the same step
 #pragma unroll
                     for (int mb = 0; mb < MB; mb++)
                         a[mb] = __builtin_bit_cast(
-                            bf16x8_t, *(const u32x4*)(lds + (wm * 16 * MB + mb * 16 + roff) * ldw + kc * 32 +
+                            bf16x8_t, *(const u32x4*)(lds + (rows + wm * 16 * MB + mb * 16 + roff) * LDW + kc * 32 +
                                                       (lane >> 4) * 8));
 #pragma unroll
                     for (int mb = 0; mb < MB; mb++)
 #pragma unroll
                         for (int nb = 0; nb < NB; nb++)
-                            acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                __builtin_bit_cast(bf16x8_t, w[nb]), a[mb], acc[si][mb][nb], 0, 0, 0);
-                    if (p.split) {   // the low halves, right after the high halves of the same step
+                            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8_t, w[ki][nb]), a[mb], acc[mb][nb], 0, 0, 0);
+                }
+            } else {
+                f32x4 a[MB];
 #pragma unroll
-                        for (int mb = 0; mb < MB; mb++)
-                            a[mb] = __builtin_bit_cast(
-                                bf16x8_t, *(const u32x4*)(lds + (rows + wm * 16 * MB + mb * 16 + roff) * ldw +
-                                                          kc * 32 + (lane >> 4) * 8));
+                for (int mb = 0; mb < MB; mb++)
+                    a[mb] = *(const f32x4*)(lds + (wm * 16 * MB + mb * 16 + roff) * LDW + kc * 16 + (lane >> 4) * 4);
 #pragma unroll
-                        for (int mb = 0; mb < MB; mb++)
-#pragma unroll
-                            for (int nb = 0; nb < NB; nb++)
-                                acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                    __builtin_bit_cast(bf16x8_t, w[nb]), a[mb], acc[si][mb][nb], 0, 0, 0);
-                    }
-                } else {
-                    f32x4 a[MB];
+                for (int q = 0; q < 4; q++)
 #pragma unroll
                     for (int mb = 0; mb < MB; mb++)
-                        a[mb] = *(const f32x4*)(lds + (wm * 16 * MB + mb * 16 + roff) * ldw + kc * 16 +
-                                                (lane >> 4) * 4);
 #pragma unroll
-                    for (int q = 0; q < 4; q++)
-#pragma unroll
-                        for (int mb = 0; mb < MB; mb++)
-#pragma unroll
-                            for (int nb = 0; nb < NB; nb++)
-                                acc[si][mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[nb][q], a[mb][q],
-                                                                                      acc[si][mb][nb], 0, 0, 0);
-                }
+                        for (int nb = 0; nb < NB; nb++)
+                            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[ki][nb][q], a[mb][q], acc[mb][nb],
+                                                                              0, 0, 0);
             }
         }
+    };
+
+    // Operand rows [t0 - halo, t0 + BM) of channel block cb, through the ring.
+    auto load_operand = [&](int cb) {
+        for (int v = tid; v < rows * VPR; v += 256) {
+            const int r = v / VPR, c8 = (v - r * VPR) * 8;
+            const int t = t0 - halo + r;
+            const int ch = cb * CB + c8;
+            float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            if (t < p.F && ch < p.in_C) {
+                load8(p.in, p.in_elem, ((size_t)b * p.in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x);
+                if (p.in_act) {
+#pragma unroll
+                    for (int e = 0; e < 8; e++) x[e] = lrelu(x[e], p.slope);
+                }
+            }
+            if constexpr (BF16) {
+                if (p.split)
+                    store8_lds_split(lds + r * LDW + c8, lds + (rows + r) * LDW + c8, x);
+                else
+                    store8_lds(lds + r * LDW + c8, x);
+            } else {
+                store8_lds(lds + r * LDW + c8, x);
+            }
+        }
+    };
+
+    // Taps in pairs: the weights of the next tap are in flight while this
+    // tap's MFMAs run (two register buffers, no copies between them).
+    Frag w0[KPW][NB], w1[KPW][NB];
+    for (int cb = 0; cb < p.n_cb; cb++) {
+        __syncthreads();
+        load_tap(cb, 0, w0);
+        load_operand(cb);
+        __syncthreads();
+        int j = 0;
+        for (; j + 1 < p.k; j += 2) {
+            load_tap(cb, j + 1, w1);
+            compute_tap(j, w0);
+            load_tap(cb, j + 2 < p.k ? j + 2 : j + 1, w0);
+            compute_tap(j + 1, w1);
+        }
+        if (j < p.k) compute_tap(j, w0);
     }
 
     // ---- epilogue: bias, residual, branch mean, LeakyReLU, store through the rings
@@ -380,9 +358,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 #pragma unroll
             for (int nb = 0; nb < NB; nb++) {
                 if (nv[nb] <= 0) continue;
-                f32x4 v = acc[0][mb][nb];
-#pragma unroll
-                for (int si = 1; si < SI; si++) v = v + acc[si][mb][nb];
+                f32x4 v = acc[mb][nb];
                 store_out4(p, b, rs, tl * p.u + rp[nb], co[nb], v + bias[nb], nv[nb]);
             }
         }
@@ -391,16 +367,13 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
         __syncthreads();
         float* red = reinterpret_cast<float*>(smem);
 #pragma unroll
-        for (int si = 0; si < SI; si++)
+        for (int mb = 0; mb < MB; mb++)
 #pragma unroll
-            for (int mb = 0; mb < MB; mb++)
-#pragma unroll
-                for (int nb = 0; nb < NB; nb++) {
-                    const int pidx = si * WGK + wk;
-                    const int row = wm * 16 * MB + mb * 16 + fl;
-                    const int col = (wn * NB + nb) * 16 + cg;
-                    *(f32x4*)(red + (pidx * BM + row) * BN + col) = acc[si][mb][nb];
-                }
+            for (int nb = 0; nb < NB; nb++) {
+                const int row = wm * 16 * MB + mb * 16 + fl;
+                const int col = (wn * NB + nb) * 16 + cg;
+                *(f32x4*)(red + (wk * BM + row) * BN + col) = acc[mb][nb];
+            }
         __syncthreads();
         for (int idx = tid * 4; idx < BM * BN; idx += 256 * 4) {
             const int tl = idx / BN, nl = idx - tl * BN;
@@ -421,20 +394,30 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 
 // ------------------------------------------------------------- tile table
 
+// Every shape exists for both operand types; KCH is the channel block in
+// MFMA K chunks (bf16: 32 channels, fp32: 16 channels per chunk).
 static const TileShape kTiles[] = {
-    //  MB NB WGM WGN WGK SI PD
-    {1, 1, 1, 1, 4, 1, DC_PD_SMALL},   // 0: 16x16, K in 4 partitions across waves
-    {1, 2, 1, 1, 4, 1, DC_PD_SMALL},   // 1: 16x32, 4 partitions
-    {2, 2, 1, 1, 4, 1, DC_PD_MED},   // 2: 32x32, 4 partitions
-    {1, 1, 2, 2, 1, 1, DC_PD_SMALL},   // 3: 32x32
-    {1, 2, 2, 2, 1, 1, DC_PD_SMALL},   // 4: 32x64
-    {2, 2, 2, 2, 1, 1, DC_PD_MED},   // 5: 64x64
-    {2, 4, 2, 2, 1, 1, DC_PD_BIG},   // 6: 64x128
-    {2, 4, 4, 1, 1, 1, DC_PD_BIG},   // 7: 128x64
-    {4, 4, 2, 2, 1, 1, DC_PD_BIG},   // 8: 128x128
-    {4, 4, 4, 1, 1, 1, DC_PD_BIG},   // 9: 256x64
-    {2, 2, 2, 1, 2, 1, DC_PD_MED},   // 10: 64x32, 2 partitions across waves
-    {2, 2, 2, 2, 1, 2, DC_PD_MED},   // 11: 64x64, 2 chains per wave
+    // MB NB WGM WGN WGK KCH
+    {1, 1, 1, 1, 4, 4},    // 0: 16x16, K in 4 partitions across waves
+    {1, 1, 1, 1, 4, 8},    // 1
+    {1, 1, 1, 1, 4, 16},   // 2
+    {1, 2, 1, 1, 4, 4},    // 3: 16x32, 4 partitions
+    {1, 2, 1, 1, 4, 8},    // 4
+    {2, 2, 1, 1, 4, 4},    // 5: 32x32, 4 partitions
+    {1, 1, 2, 2, 1, 2},    // 6: 32x32
+    {1, 1, 2, 2, 1, 4},    // 7
+    {1, 2, 2, 2, 1, 4},    // 8: 32x64
+    {2, 2, 2, 2, 1, 2},    // 9: 64x64
+    {2, 2, 2, 2, 1, 4},    // 10
+    {2, 4, 2, 2, 1, 4},    // 11: 64x128
+    {2, 4, 4, 1, 1, 2},    // 12: 128x64
+    {2, 4, 4, 1, 1, 4},    // 13
+    {4, 4, 2, 2, 1, 4},    // 14: 128x128
+    {4, 4, 4, 1, 1, 2},    // 15: 256x64
+    {4, 4, 4, 1, 1, 4},    // 16
+    {1, 1, 1, 1, 4, 32},   // 17: 16x16, 4 partitions, wide channel block
+    {1, 2, 1, 1, 4, 16},   // 18: 16x32
+    {1, 1, 2, 2, 1, 1},    // 19: 32x32, narrow channel block
 };
 
 int num_tile_variants() { return (int)(sizeof(kTiles) / sizeof(kTiles[0])); }
@@ -445,12 +428,13 @@ size_t conv_lds_bytes(int v, bool bf16, const ConvParams& p)
     const TileShape& t = kTiles[v];
     const int rows = t.BM() + (p.k - 1) * p.d;
     const int pad = bf16 ? OpT<true>::PAD : OpT<false>::PAD;
-    size_t a = (size_t)rows * (p.CB + pad) * (bf16 ? 2 : 4) * (bf16 && p.split ? 2 : 1);
+    const int cb = t.KCH * (bf16 ? OpT<true>::KQ : OpT<false>::KQ);
+    const size_t a = (size_t)rows * (cb + pad) * (bf16 ? 2 : 4) * (bf16 && p.split ? 2 : 1);
     const size_t red = t.WGK > 1 ? (size_t)t.S() * t.BM() * t.BN() * 4 : 0;
     return a > red ? a : red;
 }
 
-template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int SI, int PD>
+template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int KCH>
 static hipError_t launch_t(const ConvParams& p, size_t lds, hipStream_t st)
 {
     constexpr int BN = 16 * NB * WGN;
@@ -458,12 +442,12 @@ static hipError_t launch_t(const ConvParams& p, size_t lds, hipStream_t st)
     static size_t lds_set = 64 * 1024;   // the default dynamic LDS limit of a kernel
     if (lds > lds_set) {
         const hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&conv_kernel<BF16, MB, NB, WGM, WGN, WGK, SI, PD>),
+            reinterpret_cast<const void*>(&conv_kernel<BF16, MB, NB, WGM, WGN, WGK, KCH>),
             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         lds_set = lds;
     }
-    hipLaunchKernelGGL((conv_kernel<BF16, MB, NB, WGM, WGN, WGK, SI, PD>), grid, dim3(256), lds, st, p);
+    hipLaunchKernelGGL((conv_kernel<BF16, MB, NB, WGM, WGN, WGK, KCH>), grid, dim3(256), lds, st, p);
     return hipGetLastError();
 }
 
@@ -471,18 +455,26 @@ template <bool BF16>
 static hipError_t launch_dt(int v, const ConvParams& p, size_t lds, hipStream_t st)
 {
     switch (v) {
-    case 0: return launch_t<BF16, 1, 1, 1, 1, 4, 1, DC_PD_SMALL>(p, lds, st);
-    case 1: return launch_t<BF16, 1, 2, 1, 1, 4, 1, DC_PD_SMALL>(p, lds, st);
-    case 2: return launch_t<BF16, 2, 2, 1, 1, 4, 1, DC_PD_MED>(p, lds, st);
-    case 3: return launch_t<BF16, 1, 1, 2, 2, 1, 1, DC_PD_SMALL>(p, lds, st);
-    case 4: return launch_t<BF16, 1, 2, 2, 2, 1, 1, DC_PD_SMALL>(p, lds, st);
-    case 5: return launch_t<BF16, 2, 2, 2, 2, 1, 1, DC_PD_MED>(p, lds, st);
-    case 6: return launch_t<BF16, 2, 4, 2, 2, 1, 1, DC_PD_BIG>(p, lds, st);
-    case 7: return launch_t<BF16, 2, 4, 4, 1, 1, 1, DC_PD_BIG>(p, lds, st);
-    case 8: return launch_t<BF16, 4, 4, 2, 2, 1, 1, DC_PD_BIG>(p, lds, st);
-    case 9: return launch_t<BF16, 4, 4, 4, 1, 1, 1, DC_PD_BIG>(p, lds, st);
-    case 10: return launch_t<BF16, 2, 2, 2, 1, 2, 1, DC_PD_MED>(p, lds, st);
-    case 11: return launch_t<BF16, 2, 2, 2, 2, 1, 2, DC_PD_MED>(p, lds, st);
+    case 0: return launch_t<BF16, 1, 1, 1, 1, 4, 4>(p, lds, st);
+    case 1: return launch_t<BF16, 1, 1, 1, 1, 4, 8>(p, lds, st);
+    case 2: return launch_t<BF16, 1, 1, 1, 1, 4, 16>(p, lds, st);
+    case 3: return launch_t<BF16, 1, 2, 1, 1, 4, 4>(p, lds, st);
+    case 4: return launch_t<BF16, 1, 2, 1, 1, 4, 8>(p, lds, st);
+    case 5: return launch_t<BF16, 2, 2, 1, 1, 4, 4>(p, lds, st);
+    case 6: return launch_t<BF16, 1, 1, 2, 2, 1, 2>(p, lds, st);
+    case 7: return launch_t<BF16, 1, 1, 2, 2, 1, 4>(p, lds, st);
+    case 8: return launch_t<BF16, 1, 2, 2, 2, 1, 4>(p, lds, st);
+    case 9: return launch_t<BF16, 2, 2, 2, 2, 1, 2>(p, lds, st);
+    case 10: return launch_t<BF16, 2, 2, 2, 2, 1, 4>(p, lds, st);
+    case 11: return launch_t<BF16, 2, 4, 2, 2, 1, 4>(p, lds, st);
+    case 12: return launch_t<BF16, 2, 4, 4, 1, 1, 2>(p, lds, st);
+    case 13: return launch_t<BF16, 2, 4, 4, 1, 1, 4>(p, lds, st);
+    case 14: return launch_t<BF16, 4, 4, 2, 2, 1, 4>(p, lds, st);
+    case 15: return launch_t<BF16, 4, 4, 4, 1, 1, 2>(p, lds, st);
+    case 16: return launch_t<BF16, 4, 4, 4, 1, 1, 4>(p, lds, st);
+    case 17: return launch_t<BF16, 1, 1, 1, 1, 4, 32>(p, lds, st);
+    case 18: return launch_t<BF16, 1, 2, 1, 1, 4, 16>(p, lds, st);
+    case 19: return launch_t<BF16, 1, 1, 2, 2, 1, 1>(p, lds, st);
     default: return hipErrorInvalidValue;
     }
 }

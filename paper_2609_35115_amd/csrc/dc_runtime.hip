@@ -168,24 +168,13 @@ static std::string validate(const dc_cfg* c)
     return "";
 }
 
-// Geometry of the packed weights of one conv (operand type decides the K
-// quantum).  Channel block CB: bf16 layers take 128 channels per block; fp32
-// layers take as many as keep a 16-row operand tile with its left context
-// within 64 KB of LDS (fewer blocks = fewer dependent load phases for the
-// small-batch shapes fp32 serves).
+// Geometry of the packed weights of one conv for its tile shape: channel
+// block CB = K quantum x KCH channels, ceil(Ci / CB) blocks (zero padded).
 static void set_blocks(ConvOp& op)
 {
     const int kq = op.bf16 ? 32 : 16;
-    const int cpad = (op.Ci + kq - 1) / kq * kq;
-    int cmax = 128;
-    if (!op.bf16) {
-        cmax = cpad;
-        const int rows = 16 + (op.k - 1) * op.d;
-        while (cmax > kq && (size_t)rows * (cmax + 4) * 4 > 64 * 1024) cmax /= 2;
-        if (cmax % kq) cmax = kq;
-    }
-    op.CB = cpad < cmax ? cpad : cmax;
-    op.n_cb = (cpad + op.CB - 1) / op.CB;
+    op.CB = kq * tile_variant(op.variant).KCH;
+    op.n_cb = (op.Ci + op.CB - 1) / op.CB;
     op.NB16 = (op.N + 15) / 16;
     op.w_bytes = (size_t)op.n_cb * op.k * (op.CB / kq) * op.NB16 * 64 * 16;
 }
@@ -239,50 +228,71 @@ static void pack_weights(const ConvOp& op, const float* blob, bool round_bf16, c
 // enough blocks.
 // LDS budget of one block: at most 80 KB of the CU's 160 KB, so two blocks
 // stay resident.
-
 static bool variant_fits(const ConvOp& op, int v)
 {
     ConvParams p{};
     p.k = op.k;
     p.d = op.d;
-    p.CB = op.CB;
     p.split = op.split;
     const TileShape t = tile_variant(v);
-    const int kq = op.bf16 ? 32 : 16;
-    const int qcb = op.k * (op.CB / kq);
     const int npad = (op.N + 15) / 16 * 16;
-    return conv_lds_bytes(v, op.bf16, p) <= 80 * 1024 && qcb % t.S() == 0 && t.BN() <= (npad > 16 ? npad : 16);
+    return conv_lds_bytes(v, op.bf16, p) <= 80 * 1024 && t.BN() <= (npad > 16 ? npad : 16);
 }
 
+// Tile shape of a conv for this state.  Deterministic: it depends on the
+// layer, the batch and the chunk size only (never on a call's n), so every
+// call of a state -- replayed or direct, chunked or offline -- runs the same
+// arithmetic.  First the K partitions: 4 (waves split K) when even 32x32
+// output tiles leave fewer than 512 blocks, else 1.  Then the channel block:
+// as wide as the layer's channels (capped at 4 chunks for unsplit tiles),
+// so no K step is padding.  Then the largest tile with enough blocks.
 static int pick_variant(const dc_state* s, const ConvOp& op)
 {
     const int64_t B = s->cfg.batch;
     const int64_t F = (int64_t)s->cfg.chunk_tokens * s->fpt[op.level_in];
+    const int nv = num_tile_variants();
     if (s->cfg.tile_variant > 0) {
         // a forced shape that does not fit this layer falls back to the largest
-        // fitting shape with the same number of K partitions
+        // fitting shape with the same arithmetic (K partitions, channel block)
         const int fv = s->cfg.tile_variant - 1;
         if (variant_fits(op, fv)) return fv;
-        for (int v : {9, 8, 7, 6, 5, 4, 3, 11, 10, 2, 1, 0})
-            if (tile_variant(v).S() == tile_variant(fv).S() && variant_fits(op, v)) return v;
+        int best = -1;
+        for (int v = 0; v < nv; v++)
+            if (tile_variant(v).WGK == tile_variant(fv).WGK && tile_variant(v).KCH == tile_variant(fv).KCH &&
+                variant_fits(op, v) && (best < 0 || tile_variant(v).BM() * tile_variant(v).BN() >
+                                                        tile_variant(best).BM() * tile_variant(best).BN()))
+                best = v;
+        if (best >= 0) return best;
     }
-    auto blocks = [&](int v) {
-        const TileShape t = tile_variant(v);
+    auto blocks = [&](const TileShape& t) {
         return B * ((F + t.BM() - 1) / t.BM()) * ((op.N + t.BN() - 1) / t.BN());
     };
-    auto eff = [&](int v) {
-        const int bm = tile_variant(v).BM();
+    auto eff = [&](const TileShape& t) {
+        const int bm = t.BM();
         return (double)F / (double)(((F + bm - 1) / bm) * bm);
     };
-    const bool small = blocks(3) < 512;
-    if (small) {
+    const int kq = op.bf16 ? 32 : 16;
+    const int kch_all = (op.Ci + kq - 1) / kq;      // chunks covering every input channel
+    const TileShape t32 = {1, 1, 2, 2, 1, 1};
+    const int wgk = blocks(t32) < 512 ? 4 : 1;
+    // channel-block candidates, widest first: no wider than the channels
+    // (nor than 4 chunks when waves do not split K)
+    for (int kch = 32; kch >= 1; kch /= 2) {
+        if (kch > kch_all && kch > 1) continue;
+        if (wgk == 1 && kch > 4) continue;
         int best = -1;
         double best_score = -1.0;
-        for (int v : {2, 1, 0}) {
-            if (!variant_fits(op, v)) continue;
+        for (int v = 0; v < nv; v++) {
             const TileShape t = tile_variant(v);
-            const double waves = (double)blocks(v) * 4.0;
-            const double score = (waves < 2048.0 ? waves : 2048.0) * eff(v) * (t.MB * t.NB >= 2 ? 1.0 : 0.85);
+            if (t.WGK != wgk || t.KCH != kch || !variant_fits(op, v)) continue;
+            double score;
+            if (wgk == 4) {
+                const double waves = (double)blocks(t) * 4.0;
+                score = (waves < 2048.0 ? waves : 2048.0) * eff(t) * (t.MB * t.NB >= 2 ? 1.0 : 0.85);
+            } else {
+                const bool enough = blocks(t) >= 512 && eff(t) >= 0.75;
+                score = enough ? 1e9 + t.BM() * t.BN() : (double)(blocks(t) < 512 ? blocks(t) : 512) * eff(t);
+            }
             if (score > best_score) {
                 best_score = score;
                 best = v;
@@ -290,18 +300,10 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
         }
         if (best >= 0) return best;
     }
-    int best = -1;
-    double best_score = -1.0;
-    for (int v : {9, 8, 7, 6, 5, 4, 3}) {
-        if (!variant_fits(op, v)) continue;
-        if (blocks(v) >= 512 && eff(v) >= 0.75) return v;
-        const double score = (double)(blocks(v) < 512 ? blocks(v) : 512) * eff(v);
-        if (score > best_score) {
-            best_score = score;
-            best = v;
-        }
-    }
-    return best < 0 ? 3 : best;
+    // nothing with the preferred partitions: any fitting shape, unsplit first
+    for (int v = 0; v < nv; v++)
+        if (tile_variant(v).WGK == 1 && variant_fits(op, v)) return v;
+    return 0;
 }
 
 // ------------------------------------------------------------ the network
@@ -435,7 +437,6 @@ static void build_network(dc_state* s)
     }
     s->ring_G = add_ring(s, "G", c.n_fft, kF32, L);
     need_ctx(s, s->ring_G, c.n_fft / c.hop - 1);
-    for (auto& op : s->convs) set_blocks(op);
 }
 
 // ------------------------------------------------------------ one chunk step
@@ -556,7 +557,10 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     for (int i = 0; i < c.n_stages; i++) s->fpt[i + 1] = s->fpt[i] * c.up_rate[i];
     s->spt = samples_per_token(&c);
     build_network(s);
-    for (auto& op : s->convs) op.variant = pick_variant(s, op);
+    for (auto& op : s->convs) {
+        op.variant = pick_variant(s, op);
+        set_blocks(op);
+    }
 
     // ---- arena layout: constants and weights, then rings, then I/O buffers
     const float* blob = (const float*)weights_blob;
@@ -857,8 +861,7 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
         const TileShape t = tile_variant(op.variant);
         set(op.name, "dc::conv_kernel<" + std::string(op.bf16 ? "true" : "false") + ", " + std::to_string(t.MB) +
                          ", " + std::to_string(t.NB) + ", " + std::to_string(t.WGM) + ", " + std::to_string(t.WGN) +
-                         ", " + std::to_string(t.WGK) + ", " + std::to_string(t.SI) + ", " + std::to_string(t.PD) +
-                         ">");
+                         ", " + std::to_string(t.WGK) + ", " + std::to_string(t.KCH) + ">");
         const double F = (double)n * s->fpt[op.level_in];
         const Ring& in = s->rings[op.in];
         const Ring& o = s->rings[op.out];

@@ -105,27 +105,32 @@ def test_graph_replay_equals_direct_launch(arch_name, dtype):
     b.close()
 
 
-# Forced tile shapes grouped by their number of K partitions S (the only tile
-# parameter that enters the arithmetic): within a group results are identical.
-TILE_GROUPS = {4: [1, 2, 3], 1: [4, 5, 6, 7, 8, 9, 10], 2: [11, 12]}
+# Forced tile shapes (1-based tile_variant) that share the arithmetic -- K
+# partitions across waves and channel block -- and fit every layer of the
+# case: their results must be identical.
+TILE_GROUPS = {
+    ("tiny", "f32"): [7, 10, 13],      # 32x32, 64x64, 128x64; unsplit K, 32-channel blocks
+    ("real", "f32"): [1, 4, 6],        # 16x16, 16x32, 32x32; K in 4 partitions, 64-channel blocks
+    ("real", "bf16"): [8, 9, 11],      # 32x32, 32x64, 64x64; unsplit K, 128-channel blocks
+}
 
 
-@pytest.mark.parametrize("arch_name,dtype", [("tiny", "f32"), ("real", "f32"), ("real", "bf16")])
+@pytest.mark.parametrize("arch_name,dtype", list(TILE_GROUPS))
 def test_tile_shape_does_not_change_results(arch_name, dtype):
     arch = TINY if arch_name == "tiny" else REAL
     n = 8 if arch_name == "tiny" else 3
     blob = synth.make_weights(arch, 2)
     ids = synth.make_tokens(arch, 1, 2 * n)
-    for S, variants in TILE_GROUPS.items():
-        ref = None
-        for v in variants:
-            dec = dc.Decoder(arch, dtype, blob, batch=1, chunk_tokens=n, tile_variant=v)
-            pcm = decode_chunks(dec, ids, [n, n])
-            dec.close()
-            if ref is None:
-                ref = pcm
-            else:
-                assert bits_equal(pcm, ref), f"S={S}: tile variant {v} differs from {variants[0]}"
+    variants = TILE_GROUPS[(arch_name, dtype)]
+    ref = None
+    for v in variants:
+        dec = dc.Decoder(arch, dtype, blob, batch=1, chunk_tokens=n, tile_variant=v)
+        pcm = decode_chunks(dec, ids, [n, n])
+        dec.close()
+        if ref is None:
+            ref = pcm
+        else:
+            assert bits_equal(pcm, ref), f"tile variant {v} differs from {variants[0]}"
 
 
 def test_real_f32_matches_oracle():
@@ -152,10 +157,10 @@ def test_real_bf16_matches_oracle():
 def test_stream_in_batch_equals_stream_alone(dtype):
     blob = synth.make_weights(REAL, 0)
     ids = synth.make_tokens(REAL, 3, 8)
-    big = dc.Decoder(REAL, dtype, blob, batch=3, chunk_tokens=4, tile_variant=6)
+    big = dc.Decoder(REAL, dtype, blob, batch=3, chunk_tokens=4, tile_variant=11)
     pb = decode_chunks(big, ids, [4, 4])
     big.close()
-    one = dc.Decoder(REAL, dtype, blob, batch=1, chunk_tokens=4, tile_variant=4)
+    one = dc.Decoder(REAL, dtype, blob, batch=1, chunk_tokens=4, tile_variant=8)
     p1 = decode_chunks(one, ids[2:3], [4, 4])
     one.close()
     assert bits_equal(pb[2:3], p1)

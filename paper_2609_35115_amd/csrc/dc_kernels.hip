@@ -39,6 +39,15 @@ __device__ __forceinline__ uint32_t f2bf(float f)
 
 __device__ __forceinline__ float bf2f(uint32_t h) { return __uint_as_float(h << 16); }
 
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
+// Two floats -> packed bfloat16 pair (v_cvt_pk_bf16_f32: round to nearest even).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
+{
+    const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
 __device__ __forceinline__ float lrelu(float v, float s) { return v >= 0.0f ? v : v * s; }
 
 __device__ __forceinline__ int64_t ring_slot(int64_t tau, int64_t R)
@@ -90,7 +99,7 @@ __device__ __forceinline__ void store8_lds(uint16_t* dst, const float v[8])
 {
     u32x4 w;
 #pragma unroll
-    for (int e = 0; e < 4; e++) w[e] = f2bf(v[2 * e]) | (f2bf(v[2 * e + 1]) << 16);
+    for (int e = 0; e < 4; e++) w[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
     *(u32x4*)dst = w;
 }
 
@@ -100,9 +109,8 @@ __device__ __forceinline__ void store8_lds_split(uint16_t* hi, uint16_t* lo, con
     u32x4 h, l;
 #pragma unroll
     for (int e = 0; e < 4; e++) {
-        const uint32_t h0 = f2bf(v[2 * e]), h1 = f2bf(v[2 * e + 1]);
-        h[e] = h0 | (h1 << 16);
-        l[e] = f2bf(v[2 * e] - bf2f(h0)) | (f2bf(v[2 * e + 1] - bf2f(h1)) << 16);
+        h[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+        l[e] = pack_bf16x2(v[2 * e] - bf2f(h[e] & 0xffffu), v[2 * e + 1] - bf2f(h[e] >> 16));
     }
     *(u32x4*)hi = h;
     *(u32x4*)lo = l;
@@ -182,7 +190,7 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Row
         *(f32x4*)((float*)p.out + oo) = v;
     } else {
         typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
-        u32x2 h = {f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16)};
+        u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
         *(u32x2*)((uint16_t*)p.out + oo) = h;
     }
 }
@@ -237,18 +245,22 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
             }
     };
 
-    // MFMAs of tap j: weights are the A operand, frames the B operand.
+    // MFMAs of tap j: weights are the A operand, frames the B operand.  This
+    // lane's fragment address is fixed; a tap adds a scalar row offset, a
+    // block / chunk an immediate.
+    constexpr int VEC = BF16 ? 8 : 4;       // operand elements per lane per K chunk
+    const T* a_lane = lds + (wm * 16 * MB + (lane & 15)) * LDW + (lane >> 4) * VEC + wk * Tr::KQ;
+    const int lo_off = rows * LDW;          // low halves of a split operand
     auto compute_tap = [&](int j, const Frag (&w)[KPW][NB]) {
-        const int roff = j * p.d + (lane & 15);
+        const T* aj = a_lane + j * p.d * LDW;
 #pragma unroll
         for (int ki = 0; ki < KPW; ki++) {
-            const int kc = ki * WGK + wk;
+            const int koff = ki * WGK * Tr::KQ;
             if constexpr (BF16) {
                 bf16x8_t a[MB];
 #pragma unroll
                 for (int mb = 0; mb < MB; mb++)
-                    a[mb] = __builtin_bit_cast(
-                        bf16x8_t, *(const u32x4*)(lds + (wm * 16 * MB + mb * 16 + roff) * LDW + kc * 32 + (lane >> 4) * 8));
+                    a[mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(aj + mb * 16 * LDW + koff));
 #pragma unroll
                 for (int mb = 0; mb < MB; mb++)
 #pragma unroll
@@ -258,9 +270,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
                 if (p.split) {   // the low halves, right after the high halves of the same step
 #pragma unroll
                     for (int mb = 0; mb < MB; mb++)
-                        a[mb] = __builtin_bit_cast(
-                            bf16x8_t, *(const u32x4*)(lds + (rows + wm * 16 * MB + mb * 16 + roff) * LDW + kc * 32 +
-                                                      (lane >> 4) * 8));
+                        a[mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(aj + lo_off + mb * 16 * LDW + koff));
 #pragma unroll
                     for (int mb = 0; mb < MB; mb++)
 #pragma unroll
@@ -271,8 +281,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
             } else {
                 f32x4 a[MB];
 #pragma unroll
-                for (int mb = 0; mb < MB; mb++)
-                    a[mb] = *(const f32x4*)(lds + (wm * 16 * MB + mb * 16 + roff) * LDW + kc * 16 + (lane >> 4) * 4);
+                for (int mb = 0; mb < MB; mb++) a[mb] = *(const f32x4*)(aj + mb * 16 * LDW + koff);
 #pragma unroll
                 for (int q = 0; q < 4; q++)
 #pragma unroll

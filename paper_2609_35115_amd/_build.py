@@ -25,7 +25,14 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
            *[os.path.join(CSRC, s) for s in SOURCES]]
     if verbose:
         print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    # the host pass does not know the (device) feature flag: drop that notice
+    noise = "'-packed-fp32-ops' is not a recognized feature"
+    msg = "\n".join(l for l in (r.stdout + r.stderr).splitlines() if noise not in l)
+    if msg.strip():
+        print(msg, flush=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed ({r.returncode})")
     os.replace(tmp, out)
     return out
 

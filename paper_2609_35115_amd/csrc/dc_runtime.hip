@@ -219,13 +219,14 @@ static void pack_weights(const ConvOp& op, const float* blob, bool round_bf16, c
                     }
 }
 
-// Tile shape of a conv for this state.  Deterministic: it depends on the
-// layer, the batch and the chunk size only (never on a call's n), so every
-// call of a state -- replayed or direct, chunked or offline -- runs the same
-// arithmetic.  The number of K partitions S is chosen first (4 when even
-// 32x32 output tiles leave fewer than 512 blocks, so waves split K to fill
-// the machine; 1 otherwise), then the largest tile of that S that keeps
-// enough blocks.
+// Unsplit tile shapes in order of preference (ids of the kernel's shape
+// table).  Layers that read a residual and write fp32 -- and every layer of
+// the 64-channel stage -- move more bytes per FLOP and run best on 64x64
+// tiles, whose lower register use keeps more waves (and loads) in flight;
+// the others favour the largest tiles.
+static const int kPreferLarge[] = {14, 15, 16, 11, 12, 13, 9, 10, 8, 6, 7, 19};
+static const int kPrefer64[] = {9, 10, 11, 12, 13, 14, 15, 16, 8, 6, 7, 19};
+
 // LDS budget of one block: at most 80 KB of the CU's 160 KB, so two blocks
 // stay resident.
 static bool variant_fits(const ConvOp& op, int v)
@@ -245,7 +246,9 @@ static bool variant_fits(const ConvOp& op, int v)
 // arithmetic.  First the K partitions: 4 (waves split K) when even 32x32
 // output tiles leave fewer than 512 blocks, else 1.  Then the channel block:
 // as wide as the layer's channels (capped at 4 chunks for unsplit tiles),
-// so no K step is padding.  Then the largest tile with enough blocks.
+// so no K step is padding.  Then the tile: for split K the one that best
+// fills the machine, otherwise the first in preference order that keeps
+// enough blocks.
 static int pick_variant(const dc_state* s, const ConvOp& op)
 {
     const int64_t B = s->cfg.batch;
@@ -282,7 +285,12 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
         if (wgk == 1 && kch > 4) continue;
         int best = -1;
         double best_score = -1.0;
-        for (int v = 0; v < nv; v++) {
+        const bool bytes_heavy = op.res >= 0 || op.N <= 64;
+        const int* pref = bytes_heavy ? kPrefer64 : kPreferLarge;
+        const int npref = bytes_heavy ? (int)(sizeof(kPrefer64) / sizeof(int)) : (int)(sizeof(kPreferLarge) / sizeof(int));
+        const int* order = wgk == 4 ? nullptr : pref;
+        for (int oi = 0; oi < (wgk == 4 ? nv : npref); oi++) {
+            const int v = order ? order[oi] : oi;
             const TileShape t = tile_variant(v);
             if (t.WGK != wgk || t.KCH != kch || !variant_fits(op, v)) continue;
             double score;
@@ -290,8 +298,9 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
                 const double waves = (double)blocks(t) * 4.0;
                 score = (waves < 2048.0 ? waves : 2048.0) * eff(t) * (t.MB * t.NB >= 2 ? 1.0 : 0.85);
             } else {
-                const bool enough = blocks(t) >= 512 && eff(t) >= 0.75;
-                score = enough ? 1e9 + t.BM() * t.BN() : (double)(blocks(t) < 512 ? blocks(t) : 512) * eff(t);
+                // the first shape in preference order that keeps enough blocks
+                if (blocks(t) >= 512 && eff(t) >= 0.75) return v;
+                score = (double)(blocks(t) < 512 ? blocks(t) : 512) * eff(t);
             }
             if (score > best_score) {
                 best_score = score;

@@ -187,13 +187,15 @@ dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32
 
 /*
  * Measurement (roofline reporting).  A chunk step is a fixed sequence of
- * kernel launches ("layers": embed, every conv / transposed conv, head,
- * spectrum, overlap-add, clock).  dc_layer_info describes layer i at n =
- * chunk_tokens: its kernel (the demangled name a profiler shows), the GEMM
- * shape of a conv (rows = batch * frames, cols, depth = taps * input
- * channels), its algorithmic FLOPs (2 * multiply-adds of the convolution) and
- * its algorithmic HBM bytes (weights once, operand frames including left
- * context, residual / branch inputs, output frames).  dc_time_layers launches
+ * kernel launches ("layers": embed, each conv / transposed conv -- the
+ * convs at one position of the parallel resblock branches share a launch --,
+ * head, spectrum, overlap-add, clock).  dc_layer_info describes launch i at
+ * n = chunk_tokens: its kernel (the demangled name a profiler shows), the
+ * GEMM shape of a conv (rows = batch * frames, cols, depth = taps * input
+ * channels, summed over the launch's convs), its algorithmic FLOPs (2 *
+ * multiply-adds of the convolutions) and its algorithmic HBM bytes (weights
+ * once, operand frames including left context, residual / branch inputs,
+ * output frames).  dc_time_layers launches
  * every layer reps times in isolation on the state's stream, bracketed by HIP
  * events, and writes the mean microseconds per launch into us_per_launch
  * [dc_layer_count].  Re-running a layer rewrites only ring slots of frames the

@@ -67,6 +67,28 @@ struct ConvParams {
 // tap).  KCH is the channel block in MFMA K chunks.  WGK and KCH are part of
 // a layer's arithmetic (they fix the order of the fp32 sums); MB, NB, WGM
 // and WGN are not.
+// One launch runs the same tile shape over up to kMaxGroup convs that differ
+// only in taps, weights, bias and their input, output and residual rings
+// (the parallel branches of a resblock stage): blockIdx.z selects the member.
+// Member 0 is a full parameter set; the others carry only what differs, so
+// every shared field stays at a fixed kernel-argument offset.
+constexpr int kMaxGroup = 4;
+struct ConvMember {
+    const void* in;
+    int64_t in_R;
+    const void* wp;
+    const float* bias;
+    void* out;
+    int64_t out_R;
+    const float* res;
+    int64_t res_R;
+    int k;
+};
+struct ConvGroup {
+    ConvParams p;                      // member 0
+    ConvMember m[kMaxGroup - 1];       // members 1..count-1
+};
+
 struct TileShape {
     int MB, NB, WGM, WGN, WGK, KCH;
     int BM() const { return 16 * MB * WGM; }
@@ -81,7 +103,8 @@ TileShape tile_variant(int v);
 // LDS bytes a conv launch needs with tile shape v.
 size_t conv_lds_bytes(int v, bool bf16, const ConvParams& p);
 
-hipError_t launch_conv(int v, bool bf16, const ConvParams& p, hipStream_t st);
+// LDS bytes of a launch of `count` convs (the largest member).
+hipError_t launch_conv(int v, bool bf16, const ConvParams* ps, int count, hipStream_t st);
 
 hipError_t launch_embed(const int32_t* tokens, int n, int B, const void* table, int vocab, int C,
                         int elem, int fpt, Ring out, const int64_t* clock, int* err, hipStream_t st);

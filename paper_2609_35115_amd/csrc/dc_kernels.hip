@@ -132,8 +132,13 @@ __device__ __forceinline__ void store8_lds(float* dst, const float v[8])
 // tap, accumulates them in that order in fp32, and the block adds the WGK
 // partial sums in wave order: ((P_0 + P_1) + ...) + P_{WGK-1}.
 
-struct RowSlots {
-    int out, res, mean;   // ring slots of output frame (block row 0, phase 0)
+// This block's output and residual rings (of its group member) and the ring
+// slots of its output frame at block row 0, phase 0.
+struct OutRef {
+    void* out;
+    const float* res;
+    int out_R, res_R;
+    int out_s, res_s, mean_s;
 };
 
 // Slot of a frame `off` frames after a base slot, for 0 <= off < R.
@@ -143,38 +148,38 @@ __device__ __forceinline__ int slot_add(int base, int off, int R)
     return s >= R ? s - R : s;
 }
 
-__device__ __forceinline__ void store_out(const ConvParams& p, int b, const RowSlots& rs, int off, int co,
+__device__ __forceinline__ void store_out(const ConvParams& p, int b, const OutRef& rs, int off, int co,
                                           float v)
 {
     // off: output frame offset from the block's base frame; co: output channel
-    if (p.res) v = p.res[((size_t)b * p.res_R + slot_add(rs.res, off, (int)p.res_R)) * p.out_C + co] + v;
+    if (rs.res) v = rs.res[((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co] + v;
     if (p.n_mean) {
-        const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean, off, (int)p.mean_R)) * p.out_C + co;
+        const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean_s, off, (int)p.mean_R)) * p.out_C + co;
         float x = p.mean[0][mo];
         for (int i = 1; i < p.n_mean; i++) x = x + p.mean[i][mo];
         x = x + v;
         v = x / (float)(p.n_mean + 1);
     }
     if (p.out_act) v = lrelu(v, p.slope);
-    const size_t oo = ((size_t)b * p.out_R + slot_add(rs.out, off, (int)p.out_R)) * p.out_C + co;
+    const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co;
     if (p.out_elem == kF32)
-        ((float*)p.out)[oo] = v;
+        ((float*)rs.out)[oo] = v;
     else
-        ((uint16_t*)p.out)[oo] = (uint16_t)f2bf(v);
+        ((uint16_t*)rs.out)[oo] = (uint16_t)f2bf(v);
 }
 
 // Four consecutive output channels co .. co+3 of one frame (nv < 4 at the
 // edge of an output whose width is not a multiple of 4).
-__device__ __forceinline__ void store_out4(const ConvParams& p, int b, const RowSlots& rs, int off, int co,
+__device__ __forceinline__ void store_out4(const ConvParams& p, int b, const OutRef& rs, int off, int co,
                                            f32x4 v, int nv)
 {
     if (nv < 4 || (p.out_C & 3)) {
         for (int e = 0; e < nv; e++) store_out(p, b, rs, off, co + e, v[e]);
         return;
     }
-    if (p.res) v = *(const f32x4*)(p.res + ((size_t)b * p.res_R + slot_add(rs.res, off, (int)p.res_R)) * p.out_C + co) + v;
+    if (rs.res) v = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co) + v;
     if (p.n_mean) {
-        const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean, off, (int)p.mean_R)) * p.out_C + co;
+        const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean_s, off, (int)p.mean_R)) * p.out_C + co;
         f32x4 x = *(const f32x4*)(p.mean[0] + mo);
         for (int i = 1; i < p.n_mean; i++) x = x + *(const f32x4*)(p.mean[i] + mo);
         x = x + v;
@@ -185,19 +190,39 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Row
 #pragma unroll
         for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
     }
-    const size_t oo = ((size_t)b * p.out_R + slot_add(rs.out, off, (int)p.out_R)) * p.out_C + co;
+    const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co;
     if (p.out_elem == kF32) {
-        *(f32x4*)((float*)p.out + oo) = v;
+        *(f32x4*)((float*)rs.out + oo) = v;
     } else {
         typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
         u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-        *(u32x2*)((uint16_t*)p.out + oo) = h;
+        *(u32x2*)((uint16_t*)rs.out + oo) = h;
     }
 }
 
 template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int KCH>
-__global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
+__global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
 {
+    // shared fields from member 0; this block's member supplies the rest
+    const ConvParams& p = g.p;
+    const void* in_ptr = p.in;
+    int in_R = (int)p.in_R;
+    const void* w_ptr = p.wp;
+    const float* bias_ptr = p.bias;
+    OutRef rs{p.out, p.res, (int)p.out_R, (int)p.res_R, 0, 0, 0};
+    int k = p.k;
+    if (blockIdx.z > 0) {
+        const ConvMember& m = g.m[blockIdx.z - 1];
+        in_ptr = m.in;
+        in_R = (int)m.in_R;
+        w_ptr = m.wp;
+        bias_ptr = m.bias;
+        rs.out = m.out;
+        rs.out_R = (int)m.out_R;
+        rs.res = m.res;
+        rs.res_R = (int)m.res_R;
+        k = m.k;
+    }
     using Tr = OpT<BF16>;
     using T = typename Tr::T;
     using Frag = typename std::conditional<BF16, u32x4, f32x4>::type;
@@ -217,13 +242,12 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
     const int b = blockIdx.x / p.tiles_t;
     const int t0 = (blockIdx.x - b * p.tiles_t) * BM;
     const int n0 = blockIdx.y * BN;
-    const int halo = (p.k - 1) * p.d;
+    const int halo = (k - 1) * p.d;
     const int rows = BM + halo;
     const int64_t tau0 = p.clock[0] * p.in_fpt;
-    const int in_R = (int)p.in_R;
-    const int base_in = (int)ring_slot(tau0 + t0 - halo, p.in_R);
+    const int base_in = (int)ring_slot(tau0 + t0 - halo, in_R);
     const int nblk0 = n0 / 16 + wn * NB;
-    const Frag* wp = reinterpret_cast<const Frag*>(p.wp);
+    const Frag* wp = reinterpret_cast<const Frag*>(w_ptr);
 
     f32x4 acc[MB][NB];
 #pragma unroll
@@ -233,7 +257,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
 
     // Weight fragments of this wave for tap j of channel block cb.
     auto load_tap = [&](int cb, int j, Frag (&w)[KPW][NB]) {
-        const size_t base = (size_t)(cb * p.k + j) * KCH * p.NB16;
+        const size_t base = (size_t)(cb * k + j) * KCH * p.NB16;
 #pragma unroll
         for (int ki = 0; ki < KPW; ki++)
 #pragma unroll
@@ -302,7 +326,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
             const int ch = cb * CB + c8;
             float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
             if (t < p.F && ch < p.in_C) {
-                load8(p.in, p.in_elem, ((size_t)b * p.in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x);
+                load8(in_ptr, p.in_elem, ((size_t)b * in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x);
                 if (p.in_act) {
 #pragma unroll
                     for (int e = 0; e < 8; e++) x[e] = lrelu(x[e], p.slope);
@@ -328,21 +352,20 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
         load_operand(cb);
         __syncthreads();
         int j = 0;
-        for (; j + 1 < p.k; j += 2) {
+        for (; j + 1 < k; j += 2) {
             load_tap(cb, j + 1, w1);
             compute_tap(j, w0);
-            load_tap(cb, j + 2 < p.k ? j + 2 : j + 1, w0);
+            load_tap(cb, j + 2 < k ? j + 2 : j + 1, w0);
             compute_tap(j + 1, w1);
         }
-        if (j < p.k) compute_tap(j, w0);
+        if (j < k) compute_tap(j, w0);
     }
 
     // ---- epilogue: bias, residual, branch mean, LeakyReLU, store through the rings
     const int64_t tau_out0 = (tau0 + t0) * p.u;   // output frame of block row 0, phase 0
-    RowSlots rs;
-    rs.out = (int)ring_slot(tau_out0, p.out_R);
-    rs.res = p.res ? (int)ring_slot(tau_out0, p.res_R) : 0;
-    rs.mean = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
+    rs.out_s = (int)ring_slot(tau_out0, rs.out_R);
+    rs.res_s = rs.res ? (int)ring_slot(tau_out0, rs.res_R) : 0;
+    rs.mean_s = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
 
     // The weights are the MFMA A operand and the frames the B operand, so lane
     // l holds output channels 4*(l/16) .. +3 of frame l%16 of each 16x16 block:
@@ -358,7 +381,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
             co[nb] = n4 - rp[nb] * p.out_C;
             nv[nb] = p.N - n4 < 4 ? p.N - n4 : 4;
 #pragma unroll
-            for (int e = 0; e < 4; e++) bias[nb][e] = e < nv[nb] ? p.bias[n4 + e] : 0.f;
+            for (int e = 0; e < 4; e++) bias[nb][e] = e < nv[nb] ? bias_ptr[n4 + e] : 0.f;
         }
 #pragma unroll
         for (int mb = 0; mb < MB; mb++) {
@@ -394,7 +417,7 @@ __global__ __launch_bounds__(256) void conv_kernel(ConvParams p)
             const int nv = p.N - n4 < 4 ? p.N - n4 : 4;
             f32x4 bias;
 #pragma unroll
-            for (int e = 0; e < 4; e++) bias[e] = e < nv ? p.bias[n4 + e] : 0.f;
+            for (int e = 0; e < 4; e++) bias[e] = e < nv ? bias_ptr[n4 + e] : 0.f;
             const int rpn = p.u == 1 ? 0 : n4 / p.out_C;
             store_out4(p, b, rs, tl * p.u + rpn, n4 - rpn * p.out_C, v + bias, nv);
         }
@@ -444,10 +467,11 @@ size_t conv_lds_bytes(int v, bool bf16, const ConvParams& p)
 }
 
 template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int KCH>
-static hipError_t launch_t(const ConvParams& p, size_t lds, hipStream_t st)
+static hipError_t launch_t(const ConvGroup& g, int count, size_t lds, hipStream_t st)
 {
     constexpr int BN = 16 * NB * WGN;
-    dim3 grid((unsigned)(p.B * p.tiles_t), (unsigned)((p.N + BN - 1) / BN));
+    const ConvParams& p = g.p;   // members share B, F, N and the tiling
+    dim3 grid((unsigned)(p.B * p.tiles_t), (unsigned)((p.N + BN - 1) / BN), (unsigned)count);
     static size_t lds_set = 64 * 1024;   // the default dynamic LDS limit of a kernel
     if (lds > lds_set) {
         const hipError_t e = hipFuncSetAttribute(
@@ -456,42 +480,64 @@ static hipError_t launch_t(const ConvParams& p, size_t lds, hipStream_t st)
         if (e != hipSuccess) return e;
         lds_set = lds;
     }
-    hipLaunchKernelGGL((conv_kernel<BF16, MB, NB, WGM, WGN, WGK, KCH>), grid, dim3(256), lds, st, p);
+    hipLaunchKernelGGL((conv_kernel<BF16, MB, NB, WGM, WGN, WGK, KCH>), grid, dim3(256), lds, st, g);
     return hipGetLastError();
 }
 
 template <bool BF16>
-static hipError_t launch_dt(int v, const ConvParams& p, size_t lds, hipStream_t st)
+static hipError_t launch_dt(int v, const ConvGroup& p, int count, size_t lds, hipStream_t st)
 {
     switch (v) {
-    case 0: return launch_t<BF16, 1, 1, 1, 1, 4, 4>(p, lds, st);
-    case 1: return launch_t<BF16, 1, 1, 1, 1, 4, 8>(p, lds, st);
-    case 2: return launch_t<BF16, 1, 1, 1, 1, 4, 16>(p, lds, st);
-    case 3: return launch_t<BF16, 1, 2, 1, 1, 4, 4>(p, lds, st);
-    case 4: return launch_t<BF16, 1, 2, 1, 1, 4, 8>(p, lds, st);
-    case 5: return launch_t<BF16, 2, 2, 1, 1, 4, 4>(p, lds, st);
-    case 6: return launch_t<BF16, 1, 1, 2, 2, 1, 2>(p, lds, st);
-    case 7: return launch_t<BF16, 1, 1, 2, 2, 1, 4>(p, lds, st);
-    case 8: return launch_t<BF16, 1, 2, 2, 2, 1, 4>(p, lds, st);
-    case 9: return launch_t<BF16, 2, 2, 2, 2, 1, 2>(p, lds, st);
-    case 10: return launch_t<BF16, 2, 2, 2, 2, 1, 4>(p, lds, st);
-    case 11: return launch_t<BF16, 2, 4, 2, 2, 1, 4>(p, lds, st);
-    case 12: return launch_t<BF16, 2, 4, 4, 1, 1, 2>(p, lds, st);
-    case 13: return launch_t<BF16, 2, 4, 4, 1, 1, 4>(p, lds, st);
-    case 14: return launch_t<BF16, 4, 4, 2, 2, 1, 4>(p, lds, st);
-    case 15: return launch_t<BF16, 4, 4, 4, 1, 1, 2>(p, lds, st);
-    case 16: return launch_t<BF16, 4, 4, 4, 1, 1, 4>(p, lds, st);
-    case 17: return launch_t<BF16, 1, 1, 1, 1, 4, 32>(p, lds, st);
-    case 18: return launch_t<BF16, 1, 2, 1, 1, 4, 16>(p, lds, st);
-    case 19: return launch_t<BF16, 1, 1, 2, 2, 1, 1>(p, lds, st);
+    case 0: return launch_t<BF16, 1, 1, 1, 1, 4, 4>(p, count, lds, st);
+    case 1: return launch_t<BF16, 1, 1, 1, 1, 4, 8>(p, count, lds, st);
+    case 2: return launch_t<BF16, 1, 1, 1, 1, 4, 16>(p, count, lds, st);
+    case 3: return launch_t<BF16, 1, 2, 1, 1, 4, 4>(p, count, lds, st);
+    case 4: return launch_t<BF16, 1, 2, 1, 1, 4, 8>(p, count, lds, st);
+    case 5: return launch_t<BF16, 2, 2, 1, 1, 4, 4>(p, count, lds, st);
+    case 6: return launch_t<BF16, 1, 1, 2, 2, 1, 2>(p, count, lds, st);
+    case 7: return launch_t<BF16, 1, 1, 2, 2, 1, 4>(p, count, lds, st);
+    case 8: return launch_t<BF16, 1, 2, 2, 2, 1, 4>(p, count, lds, st);
+    case 9: return launch_t<BF16, 2, 2, 2, 2, 1, 2>(p, count, lds, st);
+    case 10: return launch_t<BF16, 2, 2, 2, 2, 1, 4>(p, count, lds, st);
+    case 11: return launch_t<BF16, 2, 4, 2, 2, 1, 4>(p, count, lds, st);
+    case 12: return launch_t<BF16, 2, 4, 4, 1, 1, 2>(p, count, lds, st);
+    case 13: return launch_t<BF16, 2, 4, 4, 1, 1, 4>(p, count, lds, st);
+    case 14: return launch_t<BF16, 4, 4, 2, 2, 1, 4>(p, count, lds, st);
+    case 15: return launch_t<BF16, 4, 4, 4, 1, 1, 2>(p, count, lds, st);
+    case 16: return launch_t<BF16, 4, 4, 4, 1, 1, 4>(p, count, lds, st);
+    case 17: return launch_t<BF16, 1, 1, 1, 1, 4, 32>(p, count, lds, st);
+    case 18: return launch_t<BF16, 1, 2, 1, 1, 4, 16>(p, count, lds, st);
+    case 19: return launch_t<BF16, 1, 1, 2, 2, 1, 1>(p, count, lds, st);
     default: return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_conv(int v, bool bf16, const ConvParams& p, hipStream_t st)
+// Members beyond the first may differ from it only in the ConvMember fields.
+static bool same_shape(const ConvParams& a, const ConvParams& b)
 {
-    const size_t lds = conv_lds_bytes(v, bf16, p);
-    return bf16 ? launch_dt<true>(v, p, lds, st) : launch_dt<false>(v, p, lds, st);
+    return a.in_C == b.in_C && a.in_elem == b.in_elem &&
+           a.in_act == b.in_act && a.split == b.split && a.CB == b.CB && a.n_cb == b.n_cb && a.d == b.d &&
+           a.N == b.N && a.NB16 == b.NB16 && a.out_C == b.out_C && a.out_elem == b.out_elem &&
+           a.out_act == b.out_act && a.u == b.u && a.n_mean == b.n_mean && a.B == b.B && a.F == b.F &&
+           a.tiles_t == b.tiles_t && a.clock == b.clock && a.in_fpt == b.in_fpt && a.slope == b.slope &&
+           (a.res == nullptr) == (b.res == nullptr) && (a.n_mean == 0 || (a.mean_R == b.mean_R &&
+           a.mean[0] == b.mean[0] && a.mean[1] == b.mean[1] && a.mean[2] == b.mean[2]));
+}
+
+hipError_t launch_conv(int v, bool bf16, const ConvParams* ps, int count, hipStream_t st)
+{
+    if (count < 1 || count > kMaxGroup) return hipErrorInvalidValue;
+    ConvGroup g{};
+    g.p = ps[0];
+    size_t lds = conv_lds_bytes(v, bf16, ps[0]);
+    for (int i = 1; i < count; i++) {
+        if (!same_shape(ps[0], ps[i])) return hipErrorInvalidValue;
+        g.m[i - 1] = ConvMember{ps[i].in, ps[i].in_R, ps[i].wp, ps[i].bias, ps[i].out,
+                                ps[i].out_R, ps[i].res, ps[i].res_R, ps[i].k};
+        const size_t l = conv_lds_bytes(v, bf16, ps[i]);
+        lds = l > lds ? l : lds;
+    }
+    return bf16 ? launch_dt<true>(v, g, count, lds, st) : launch_dt<false>(v, g, count, lds, st);
 }
 
 // ----------------------------------------------------------- embedding

@@ -45,6 +45,15 @@ struct ConvOp {
     int CB = 0, n_cb = 0, NB16 = 0;
     int variant = 0;
     int level_in = 0;
+    int stage = -1, branch = -1, dil_i = -1, half = 0;   // resblock position (-1: not a resblock conv)
+};
+
+// One kernel launch of a chunk step.
+enum LaunchKind { L_EMBED, L_CONV, L_SPECTRUM, L_OLA, L_CLOCK };
+struct Launch {
+    LaunchKind kind;
+    std::vector<int> convs;   // members of a conv launch (same tile shape; parallel branches)
+    std::string name;
 };
 
 thread_local std::string g_init_error;
@@ -81,6 +90,7 @@ struct dc_state {
     std::vector<std::string> ring_names;
     std::vector<int> ring_ctx;
     std::vector<ConvOp> convs;
+    std::vector<Launch> launches;
     int ring_E = -1, ring_S = -1, ring_G = -1;
     int levels = 0;
     int64_t fpt[DC_MAX_STAGES + 2] = {};
@@ -412,6 +422,10 @@ static void build_network(dc_state* s)
                     ConvOp& op = conv(pn + ".d" + std::to_string(i) + ".c1", zin, H, co, co, kj, c.dil[i], st + 1);
                     op.in_act = 1;
                     op.out_act = 1;
+                    op.stage = st;
+                    op.branch = j;
+                    op.dil_i = i;
+                    op.half = 1;
                     need_ctx(s, zin, (kj - 1) * c.dil[i]);
                 }
                 const bool last = i == c.n_dil - 1;
@@ -422,6 +436,10 @@ static void build_network(dc_state* s)
                     Z = add_ring(s, pn + ".z" + std::to_string(i), co, kF32, st + 1);
                 ConvOp& op = conv(pn + ".d" + std::to_string(i) + ".c2", H, Z, co, co, kj, 1, st + 1);
                 op.res = zin;
+                op.stage = st;
+                op.branch = j;
+                op.dil_i = i;
+                op.half = 2;
                 need_ctx(s, H, kj - 1);
                 if (Z == X) {
                     op.n_mean = (int)zlast.size();
@@ -448,12 +466,73 @@ static void build_network(dc_state* s)
     need_ctx(s, s->ring_G, c.n_fft / c.hop - 1);
 }
 
+// The launch schedule of a chunk step.  Resblock convs at the same position
+// (stage, dilation, first or second conv) of the parallel branches run as
+// one launch; the branch-mean conv runs after the other branches' last convs
+// it reads.  Members share the tile shape of the member with the widest left
+// context (their arithmetic is the same: K partitions and channel block
+// depend only on the channels).
+static void build_schedule(dc_state* s)
+{
+    const dc_cfg& c = s->cfg;
+    s->launches.push_back({L_EMBED, {}, "embed"});
+    auto add_group = [&](std::vector<int> m, const std::string& name) {
+        int widest = m[0];
+        for (int i : m)
+            if ((s->convs[i].k - 1) * s->convs[i].d > (s->convs[widest].k - 1) * s->convs[widest].d) widest = i;
+        const TileShape tw = tile_variant(s->convs[widest].variant);
+        bool same = true;
+        for (int i : m) {
+            const TileShape ti = tile_variant(s->convs[i].variant);
+            same = same && ti.WGK == tw.WGK && ti.KCH == tw.KCH;
+        }
+        if (!same || m.size() > (size_t)kMaxGroup) {
+            for (int i : m) s->launches.push_back({L_CONV, {i}, s->convs[i].name});
+            return;
+        }
+        for (int i : m) s->convs[i].variant = s->convs[widest].variant;
+        s->launches.push_back({L_CONV, m, name});
+    };
+    const int nconv = (int)s->convs.size();
+    int i = 0;
+    while (i < nconv) {
+        const ConvOp& op = s->convs[i];
+        if (op.stage < 0) {
+            s->launches.push_back({L_CONV, {i}, op.name});
+            i++;
+            continue;
+        }
+        const int st = op.stage;
+        std::vector<int> region;
+        while (i < nconv && s->convs[i].stage == st) region.push_back(i++);
+        const std::string sn = "s" + std::to_string(st);
+        for (int di = 0; di < c.n_dil; di++)
+            for (int half = 1; half <= 2; half++) {
+                std::vector<int> m;
+                for (int j = 0; j < c.n_rb; j++)
+                    for (int r : region)
+                        if (s->convs[r].branch == j && s->convs[r].dil_i == di && s->convs[r].half == half) m.push_back(r);
+                const std::string pos = ".d" + std::to_string(di) + ".c" + std::to_string(half);
+                const bool mean = half == 2 && di == c.n_dil - 1 && c.n_rb > 1;
+                if (!mean) {
+                    add_group(m, sn + ".rb*" + pos);
+                } else {
+                    add_group(std::vector<int>(m.begin(), m.end() - 1), sn + ".rb<" + std::to_string(c.n_rb - 1) + pos);
+                    add_group({m.back()}, sn + ".rb" + std::to_string(c.n_rb - 1) + pos + ".mean");
+                }
+            }
+    }
+    s->launches.push_back({L_SPECTRUM, {}, "spectrum"});
+    s->launches.push_back({L_OLA, {}, "ola"});
+    s->launches.push_back({L_CLOCK, {}, "clock"});
+}
+
 // ------------------------------------------------------------ one chunk step
 //
 // A step is a fixed list of launches ("layers"): 0 embed, 1..C the convs in
 // network order, then spectrum, overlap-add and clock.
 
-static int layer_count(const dc_state* s) { return (int)s->convs.size() + 4; }
+static int layer_count(const dc_state* s) { return (int)s->launches.size(); }
 
 static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
 {
@@ -502,22 +581,28 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
 static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
 {
     const dc_cfg& c = s->cfg;
-    const int nc = (int)s->convs.size();
     const int L = c.n_stages;
     const int FL = (int)(n * s->fpt[L]);
-    if (i == 0)
+    const Launch& la = s->launches[i];
+    switch (la.kind) {
+    case L_EMBED:
         return launch_embed(s->tok, n, c.batch, s->emb, c.vocab, c.embed, s->rings[s->ring_E].elem,
                             c.frames_per_token, s->rings[s->ring_E], s->clock, s->err, st);
-    if (i <= nc) {
-        const ConvOp& op = s->convs[i - 1];
-        return launch_conv(op.variant, op.bf16, conv_params(s, op, n), st);
+    case L_CONV: {
+        ConvParams ps[kMaxGroup];
+        const int cnt = (int)la.convs.size();
+        for (int m = 0; m < cnt; m++) ps[m] = conv_params(s, s->convs[la.convs[m]], n);
+        const ConvOp& op = s->convs[la.convs[0]];
+        return launch_conv(op.variant, op.bf16, ps, cnt, st);
     }
-    if (i == nc + 1)
+    case L_SPECTRUM:
         return launch_spectrum((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL,
                                s->table, s->rings[s->ring_G], s->clock, s->fpt[L], st);
-    if (i == nc + 2)
+    case L_OLA:
         return launch_ola(s->rings[s->ring_G], c.batch, FL, c.hop, c.n_fft, s->audio, s->clock, s->fpt[L], st);
-    return launch_clock(s->clock, n, st);
+    default:
+        return launch_clock(s->clock, n, st);
+    }
 }
 
 static hipError_t enqueue_step(dc_state* s, int n, hipStream_t st)
@@ -570,6 +655,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
         op.variant = pick_variant(s, op);
         set_blocks(op);
     }
+    build_schedule(s);
 
     // ---- arena layout: constants and weights, then rings, then I/O buffers
     const float* blob = (const float*)weights_blob;
@@ -664,7 +750,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     s->st.arena_bytes = (int64_t)s->arena_bytes;
     s->st.carry_bytes = carry;
     s->st.ring_bytes = (int64_t)(s->ring_end - s->ring_begin);
-    s->st.kernels_per_step = (int32_t)s->convs.size() + 4;
+    s->st.kernels_per_step = (int32_t)s->launches.size();
 
     e = hipMemcpy(s->arena, host.data(), weights_end, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemsetAsync(s->arena + weights_end, 0, s->arena_bytes - weights_end, s->stream);
@@ -850,47 +936,57 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
     if (!s || !out || i < 0 || i >= layer_count(s)) return DC_EINVAL;
     const dc_cfg& c = s->cfg;
     std::memset(out, 0, sizeof *out);
-    const int nc = (int)s->convs.size();
     const int n = c.chunk_tokens;
     const double B = c.batch;
     const int L = c.n_stages;
     const double FL = (double)n * s->fpt[L];
-    auto set = [&](const std::string& name, const std::string& kernel) {
-        std::snprintf(out->name, sizeof out->name, "%s", name.c_str());
+    const Launch& la = s->launches[i];
+    auto set = [&](const std::string& kernel) {
+        std::snprintf(out->name, sizeof out->name, "%s", la.name.c_str());
         std::snprintf(out->kernel, sizeof out->kernel, "%s", kernel.c_str());
     };
-    if (i == 0) {
+    switch (la.kind) {
+    case L_EMBED: {
         const Ring& E = s->rings[s->ring_E];
         const double es = E.elem == kBF16 ? 2 : 4;
         const double F = (double)n * c.frames_per_token;
-        set("embed", "dc::embed_kernel");
+        set("dc::embed_kernel");
         out->bytes = B * n * 4 + B * n * c.embed * es + B * F * c.embed * es;
-    } else if (i <= nc) {
-        const ConvOp& op = s->convs[i - 1];
-        const TileShape t = tile_variant(op.variant);
-        set(op.name, "dc::conv_kernel<" + std::string(op.bf16 ? "true" : "false") + ", " + std::to_string(t.MB) +
-                         ", " + std::to_string(t.NB) + ", " + std::to_string(t.WGM) + ", " + std::to_string(t.WGN) +
-                         ", " + std::to_string(t.WGK) + ", " + std::to_string(t.KCH) + ">");
-        const double F = (double)n * s->fpt[op.level_in];
-        const Ring& in = s->rings[op.in];
-        const Ring& o = s->rings[op.out];
-        out->rows = (int64_t)(B * F);
-        out->cols = op.N;
-        out->depth = (int64_t)op.k * op.Ci;
-        out->flops = 2.0 * B * F * op.N * op.Ci * op.k;
-        const double wes = op.bf16 ? 2 : 4;
-        const double ies = in.elem == kBF16 ? 2 : 4, oes = o.elem == kBF16 ? 2 : 4;
-        const double Fo = F * op.u;
-        out->bytes = (double)op.N * op.Ci * op.k * wes + B * (F + (op.k - 1) * op.d) * op.Ci * ies +
-                     B * Fo * o.C * oes + (op.res >= 0 ? B * Fo * o.C * 4 : 0) + op.n_mean * B * Fo * o.C * 4;
-    } else if (i == nc + 1) {
-        set("spectrum", "dc::spectrum_kernel");
+        break;
+    }
+    case L_CONV: {
+        const ConvOp& op0 = s->convs[la.convs[0]];
+        const TileShape t = tile_variant(op0.variant);
+        set("dc::conv_kernel<" + std::string(op0.bf16 ? "true" : "false") + ", " + std::to_string(t.MB) + ", " +
+            std::to_string(t.NB) + ", " + std::to_string(t.WGM) + ", " + std::to_string(t.WGN) + ", " +
+            std::to_string(t.WGK) + ", " + std::to_string(t.KCH) + ">");
+        for (int ci : la.convs) {   // the members' work and compulsory bytes add up
+            const ConvOp& op = s->convs[ci];
+            const double F = (double)n * s->fpt[op.level_in];
+            const Ring& in = s->rings[op.in];
+            const Ring& o = s->rings[op.out];
+            out->rows = (int64_t)(B * F);
+            out->cols = op.N;
+            out->depth += (int64_t)op.k * op.Ci;
+            out->flops += 2.0 * B * F * op.N * op.Ci * op.k;
+            const double wes = op.bf16 ? 2 : 4;
+            const double ies = in.elem == kBF16 ? 2 : 4, oes = o.elem == kBF16 ? 2 : 4;
+            const double Fo = F * op.u;
+            out->bytes += (double)op.N * op.Ci * op.k * wes + B * (F + (op.k - 1) * op.d) * op.Ci * ies +
+                          B * Fo * o.C * oes + (op.res >= 0 ? B * Fo * o.C * 4 : 0) + op.n_mean * B * Fo * o.C * 4;
+        }
+        break;
+    }
+    case L_SPECTRUM:
+        set("dc::spectrum_kernel");
         out->bytes = B * FL * (2 * (c.n_fft / 2 + 1) + c.n_fft) * 4;
-    } else if (i == nc + 2) {
-        set("ola", "dc::ola_kernel");
+        break;
+    case L_OLA:
+        set("dc::ola_kernel");
         out->bytes = B * FL * c.n_fft * 4 + B * FL * c.hop * 4;
-    } else {
-        set("clock", "dc::clock_kernel");
+        break;
+    default:
+        set("dc::clock_kernel");
         out->bytes = 16;
     }
     return DC_OK;

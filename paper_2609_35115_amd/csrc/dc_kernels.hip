@@ -255,18 +255,19 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
 #pragma unroll
         for (int j = 0; j < NB; j++) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // Weight fragments of this wave for tap j of channel block cb.
+    // Weight fragments of this wave for tap j of channel block cb.  Column
+    // blocks past the layer's last one re-read that block (unconditional
+    // loads keep the compiler's wait counts exact); their columns are never
+    // stored.
+    int nblk[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; nb++) nblk[nb] = nblk0 + nb < p.NB16 ? nblk0 + nb : p.NB16 - 1;
     auto load_tap = [&](int cb, int j, Frag (&w)[KPW][NB]) {
-        const size_t base = (size_t)(cb * k + j) * KCH * p.NB16;
+        const Frag* wt = wp + (size_t)(cb * k + j) * KCH * p.NB16 * 64 + lane;
 #pragma unroll
         for (int ki = 0; ki < KPW; ki++)
 #pragma unroll
-            for (int nb = 0; nb < NB; nb++) {
-                const int kc = ki * WGK + wk;
-                Frag z = {};
-                if (nblk0 + nb < p.NB16) z = wp[(base + (size_t)kc * p.NB16 + nblk0 + nb) * 64 + lane];
-                w[ki][nb] = z;
-            }
+            for (int nb = 0; nb < NB; nb++) w[ki][nb] = wt[((size_t)(ki * WGK + wk) * p.NB16 + nblk[nb]) * 64];
     };
 
     // MFMAs of tap j: weights are the A operand, frames the B operand.  This
@@ -352,11 +353,17 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
         load_operand(cb);
         __syncthreads();
         int j = 0;
+        // scheduling barriers keep each tap's loads ahead of the previous
+        // tap's MFMAs (the scheduler would otherwise sink them to their use)
         for (; j + 1 < k; j += 2) {
             load_tap(cb, j + 1, w1);
+            __builtin_amdgcn_sched_barrier(0);
             compute_tap(j, w0);
+            __builtin_amdgcn_sched_barrier(0);
             load_tap(cb, j + 2 < k ? j + 2 : j + 1, w0);
+            __builtin_amdgcn_sched_barrier(0);
             compute_tap(j + 1, w1);
+            __builtin_amdgcn_sched_barrier(0);
         }
         if (j < k) compute_tap(j, w0);
     }

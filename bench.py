@@ -104,8 +104,8 @@ def roofline(layers, us, dtype):
         g["launches"] += 1
     name, g = max(groups.items(), key=lambda kv: kv[1]["us"])
     step_us = sum(us)
-    conv = name.startswith("dc::conv_kernel")
-    op = "bf16" if "<true" in name else "f32"
+    conv = name.startswith(("dc::conv_kernel", "dc::pair_kernel"))   # MFMA kernels (a fused pair is bf16)
+    op = "bf16" if "<true" in name or name.startswith("dc::pair_kernel") else "f32"
     if conv and g["flops"] / g["bytes"] > PEAK[op] * 1e12 / (PEAK["hbm"] * 1e9):
         bound, achieved, peak, unit = "mfma", g["flops"] / (g["us"] * 1e-6) / 1e12, PEAK[op], "TFLOP/s"
     else:

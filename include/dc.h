@@ -54,7 +54,8 @@ typedef enum { DC_F32 = 0, DC_BF16 = 1 } dc_dtype;
 
 enum {
     DC_HOST_PTRS = 1u << 0, /* tokens/audio are host pointers; each call is synchronous          */
-    DC_NO_GRAPH = 1u << 1   /* never capture or replay a graph; always launch kernels directly   */
+    DC_NO_GRAPH = 1u << 1,  /* never capture or replay a graph; always launch kernels directly   */
+    DC_NO_FUSE = 1u << 2    /* run every resblock conv as its own launch (no fused pairs)        */
 };
 
 /*
@@ -81,7 +82,7 @@ typedef struct dc_cfg {
     int32_t batch;                       /* B independent streams sharing the weights             */
     int32_t chunk_tokens;                /* the chunk shape captured as a graph                   */
     int32_t max_tokens;                  /* largest n accepted by dc_decode_chunk                 */
-    uint32_t flags;                      /* DC_HOST_PTRS | DC_NO_GRAPH                            */
+    uint32_t flags;                      /* DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE               */
     int32_t tile_variant;                /* 0: automatic; v > 0 forces tile shape v-1 everywhere
                                             it fits (results are identical by construction)      */
     void* hip_stream;                    /* hipStream_t all work is ordered on; NULL: own stream  */
@@ -179,7 +180,9 @@ dc_status dc_get_stats(const dc_state* s, dc_stats* out);
  * with absolute index [frame0, frame0 + nframes) of that ring into host
  * memory as float32 [nframes][C]; *channels receives C.  Only frames still held
  * by the ring (the last call's frames and the carried left context) are
- * readable; others give DC_ERANGE.  Synchronous.
+ * readable; others give DC_ERANGE.  Where a resblock pair runs fused (bf16,
+ * batch >= 8, 64 or 128 channels, unless DC_NO_FUSE), its h stays on chip and
+ * the "h" intermediate holds no frames (DC_ERANGE).  Synchronous.
  */
 int32_t dc_tap_find(const dc_state* s, const char* name);
 dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32_t nframes,
@@ -188,7 +191,8 @@ dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32
 /*
  * Measurement (roofline reporting).  A chunk step is a fixed sequence of
  * kernel launches ("layers": embed, each conv / transposed conv -- the
- * convs at one position of the parallel resblock branches share a launch --,
+ * convs at one position of the parallel resblock branches share a launch,
+ * and a fused resblock pair is one launch --,
  * head, spectrum, overlap-add, clock).  dc_layer_info describes launch i at
  * n = chunk_tokens: its kernel (the demangled name a profiler shows), the
  * GEMM shape of a conv (rows = batch * frames, cols, depth = taps * input

@@ -96,6 +96,61 @@ struct TileShape {
     int S() const { return WGK; }
 };
 
+// One fused resblock pair (bf16 operands): h = LeakyReLU(conv_k,d(LeakyReLU(z)) + b1)
+// stays in LDS, and out = z + conv_k,1(h) + b2 (optionally averaged with
+// earlier branch results).  A block owns BM frames x all C channels; the
+// first conv covers the BM + k - 1 frames the second one reads.
+struct PairParams {
+    const float* z;       // fp32 ring: the first conv's input and the residual
+    int64_t z_R;
+    const void* w1;       // packed like a conv with channel block C (one partition)
+    const float* b1;
+    const void* w2;
+    const float* b2;
+    float* out;           // fp32 ring
+    int64_t out_R;
+    int k, d;             // taps; dilation of the first conv (the second has 1)
+    int C;                // channels in and out of both convs
+    int NB16;             // C / 16
+    const float* mean[3]; // earlier branch results (fp32 rings, out geometry)
+    int64_t mean_R;
+    int n_mean;
+    int B, F, tiles_t;
+    const int64_t* clock;
+    const int64_t* start; // [B]: tokens decoded when each stream last started
+    int64_t in_fpt;
+    float slope;
+};
+struct PairMember {
+    const float* z;
+    int64_t z_R;
+    const void* w1;
+    const float* b1;
+    const void* w2;
+    const float* b2;
+    float* out;
+    int64_t out_R;
+    int k;
+};
+struct PairGroup {
+    PairParams p;
+    PairMember m[kMaxGroup - 1];
+};
+
+// Fused-pair shapes: MB x NB blocks of 16x16 per wave for the second conv,
+// WGM x WGN waves, channel block KCH chunks (C = 32 KCH), MB1 16-row blocks
+// per wave for the first conv (16 MB1 WGM >= BM + k - 1).
+struct PairShape {
+    int MB, NB, WGM, WGN, KCH, MB1;
+    int BM() const { return 16 * MB * WGM; }
+    int C() const { return 32 * KCH; }
+    int M1() const { return 16 * MB1 * WGM; }
+};
+int num_pair_variants();
+PairShape pair_variant(int v);
+size_t pair_lds_bytes(int v, int k_max, int d);
+hipError_t launch_pair(int v, const PairParams* ps, int count, hipStream_t st);
+
 // The tile shapes compiled for each operand type.
 int num_tile_variants();
 TileShape tile_variant(int v);
@@ -118,5 +173,6 @@ hipError_t launch_ola(Ring g, int B, int F, int hop, int n_fft, float* pcm, cons
                       int64_t fpt, hipStream_t st);
 
 hipError_t launch_clock(int64_t* clock, int n, hipStream_t st);
+hipError_t launch_mark_start(int64_t* start, int b, const int64_t* clock, hipStream_t st);
 
 }  // namespace dc

@@ -547,6 +547,275 @@ hipError_t launch_conv(int v, bool bf16, const ConvParams* ps, int count, hipStr
     return bf16 ? launch_dt<true>(v, g, count, lds, st) : launch_dt<false>(v, g, count, lds, st);
 }
 
+// ------------------------------------------------------ fused resblock pair
+//
+// One block: output frames [t0, t0 + BM) x all C channels of one branch's
+// pair at one dilation.  The operand rows of the first conv go to LDS once;
+// its output h for frames [t0 - (k-1), t0 + BM) goes to LDS as bf16 (zero for
+// frames before the stream start, as in a freshly reset ring); the second
+// conv reads h from LDS and adds bias and the fp32 residual.  Both convs use
+// one K partition and a channel block of all C channels, i.e. the arithmetic
+// of the unfused launches with those parameters, bit for bit.
+
+template <int MB, int NB, int WGM, int WGN, int KCH, int MB1>
+__global__ __launch_bounds__(256) void pair_kernel(const PairGroup g)
+{
+    const PairParams& p = g.p;
+    const float* z = p.z;
+    int z_R = (int)p.z_R;
+    const void* w1p = p.w1;
+    const float* b1 = p.b1;
+    const void* w2p = p.w2;
+    const float* b2 = p.b2;
+    float* out = p.out;
+    int out_R = (int)p.out_R;
+    int k = p.k;
+    if (blockIdx.z > 0) {
+        const PairMember& m = g.m[blockIdx.z - 1];
+        z = m.z;
+        z_R = (int)m.z_R;
+        w1p = m.w1;
+        b1 = m.b1;
+        w2p = m.w2;
+        b2 = m.b2;
+        out = m.out;
+        out_R = (int)m.out_R;
+        k = m.k;
+    }
+    constexpr int KQ = 32;
+    constexpr int C = KQ * KCH;
+    constexpr int BM = 16 * MB * WGM, BN = 16 * NB * WGN;
+    constexpr int LDW = C + OpT<true>::PAD;
+    constexpr int VPR = C / 8;
+    static_assert(WGM * WGN == 4 && BN == C, "pair tile shape");
+    using Frag = u32x4;
+
+    const int H1 = (k - 1) * p.d, H2 = k - 1;
+    const int rowsA = BM + H1 + H2;            // first conv operand rows
+    const int rows1 = BM + H2;                 // first conv output rows (h)
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t* A = reinterpret_cast<uint16_t*>(smem);
+    uint16_t* Hs = A + (rowsA + 16) * LDW;     // 16 spare rows: partial row blocks read past rowsA
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WGM, wn = wave / WGM;
+    const int b = blockIdx.x / p.tiles_t;
+    const int t0 = (blockIdx.x - b * p.tiles_t) * BM;
+    const int64_t tau0 = p.clock[0] * p.in_fpt;
+    const int64_t start_f = p.start[b] * p.in_fpt;   // this stream's first frame since its reset
+    const int fl = lane & 15, cg = (lane >> 4) * 4;
+
+    // ---- first conv operand: LeakyReLU(z) for frames [t0 - H1 - H2, t0 + BM)
+    {
+        const int base = (int)ring_slot(tau0 + t0 - H1 - H2, z_R);
+        for (int v = tid; v < rowsA * VPR; v += 256) {
+            const int r = v / VPR, c8 = (v - r * VPR) * 8;
+            float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            if (t0 - H1 - H2 + r < p.F) {
+                const f32x4* q = (const f32x4*)(z + ((size_t)b * z_R + slot_add(base, r, z_R)) * C + c8);
+                const f32x4 a0 = q[0], a1 = q[1];
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    x[e] = lrelu(a0[e], p.slope);
+                    x[4 + e] = lrelu(a1[e], p.slope);
+                }
+            }
+            store8_lds(A + r * LDW + c8, x);
+        }
+    }
+
+    // weight fragments of tap j (channel block of all C channels, one partition)
+    const int nblk0 = wn * NB;
+    auto load_tap = [&](const Frag* wp, int j, Frag (&w)[KCH][NB]) {
+        const Frag* wt = wp + (size_t)j * KCH * p.NB16 * 64 + lane;
+#pragma unroll
+        for (int ki = 0; ki < KCH; ki++)
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++) w[ki][nb] = wt[((size_t)ki * p.NB16 + nblk0 + nb) * 64];
+    };
+    // the taps of one conv in pairs, weights one tap ahead (as in conv_kernel)
+    auto run_taps = [&](const Frag* wp, auto&& tap) {
+        Frag w0[KCH][NB], w1[KCH][NB];
+        load_tap(wp, 0, w0);
+        int j = 0;
+        for (; j + 1 < k; j += 2) {
+            load_tap(wp, j + 1, w1);
+            __builtin_amdgcn_sched_barrier(0);
+            tap(j, w0);
+            __builtin_amdgcn_sched_barrier(0);
+            load_tap(wp, j + 2 < k ? j + 2 : j + 1, w0);
+            __builtin_amdgcn_sched_barrier(0);
+            tap(j + 1, w1);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (j < k) tap(j, w0);
+    };
+    __syncthreads();
+
+    // ---- first conv: h rows in 16-row blocks wm, wm + WGM, ... (interleaved)
+    {
+        f32x4 acc[MB1][NB];
+#pragma unroll
+        for (int i = 0; i < MB1; i++)
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++) acc[i][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const uint16_t* a_lane = A + fl * LDW + (lane >> 4) * 8;
+        auto tap1 = [&](int j, const Frag (&w)[KCH][NB]) {
+            const uint16_t* aj = a_lane + j * p.d * LDW;
+#pragma unroll
+            for (int ki = 0; ki < KCH; ki++) {
+#pragma unroll
+                for (int i = 0; i < MB1; i++) {
+                    const int rb = wm + WGM * i;
+                    if (16 * rb >= rows1) break;
+                    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(aj + rb * 16 * LDW + ki * KQ));
+#pragma unroll
+                    for (int nb = 0; nb < NB; nb++)
+                        acc[i][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[ki][nb]),
+                                                                            a, acc[i][nb], 0, 0, 0);
+                }
+            }
+        };
+        run_taps(reinterpret_cast<const Frag*>(w1p), tap1);
+        f32x4 bias[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++) bias[nb] = *(const f32x4*)(b1 + (nblk0 + nb) * 16 + cg);
+#pragma unroll
+        for (int i = 0; i < MB1; i++) {
+            const int rb = wm + WGM * i;
+            if (16 * rb >= rows1) break;
+            const int r1 = rb * 16 + fl;
+            const bool before = tau0 + t0 - H2 + r1 < start_f;   // h of a frame before the stream start is 0
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++) {
+                f32x4 v = acc[i][nb] + bias[nb];
+#pragma unroll
+                for (int e = 0; e < 4; e++) v[e] = before ? 0.f : lrelu(v[e], p.slope);
+                typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+                const u32x2 hv = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                *(u32x2*)(Hs + r1 * LDW + (nblk0 + nb) * 16 + cg) = hv;
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- second conv: output rows wm*16*MB .. (contiguous), h from LDS
+    f32x4 acc[MB][NB];
+#pragma unroll
+    for (int i = 0; i < MB; i++)
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++) acc[i][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint16_t* h_lane = Hs + (wm * 16 * MB + fl) * LDW + (lane >> 4) * 8;
+    auto tap2 = [&](int j, const Frag (&w)[KCH][NB]) {
+        const uint16_t* hj = h_lane + j * LDW;
+#pragma unroll
+        for (int ki = 0; ki < KCH; ki++) {
+            bf16x8_t a[MB];
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+                a[mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(hj + mb * 16 * LDW + ki * KQ));
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++)
+                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[ki][nb]),
+                                                                         a[mb], acc[mb][nb], 0, 0, 0);
+        }
+    };
+    run_taps(reinterpret_cast<const Frag*>(w2p), tap2);
+
+    // ---- epilogue: bias, residual z, branch mean; fp32 through the output ring
+    const int out_s = (int)ring_slot(tau0 + t0, out_R);
+    const int res_s = (int)ring_slot(tau0 + t0, z_R);
+    const int mean_s = p.n_mean ? (int)ring_slot(tau0 + t0, p.mean_R) : 0;
+    f32x4 bias[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; nb++) bias[nb] = *(const f32x4*)(b2 + (nblk0 + nb) * 16 + cg);
+#pragma unroll
+    for (int mb = 0; mb < MB; mb++) {
+        const int tl = wm * 16 * MB + mb * 16 + fl;
+        if (t0 + tl >= p.F) continue;
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++) {
+            const int n4 = (nblk0 + nb) * 16 + cg;
+            f32x4 v = acc[mb][nb] + bias[nb];
+            v = *(const f32x4*)(z + ((size_t)b * z_R + slot_add(res_s, tl, z_R)) * C + n4) + v;
+            if (p.n_mean) {
+                const size_t mo = ((size_t)b * p.mean_R + slot_add(mean_s, tl, (int)p.mean_R)) * C + n4;
+                f32x4 x = *(const f32x4*)(p.mean[0] + mo);
+                for (int i = 1; i < p.n_mean; i++) x = x + *(const f32x4*)(p.mean[i] + mo);
+                x = x + v;
+                const float J = (float)(p.n_mean + 1);
+                v = f32x4{x[0] / J, x[1] / J, x[2] / J, x[3] / J};
+            }
+            *(f32x4*)(out + ((size_t)b * out_R + slot_add(out_s, tl, out_R)) * C + n4) = v;
+        }
+    }
+}
+
+// Fused-pair shapes (ids of this table).
+static const PairShape kPairs[] = {
+    // MB NB WGM WGN KCH MB1
+    {2, 2, 2, 2, 2, 3},   // 0: C = 64, 64 frames per block (first conv: 96 rows)
+    {4, 2, 2, 2, 2, 5},   // 1: C = 64, 128 frames per block (160 rows)
+    {4, 2, 1, 4, 4, 5},   // 2: C = 128, 64 frames per block (80 rows)
+};
+
+int num_pair_variants() { return (int)(sizeof(kPairs) / sizeof(kPairs[0])); }
+PairShape pair_variant(int v) { return kPairs[v]; }
+
+size_t pair_lds_bytes(int v, int k_max, int d)
+{
+    const PairShape& t = kPairs[v];
+    const int ldw = t.C() + OpT<true>::PAD;
+    const int rowsA = t.BM() + (k_max - 1) * d + (k_max - 1);
+    return ((size_t)(rowsA + 16) + t.M1()) * ldw * 2;
+}
+
+template <int MB, int NB, int WGM, int WGN, int KCH, int MB1>
+static hipError_t launch_pair_t(const PairGroup& g, int count, size_t lds, hipStream_t st)
+{
+    const PairParams& p = g.p;
+    dim3 grid((unsigned)(p.B * p.tiles_t), 1u, (unsigned)count);
+    static size_t lds_set = 64 * 1024;
+    if (lds > lds_set) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&pair_kernel<MB, NB, WGM, WGN, KCH, MB1>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        lds_set = lds;
+    }
+    hipLaunchKernelGGL((pair_kernel<MB, NB, WGM, WGN, KCH, MB1>), grid, dim3(256), lds, st, g);
+    return hipGetLastError();
+}
+
+hipError_t launch_pair(int v, const PairParams* ps, int count, hipStream_t st)
+{
+    if (count < 1 || count > kMaxGroup || v < 0 || v >= num_pair_variants()) return hipErrorInvalidValue;
+    const PairShape t = kPairs[v];
+    PairGroup g{};
+    g.p = ps[0];
+    int k_max = ps[0].k;
+    for (int i = 1; i < count; i++) {
+        const PairParams& a = ps[0];
+        const PairParams& q = ps[i];
+        if (q.d != a.d || q.C != a.C || q.NB16 != a.NB16 || q.B != a.B || q.F != a.F || q.tiles_t != a.tiles_t ||
+            q.n_mean != a.n_mean || q.clock != a.clock || q.start != a.start || q.in_fpt != a.in_fpt ||
+            q.slope != a.slope)
+            return hipErrorInvalidValue;
+        g.m[i - 1] = PairMember{q.z, q.z_R, q.w1, q.b1, q.w2, q.b2, q.out, q.out_R, q.k};
+        k_max = q.k > k_max ? q.k : k_max;
+    }
+    if (ps[0].C != t.C() || t.M1() < t.BM() + k_max - 1) return hipErrorInvalidValue;
+    const size_t lds = pair_lds_bytes(v, k_max, ps[0].d);
+    switch (v) {
+    case 0: return launch_pair_t<2, 2, 2, 2, 2, 3>(g, count, lds, st);
+    case 1: return launch_pair_t<4, 2, 2, 2, 2, 5>(g, count, lds, st);
+    case 2: return launch_pair_t<4, 2, 1, 4, 4, 5>(g, count, lds, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 // ----------------------------------------------------------- embedding
 
 // E[b][tau0 + f] = table[tokens[b][f / fpt]] for f in [0, n*fpt): the token
@@ -694,6 +963,18 @@ __global__ void clock_kernel(int64_t* clock, int n)
 hipError_t launch_clock(int64_t* clock, int n, hipStream_t st)
 {
     hipLaunchKernelGGL(clock_kernel, dim3(1), dim3(64), 0, st, clock, n);
+    return hipGetLastError();
+}
+
+// start[b] = the clock (in stream order): stream b restarts here.
+__global__ void mark_start_kernel(int64_t* start, int b, const int64_t* clock)
+{
+    if (threadIdx.x == 0) start[b] = clock[0];
+}
+
+hipError_t launch_mark_start(int64_t* start, int b, const int64_t* clock, hipStream_t st)
+{
+    hipLaunchKernelGGL(mark_start_kernel, dim3(1), dim3(64), 0, st, start, b, clock);
     return hipGetLastError();
 }
 

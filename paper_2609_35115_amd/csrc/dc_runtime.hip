@@ -46,14 +46,17 @@ struct ConvOp {
     int variant = 0;
     int level_in = 0;
     int stage = -1, branch = -1, dil_i = -1, half = 0;   // resblock position (-1: not a resblock conv)
+    int partner = -1;    // fused pair: the other conv of the pair (h stays on chip)
 };
 
 // One kernel launch of a chunk step.
-enum LaunchKind { L_EMBED, L_CONV, L_SPECTRUM, L_OLA, L_CLOCK };
+enum LaunchKind { L_EMBED, L_CONV, L_PAIR, L_SPECTRUM, L_OLA, L_CLOCK };
 struct Launch {
     LaunchKind kind;
-    std::vector<int> convs;   // members of a conv launch (same tile shape; parallel branches)
+    std::vector<int> convs;   // members of a conv launch (same tile shape; parallel branches);
+                              // of a pair launch, each member's first conv
     std::string name;
+    int pair_variant = 0;     // L_PAIR: fused-pair shape
 };
 
 thread_local std::string g_init_error;
@@ -89,17 +92,19 @@ struct dc_state {
     std::vector<Ring> rings;
     std::vector<std::string> ring_names;
     std::vector<int> ring_ctx;
+    std::vector<bool> ring_onchip;   // h of a fused pair: never materialised (R = 0)
     std::vector<ConvOp> convs;
     std::vector<Launch> launches;
     int ring_E = -1, ring_S = -1, ring_G = -1;
     int levels = 0;
     int64_t fpt[DC_MAX_STAGES + 2] = {};
     int64_t spt = 0;
-    size_t emb_off = 0, table_off = 0, tok_off = 0, audio_off = 0, clock_off = 0, err_off = 0;
+    size_t emb_off = 0, table_off = 0, tok_off = 0, audio_off = 0, clock_off = 0, start_off = 0, err_off = 0;
     size_t ring_begin = 0, ring_end = 0;
     int32_t* tok = nullptr;
     float* audio = nullptr;
     int64_t* clock = nullptr;
+    int64_t* start = nullptr;   // [B] tokens decoded when each stream last started
     int* err = nullptr;
     void* emb = nullptr;
     float* table = nullptr;
@@ -173,7 +178,7 @@ static std::string validate(const dc_cfg* c)
     if (c->batch < 1 || c->batch > 65536) return "batch must be in [1, 65536]";
     if (c->chunk_tokens < 1 || c->max_tokens < c->chunk_tokens) return "need 1 <= chunk_tokens <= max_tokens";
     if ((int64_t)c->max_tokens * samples_per_token(c) > (int64_t)1 << 30) return "max_tokens too large";
-    if (c->flags & ~(uint32_t)(DC_HOST_PTRS | DC_NO_GRAPH)) return "unknown flag bits";
+    if (c->flags & ~(uint32_t)(DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE)) return "unknown flag bits";
     if (c->tile_variant < 0 || c->tile_variant > num_tile_variants()) return "tile_variant out of range";
     return "";
 }
@@ -336,12 +341,32 @@ static int add_ring(dc_state* s, const std::string& name, int C, int elem, int l
     s->rings.push_back(r);
     s->ring_names.push_back(name);
     s->ring_ctx.push_back(0);
+    s->ring_onchip.push_back(false);
     return (int)s->rings.size() - 1;
 }
 
 static void need_ctx(dc_state* s, int ring, int ctx)
 {
     if (ctx > s->ring_ctx[ring]) s->ring_ctx[ring] = ctx;
+}
+
+// Resblock pairs of a stage run fused (h on chip) for bf16 with enough
+// streams to fill the machine, at the channel counts the fused kernel has
+// shapes for, unless the caller forces a tile shape or asks for no fusion.
+#ifndef DC_FUSE_MIN_BATCH
+#define DC_FUSE_MIN_BATCH 8
+#endif
+static bool fuse_stage(const dc_cfg& c, int channels)
+{
+    if (c.dtype != DC_BF16 || (c.flags & DC_NO_FUSE) || c.tile_variant != 0 || c.batch < DC_FUSE_MIN_BATCH)
+        return false;
+    int k_max = 1, d_max = 1;
+    for (int j = 0; j < c.n_rb; j++) k_max = c.rb_kernel[j] > k_max ? c.rb_kernel[j] : k_max;
+    for (int i = 0; i < c.n_dil; i++) d_max = c.dil[i] > d_max ? c.dil[i] : d_max;
+    for (int v = 0; v < num_pair_variants(); v++)
+        if (pair_variant(v).C() == channels)
+            return pair_variant(v).M1() >= pair_variant(v).BM() + k_max - 1 && pair_lds_bytes(v, k_max, d_max) <= 96 * 1024;
+    return false;
 }
 
 static void build_network(dc_state* s)
@@ -412,6 +437,7 @@ static void build_network(dc_state* s)
         }
         std::vector<int> zlast;
         int X = -1;
+        const bool fuse = fuse_stage(c, co);
         for (int j = 0; j < c.n_rb; j++) {
             const int kj = c.rb_kernel[j];
             int zin = Y;
@@ -426,7 +452,12 @@ static void build_network(dc_state* s)
                     op.branch = j;
                     op.dil_i = i;
                     op.half = 1;
-                    need_ctx(s, zin, (kj - 1) * c.dil[i]);
+                    // fused: the pair reads z back far enough for both convs
+                    need_ctx(s, zin, (kj - 1) * c.dil[i] + (fuse ? kj - 1 : 0));
+                }
+                if (fuse) {
+                    s->ring_onchip[H] = true;
+                    s->convs.back().partner = (int)s->convs.size();
                 }
                 const bool last = i == c.n_dil - 1;
                 int Z;
@@ -440,6 +471,7 @@ static void build_network(dc_state* s)
                 op.branch = j;
                 op.dil_i = i;
                 op.half = 2;
+                if (fuse) op.partner = (int)s->convs.size() - 2;
                 need_ctx(s, H, kj - 1);
                 if (Z == X) {
                     op.n_mean = (int)zlast.size();
@@ -472,6 +504,19 @@ static void build_network(dc_state* s)
 // it reads.  Members share the tile shape of the member with the widest left
 // context (their arithmetic is the same: K partitions and channel block
 // depend only on the channels).
+// Fused-pair shape for a channel count: for 64 channels the 128-frame
+// block (more reuse of each weight fragment), else the one shape there is.
+#ifndef DC_PAIR64_VARIANT
+#define DC_PAIR64_VARIANT 1
+#endif
+static int pair_shape_for(int channels)
+{
+    if (channels == 64) return DC_PAIR64_VARIANT;
+    for (int v = 0; v < num_pair_variants(); v++)
+        if (pair_variant(v).C() == channels) return v;
+    return 0;
+}
+
 static void build_schedule(dc_state* s)
 {
     const dc_cfg& c = s->cfg;
@@ -506,6 +551,32 @@ static void build_schedule(dc_state* s)
         std::vector<int> region;
         while (i < nconv && s->convs[i].stage == st) region.push_back(i++);
         const std::string sn = "s" + std::to_string(st);
+        if (s->convs[region[0]].partner >= 0) {
+            // fused pairs: one launch per dilation position (members: the
+            // branches' first convs); the branch-mean pair runs last, alone
+            const int pv = pair_shape_for(s->convs[region[0]].Ci);
+            for (int di = 0; di < c.n_dil; di++) {
+                std::vector<int> m;
+                for (int j = 0; j < c.n_rb; j++)
+                    for (int r : region)
+                        if (s->convs[r].branch == j && s->convs[r].dil_i == di && s->convs[r].half == 1) m.push_back(r);
+                const std::string pos = ".d" + std::to_string(di) + ".pair";
+                Launch la{L_PAIR, {}, "", pv};
+                if (di == c.n_dil - 1 && c.n_rb > 1) {
+                    la.convs.assign(m.begin(), m.end() - 1);
+                    la.name = sn + ".rb<" + std::to_string(c.n_rb - 1) + pos;
+                    s->launches.push_back(la);
+                    la.convs = {m.back()};
+                    la.name = sn + ".rb" + std::to_string(c.n_rb - 1) + pos + ".mean";
+                    s->launches.push_back(la);
+                } else {
+                    la.convs = m;
+                    la.name = sn + ".rb*" + pos;
+                    s->launches.push_back(la);
+                }
+            }
+            continue;
+        }
         for (int di = 0; di < c.n_dil; di++)
             for (int half = 1; half <= 2; half++) {
                 std::vector<int> m;
@@ -578,6 +649,40 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
     return p;
 }
 
+static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n)
+{
+    const dc_cfg& c = s->cfg;
+    const ConvOp& c2 = s->convs[c1.partner];
+    const Ring& z = s->rings[c1.in];
+    const Ring& o = s->rings[c2.out];
+    PairParams p{};
+    p.z = (const float*)z.ptr;
+    p.z_R = z.R;
+    p.w1 = s->arena + c1.w_off;
+    p.b1 = (const float*)(s->arena + c1.b_off);
+    p.w2 = s->arena + c2.w_off;
+    p.b2 = (const float*)(s->arena + c2.b_off);
+    p.out = (float*)o.ptr;
+    p.out_R = o.R;
+    p.k = c1.k;
+    p.d = c1.d;
+    p.C = c1.Ci;
+    p.NB16 = c1.NB16;
+    p.n_mean = c2.n_mean;
+    for (int m = 0; m < c2.n_mean; m++) {
+        p.mean[m] = (const float*)s->rings[c2.mean[m]].ptr;
+        p.mean_R = s->rings[c2.mean[m]].R;
+    }
+    p.B = c.batch;
+    p.F = (int)(n * s->fpt[c1.level_in]);
+    p.tiles_t = (p.F + pair_variant(pv).BM() - 1) / pair_variant(pv).BM();
+    p.clock = s->clock;
+    p.start = s->start;
+    p.in_fpt = s->fpt[c1.level_in];
+    p.slope = c.lrelu_slope;
+    return p;
+}
+
 static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
 {
     const dc_cfg& c = s->cfg;
@@ -594,6 +699,12 @@ static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
         for (int m = 0; m < cnt; m++) ps[m] = conv_params(s, s->convs[la.convs[m]], n);
         const ConvOp& op = s->convs[la.convs[0]];
         return launch_conv(op.variant, op.bf16, ps, cnt, st);
+    }
+    case L_PAIR: {
+        PairParams ps[kMaxGroup];
+        const int cnt = (int)la.convs.size();
+        for (int m = 0; m < cnt; m++) ps[m] = pair_params(s, s->convs[la.convs[m]], la.pair_variant, n);
+        return launch_pair(la.pair_variant, ps, cnt, st);
     }
     case L_SPECTRUM:
         return launch_spectrum((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL,
@@ -619,6 +730,8 @@ static hipError_t zero_state(dc_state* s)
     hipError_t e = hipMemsetAsync(s->arena + s->ring_begin, 0, s->ring_end - s->ring_begin, s->stream);
     if (e != hipSuccess) return e;
     e = hipMemsetAsync(s->clock, 0, sizeof(int64_t), s->stream);
+    if (e != hipSuccess) return e;
+    e = hipMemsetAsync(s->start, 0, (size_t)s->cfg.batch * sizeof(int64_t), s->stream);
     if (e != hipSuccess) return e;
     return hipMemsetAsync(s->err, 0, sizeof(int), s->stream);
 }
@@ -653,6 +766,15 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     build_network(s);
     for (auto& op : s->convs) {
         op.variant = pick_variant(s, op);
+        if (op.partner >= 0) {
+            // a fused pair's convs are packed for one partition and a channel
+            // block of all their channels, the arithmetic of the pair kernel
+            for (int v = 0; v < num_tile_variants(); v++)
+                if (tile_variant(v).WGK == 1 && tile_variant(v).KCH * 32 == op.Ci) {
+                    op.variant = v;
+                    break;
+                }
+        }
         set_blocks(op);
     }
     build_schedule(s);
@@ -676,8 +798,8 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     int64_t carry = 0;
     for (size_t i = 0; i < s->rings.size(); i++) {
         Ring& r = s->rings[i];
-        r.ctx = s->ring_ctx[i];
-        r.R = r.ctx + (int64_t)c.max_tokens * s->fpt[r.level];
+        r.ctx = s->ring_onchip[i] ? 0 : s->ring_ctx[i];
+        r.R = s->ring_onchip[i] ? 0 : r.ctx + (int64_t)c.max_tokens * s->fpt[r.level];
         const size_t es = r.elem == kBF16 ? 2 : 4;
         r.ptr = (void*)take((size_t)c.batch * r.R * r.C * es);  // offset for now
         carry += (int64_t)c.batch * r.ctx * r.C * es;
@@ -686,6 +808,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     s->tok_off = take((size_t)c.batch * c.max_tokens * sizeof(int32_t));
     s->audio_off = take((size_t)c.batch * c.max_tokens * s->spt * sizeof(float));
     s->clock_off = take(sizeof(int64_t));
+    s->start_off = take((size_t)c.batch * sizeof(int64_t));
     s->err_off = take(sizeof(int));
     s->arena_bytes = off;
 
@@ -700,6 +823,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     s->tok = (int32_t*)(s->arena + s->tok_off);
     s->audio = (float*)(s->arena + s->audio_off);
     s->clock = (int64_t*)(s->arena + s->clock_off);
+    s->start = (int64_t*)(s->arena + s->start_off);
     s->err = (int*)(s->arena + s->err_off);
 
     if (c.hip_stream) {
@@ -879,6 +1003,9 @@ dc_status dc_reset_stream(dc_state* s, int32_t b)
         hipError_t e = hipMemsetAsync((char*)r.ptr + (size_t)b * per, 0, per, s->stream);
         if (e != hipSuccess) return device_fail(s, e, "dc_reset_stream");
     }
+    // fused pairs recompute h of the left context: frames before this point are zeros
+    hipError_t e = launch_mark_start(s->start, b, s->clock, s->stream);
+    if (e != hipSuccess) return device_fail(s, e, "dc_reset_stream");
     return DC_OK;
 }
 
@@ -974,6 +1101,24 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
             const double Fo = F * op.u;
             out->bytes += (double)op.N * op.Ci * op.k * wes + B * (F + (op.k - 1) * op.d) * op.Ci * ies +
                           B * Fo * o.C * oes + (op.res >= 0 ? B * Fo * o.C * 4 : 0) + op.n_mean * B * Fo * o.C * 4;
+        }
+        break;
+    }
+    case L_PAIR: {
+        const PairShape t = pair_variant(la.pair_variant);
+        set("dc::pair_kernel<" + std::to_string(t.MB) + ", " + std::to_string(t.NB) + ", " + std::to_string(t.WGM) +
+            ", " + std::to_string(t.WGN) + ", " + std::to_string(t.KCH) + ", " + std::to_string(t.MB1) + ">");
+        for (int ci : la.convs) {   // both convs' work; z once, the output once, both weights
+            const ConvOp& a = s->convs[ci];
+            const ConvOp& b2 = s->convs[a.partner];
+            const double F = (double)n * s->fpt[a.level_in];
+            out->rows = (int64_t)(B * F);
+            out->cols = a.N;
+            out->depth += (int64_t)a.k * a.Ci + (int64_t)b2.k * b2.Ci;
+            out->flops += 2.0 * B * F * a.N * a.Ci * a.k + 2.0 * B * F * b2.N * b2.Ci * b2.k;
+            out->bytes += 2.0 * ((double)a.N * a.Ci * a.k + (double)b2.N * b2.Ci * b2.k) +
+                          B * (F + (a.k - 1) * a.d + (a.k - 1)) * a.Ci * 4 + B * F * b2.N * 4 +
+                          b2.n_mean * B * F * b2.N * 4;
         }
         break;
     }

@@ -262,60 +262,61 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
     int nblk[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; nb++) nblk[nb] = nblk0 + nb < p.NB16 ? nblk0 + nb : p.NB16 - 1;
-    auto load_tap = [&](int cb, int j, Frag (&w)[KPW][NB]) {
-        const Frag* wt = wp + (size_t)(cb * k + j) * KCH * p.NB16 * 64 + lane;
-#pragma unroll
-        for (int ki = 0; ki < KPW; ki++)
-#pragma unroll
-            for (int nb = 0; nb < NB; nb++) w[ki][nb] = wt[((size_t)(ki * WGK + wk) * p.NB16 + nblk[nb]) * 64];
-    };
-
-    // MFMAs of tap j: weights are the A operand, frames the B operand.  This
-    // lane's fragment address is fixed; a tap adds a scalar row offset, a
-    // block / chunk an immediate.
+    // K steps of one channel block: step s = tap j * KPW + this wave's chunk
+    // ki of the tap.  Weight fragments run two steps ahead and frame
+    // fragments one step ahead, each in a ring of three register buffers,
+    // so neither the L2 nor the LDS latency sits between two steps' MFMAs.
+    // Every accumulator still adds its steps in ascending (tap, chunk) order.
+    using AFrag = typename std::conditional<BF16, u32x4, f32x4>::type;   // frames of one K chunk
     constexpr int VEC = BF16 ? 8 : 4;       // operand elements per lane per K chunk
     const T* a_lane = lds + (wm * 16 * MB + (lane & 15)) * LDW + (lane >> 4) * VEC + wk * Tr::KQ;
     const int lo_off = rows * LDW;          // low halves of a split operand
-    auto compute_tap = [&](int j, const Frag (&w)[KPW][NB]) {
-        const T* aj = a_lane + j * p.d * LDW;
+    const int nsteps = k * KPW;
+    auto load_w = [&](int cb, int st, Frag (&w)[NB]) {
+        st = st < nsteps ? st : nsteps - 1;
+        const int j = st / KPW, ki = st - (st / KPW) * KPW;
+        const Frag* wt = wp + ((size_t)(cb * k + j) * KCH + ki * WGK + wk) * p.NB16 * 64 + lane;
 #pragma unroll
-        for (int ki = 0; ki < KPW; ki++) {
-            const int koff = ki * WGK * Tr::KQ;
-            if constexpr (BF16) {
-                bf16x8_t a[MB];
+        for (int nb = 0; nb < NB; nb++) w[nb] = wt[(size_t)nblk[nb] * 64];
+    };
+    auto step_a = [&](int st) {   // this lane's frame fragment of step st, block row 0
+        const int j = st / KPW, ki = st - (st / KPW) * KPW;
+        return a_lane + j * p.d * LDW + ki * WGK * Tr::KQ;
+    };
+    auto load_a = [&](int st, AFrag (&a)[MB]) {
+        const T* as = step_a(st < nsteps ? st : nsteps - 1);
 #pragma unroll
-                for (int mb = 0; mb < MB; mb++)
-                    a[mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(aj + mb * 16 * LDW + koff));
+        for (int mb = 0; mb < MB; mb++) a[mb] = *(const AFrag*)(as + mb * 16 * LDW);
+    };
+    auto mma = [&](int st, const Frag (&w)[NB], const AFrag (&a)[MB]) {
+        if constexpr (BF16) {
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++)
+                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[nb]),
+                                                                         __builtin_bit_cast(bf16x8_t, a[mb]),
+                                                                         acc[mb][nb], 0, 0, 0);
+            if (p.split) {   // the low halves, right after the high halves of the same step
+                const T* as = step_a(st) + lo_off;
+                bf16x8_t lo[MB];
+#pragma unroll
+                for (int mb = 0; mb < MB; mb++) lo[mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(as + mb * 16 * LDW));
 #pragma unroll
                 for (int mb = 0; mb < MB; mb++)
 #pragma unroll
                     for (int nb = 0; nb < NB; nb++)
-                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            __builtin_bit_cast(bf16x8_t, w[ki][nb]), a[mb], acc[mb][nb], 0, 0, 0);
-                if (p.split) {   // the low halves, right after the high halves of the same step
-#pragma unroll
-                    for (int mb = 0; mb < MB; mb++)
-                        a[mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(aj + lo_off + mb * 16 * LDW + koff));
-#pragma unroll
-                    for (int mb = 0; mb < MB; mb++)
-#pragma unroll
-                        for (int nb = 0; nb < NB; nb++)
-                            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                __builtin_bit_cast(bf16x8_t, w[ki][nb]), a[mb], acc[mb][nb], 0, 0, 0);
-                }
-            } else {
-                f32x4 a[MB];
-#pragma unroll
-                for (int mb = 0; mb < MB; mb++) a[mb] = *(const f32x4*)(aj + mb * 16 * LDW + koff);
-#pragma unroll
-                for (int q = 0; q < 4; q++)
-#pragma unroll
-                    for (int mb = 0; mb < MB; mb++)
-#pragma unroll
-                        for (int nb = 0; nb < NB; nb++)
-                            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[ki][nb][q], a[mb][q], acc[mb][nb],
-                                                                              0, 0, 0);
+                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[nb]),
+                                                                             lo[mb], acc[mb][nb], 0, 0, 0);
             }
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; q++)
+#pragma unroll
+                for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                    for (int nb = 0; nb < NB; nb++)
+                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[nb][q], a[mb][q], acc[mb][nb], 0, 0, 0);
         }
     };
 
@@ -344,28 +345,112 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
         }
     };
 
-    // Taps in pairs: the weights of the next tap are in flight while this
-    // tap's MFMAs run (two register buffers, no copies between them).
-    Frag w0[KPW][NB], w1[KPW][NB];
+    // Large per-wave tiles (at least 8 fragments): the step pipeline below.
+    // Small ones: whole taps in pairs (two tap buffers of weights, frames read
+    // as needed), where the per-step bookkeeping would outweigh the MFMAs.
+    constexpr bool PIPE = MB * NB >= 8;
+    if constexpr (!PIPE) {
+        // weight fragments of this wave for tap j of channel block cb
+        auto load_tap = [&](int cb, int j, Frag (&w)[KPW][NB]) {
+            const Frag* wt = wp + (size_t)(cb * k + j) * KCH * p.NB16 * 64 + lane;
+#pragma unroll
+            for (int ki = 0; ki < KPW; ki++)
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) w[ki][nb] = wt[((size_t)(ki * WGK + wk) * p.NB16 + nblk[nb]) * 64];
+        };
+        // MFMAs of tap j: this lane's fragment address is fixed; a tap adds a
+        // row offset, a block / chunk an immediate
+        auto compute_tap = [&](int j, const Frag (&w)[KPW][NB]) {
+            const T* aj = a_lane + j * p.d * LDW;
+#pragma unroll
+            for (int ki = 0; ki < KPW; ki++) {
+                const int koff = ki * WGK * Tr::KQ;
+                AFrag a[MB];
+#pragma unroll
+                for (int mb = 0; mb < MB; mb++) a[mb] = *(const AFrag*)(aj + mb * 16 * LDW + koff);
+                if constexpr (BF16) {
+#pragma unroll
+                    for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                        for (int nb = 0; nb < NB; nb++)
+                            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8_t, w[ki][nb]), __builtin_bit_cast(bf16x8_t, a[mb]),
+                                acc[mb][nb], 0, 0, 0);
+                    if (p.split) {   // the low halves, right after the high halves of the same step
+#pragma unroll
+                        for (int mb = 0; mb < MB; mb++) a[mb] = *(const AFrag*)(aj + lo_off + mb * 16 * LDW + koff);
+#pragma unroll
+                        for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                            for (int nb = 0; nb < NB; nb++)
+                                acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    __builtin_bit_cast(bf16x8_t, w[ki][nb]), __builtin_bit_cast(bf16x8_t, a[mb]),
+                                    acc[mb][nb], 0, 0, 0);
+                    }
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 4; q++)
+#pragma unroll
+                        for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                            for (int nb = 0; nb < NB; nb++)
+                                acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[ki][nb][q], a[mb][q], acc[mb][nb],
+                                                                                  0, 0, 0);
+                }
+            }
+        };
+        Frag w0[KPW][NB], w1[KPW][NB];
+        for (int cb = 0; cb < p.n_cb; cb++) {
+            __syncthreads();
+            load_tap(cb, 0, w0);
+            load_operand(cb);
+            __syncthreads();
+            int j = 0;
+            // scheduling barriers keep each tap's loads ahead of the previous
+            // tap's MFMAs (the scheduler would otherwise sink them to their use)
+            for (; j + 1 < k; j += 2) {
+                load_tap(cb, j + 1, w1);
+                __builtin_amdgcn_sched_barrier(0);
+                compute_tap(j, w0);
+                __builtin_amdgcn_sched_barrier(0);
+                load_tap(cb, j + 2 < k ? j + 2 : j + 1, w0);
+                __builtin_amdgcn_sched_barrier(0);
+                compute_tap(j + 1, w1);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if (j < k) compute_tap(j, w0);
+        }
+    } else {
+    Frag W0[NB], W1[NB], W2[NB];
+    AFrag A0[MB], A1[MB], A2[MB];
     for (int cb = 0; cb < p.n_cb; cb++) {
         __syncthreads();
-        load_tap(cb, 0, w0);
+        load_w(cb, 0, W0);
+        load_w(cb, 1, W1);
         load_operand(cb);
         __syncthreads();
-        int j = 0;
-        // scheduling barriers keep each tap's loads ahead of the previous
-        // tap's MFMAs (the scheduler would otherwise sink them to their use)
-        for (; j + 1 < k; j += 2) {
-            load_tap(cb, j + 1, w1);
+        load_a(0, A0);
+        // three steps per iteration: step s uses W[s % 3] and A[s % 3]
+        for (int st = 0; st < nsteps; st += 3) {
+            load_w(cb, st + 2, W2);
+            load_a(st + 1, A1);
             __builtin_amdgcn_sched_barrier(0);
-            compute_tap(j, w0);
+            mma(st, W0, A0);
             __builtin_amdgcn_sched_barrier(0);
-            load_tap(cb, j + 2 < k ? j + 2 : j + 1, w0);
+            if (st + 1 >= nsteps) break;
+            load_w(cb, st + 3, W0);
+            load_a(st + 2, A2);
             __builtin_amdgcn_sched_barrier(0);
-            compute_tap(j + 1, w1);
+            mma(st + 1, W1, A1);
+            __builtin_amdgcn_sched_barrier(0);
+            if (st + 2 >= nsteps) break;
+            load_w(cb, st + 4, W1);
+            load_a(st + 3, A0);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(st + 2, W2, A2);
             __builtin_amdgcn_sched_barrier(0);
         }
-        if (j < k) compute_tap(j, w0);
+    }
     }
 
     // ---- epilogue: bias, residual, branch mean, LeakyReLU, store through the rings

@@ -238,8 +238,9 @@ static void pack_weights(const ConvOp& op, const float* blob, bool round_bf16, c
 // table).  Layers that read a residual and write fp32 -- and every layer of
 // the 64-channel stage -- move more bytes per FLOP and run best on 64x64
 // tiles, whose lower register use keeps more waves (and loads) in flight;
-// the others favour the largest tiles.
-static const int kPreferLarge[] = {14, 15, 16, 11, 12, 13, 9, 10, 8, 6, 7, 19};
+// the others favour 64x128 tiles (four waves per SIMD with the step
+// pipeline), then 128x128.
+static const int kPreferLarge[] = {11, 14, 12, 13, 9, 10, 15, 16, 8, 6, 7, 19};
 static const int kPrefer64[] = {9, 10, 11, 12, 13, 14, 15, 16, 8, 6, 7, 19};
 
 // LDS budget of one block: at most 80 KB of the CU's 160 KB, so two blocks
@@ -285,6 +286,10 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
     auto blocks = [&](const TileShape& t) {
         return B * ((F + t.BM() - 1) / t.BM()) * ((op.N + t.BN() - 1) / t.BN());
     };
+    // a resblock conv shares its launch with the parallel branches' convs:
+    // the launch has that many times the blocks (the K-partition choice
+    // below still looks at one conv)
+    const int64_t members = op.stage >= 0 ? s->cfg.n_rb : 1;
     auto eff = [&](const TileShape& t) {
         const int bm = t.BM();
         return (double)F / (double)(((F + bm - 1) / bm) * bm);
@@ -314,8 +319,8 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
                 score = (waves < 2048.0 ? waves : 2048.0) * eff(t) * (t.MB * t.NB >= 2 ? 1.0 : 0.85);
             } else {
                 // the first shape in preference order that keeps enough blocks
-                if (blocks(t) >= 512 && eff(t) >= 0.75) return v;
-                score = (double)(blocks(t) < 512 ? blocks(t) : 512) * eff(t);
+                if (members * blocks(t) >= 512 && eff(t) >= 0.75) return v;
+                score = (double)(members * blocks(t) < 512 ? members * blocks(t) : 512) * eff(t);
             }
             if (score > best_score) {
                 best_score = score;

@@ -11,10 +11,15 @@ state's audio buffer.  Prints one JSON line:
 
   value        audio-seconds decoded per wall-second (streams * samples / 24 kHz)
   ms_per_step  wall milliseconds per chunk step in the timed loop
-  p50/p99      per-chunk latency, host submit to PCM ready on the device
+  p50/p99      per-chunk latency: host wall time of dc_decode_chunk with host
+               token and PCM buffers (synchronous call: token upload, graph
+               replay, PCM download); the same for device-resident buffers and
+               the HIP-event device time of one replay are reported beside it
   roofline     the kernel with the largest share of step time, its algorithmic
                FLOPs (or bytes) per launch over its mean launch duration, timed
                with HIP events on the state's stream
+               and against peaks measured on this device (a device copy and
+               library GEMMs), beside the datasheet ones
   cpu_baseline the plain fp64 oracle on the host cores, on a bounded sample
 """
 from __future__ import annotations
@@ -113,7 +118,7 @@ def roofline(layers, us, dtype):
     per_kernel = sorted(((k, v["us"] / step_us) for k, v in groups.items()), key=lambda kv: -kv[1])
     return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": None,
-            "kernel": name, "launches_per_step": g["launches"],
+            "kernel": name, "operand": op, "launches_per_step": g["launches"],
             "mean_launch_us": round(g["us"] / g["launches"], 3),
             "flops_per_launch": g["flops"] / g["launches"], "bytes_per_launch": g["bytes"] / g["launches"],
             "share_of_step": round(g["us"] / step_us, 4),
@@ -130,6 +135,40 @@ def calibrate_copy():
         b.copy_(a)
     torch.cuda.synchronize()
     print(f"copied {n} bytes 3 times", flush=True)
+
+
+def measured_peaks():
+    """Achievable rates on this device: a 1 GiB device copy (read + write bytes)
+    and 8192^3 library GEMMs in bf16 and fp32, best of several timed runs."""
+    import torch
+    out = {}
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def best(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(reps):
+            ev[0].record()
+            fn()
+            ev[1].record()
+            ev[1].synchronize()
+            t.append(ev[0].elapsed_time(ev[1]) * 1e-3)
+        return min(t)
+
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    out["hbm_copy_GBs"] = round(2 * n / best(lambda: b.copy_(a), 10) / 1e9, 1)
+    del a, b
+    m = 8192
+    for name, dt, reps in (("bf16_gemm_TFLOPs", torch.bfloat16, 10), ("f32_gemm_TFLOPs", torch.float32, 5)):
+        x = torch.randn(m, m, device="cuda").to(dt)
+        y = torch.randn(m, m, device="cuda").to(dt)
+        out[name] = round(2 * m ** 3 / best(lambda: torch.mm(x, y), reps) / 1e12, 1)
+        del x, y
+    torch.cuda.empty_cache()
+    return out
 
 
 def _csv(path):
@@ -243,14 +282,18 @@ def main():
     value = audio_s * args.steps / wall
     print(f"# timed {args.steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
 
-    lat = []
+    # device-resident buffers: submit, then wait for the PCM on the device
+    lat_dev, lat_ev = [], []
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     for i in range(args.latency_chunks):
         t = time.perf_counter()
+        ev[0].record(dec.stream)
         step(i)
+        ev[1].record(dec.stream)
         dec.stream.synchronize()
-        lat.append(1000.0 * (time.perf_counter() - t))
+        lat_dev.append(1000.0 * (time.perf_counter() - t))
+        lat_ev.append(ev[0].elapsed_time(ev[1]))
     dec.sync()
-    lat = np.array(lat)
 
     layers = dec.layers()
     us = dec.time_layers(args.layer_reps)
@@ -258,6 +301,29 @@ def main():
     roof["traffic"] = traffic_from_profiles(args.workload, roof["kernel"])
     stats = dec.stats()
     dec.close()
+
+    # host buffers: dc_decode_chunk uploads the tokens, replays the step and
+    # returns once the PCM is in host memory
+    hdec = dc.Decoder(arch, dtype, blob, batch=B, chunk_tokens=n, flags=dc.DC_HOST_PTRS,
+                      tile_variant=args.tile_variant)
+    pcm = np.empty((B, n * spt), dtype=np.float32)
+    host_tok = [np.ascontiguousarray(tokens[:, c * n:(c + 1) * n]) for c in range(chunks)]
+    lat = []
+    for i in range(args.warmup + args.latency_chunks):
+        t = time.perf_counter()
+        st = dc.dc_decode_chunk(hdec.h, host_tok[i % chunks], n, pcm)
+        dt = 1000.0 * (time.perf_counter() - t)
+        if st != dc.DC_OK:
+            raise dc.DcError(st, dc.dc_last_error(hdec.h))
+        if i >= args.warmup:
+            lat.append(dt)
+    hdec.close()
+
+    peaks = measured_peaks()
+    key = "hbm_copy_GBs" if roof["bound"] == "hbm" else f"{roof['operand']}_gemm_TFLOPs"
+    roof["measured_peak"] = peaks[key]
+    roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
+    roof["measured_peaks"] = peaks
     print(f"# roofline: {roof['kernel']} {roof['achieved']} {roof['unit']} ({roof['frac']:.1%})",
           file=sys.stderr, flush=True)
 
@@ -277,6 +343,11 @@ def main():
                    "flops_per_step": sum(l["flops"] for l in layers)},
         "p50_chunk_ms": round(float(np.percentile(lat, 50)), 4),
         "p99_chunk_ms": round(float(np.percentile(lat, 99)), 4),
+        "latency_path": "host tokens in, host PCM out, synchronous dc_decode_chunk",
+        "p50_chunk_ms_device_buffers": round(float(np.percentile(lat_dev, 50)), 4),
+        "p99_chunk_ms_device_buffers": round(float(np.percentile(lat_dev, 99)), 4),
+        "p50_replay_ms_hip_events": round(float(np.percentile(lat_ev, 50)), 4),
+        "capture_ms": round(stats["capture_ms"], 3),
         "roofline": roof,
         "cpu_baseline": cpu,
     }

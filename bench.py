@@ -219,7 +219,46 @@ def summarize_traffic(fetch_dir: str, write_dir: str, workload: str, kernel: str
     print("\n".join(lines))
 
 
+def summarize_mfma(prof_dir: str, workload: str, out: str, command: str):
+    """Per-kernel MFMA counters of a rocprofv3 --pmc run (one row per dispatch
+    and counter, values summed over the device's XCDs)."""
+    import glob
+    rows = _csv(glob.glob(os.path.join(prof_dir, "**", "*counter_collection.csv"), recursive=True)[0])
+    per = {}
+    for r in rows:
+        name = r["Kernel_Name"].replace("void ", "")
+        name = name[:name.index("(")] if "(" in name else name
+        if not name.startswith("dc::"):
+            continue
+        d = per.setdefault(name, {}).setdefault(r["Dispatch_Id"], {})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+        d["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    xcds, simds = 8, 1024
+    lines = ["# MFMA counters per kernel from rocprofv3 PMC counters", f"# command: {command}",
+             f"# workload: {workload}", f"# kernel sources: {kernel_source_hash()}",
+             "# mfma_flops = (SQ_INSTS_VALU_MFMA_MOPS_BF16 + SQ_INSTS_VALU_MFMA_MOPS_F32) * 512 per dispatch",
+             "# mfma_util  = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs * 1024 SIMDs); for dispatches "
+             "of a few microseconds GRBM_GUI_ACTIVE also counts the collection window, so it reads low there",
+             "# us = mean dispatch duration under counter collection (dispatches are serialised)", "",
+             f"{'kernel':48s} {'disp':>5s} {'us':>8s} {'mfma_GFLOP':>11s} {'TFLOP/s':>8s} {'util%':>6s}"]
+    tot = []
+    for name, ds in per.items():
+        n = len(ds)
+        us = sum(d["ns"] for d in ds.values()) / n / 1e3
+        fl = sum((d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) + d.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0)) * 512
+                 for d in ds.values()) / n
+        busy = sum(d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for d in ds.values())
+        gui = sum(d.get("GRBM_GUI_ACTIVE", 0) for d in ds.values()) / xcds
+        tot.append((us * n, f"{name[:48]:48s} {n:5d} {us:8.2f} {fl / 1e9:11.3f} {fl / (us * 1e-6) / 1e12:8.1f} "
+                            f"{100.0 * busy / max(gui * simds, 1.0):6.1f}"))
+    lines += [l for _, l in sorted(tot, key=lambda t: -t[0])]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
+    if len(sys.argv) > 1 and sys.argv[1] == "--summarize-mfma":
+        return summarize_mfma(*sys.argv[2:6])
     if len(sys.argv) > 1 and sys.argv[1] == "--calibrate-copy":
         return calibrate_copy()
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize-stats":

@@ -98,8 +98,11 @@ struct TileShape {
 
 // One fused resblock pair (bf16 operands): h = LeakyReLU(conv_k,d(LeakyReLU(z)) + b1)
 // stays in LDS, and out = z + conv_k,1(h) + b2 (optionally averaged with
-// earlier branch results).  A block owns BM frames x all C channels; the
-// first conv covers the BM + k - 1 frames the second one reads.
+// earlier branch results).  A block owns one stream's frames
+// [seg * seg_t * BM, (seg + 1) * seg_t * BM) x all C channels and walks them
+// in sub-tiles of BM frames, keeping LeakyReLU(z) and h in LDS windows that
+// slide with the sub-tile: the first sub-tile computes the k - 1 frames of h
+// left of the run, later ones only their own BM frames.
 struct PairParams {
     const float* z;       // fp32 ring: the first conv's input and the residual
     int64_t z_R;
@@ -115,7 +118,8 @@ struct PairParams {
     const float* mean[3]; // earlier branch results (fp32 rings, out geometry)
     int64_t mean_R;
     int n_mean;
-    int B, F, tiles_t;
+    int B, F, tiles_t;    // tiles_t = ceil(F / BM) sub-tiles per stream
+    int seg_t, segs;      // sub-tiles per block, blocks per stream (segs * seg_t >= tiles_t)
     const int64_t* clock;
     const int64_t* start; // [B]: tokens decoded when each stream last started
     int64_t in_fpt;
@@ -137,18 +141,20 @@ struct PairGroup {
     PairMember m[kMaxGroup - 1];
 };
 
-// Fused-pair shapes: MB x NB blocks of 16x16 per wave for the second conv,
-// WGM x WGN waves, channel block KCH chunks (C = 32 KCH), MB1 16-row blocks
-// per wave for the first conv (16 MB1 WGM >= BM + k - 1).
+// Fused-pair shapes: MB x NB blocks of 16x16 per wave (both convs), WGM x WGN
+// waves, channel block KCH chunks (C = 32 KCH); LDS windows of 2^LZ frames of
+// LeakyReLU(z) (>= BM + (k-1)(d+1)) and 2^LH frames of h (>= BM + 16).
 struct PairShape {
-    int MB, NB, WGM, WGN, KCH, MB1;
+    int MB, NB, WGM, WGN, KCH, LZ, LH;
     int BM() const { return 16 * MB * WGM; }
     int C() const { return 32 * KCH; }
-    int M1() const { return 16 * MB1 * WGM; }
+    int WZ() const { return 1 << LZ; }
+    int WH() const { return 1 << LH; }
+    bool fits(int k, int d) const { return WZ() >= BM() + (k - 1) * (d + 1) && WH() >= BM() + 16 && k - 1 <= 16; }
 };
 int num_pair_variants();
 PairShape pair_variant(int v);
-size_t pair_lds_bytes(int v, int k_max, int d);
+size_t pair_lds_bytes(int v);
 hipError_t launch_pair(int v, const PairParams* ps, int count, hipStream_t st);
 
 // The tile shapes compiled for each operand type.

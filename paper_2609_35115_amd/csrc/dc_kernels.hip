@@ -475,15 +475,60 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
 #pragma unroll
             for (int e = 0; e < 4; e++) bias[nb][e] = e < nv[nb] ? bias_ptr[n4 + e] : 0.f;
         }
+        // the wave's columns are all real and vector-aligned, and no branch mean:
+        // the residual loads of row block mb + 1 are issued before row block mb
+        // is finished (rows past the call's frames read its last frame and
+        // store nothing).  Otherwise each output vector loads what it adds.
+        const bool full = (p.out_C & 3) == 0 && n0 + (wn * NB + NB) * 16 <= p.N && p.n_mean == 0;
+        if (full) {
+            auto off_of = [&](int mb) {
+                const int tl = wm * 16 * MB + mb * 16 + fl;
+                return (t0 + tl < p.F ? tl : p.F - 1 - t0) * p.u;
+            };
+            f32x4 ld[2][NB];
+            auto issue = [&](int mb, f32x4 (&q)[NB]) {
+                const int off = off_of(mb);
 #pragma unroll
-        for (int mb = 0; mb < MB; mb++) {
-            const int tl = wm * 16 * MB + mb * 16 + fl;
-            if (t0 + tl >= p.F) continue;
+                for (int nb = 0; nb < NB; nb++)
+                    q[nb] = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(rs.res_s, off + rp[nb], rs.res_R)) *
+                                                         p.out_C + co[nb]);
+            };
+            if (rs.res) issue(0, ld[0]);
 #pragma unroll
-            for (int nb = 0; nb < NB; nb++) {
-                if (nv[nb] <= 0) continue;
-                f32x4 v = acc[mb][nb];
-                store_out4(p, b, rs, tl * p.u + rp[nb], co[nb], v + bias[nb], nv[nb]);
+            for (int mb = 0; mb < MB; mb++) {
+                if (rs.res && mb + 1 < MB) issue(mb + 1, ld[(mb + 1) & 1]);
+                const int off = off_of(mb);
+                const bool live = t0 + wm * 16 * MB + mb * 16 + fl < p.F;
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) {
+                    f32x4 v = acc[mb][nb] + bias[nb];
+                    if (rs.res) v = ld[mb & 1][nb] + v;
+                    if (p.out_act) {
+#pragma unroll
+                        for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
+                    }
+                    if (!live) continue;
+                    const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off + rp[nb], rs.out_R)) * p.out_C + co[nb];
+                    if (p.out_elem == kF32) {
+                        *(f32x4*)((float*)rs.out + oo) = v;
+                    } else {
+                        typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+                        u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                        *(u32x2*)((uint16_t*)rs.out + oo) = h;
+                    }
+                }
+            }
+        } else {
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++) {
+                const int tl = wm * 16 * MB + mb * 16 + fl;
+                if (t0 + tl >= p.F) continue;
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) {
+                    if (nv[nb] <= 0) continue;
+                    f32x4 v = acc[mb][nb];
+                    store_out4(p, b, rs, tl * p.u + rp[nb], co[nb], v + bias[nb], nv[nb]);
+                }
             }
         }
     } else {
@@ -634,16 +679,25 @@ hipError_t launch_conv(int v, bool bf16, const ConvParams* ps, int count, hipStr
 
 // ------------------------------------------------------ fused resblock pair
 //
-// One block: output frames [t0, t0 + BM) x all C channels of one branch's
-// pair at one dilation.  The operand rows of the first conv go to LDS once;
-// its output h for frames [t0 - (k-1), t0 + BM) goes to LDS as bf16 (zero for
-// frames before the stream start, as in a freshly reset ring); the second
-// conv reads h from LDS and adds bias and the fp32 residual.  Both convs use
-// one K partition and a channel block of all C channels, i.e. the arithmetic
-// of the unfused launches with those parameters, bit for bit.
+// One block: one branch's pair at one dilation, for stream b and the frames
+// [f0, f1) of its segment, all C channels, in sub-tiles of BM frames.  LDS
+// holds two windows indexed by frame modulo their size:
+//   Zs  LeakyReLU(z) as bf16 for the frames the first conv reads
+//       ([t - (k-1)d - (k-1), t + BM) for the sub-tile at t), WZ = 2^LZ frames;
+//   Hs  h = LeakyReLU(conv1 + b1) as bf16 ([t - (k-1), t + BM)), WH = 2^LH
+//       frames; zero for frames before the stream's start, as a freshly reset
+//       ring holds.
+// Per sub-tile: the first conv writes h for its BM frames (the first sub-tile
+// of the segment also the 16 frames left of it, of which the second conv reads
+// the last k - 1); after a barrier the second conv reads Hs and the epilogue
+// adds b2, the fp32 residual z and the branch mean; then the next sub-tile's
+// BM z frames go to Zs, replacing frames older than any the next first conv
+// reads.  Both convs use one K partition and a channel block of all C
+// channels, i.e. the arithmetic of the unfused launches with those
+// parameters, bit for bit.
 
-template <int MB, int NB, int WGM, int WGN, int KCH, int MB1>
-__global__ __launch_bounds__(256) void pair_kernel(const PairGroup g)
+template <int MB, int NB, int WGM, int WGN, int KCH, int LZ, int LH>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void pair_kernel(const PairGroup g)
 {
     const PairParams& p = g.p;
     const float* z = p.z;
@@ -671,34 +725,38 @@ __global__ __launch_bounds__(256) void pair_kernel(const PairGroup g)
     constexpr int C = KQ * KCH;
     constexpr int BM = 16 * MB * WGM, BN = 16 * NB * WGN;
     constexpr int LDW = C + OpT<true>::PAD;
-    constexpr int VPR = C / 8;
+    constexpr int VPR = C / 8;                 // 8-channel groups per frame
+    constexpr int ZM = (1 << LZ) - 1, HM = (1 << LH) - 1;
     static_assert(WGM * WGN == 4 && BN == C, "pair tile shape");
     using Frag = u32x4;
 
-    const int H1 = (k - 1) * p.d, H2 = k - 1;
-    const int rowsA = BM + H1 + H2;            // first conv operand rows
-    const int rows1 = BM + H2;                 // first conv output rows (h)
+    const int H1 = (k - 1) * p.d, H2 = k - 1, H = H1 + H2;
     extern __shared__ __align__(16) unsigned char smem[];
-    uint16_t* A = reinterpret_cast<uint16_t*>(smem);
-    uint16_t* Hs = A + (rowsA + 16) * LDW;     // 16 spare rows: partial row blocks read past rowsA
+    uint16_t* Zs = reinterpret_cast<uint16_t*>(smem);
+    uint16_t* Hs = Zs + (ZM + 1) * LDW;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % WGM, wn = wave / WGM;
-    const int b = blockIdx.x / p.tiles_t;
-    const int t0 = (blockIdx.x - b * p.tiles_t) * BM;
+    const int b = blockIdx.x / p.segs;
+    const int f0 = (blockIdx.x - b * p.segs) * p.seg_t * BM;
+    const int f1 = min(p.F, f0 + p.seg_t * BM);
     const int64_t tau0 = p.clock[0] * p.in_fpt;
     const int64_t start_f = p.start[b] * p.in_fpt;   // this stream's first frame since its reset
     const int fl = lane & 15, cg = (lane >> 4) * 4;
+    const float* zb = z + (size_t)b * z_R * C;
+    const int zs0 = (int)ring_slot(tau0 + f0 - H, z_R);   // ring slot of frame f0 - H
+    // ring slot of frame f of this chunk, for f0 - H <= f < f0 - H + z_R
+    auto zslot = [&](int f) { return slot_add(zs0, f - (f0 - H), z_R); };
 
-    // ---- first conv operand: LeakyReLU(z) for frames [t0 - H1 - H2, t0 + BM)
-    {
-        const int base = (int)ring_slot(tau0 + t0 - H1 - H2, z_R);
-        for (int v = tid; v < rowsA * VPR; v += 256) {
+    // z frames [fa, fa + n) -> Zs (LeakyReLU, bf16); frames at or past F are zeros
+    auto stage = [&](int fa, int n) {
+        for (int v = tid; v < n * VPR; v += 256) {
             const int r = v / VPR, c8 = (v - r * VPR) * 8;
+            const int f = fa + r;
             float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            if (t0 - H1 - H2 + r < p.F) {
-                const f32x4* q = (const f32x4*)(z + ((size_t)b * z_R + slot_add(base, r, z_R)) * C + c8);
+            if (f < p.F) {
+                const f32x4* q = (const f32x4*)(zb + (size_t)zslot(f) * C + c8);
                 const f32x4 a0 = q[0], a1 = q[1];
 #pragma unroll
                 for (int e = 0; e < 4; e++) {
@@ -706,10 +764,9 @@ __global__ __launch_bounds__(256) void pair_kernel(const PairGroup g)
                     x[4 + e] = lrelu(a1[e], p.slope);
                 }
             }
-            store8_lds(A + r * LDW + c8, x);
+            store8_lds(Zs + (f & ZM) * LDW + c8, x);
         }
-    }
-
+    };
     // weight fragments of tap j (channel block of all C channels, one partition)
     const int nblk0 = wn * NB;
     auto load_tap = [&](const Frag* wp, int j, Frag (&w)[KCH][NB]) {
@@ -719,13 +776,16 @@ __global__ __launch_bounds__(256) void pair_kernel(const PairGroup g)
 #pragma unroll
             for (int nb = 0; nb < NB; nb++) w[ki][nb] = wt[((size_t)ki * p.NB16 + nblk0 + nb) * 64];
     };
-    // the taps of one conv in pairs, weights one tap ahead (as in conv_kernel)
-    auto run_taps = [&](const Frag* wp, auto&& tap) {
+    // the taps of one conv in pairs, weights one tap ahead (as in conv_kernel);
+    // `issued` runs once the first two taps' weight loads are issued
+    auto run_taps = [&](const Frag* wp, auto&& tap, auto&& issued) {
         Frag w0[KCH][NB], w1[KCH][NB];
         load_tap(wp, 0, w0);
+        if (k == 1) issued();
         int j = 0;
         for (; j + 1 < k; j += 2) {
             load_tap(wp, j + 1, w1);
+            if (j == 0) issued();
             __builtin_amdgcn_sched_barrier(0);
             tap(j, w0);
             __builtin_amdgcn_sched_barrier(0);
@@ -736,25 +796,28 @@ __global__ __launch_bounds__(256) void pair_kernel(const PairGroup g)
         }
         if (j < k) tap(j, w0);
     };
-    __syncthreads();
+    const int koff = (lane >> 4) * 8;
+    auto nothing = [] {};
 
-    // ---- first conv: h rows in 16-row blocks wm, wm + WGM, ... (interleaved)
-    {
-        f32x4 acc[MB1][NB];
+    // first conv over R row blocks of 16 frames starting at frame fr (this
+    // lane: frames fr + 16 i + fl); h -> Hs
+    auto conv1 = [&](auto rb_tag, int fr) {
+        constexpr int R = decltype(rb_tag)::value;
+        f32x4 acc[R][NB];
 #pragma unroll
-        for (int i = 0; i < MB1; i++)
+        for (int i = 0; i < R; i++)
 #pragma unroll
             for (int nb = 0; nb < NB; nb++) acc[i][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-        const uint16_t* a_lane = A + fl * LDW + (lane >> 4) * 8;
+        const int row0 = fr + fl - H1;         // z frame of tap 0 for row block 0
         auto tap1 = [&](int j, const Frag (&w)[KCH][NB]) {
-            const uint16_t* aj = a_lane + j * p.d * LDW;
+            int ai[R];
+#pragma unroll
+            for (int i = 0; i < R; i++) ai[i] = ((row0 + 16 * i + j * p.d) & ZM) * LDW + koff;
 #pragma unroll
             for (int ki = 0; ki < KCH; ki++) {
 #pragma unroll
-                for (int i = 0; i < MB1; i++) {
-                    const int rb = wm + WGM * i;
-                    if (16 * rb >= rows1) break;
-                    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(aj + rb * 16 * LDW + ki * KQ));
+                for (int i = 0; i < R; i++) {
+                    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(Zs + ai[i] + ki * KQ));
 #pragma unroll
                     for (int nb = 0; nb < NB; nb++)
                         acc[i][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[ki][nb]),
@@ -762,115 +825,166 @@ __global__ __launch_bounds__(256) void pair_kernel(const PairGroup g)
                 }
             }
         };
-        run_taps(reinterpret_cast<const Frag*>(w1p), tap1);
-        f32x4 bias[NB];
+        run_taps(reinterpret_cast<const Frag*>(w1p), tap1, nothing);
+        f32x4 bias1[NB];
 #pragma unroll
-        for (int nb = 0; nb < NB; nb++) bias[nb] = *(const f32x4*)(b1 + (nblk0 + nb) * 16 + cg);
+        for (int nb = 0; nb < NB; nb++) bias1[nb] = *(const f32x4*)(b1 + (nblk0 + nb) * 16 + cg);
 #pragma unroll
-        for (int i = 0; i < MB1; i++) {
-            const int rb = wm + WGM * i;
-            if (16 * rb >= rows1) break;
-            const int r1 = rb * 16 + fl;
-            const bool before = tau0 + t0 - H2 + r1 < start_f;   // h of a frame before the stream start is 0
+        for (int i = 0; i < R; i++) {
+            const int f = fr + 16 * i + fl;
+            const bool before = tau0 + f < start_f;   // h of a frame before the stream start is 0
 #pragma unroll
             for (int nb = 0; nb < NB; nb++) {
-                f32x4 v = acc[i][nb] + bias[nb];
+                f32x4 v = acc[i][nb] + bias1[nb];
 #pragma unroll
                 for (int e = 0; e < 4; e++) v[e] = before ? 0.f : lrelu(v[e], p.slope);
                 typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
                 const u32x2 hv = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-                *(u32x2*)(Hs + r1 * LDW + (nblk0 + nb) * 16 + cg) = hv;
+                *(u32x2*)(Hs + (f & HM) * LDW + (nblk0 + nb) * 16 + cg) = hv;
             }
-        }
-    }
-    __syncthreads();
-
-    // ---- second conv: output rows wm*16*MB .. (contiguous), h from LDS
-    f32x4 acc[MB][NB];
-#pragma unroll
-    for (int i = 0; i < MB; i++)
-#pragma unroll
-        for (int nb = 0; nb < NB; nb++) acc[i][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint16_t* h_lane = Hs + (wm * 16 * MB + fl) * LDW + (lane >> 4) * 8;
-    auto tap2 = [&](int j, const Frag (&w)[KCH][NB]) {
-        const uint16_t* hj = h_lane + j * LDW;
-#pragma unroll
-        for (int ki = 0; ki < KCH; ki++) {
-            bf16x8_t a[MB];
-#pragma unroll
-            for (int mb = 0; mb < MB; mb++)
-                a[mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(hj + mb * 16 * LDW + ki * KQ));
-#pragma unroll
-            for (int mb = 0; mb < MB; mb++)
-#pragma unroll
-                for (int nb = 0; nb < NB; nb++)
-                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[ki][nb]),
-                                                                         a[mb], acc[mb][nb], 0, 0, 0);
         }
     };
-    run_taps(reinterpret_cast<const Frag*>(w2p), tap2);
 
-    // ---- epilogue: bias, residual z, branch mean; fp32 through the output ring
-    const int out_s = (int)ring_slot(tau0 + t0, out_R);
-    const int res_s = (int)ring_slot(tau0 + t0, z_R);
-    const int mean_s = p.n_mean ? (int)ring_slot(tau0 + t0, p.mean_R) : 0;
-    f32x4 bias[NB];
+    const int mean_R = (int)p.mean_R;
+    stage(f0 - H, BM + H);
+    __syncthreads();
+    for (int t = f0; t < f1; t += BM) {
+        // ---- first conv: h for this wave's rows of [t, t + BM) (and [t - 16, t) first)
+        if (t == f0 && wm == 0)
+            conv1(std::integral_constant<int, MB + 1>{}, t - 16);   // with the 16 frames left of the run
+        else
+            conv1(std::integral_constant<int, MB>{}, t + wm * 16 * MB);
+        __syncthreads();
+
+        // ---- second conv: output frames t + wm*16*MB + 16 mb + fl, h from Hs
+        f32x4 acc[MB][NB];
 #pragma unroll
-    for (int nb = 0; nb < NB; nb++) bias[nb] = *(const f32x4*)(b2 + (nblk0 + nb) * 16 + cg);
+        for (int i = 0; i < MB; i++)
 #pragma unroll
-    for (int mb = 0; mb < MB; mb++) {
-        const int tl = wm * 16 * MB + mb * 16 + fl;
-        if (t0 + tl >= p.F) continue;
+            for (int nb = 0; nb < NB; nb++) acc[i][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int hrow0 = t + wm * 16 * MB + fl - H2;
+        // frame fragments are read one channel chunk ahead of their MFMAs
+        auto tap2 = [&](int j, const Frag (&w)[KCH][NB]) {
+            int hi[MB];
 #pragma unroll
-        for (int nb = 0; nb < NB; nb++) {
-            const int n4 = (nblk0 + nb) * 16 + cg;
-            f32x4 v = acc[mb][nb] + bias[nb];
-            v = *(const f32x4*)(z + ((size_t)b * z_R + slot_add(res_s, tl, z_R)) * C + n4) + v;
-            if (p.n_mean) {
-                const size_t mo = ((size_t)b * p.mean_R + slot_add(mean_s, tl, (int)p.mean_R)) * C + n4;
-                f32x4 x = *(const f32x4*)(p.mean[0] + mo);
-                for (int i = 1; i < p.n_mean; i++) x = x + *(const f32x4*)(p.mean[i] + mo);
-                x = x + v;
-                const float J = (float)(p.n_mean + 1);
-                v = f32x4{x[0] / J, x[1] / J, x[2] / J, x[3] / J};
+            for (int mb = 0; mb < MB; mb++) hi[mb] = ((hrow0 + 16 * mb + j) & HM) * LDW + koff;
+            bf16x8_t a[2][MB];
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++) a[0][mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(Hs + hi[mb]));
+#pragma unroll
+            for (int ki = 0; ki < KCH; ki++) {
+                if (ki + 1 < KCH) {
+#pragma unroll
+                    for (int mb = 0; mb < MB; mb++)
+                        a[(ki + 1) & 1][mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(Hs + hi[mb] + (ki + 1) * KQ));
+                }
+                __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of these MFMAs
+#pragma unroll
+                for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                    for (int nb = 0; nb < NB; nb++)
+                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[ki][nb]),
+                                                                             a[ki & 1][mb], acc[mb][nb], 0, 0, 0);
             }
-            *(f32x4*)(out + ((size_t)b * out_R + slot_add(out_s, tl, out_R)) * C + n4) = v;
+        };
+        run_taps(reinterpret_cast<const Frag*>(w2p), tap2, nothing);
+
+        // ---- epilogue: bias, residual z, branch mean; fp32 through the output ring
+        const int out_s = (int)ring_slot(tau0 + t, out_R);
+        const int mean_s = p.n_mean ? (int)ring_slot(tau0 + t, p.mean_R) : 0;
+        f32x4 bias2[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++) bias2[nb] = *(const f32x4*)(b2 + (nblk0 + nb) * 16 + cg);
+        // the residual loads of row block mb + 1 are issued before row block mb
+        // is finished (rows past the run read its last frame and store
+        // nothing); with a branch mean, each row block loads what it adds
+        auto tl_of = [&](int mb) {
+            const int tl = wm * 16 * MB + mb * 16 + fl;
+            return t + tl < f1 ? tl : f1 - 1 - t;
+        };
+        auto store = [&](int mb, int nb, f32x4 v) {
+            const int tl = wm * 16 * MB + mb * 16 + fl;
+            if (t + tl < f1)
+                *(f32x4*)(out + ((size_t)b * out_R + slot_add(out_s, tl, out_R)) * C + (nblk0 + nb) * 16 + cg) = v;
+        };
+        if (p.n_mean == 0) {
+            f32x4 ld[2][NB];
+            auto issue = [&](int mb, f32x4 (&q)[NB]) {
+                const float* zr = zb + (size_t)zslot(t + tl_of(mb)) * C + nblk0 * 16 + cg;
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) q[nb] = *(const f32x4*)(zr + nb * 16);
+            };
+            issue(0, ld[0]);
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++) {
+                if (mb + 1 < MB) issue(mb + 1, ld[(mb + 1) & 1]);
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) store(mb, nb, ld[mb & 1][nb] + (acc[mb][nb] + bias2[nb]));
+            }
+        } else {
+            const float J = (float)(p.n_mean + 1);
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++) {
+                const int tl = tl_of(mb);
+                const float* zr = zb + (size_t)zslot(t + tl) * C + nblk0 * 16 + cg;
+                const size_t mo = ((size_t)b * mean_R + slot_add(mean_s, tl, mean_R)) * C + nblk0 * 16 + cg;
+                f32x4 r[NB], m[3][NB];
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) {
+                    r[nb] = *(const f32x4*)(zr + nb * 16);
+#pragma unroll
+                    for (int i = 0; i < 3; i++)
+                        if (i < p.n_mean) m[i][nb] = *(const f32x4*)(p.mean[i] + mo + nb * 16);
+                }
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++) {
+                    const f32x4 v = r[nb] + (acc[mb][nb] + bias2[nb]);
+                    f32x4 x = m[0][nb];
+#pragma unroll
+                    for (int i = 1; i < 3; i++)
+                        if (i < p.n_mean) x = x + m[i][nb];
+                    x = x + v;
+                    store(mb, nb, f32x4{x[0] / J, x[1] / J, x[2] / J, x[3] / J});
+                }
+            }
         }
+        // the next sub-tile's z frames (the frames they replace are older than
+        // any the next first conv reads)
+        if (t + BM < f1) stage(t + BM, BM);
+        __syncthreads();
     }
 }
 
 // Fused-pair shapes (ids of this table).
 static const PairShape kPairs[] = {
-    // MB NB WGM WGN KCH MB1
-    {2, 2, 2, 2, 2, 3},   // 0: C = 64, 64 frames per block (first conv: 96 rows)
-    {4, 2, 2, 2, 2, 5},   // 1: C = 64, 128 frames per block (160 rows)
-    {4, 2, 1, 4, 4, 5},   // 2: C = 128, 64 frames per block (80 rows)
+    // MB NB WGM WGN KCH LZ LH
+    {2, 2, 2, 2, 2, 7, 7},   // 0: C = 64, 64-frame sub-tiles
+    {4, 2, 2, 2, 2, 8, 8},   // 1: C = 64, 128-frame sub-tiles
+    {4, 2, 1, 4, 4, 7, 7},   // 2: C = 128, 64-frame sub-tiles
 };
 
 int num_pair_variants() { return (int)(sizeof(kPairs) / sizeof(kPairs[0])); }
 PairShape pair_variant(int v) { return kPairs[v]; }
 
-size_t pair_lds_bytes(int v, int k_max, int d)
+size_t pair_lds_bytes(int v)
 {
     const PairShape& t = kPairs[v];
-    const int ldw = t.C() + OpT<true>::PAD;
-    const int rowsA = t.BM() + (k_max - 1) * d + (k_max - 1);
-    return ((size_t)(rowsA + 16) + t.M1()) * ldw * 2;
+    return (size_t)(t.WZ() + t.WH()) * (t.C() + OpT<true>::PAD) * 2;
 }
 
-template <int MB, int NB, int WGM, int WGN, int KCH, int MB1>
+template <int MB, int NB, int WGM, int WGN, int KCH, int LZ, int LH>
 static hipError_t launch_pair_t(const PairGroup& g, int count, size_t lds, hipStream_t st)
 {
     const PairParams& p = g.p;
-    dim3 grid((unsigned)(p.B * p.tiles_t), 1u, (unsigned)count);
+    dim3 grid((unsigned)(p.B * p.segs), 1u, (unsigned)count);
     static size_t lds_set = 64 * 1024;
     if (lds > lds_set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&pair_kernel<MB, NB, WGM, WGN, KCH, MB1>),
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&pair_kernel<MB, NB, WGM, WGN, KCH, LZ, LH>),
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         lds_set = lds;
     }
-    hipLaunchKernelGGL((pair_kernel<MB, NB, WGM, WGN, KCH, MB1>), grid, dim3(256), lds, st, g);
+    hipLaunchKernelGGL((pair_kernel<MB, NB, WGM, WGN, KCH, LZ, LH>), grid, dim3(256), lds, st, g);
     return hipGetLastError();
 }
 
@@ -880,23 +994,24 @@ hipError_t launch_pair(int v, const PairParams* ps, int count, hipStream_t st)
     const PairShape t = kPairs[v];
     PairGroup g{};
     g.p = ps[0];
-    int k_max = ps[0].k;
-    for (int i = 1; i < count; i++) {
+    for (int i = 0; i < count; i++) {
         const PairParams& a = ps[0];
         const PairParams& q = ps[i];
         if (q.d != a.d || q.C != a.C || q.NB16 != a.NB16 || q.B != a.B || q.F != a.F || q.tiles_t != a.tiles_t ||
-            q.n_mean != a.n_mean || q.clock != a.clock || q.start != a.start || q.in_fpt != a.in_fpt ||
-            q.slope != a.slope)
+            q.seg_t != a.seg_t || q.segs != a.segs || q.n_mean != a.n_mean || q.clock != a.clock ||
+            q.start != a.start || q.in_fpt != a.in_fpt || q.slope != a.slope || !t.fits(q.k, q.d))
             return hipErrorInvalidValue;
-        g.m[i - 1] = PairMember{q.z, q.z_R, q.w1, q.b1, q.w2, q.b2, q.out, q.out_R, q.k};
-        k_max = q.k > k_max ? q.k : k_max;
+        if (i > 0) g.m[i - 1] = PairMember{q.z, q.z_R, q.w1, q.b1, q.w2, q.b2, q.out, q.out_R, q.k};
     }
-    if (ps[0].C != t.C() || t.M1() < t.BM() + k_max - 1) return hipErrorInvalidValue;
-    const size_t lds = pair_lds_bytes(v, k_max, ps[0].d);
+    const PairParams& p = ps[0];
+    if (p.C != t.C() || p.tiles_t != (p.F + t.BM() - 1) / t.BM() || p.seg_t < 1 ||
+        (int64_t)p.segs * p.seg_t < p.tiles_t || (int64_t)(p.segs - 1) * p.seg_t >= p.tiles_t)
+        return hipErrorInvalidValue;
+    const size_t lds = pair_lds_bytes(v);
     switch (v) {
-    case 0: return launch_pair_t<2, 2, 2, 2, 2, 3>(g, count, lds, st);
-    case 1: return launch_pair_t<4, 2, 2, 2, 2, 5>(g, count, lds, st);
-    case 2: return launch_pair_t<4, 2, 1, 4, 4, 5>(g, count, lds, st);
+    case 0: return launch_pair_t<2, 2, 2, 2, 2, 7, 7>(g, count, lds, st);
+    case 1: return launch_pair_t<4, 2, 2, 2, 2, 8, 8>(g, count, lds, st);
+    case 2: return launch_pair_t<4, 2, 1, 4, 4, 7, 7>(g, count, lds, st);
     default: return hipErrorInvalidValue;
     }
 }

@@ -16,6 +16,7 @@
 // graph and replayed; kernels take the time offset of a call from a device
 // clock that the last node advances, so the frozen kernel arguments stay
 // valid.  Any other admissible n launches the same kernels directly.
+#include <algorithm>
 #include <chrono>
 #include <cmath>
 #include <cstdio>
@@ -370,7 +371,7 @@ static bool fuse_stage(const dc_cfg& c, int channels)
     for (int i = 0; i < c.n_dil; i++) d_max = c.dil[i] > d_max ? c.dil[i] : d_max;
     for (int v = 0; v < num_pair_variants(); v++)
         if (pair_variant(v).C() == channels)
-            return pair_variant(v).M1() >= pair_variant(v).BM() + k_max - 1 && pair_lds_bytes(v, k_max, d_max) <= 96 * 1024;
+            return pair_variant(v).fits(k_max, d_max) && pair_lds_bytes(v) <= 80 * 1024;
     return false;
 }
 
@@ -567,8 +568,14 @@ static void build_schedule(dc_state* s)
                         if (s->convs[r].branch == j && s->convs[r].dil_i == di && s->convs[r].half == 1) m.push_back(r);
                 const std::string pos = ".d" + std::to_string(di) + ".pair";
                 Launch la{L_PAIR, {}, "", pv};
+                // members with the most taps first: their blocks are the longest,
+                // and blocks are dispatched in member order
+                auto by_taps = [&](std::vector<int>& v) {
+                    std::stable_sort(v.begin(), v.end(), [&](int a, int b) { return s->convs[a].k > s->convs[b].k; });
+                };
                 if (di == c.n_dil - 1 && c.n_rb > 1) {
                     la.convs.assign(m.begin(), m.end() - 1);
+                    by_taps(la.convs);
                     la.name = sn + ".rb<" + std::to_string(c.n_rb - 1) + pos;
                     s->launches.push_back(la);
                     la.convs = {m.back()};
@@ -576,6 +583,7 @@ static void build_schedule(dc_state* s)
                     s->launches.push_back(la);
                 } else {
                     la.convs = m;
+                    by_taps(la.convs);
                     la.name = sn + ".rb*" + pos;
                     s->launches.push_back(la);
                 }
@@ -654,7 +662,10 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
     return p;
 }
 
-static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n)
+#ifndef DC_PAIR_BLOCKS
+#define DC_PAIR_BLOCKS 2048
+#endif
+static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n, int members)
 {
     const dc_cfg& c = s->cfg;
     const ConvOp& c2 = s->convs[c1.partner];
@@ -681,6 +692,14 @@ static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n
     p.B = c.batch;
     p.F = (int)(n * s->fpt[c1.level_in]);
     p.tiles_t = (p.F + pair_variant(pv).BM() - 1) / pair_variant(pv).BM();
+    // sub-tiles per block: about DC_PAIR_BLOCKS blocks per launch (every block
+    // but the first of a stream recomputes k - 1 frames of h and reloads the
+    // z frames left of its run, so fewer, longer blocks do less work; more
+    // blocks balance the members' different tap counts over the machine)
+    const int64_t want = DC_PAIR_BLOCKS;
+    const int64_t units = (int64_t)p.B * p.tiles_t * members;
+    p.seg_t = (int)std::max<int64_t>(1, std::min<int64_t>(p.tiles_t, units / want));
+    p.segs = (p.tiles_t + p.seg_t - 1) / p.seg_t;
     p.clock = s->clock;
     p.start = s->start;
     p.in_fpt = s->fpt[c1.level_in];
@@ -708,7 +727,7 @@ static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
     case L_PAIR: {
         PairParams ps[kMaxGroup];
         const int cnt = (int)la.convs.size();
-        for (int m = 0; m < cnt; m++) ps[m] = pair_params(s, s->convs[la.convs[m]], la.pair_variant, n);
+        for (int m = 0; m < cnt; m++) ps[m] = pair_params(s, s->convs[la.convs[m]], la.pair_variant, n, cnt);
         return launch_pair(la.pair_variant, ps, cnt, st);
     }
     case L_SPECTRUM:
@@ -1112,7 +1131,8 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
     case L_PAIR: {
         const PairShape t = pair_variant(la.pair_variant);
         set("dc::pair_kernel<" + std::to_string(t.MB) + ", " + std::to_string(t.NB) + ", " + std::to_string(t.WGM) +
-            ", " + std::to_string(t.WGN) + ", " + std::to_string(t.KCH) + ", " + std::to_string(t.MB1) + ">");
+            ", " + std::to_string(t.WGN) + ", " + std::to_string(t.KCH) + ", " + std::to_string(t.LZ) + ", " +
+            std::to_string(t.LH) + ">");
         for (int ci : la.convs) {   // both convs' work; z once, the output once, both weights
             const ConvOp& a = s->convs[ci];
             const ConvOp& b2 = s->convs[a.partner];

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define DC_ABI_VERSION 1
+#define DC_ABI_VERSION 2
 #define DC_MAX_STAGES 4
 #define DC_MAX_RB 4
 #define DC_MAX_DIL 4
@@ -55,7 +55,11 @@ typedef enum { DC_F32 = 0, DC_BF16 = 1 } dc_dtype;
 enum {
     DC_HOST_PTRS = 1u << 0, /* tokens/audio are host pointers; each call is synchronous          */
     DC_NO_GRAPH = 1u << 1,  /* never capture or replay a graph; always launch kernels directly   */
-    DC_NO_FUSE = 1u << 2    /* run every resblock conv as its own launch (no fused pairs)        */
+    DC_NO_FUSE = 1u << 2,   /* run every resblock conv as its own launch (no fused pairs)        */
+    DC_FLUSH_CATALOG = 1u << 3 /* also capture one graph per partial-chunk size n in [1, chunk_tokens)
+                                  (Design, "Scope: catalog width": a flush at a turn boundary adds
+                                  at most one class per admissible extent below the chunk); not
+                                  with DC_NO_GRAPH                                                 */
 };
 
 /*
@@ -82,7 +86,7 @@ typedef struct dc_cfg {
     int32_t batch;                       /* B independent streams sharing the weights             */
     int32_t chunk_tokens;                /* the chunk shape captured as a graph                   */
     int32_t max_tokens;                  /* largest n accepted by dc_decode_chunk                 */
-    uint32_t flags;                      /* DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE               */
+    uint32_t flags;                      /* DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE | DC_FLUSH_CATALOG */
     int32_t tile_variant;                /* 0: automatic; v > 0 forces tile shape v-1 everywhere
                                             it fits (results are identical by construction)      */
     void* hip_stream;                    /* hipStream_t all work is ordered on; NULL: own stream  */
@@ -90,8 +94,8 @@ typedef struct dc_cfg {
 
 typedef struct dc_stats {
     int64_t calls;            /* dc_decode_chunk calls that launched work                       */
-    int64_t replays;          /* ... of which replayed the captured graph                       */
-    int64_t direct_shape;     /* direct launches because n != chunk_tokens                      */
+    int64_t replays;          /* ... of which replayed a captured graph (chunk or flush class)  */
+    int64_t direct_shape;     /* direct launches because no class was captured for n            */
     int64_t direct_nograph;   /* direct launches because no graph exists (DC_NO_GRAPH)          */
     int64_t staged_tokens;    /* token copies into the fixed token buffer (caller not aliased)  */
     int64_t staged_audio;     /* PCM copies out of the fixed audio buffer (caller not aliased)  */
@@ -104,6 +108,9 @@ typedef struct dc_stats {
     int32_t kernels_per_step; /* kernel launches of one chunk step                              */
     int32_t graph_nodes;      /* nodes of the captured graph (0 if none)                        */
     double capture_ms;        /* wall time of warm-up, capture and instantiation at dc_init     */
+    int64_t replays_flush;    /* replays of a partial-chunk class (DC_FLUSH_CATALOG)            */
+    int32_t graph_classes;    /* captured shape classes: 0, 1 or chunk_tokens                   */
+    int32_t reserved;
 } dc_stats;
 
 typedef struct dc_state dc_state;
@@ -135,8 +142,10 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
  * Passing dc_token_buffer(s) / dc_audio_buffer(s) aliases the fixed buffers and
  * avoids the staging copy of that side.
  * Admission (Design, compute rule clauses (i)-(ii), fail-closed): n ==
- * chunk_tokens replays the captured graph; any other 0 < n <= max_tokens runs
- * the same kernels directly (bit-identical output, counted as direct_shape).
+ * chunk_tokens replays the captured graph; with DC_FLUSH_CATALOG so does
+ * 0 < n < chunk_tokens (its own class, counted in replays and replays_flush);
+ * any other 0 < n <= max_tokens runs the same kernels directly (bit-identical
+ * output, counted as direct_shape).
  * n <= 0 or NULL pointers: DC_EINVAL; n > max_tokens: DC_ERANGE; both leave
  * the state unchanged.  Token ids outside [0, vocab): with DC_HOST_PTRS,
  * DC_ERANGE before any launch, state unchanged; with device pointers the

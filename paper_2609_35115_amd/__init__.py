@@ -17,10 +17,10 @@ from . import synth  # noqa: F401  (workload shapes and seeded inputs)
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libdc.so")
 
-DC_ABI_VERSION = 1
+DC_ABI_VERSION = 2
 DC_OK, DC_EINVAL, DC_ERANGE, DC_ENOMEM, DC_EDEVICE, DC_ESTATE, DC_EVERSION = 0, -1, -2, -3, -4, -5, -6
 DC_F32, DC_BF16 = 0, 1
-DC_HOST_PTRS, DC_NO_GRAPH, DC_NO_FUSE = 1, 2, 4
+DC_HOST_PTRS, DC_NO_GRAPH, DC_NO_FUSE, DC_FLUSH_CATALOG = 1, 2, 4, 8
 STATUS_NAMES = {0: "DC_OK", -1: "DC_EINVAL", -2: "DC_ERANGE", -3: "DC_ENOMEM", -4: "DC_EDEVICE",
                 -5: "DC_ESTATE", -6: "DC_EVERSION"}
 
@@ -61,7 +61,8 @@ class DcStats(ctypes.Structure):
         ("staged_audio", ctypes.c_int64), ("rejected", ctypes.c_int64), ("clock_tokens", ctypes.c_int64),
         ("arena_bytes", ctypes.c_int64), ("weight_bytes", ctypes.c_int64), ("carry_bytes", ctypes.c_int64),
         ("ring_bytes", ctypes.c_int64), ("kernels_per_step", ctypes.c_int32), ("graph_nodes", ctypes.c_int32),
-        ("capture_ms", ctypes.c_double),
+        ("capture_ms", ctypes.c_double), ("replays_flush", ctypes.c_int64), ("graph_classes", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:

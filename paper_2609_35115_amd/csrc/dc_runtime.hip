@@ -111,6 +111,9 @@ struct dc_state {
     float* table = nullptr;
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
+    // DC_FLUSH_CATALOG: one class per partial-chunk size n (index n, 1 <= n < chunk_tokens)
+    std::vector<hipGraph_t> flush_graph;
+    std::vector<hipGraphExec_t> flush_exec;
     dc_stats st{};
     int64_t clock_host = 0;
     bool poisoned = false;
@@ -179,7 +182,8 @@ static std::string validate(const dc_cfg* c)
     if (c->batch < 1 || c->batch > 65536) return "batch must be in [1, 65536]";
     if (c->chunk_tokens < 1 || c->max_tokens < c->chunk_tokens) return "need 1 <= chunk_tokens <= max_tokens";
     if ((int64_t)c->max_tokens * samples_per_token(c) > (int64_t)1 << 30) return "max_tokens too large";
-    if (c->flags & ~(uint32_t)(DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE)) return "unknown flag bits";
+    if (c->flags & ~(uint32_t)(DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE | DC_FLUSH_CATALOG)) return "unknown flag bits";
+    if ((c->flags & DC_FLUSH_CATALOG) && (c->flags & DC_NO_GRAPH)) return "DC_FLUSH_CATALOG needs graphs (not DC_NO_GRAPH)";
     if (c->tile_variant < 0 || c->tile_variant > num_tile_variants()) return "tile_variant out of range";
     return "";
 }
@@ -908,16 +912,30 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     if (e == hipSuccess && !(c.flags & DC_NO_GRAPH)) {
         hipStream_t cs = nullptr;
         e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
-        if (e == hipSuccess) e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
-        if (e == hipSuccess) {
-            const hipError_t le = enqueue_step(s, c.chunk_tokens, cs);
-            e = hipStreamEndCapture(cs, &s->graph);
-            if (le != hipSuccess) e = le;
-        }
-        if (e == hipSuccess) e = hipGraphInstantiate(&s->exec, s->graph, nullptr, nullptr, 0);
+        // one class: the whole step for n tokens (its kernel arguments, the
+        // clock advance included, are fixed by n)
+        auto capture = [&](int n, hipGraph_t* g, hipGraphExec_t* x) {
+            hipError_t ce = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+            if (ce != hipSuccess) return ce;
+            const hipError_t le = enqueue_step(s, n, cs);
+            ce = hipStreamEndCapture(cs, g);
+            if (le != hipSuccess) return le;
+            if (ce != hipSuccess) return ce;
+            return hipGraphInstantiate(x, *g, nullptr, nullptr, 0);
+        };
+        if (e == hipSuccess) e = capture(c.chunk_tokens, &s->graph, &s->exec);
         if (e == hipSuccess) {
             size_t nodes = 0;
             if (hipGraphGetNodes(s->graph, nullptr, &nodes) == hipSuccess) s->st.graph_nodes = (int32_t)nodes;
+            s->st.graph_classes = 1;
+        }
+        if (e == hipSuccess && (c.flags & DC_FLUSH_CATALOG)) {
+            s->flush_graph.assign(c.chunk_tokens, nullptr);
+            s->flush_exec.assign(c.chunk_tokens, nullptr);
+            for (int n = 1; n < c.chunk_tokens && e == hipSuccess; n++) {
+                e = capture(n, &s->flush_graph[n], &s->flush_exec[n]);
+                if (e == hipSuccess) s->st.graph_classes++;
+            }
         }
         if (cs) (void)hipStreamDestroy(cs);
     }
@@ -972,6 +990,11 @@ dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* 
         e = hipGraphLaunch(s->exec, s->stream);
         if (e != hipSuccess) return device_fail(s, e, "hipGraphLaunch");
         s->st.replays++;
+    } else if (n < c.chunk_tokens && (size_t)n < s->flush_exec.size() && s->flush_exec[n]) {
+        e = hipGraphLaunch(s->flush_exec[n], s->stream);
+        if (e != hipSuccess) return device_fail(s, e, "hipGraphLaunch");
+        s->st.replays++;
+        s->st.replays_flush++;
     } else {
         e = enqueue_step(s, n, s->stream);
         if (e != hipSuccess) return device_fail(s, e, "direct launch");
@@ -1195,6 +1218,10 @@ void dc_free(dc_state* s)
     if (s->stream) (void)hipStreamSynchronize(s->stream);
     if (s->exec) (void)hipGraphExecDestroy(s->exec);
     if (s->graph) (void)hipGraphDestroy(s->graph);
+    for (hipGraphExec_t x : s->flush_exec)
+        if (x) (void)hipGraphExecDestroy(x);
+    for (hipGraph_t g : s->flush_graph)
+        if (g) (void)hipGraphDestroy(g);
     if (s->arena) (void)hipFree(s->arena);
     if (s->own_stream && s->stream) (void)hipStreamDestroy(s->stream);
     delete s;

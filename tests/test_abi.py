@@ -33,7 +33,8 @@ def test_library_exports_every_declared_symbol():
 def test_struct_sizes_match_header_layout():
     # dc_cfg: 33 int32 fields + float + uint32 -> padded to 8 before the pointer
     assert ctypes.sizeof(dc.DcCfg) == 152
-    assert ctypes.sizeof(dc.DcStats) == 12 * 8 + 2 * 4 + 8
+    # dc_stats: 12 int64, 2 int32, a double, then replays_flush and two int32
+    assert ctypes.sizeof(dc.DcStats) == 12 * 8 + 2 * 4 + 8 + 8 + 2 * 4
 
 
 @pytest.mark.parametrize("name", list(synth.WORKLOADS))
@@ -73,6 +74,10 @@ def test_init_rejects_bad_configs_before_any_device_call():
     c = good()
     c.flags = 1 << 7
     assert _init_status(c, blob)[0] == dc.DC_EINVAL
+    c = good()
+    c.flags = dc.DC_FLUSH_CATALOG | dc.DC_NO_GRAPH   # a catalog needs graphs
+    assert _init_status(c, blob)[0] == dc.DC_EINVAL
+    assert "DC_FLUSH_CATALOG" in dc.dc_last_error(None)
     c = good()
     assert _init_status(c, blob[:-1])[0] == dc.DC_EINVAL
     assert "blob size" in dc.dc_last_error(None)

@@ -56,10 +56,12 @@ enum {
     DC_HOST_PTRS = 1u << 0, /* tokens/audio are host pointers; each call is synchronous          */
     DC_NO_GRAPH = 1u << 1,  /* never capture or replay a graph; always launch kernels directly   */
     DC_NO_FUSE = 1u << 2,   /* run every resblock conv as its own launch (no fused pairs)        */
-    DC_FLUSH_CATALOG = 1u << 3 /* also capture one graph per partial-chunk size n in [1, chunk_tokens)
+    DC_FLUSH_CATALOG = 1u << 3, /* also capture one graph per partial-chunk size n in [1, chunk_tokens)
                                   (Design, "Scope: catalog width": a flush at a turn boundary adds
                                   at most one class per admissible extent below the chunk); not
                                   with DC_NO_GRAPH                                                 */
+    DC_NO_RING = 1u << 4    /* bf16 convs never stage weights through the LDS ring (ablation);
+                               the PCM is bit-identical either way                                */
 };
 
 /*
@@ -86,7 +88,8 @@ typedef struct dc_cfg {
     int32_t batch;                       /* B independent streams sharing the weights             */
     int32_t chunk_tokens;                /* the chunk shape captured as a graph                   */
     int32_t max_tokens;                  /* largest n accepted by dc_decode_chunk                 */
-    uint32_t flags;                      /* DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE | DC_FLUSH_CATALOG */
+    uint32_t flags;                      /* DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE | DC_FLUSH_CATALOG |
+                                            DC_NO_RING */
     int32_t tile_variant;                /* 0: automatic; v > 0 forces tile shape v-1 everywhere
                                             it fits (results are identical by construction)      */
     void* hip_stream;                    /* hipStream_t all work is ordered on; NULL: own stream  */

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_PKG, "libdc.so")
 DC_ABI_VERSION = 2
 DC_OK, DC_EINVAL, DC_ERANGE, DC_ENOMEM, DC_EDEVICE, DC_ESTATE, DC_EVERSION = 0, -1, -2, -3, -4, -5, -6
 DC_F32, DC_BF16 = 0, 1
-DC_HOST_PTRS, DC_NO_GRAPH, DC_NO_FUSE, DC_FLUSH_CATALOG = 1, 2, 4, 8
+DC_HOST_PTRS, DC_NO_GRAPH, DC_NO_FUSE, DC_FLUSH_CATALOG, DC_NO_RING = 1, 2, 4, 8, 16
 STATUS_NAMES = {0: "DC_OK", -1: "DC_EINVAL", -2: "DC_ERANGE", -3: "DC_ENOMEM", -4: "DC_EDEVICE",
                 -5: "DC_ESTATE", -6: "DC_EVERSION"}
 

@@ -65,8 +65,8 @@ struct ConvParams {
 // Block of 4 waves: WGM x WGN waves tile the output, each wave MB x NB MFMA
 // blocks of 16x16; WGK waves split K (each takes every WGK-th K chunk of a
 // tap).  KCH is the channel block in MFMA K chunks.  WGK and KCH are part of
-// a layer's arithmetic (they fix the order of the fp32 sums); MB, NB, WGM
-// and WGN are not.
+// a layer's arithmetic (they fix the order of the fp32 sums); MB, NB, WGM,
+// WGN and W (how weight fragments reach the waves) are not.
 // One launch runs the same tile shape over up to kMaxGroup convs that differ
 // only in taps, weights, bias and their input, output and residual rings
 // (the parallel branches of a resblock stage): blockIdx.z selects the member.
@@ -91,6 +91,7 @@ struct ConvGroup {
 
 struct TileShape {
     int MB, NB, WGM, WGN, WGK, KCH;
+    int W = 0;   // 1: weights through an LDS ring shared by the block's waves (bf16, WGK = 1)
     int BM() const { return 16 * MB * WGM; }
     int BN() const { return 16 * NB * WGN; }
     int S() const { return WGK; }

@@ -200,6 +200,135 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Out
     }
 }
 
+// Operand rows [t0 - halo, t0 - halo + rows) of channel block cb of stream b,
+// read through the input ring (ring slot base_in holds row 0), LeakyReLU'd
+// if asked, converted once to the operand type (bf16: optionally as hi + lo
+// halves, the lo rows lo_off elements after the hi rows) and stored in LDS
+// rows of LDW elements.  Rows at or past the call's frames are zeros.
+template <bool BF16, int CB, int LDW>
+__device__ __forceinline__ void stage_operand(const ConvParams& p, const void* in_ptr, int in_R, int b, int t0,
+                                              int halo, int rows, int base_in, int cb,
+                                              typename OpT<BF16>::T* lds, int lo_off)
+{
+    constexpr int VPR = CB / 8;
+    for (int v = threadIdx.x; v < rows * VPR; v += 256) {
+        const int r = v / VPR, c8 = (v - r * VPR) * 8;
+        const int t = t0 - halo + r;
+        const int ch = cb * CB + c8;
+        float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        if (t < p.F && ch < p.in_C) {
+            load8(in_ptr, p.in_elem, ((size_t)b * in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x);
+            if (p.in_act) {
+#pragma unroll
+                for (int e = 0; e < 8; e++) x[e] = lrelu(x[e], p.slope);
+            }
+        }
+        if constexpr (BF16) {
+            if (p.split)
+                store8_lds_split(lds + r * LDW + c8, lds + lo_off + r * LDW + c8, x);
+            else
+                store8_lds(lds + r * LDW + c8, x);
+        } else {
+            store8_lds(lds + r * LDW + c8, x);
+        }
+    }
+}
+
+// Bias of this wave's output columns: lane l holds the four consecutive
+// columns 4*(l/16) .. +3 of each of its 16-column blocks (zeros past N).
+template <int NB>
+__device__ __forceinline__ void load_bias(const ConvParams& p, const float* bias_ptr, int n0, int colblk0, int lane,
+                                          f32x4 (&bias)[NB])
+{
+    const int cg = (lane >> 4) * 4;
+#pragma unroll
+    for (int nb = 0; nb < NB; nb++) {
+        const int n4 = n0 + (colblk0 + nb) * 16 + cg;
+        const int nv = p.N - n4 < 4 ? p.N - n4 : 4;
+#pragma unroll
+        for (int e = 0; e < 4; e++) bias[nb][e] = e < nv ? bias_ptr[n4 + e] : 0.f;
+    }
+}
+
+// Epilogue of a tile with one K partition: bias (preloaded by load_bias),
+// residual, branch mean, LeakyReLU, stored through the output ring (rs slots
+// set by the caller).  The wave holds MB x NB blocks of 16x16 whose rows start
+// at tile row row0 and whose 16-column blocks start at colblk0; the weights
+// are the MFMA A operand and the frames the B operand, so lane l holds output
+// channels 4*(l/16) .. +3 of frame l%16 of each block: four consecutive
+// channels of one frame, stored as one vector.
+template <int MB, int NB>
+__device__ __forceinline__ void store_tile(const ConvParams& p, const OutRef& rs, const f32x4 (&acc)[MB][NB],
+                                           const f32x4 (&bias)[NB], int b, int t0, int n0, int row0, int colblk0,
+                                           int lane)
+{
+    const int fl = lane & 15, cg = (lane >> 4) * 4;
+    int rp[NB], co[NB], nv[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; nb++) {
+        const int n4 = n0 + (colblk0 + nb) * 16 + cg;
+        rp[nb] = p.u == 1 ? 0 : n4 / p.out_C;
+        co[nb] = n4 - rp[nb] * p.out_C;
+        nv[nb] = p.N - n4 < 4 ? p.N - n4 : 4;
+    }
+    // the wave's columns are all real and vector-aligned, and no branch mean:
+    // the residual loads of row block mb + 1 are issued before row block mb
+    // is finished (rows past the call's frames read its last frame and
+    // store nothing).  Otherwise each output vector loads what it adds.
+    const bool full = (p.out_C & 3) == 0 && n0 + (colblk0 + NB) * 16 <= p.N && p.n_mean == 0;
+    if (full) {
+        auto off_of = [&](int mb) {
+            const int tl = row0 + mb * 16 + fl;
+            return (t0 + tl < p.F ? tl : p.F - 1 - t0) * p.u;
+        };
+        f32x4 ld[2][NB];
+        auto issue = [&](int mb, f32x4 (&q)[NB]) {
+            const int off = off_of(mb);
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++)
+                q[nb] = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(rs.res_s, off + rp[nb], rs.res_R)) *
+                                                     p.out_C + co[nb]);
+        };
+        if (rs.res) issue(0, ld[0]);
+#pragma unroll
+        for (int mb = 0; mb < MB; mb++) {
+            if (rs.res && mb + 1 < MB) issue(mb + 1, ld[(mb + 1) & 1]);
+            const int off = off_of(mb);
+            const bool live = t0 + row0 + mb * 16 + fl < p.F;
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++) {
+                f32x4 v = acc[mb][nb] + bias[nb];
+                if (rs.res) v = ld[mb & 1][nb] + v;
+                if (p.out_act) {
+#pragma unroll
+                    for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
+                }
+                if (!live) continue;
+                const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off + rp[nb], rs.out_R)) * p.out_C + co[nb];
+                if (p.out_elem == kF32) {
+                    *(f32x4*)((float*)rs.out + oo) = v;
+                } else {
+                    typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+                    u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                    *(u32x2*)((uint16_t*)rs.out + oo) = h;
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int mb = 0; mb < MB; mb++) {
+            const int tl = row0 + mb * 16 + fl;
+            if (t0 + tl >= p.F) continue;
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++) {
+                if (nv[nb] <= 0) continue;
+                f32x4 v = acc[mb][nb];
+                store_out4(p, b, rs, tl * p.u + rp[nb], co[nb], v + bias[nb], nv[nb]);
+            }
+        }
+    }
+}
+
 template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int KCH>
 __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
 {
@@ -322,27 +451,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
 
     // Operand rows [t0 - halo, t0 + BM) of channel block cb, through the ring.
     auto load_operand = [&](int cb) {
-        for (int v = tid; v < rows * VPR; v += 256) {
-            const int r = v / VPR, c8 = (v - r * VPR) * 8;
-            const int t = t0 - halo + r;
-            const int ch = cb * CB + c8;
-            float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            if (t < p.F && ch < p.in_C) {
-                load8(in_ptr, p.in_elem, ((size_t)b * in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x);
-                if (p.in_act) {
-#pragma unroll
-                    for (int e = 0; e < 8; e++) x[e] = lrelu(x[e], p.slope);
-                }
-            }
-            if constexpr (BF16) {
-                if (p.split)
-                    store8_lds_split(lds + r * LDW + c8, lds + (rows + r) * LDW + c8, x);
-                else
-                    store8_lds(lds + r * LDW + c8, x);
-            } else {
-                store8_lds(lds + r * LDW + c8, x);
-            }
-        }
+        stage_operand<BF16, CB, LDW>(p, in_ptr, in_R, b, t0, halo, rows, base_in, cb, lds, lo_off);
     };
 
     // Large per-wave tiles (at least 8 fragments): the step pipeline below.
@@ -464,73 +573,9 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
     // four consecutive channels of one frame, stored as one vector.
     const int fl = lane & 15, cg = (lane >> 4) * 4;
     if constexpr (WGK == 1) {
-        int rp[NB], co[NB], nv[NB];
         f32x4 bias[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; nb++) {
-            const int n4 = n0 + (wn * NB + nb) * 16 + cg;
-            rp[nb] = p.u == 1 ? 0 : n4 / p.out_C;
-            co[nb] = n4 - rp[nb] * p.out_C;
-            nv[nb] = p.N - n4 < 4 ? p.N - n4 : 4;
-#pragma unroll
-            for (int e = 0; e < 4; e++) bias[nb][e] = e < nv[nb] ? bias_ptr[n4 + e] : 0.f;
-        }
-        // the wave's columns are all real and vector-aligned, and no branch mean:
-        // the residual loads of row block mb + 1 are issued before row block mb
-        // is finished (rows past the call's frames read its last frame and
-        // store nothing).  Otherwise each output vector loads what it adds.
-        const bool full = (p.out_C & 3) == 0 && n0 + (wn * NB + NB) * 16 <= p.N && p.n_mean == 0;
-        if (full) {
-            auto off_of = [&](int mb) {
-                const int tl = wm * 16 * MB + mb * 16 + fl;
-                return (t0 + tl < p.F ? tl : p.F - 1 - t0) * p.u;
-            };
-            f32x4 ld[2][NB];
-            auto issue = [&](int mb, f32x4 (&q)[NB]) {
-                const int off = off_of(mb);
-#pragma unroll
-                for (int nb = 0; nb < NB; nb++)
-                    q[nb] = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(rs.res_s, off + rp[nb], rs.res_R)) *
-                                                         p.out_C + co[nb]);
-            };
-            if (rs.res) issue(0, ld[0]);
-#pragma unroll
-            for (int mb = 0; mb < MB; mb++) {
-                if (rs.res && mb + 1 < MB) issue(mb + 1, ld[(mb + 1) & 1]);
-                const int off = off_of(mb);
-                const bool live = t0 + wm * 16 * MB + mb * 16 + fl < p.F;
-#pragma unroll
-                for (int nb = 0; nb < NB; nb++) {
-                    f32x4 v = acc[mb][nb] + bias[nb];
-                    if (rs.res) v = ld[mb & 1][nb] + v;
-                    if (p.out_act) {
-#pragma unroll
-                        for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
-                    }
-                    if (!live) continue;
-                    const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off + rp[nb], rs.out_R)) * p.out_C + co[nb];
-                    if (p.out_elem == kF32) {
-                        *(f32x4*)((float*)rs.out + oo) = v;
-                    } else {
-                        typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
-                        u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-                        *(u32x2*)((uint16_t*)rs.out + oo) = h;
-                    }
-                }
-            }
-        } else {
-#pragma unroll
-            for (int mb = 0; mb < MB; mb++) {
-                const int tl = wm * 16 * MB + mb * 16 + fl;
-                if (t0 + tl >= p.F) continue;
-#pragma unroll
-                for (int nb = 0; nb < NB; nb++) {
-                    if (nv[nb] <= 0) continue;
-                    f32x4 v = acc[mb][nb];
-                    store_out4(p, b, rs, tl * p.u + rp[nb], co[nb], v + bias[nb], nv[nb]);
-                }
-            }
-        }
+        load_bias<NB>(p, bias_ptr, n0, wn * NB, lane, bias);
+        store_tile<MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
     } else {
         // partial sums of every partition through LDS, added in partition order
         __syncthreads();
@@ -561,6 +606,172 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
     }
 }
 
+// ------------------------------------------- conv with an LDS weight ring
+//
+// bf16 operands, one K partition.  The same tiling and K order as
+// conv_kernel (so the same bits for the same channel block), but the weight
+// fragments of each K step go through a ring of kRing LDS slots that every
+// wave of the block reads: the block fetches each fragment once (not once per
+// wave row), with direct global->LDS loads that hold no registers while in
+// flight, kRing - 2 steps ahead.  Each step is published by one barrier; a
+// wave reads the fragments of step s + 1 (weights from the ring, frames from
+// the operand tile) while its MFMAs of step s run.
+constexpr int kRing = 4;
+
+#define DC_LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+template <int MB, int NB, int WGM, int WGN, int KCH>
+__global__ __launch_bounds__(256, 2) void wconv_kernel(const ConvGroup g)
+{
+    const ConvParams& p = g.p;
+    const void* in_ptr = p.in;
+    int in_R = (int)p.in_R;
+    const void* w_ptr = p.wp;
+    const float* bias_ptr = p.bias;
+    OutRef rs{p.out, p.res, (int)p.out_R, (int)p.res_R, 0, 0, 0};
+    int k = p.k;
+    if (blockIdx.z > 0) {
+        const ConvMember& m = g.m[blockIdx.z - 1];
+        in_ptr = m.in;
+        in_R = (int)m.in_R;
+        w_ptr = m.wp;
+        bias_ptr = m.bias;
+        rs.out = m.out;
+        rs.out_R = (int)m.out_R;
+        rs.res = m.res;
+        rs.res_R = (int)m.res_R;
+        k = m.k;
+    }
+    using T = uint16_t;
+    constexpr int BM = 16 * MB * WGM, BN = 16 * NB * WGN;
+    constexpr int CB = 32 * KCH, LDW = CB + OpT<true>::PAD;
+    constexpr int NFR = BN / 16;            // weight fragments (16 columns x 32 channels) per K step
+    constexpr int FPW = NFR / 4;            // of which each wave loads FPW
+    static_assert(WGM * WGN == 4 && NFR % 4 == 0, "wide tile shape");
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    u32x4* ring = reinterpret_cast<u32x4*>(smem);                            // [kRing][NFR][64 lanes]
+    T* lds = reinterpret_cast<T*>(smem + kRing * NFR * 1024);                // operand rows
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WGM, wn = wave / WGM;
+    const int b = blockIdx.x / p.tiles_t;
+    const int t0 = (blockIdx.x - b * p.tiles_t) * BM;
+    const int n0 = blockIdx.y * BN;
+    const int halo = (k - 1) * p.d;
+    const int rows = BM + halo;
+    const int64_t tau0 = p.clock[0] * p.in_fpt;
+    const int base_in = (int)ring_slot(tau0 + t0 - halo, in_R);
+    const int lo_off = rows * LDW;
+    const int kk = k * KCH;                 // K steps per channel block
+    const int nsteps = p.n_cb * kk;
+    const u32x4* wp = reinterpret_cast<const u32x4*>(w_ptr);
+
+    // direct loads of K step st into ring slot st % kRing (steps past the
+    // last load the last step again, into a slot already consumed, so every
+    // wave issues the same number of loads per step and its wait counts stay
+    // exact); column blocks past the layer's last re-read it
+    int fcol[FPW];
+#pragma unroll
+    for (int q = 0; q < FPW; q++) {
+        const int c = n0 / 16 + wave + 4 * q;
+        fcol[q] = c < p.NB16 ? c : p.NB16 - 1;
+    }
+    auto issue = [&](int st) {
+        u32x4* dst = ring + (st % kRing) * NFR * 64;
+        st = st < nsteps ? st : nsteps - 1;
+        const u32x4* src = wp + (size_t)st * p.NB16 * 64 + lane;
+#pragma unroll
+        for (int q = 0; q < FPW; q++)
+            __builtin_amdgcn_global_load_lds((const void*)(src + (size_t)fcol[q] * 64),
+                                             DC_LDS_PTR(dst + (wave + 4 * q) * 64), 16, 0, 0);
+    };
+
+    f32x4 acc[MB][NB];
+#pragma unroll
+    for (int i = 0; i < MB; i++)
+#pragma unroll
+        for (int j = 0; j < NB; j++) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const T* a_lane = lds + (wm * 16 * MB + (lane & 15)) * LDW + (lane >> 4) * 8;
+    // fragments of K step st (local step sl within its channel block)
+    auto readf = [&](int st, int sl, u32x4 (&a)[MB], u32x4 (&w)[NB]) {
+        const int j = sl / KCH, kc = sl - (sl / KCH) * KCH;
+        const u32x4* wr = ring + (st % kRing) * NFR * 64 + wn * NB * 64 + lane;
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++) w[nb] = wr[nb * 64];
+        const T* as = a_lane + j * p.d * LDW + kc * 32;
+#pragma unroll
+        for (int mb = 0; mb < MB; mb++) a[mb] = *(const u32x4*)(as + mb * 16 * LDW);
+    };
+    auto mma = [&](int sl, const u32x4 (&a)[MB], const u32x4 (&w)[NB]) {
+#pragma unroll
+        for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++)
+                acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[nb]),
+                                                                     __builtin_bit_cast(bf16x8_t, a[mb]),
+                                                                     acc[mb][nb], 0, 0, 0);
+        if (p.split) {   // the low halves, right after the high halves of the same step
+            const int j = sl / KCH, kc = sl - (sl / KCH) * KCH;
+            const T* as = a_lane + lo_off + j * p.d * LDW + kc * 32;
+            bf16x8_t lo[MB];
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++) lo[mb] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(as + mb * 16 * LDW));
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++)
+                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[nb]), lo[mb],
+                                                                         acc[mb][nb], 0, 0, 0);
+        }
+    };
+    // own loads of the next step done (kRing - 3 later steps may stay in
+    // flight), then the barrier publishes everyone's
+    auto wait_step = [&] {
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kRing - 3) * FPW));
+        __builtin_amdgcn_s_barrier();
+    };
+
+    for (int q = 0; q < kRing - 1; q++) issue(q);
+    f32x4 bias[NB];   // loaded now, used by the epilogue
+    load_bias<NB>(p, bias_ptr, n0, wn * NB, lane, bias);
+    u32x4 a0[MB], w0[NB], a1[MB], w1[NB];
+    for (int cb = 0; cb < p.n_cb; cb++) {
+        const int s0 = cb * kk;
+        if (cb > 0) __syncthreads();   // every wave is done with the previous channel block's rows
+        stage_operand<true, CB, LDW>(p, in_ptr, in_R, b, t0, halo, rows, base_in, cb, lds, lo_off);
+        // the rows (and, since their loads wait for every earlier load, the
+        // ring slots of steps up to s0 + kRing - 2) are in place
+        __syncthreads();
+        readf(s0, 0, a0, w0);
+        int sl = 0;
+        for (; sl + 1 < kk; sl += 2) {
+            wait_step();
+            issue(s0 + sl + kRing - 1);
+            readf(s0 + sl + 1, sl + 1, a1, w1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(sl, a0, w0);
+            __builtin_amdgcn_sched_barrier(0);
+            wait_step();
+            issue(s0 + sl + kRing);
+            const int nx = sl + 2 < kk ? sl + 2 : sl + 1;   // (the block's last step re-reads itself)
+            readf(s0 + nx, nx, a0, w0);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(sl + 1, a1, w1);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (sl < kk) mma(sl, a0, w0);
+    }
+
+    const int64_t tau_out0 = (tau0 + t0) * p.u;
+    rs.out_s = (int)ring_slot(tau_out0, rs.out_R);
+    rs.res_s = rs.res ? (int)ring_slot(tau_out0, rs.res_R) : 0;
+    rs.mean_s = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
+    store_tile<MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
+}
+
 // ------------------------------------------------------------- tile table
 
 // Every shape exists for both operand types; KCH is the channel block in
@@ -587,6 +798,14 @@ static const TileShape kTiles[] = {
     {1, 1, 1, 1, 4, 32},   // 17: 16x16, 4 partitions, wide channel block
     {1, 2, 1, 1, 4, 16},   // 18: 16x32
     {1, 1, 2, 2, 1, 1},    // 19: 32x32, narrow channel block
+    // weights through the LDS ring (wconv_kernel; bf16 only)
+    {4, 4, 2, 2, 1, 4, 1}, // 20: 128x128
+    {2, 4, 2, 2, 1, 4, 1}, // 21: 64x128
+    {4, 4, 4, 1, 1, 2, 1}, // 22: 256x64, 64-channel blocks
+    {2, 4, 4, 1, 1, 2, 1}, // 23: 128x64, 64-channel blocks
+    {4, 4, 4, 1, 1, 4, 1}, // 24: 256x64
+    {2, 4, 4, 1, 1, 4, 1}, // 25: 128x64
+    {1, 4, 4, 1, 1, 4, 1}, // 26: 64x64
 };
 
 int num_tile_variants() { return (int)(sizeof(kTiles) / sizeof(kTiles[0])); }
@@ -599,6 +818,7 @@ size_t conv_lds_bytes(int v, bool bf16, const ConvParams& p)
     const int pad = bf16 ? OpT<true>::PAD : OpT<false>::PAD;
     const int cb = t.KCH * (bf16 ? OpT<true>::KQ : OpT<false>::KQ);
     const size_t a = (size_t)rows * (cb + pad) * (bf16 ? 2 : 4) * (bf16 && p.split ? 2 : 1);
+    if (t.W) return (size_t)kRing * (t.BN() / 16) * 1024 + a;
     const size_t red = t.WGK > 1 ? (size_t)t.S() * t.BM() * t.BN() * 4 : 0;
     return a > red ? a : red;
 }
@@ -621,9 +841,39 @@ static hipError_t launch_t(const ConvGroup& g, int count, size_t lds, hipStream_
     return hipGetLastError();
 }
 
+template <int MB, int NB, int WGM, int WGN, int KCH>
+static hipError_t launch_w(const ConvGroup& g, int count, size_t lds, hipStream_t st)
+{
+    constexpr int BN = 16 * NB * WGN;
+    const ConvParams& p = g.p;
+    dim3 grid((unsigned)(p.B * p.tiles_t), (unsigned)((p.N + BN - 1) / BN), (unsigned)count);
+    static size_t lds_set = 64 * 1024;
+    if (lds > lds_set) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&wconv_kernel<MB, NB, WGM, WGN, KCH>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        lds_set = lds;
+    }
+    hipLaunchKernelGGL((wconv_kernel<MB, NB, WGM, WGN, KCH>), grid, dim3(256), lds, st, g);
+    return hipGetLastError();
+}
+
 template <bool BF16>
 static hipError_t launch_dt(int v, const ConvGroup& p, int count, size_t lds, hipStream_t st)
 {
+    if (v >= 20) {
+        if (!BF16) return hipErrorInvalidValue;
+        switch (v) {
+        case 20: return launch_w<4, 4, 2, 2, 4>(p, count, lds, st);
+        case 21: return launch_w<2, 4, 2, 2, 4>(p, count, lds, st);
+        case 22: return launch_w<4, 4, 4, 1, 2>(p, count, lds, st);
+        case 23: return launch_w<2, 4, 4, 1, 2>(p, count, lds, st);
+        case 24: return launch_w<4, 4, 4, 1, 4>(p, count, lds, st);
+        case 25: return launch_w<2, 4, 4, 1, 4>(p, count, lds, st);
+        case 26: return launch_w<1, 4, 4, 1, 4>(p, count, lds, st);
+        default: return hipErrorInvalidValue;
+        }
+    }
     switch (v) {
     case 0: return launch_t<BF16, 1, 1, 1, 1, 4, 4>(p, count, lds, st);
     case 1: return launch_t<BF16, 1, 1, 1, 1, 4, 8>(p, count, lds, st);

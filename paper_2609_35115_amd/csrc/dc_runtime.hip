@@ -182,7 +182,8 @@ static std::string validate(const dc_cfg* c)
     if (c->batch < 1 || c->batch > 65536) return "batch must be in [1, 65536]";
     if (c->chunk_tokens < 1 || c->max_tokens < c->chunk_tokens) return "need 1 <= chunk_tokens <= max_tokens";
     if ((int64_t)c->max_tokens * samples_per_token(c) > (int64_t)1 << 30) return "max_tokens too large";
-    if (c->flags & ~(uint32_t)(DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE | DC_FLUSH_CATALOG)) return "unknown flag bits";
+    if (c->flags & ~(uint32_t)(DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE | DC_FLUSH_CATALOG | DC_NO_RING))
+        return "unknown flag bits";
     if ((c->flags & DC_FLUSH_CATALOG) && (c->flags & DC_NO_GRAPH)) return "DC_FLUSH_CATALOG needs graphs (not DC_NO_GRAPH)";
     if (c->tile_variant < 0 || c->tile_variant > num_tile_variants()) return "tile_variant out of range";
     return "";
@@ -257,9 +258,14 @@ static bool variant_fits(const ConvOp& op, int v)
     p.d = op.d;
     p.split = op.split;
     const TileShape t = tile_variant(v);
+    if (t.W && !op.bf16) return false;   // the LDS weight ring exists for bf16 operands only
     const int npad = (op.N + 15) / 16 * 16;
     return conv_lds_bytes(v, op.bf16, p) <= 80 * 1024 && t.BN() <= (npad > 16 ? npad : 16);
 }
+
+// Shapes with the weight fragments in an LDS ring (bf16, one K partition),
+// largest first.
+static const int kPreferRing[] = {20, 24, 22, 21, 25, 23, 26};
 
 // Tile shape of a conv for this state.  Deterministic: it depends on the
 // layer, the batch and the chunk size only (never on a call's n), so every
@@ -308,6 +314,25 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
     for (int kch = 32; kch >= 1; kch /= 2) {
         if (kch > kch_all && kch > 1) continue;
         if (wgk == 1 && kch > 4) continue;
+        if (wgk == 1 && op.bf16 && !op.split && !(s->cfg.flags & DC_NO_RING)) {
+            // the ring shapes first (split operands read their low halves
+            // unprefetched there: they stay on the register-weight kernel): of those that keep enough blocks, the one
+            // with the least padding in rows and columns (then the largest)
+            int bestr = -1;
+            double bestr_score = -1.0;
+            for (int v : kPreferRing) {
+                const TileShape t = tile_variant(v);
+                if (t.KCH != kch || !variant_fits(op, v) || members * blocks(t) < 512) continue;
+                const int bn = t.BN();
+                const double col = (double)op.N / (double)(((op.N + bn - 1) / bn) * bn);
+                const double score = eff(t) * col;
+                if (score > bestr_score + 1e-9) {
+                    bestr_score = score;
+                    bestr = v;
+                }
+            }
+            if (bestr >= 0 && bestr_score >= 0.7) return bestr;
+        }
         int best = -1;
         double best_score = -1.0;
         const bool bytes_heavy = op.res >= 0 || op.N <= 64;
@@ -1131,9 +1156,13 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
     case L_CONV: {
         const ConvOp& op0 = s->convs[la.convs[0]];
         const TileShape t = tile_variant(op0.variant);
-        set("dc::conv_kernel<" + std::string(op0.bf16 ? "true" : "false") + ", " + std::to_string(t.MB) + ", " +
-            std::to_string(t.NB) + ", " + std::to_string(t.WGM) + ", " + std::to_string(t.WGN) + ", " +
-            std::to_string(t.WGK) + ", " + std::to_string(t.KCH) + ">");
+        if (t.W)
+            set("dc::wconv_kernel<" + std::to_string(t.MB) + ", " + std::to_string(t.NB) + ", " +
+                std::to_string(t.WGM) + ", " + std::to_string(t.WGN) + ", " + std::to_string(t.KCH) + ">");
+        else
+            set("dc::conv_kernel<" + std::string(op0.bf16 ? "true" : "false") + ", " + std::to_string(t.MB) + ", " +
+                std::to_string(t.NB) + ", " + std::to_string(t.WGM) + ", " + std::to_string(t.WGN) + ", " +
+                std::to_string(t.WGK) + ", " + std::to_string(t.KCH) + ">");
         for (int ci : la.convs) {   // the members' work and compulsory bytes add up
             const ConvOp& op = s->convs[ci];
             const double F = (double)n * s->fpt[op.level_in];

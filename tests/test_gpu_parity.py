@@ -111,7 +111,8 @@ def test_graph_replay_equals_direct_launch(arch_name, dtype):
 TILE_GROUPS = {
     ("tiny", "f32"): [7, 10, 13],      # 32x32, 64x64, 128x64; unsplit K, 32-channel blocks
     ("real", "f32"): [1, 4, 6],        # 16x16, 16x32, 32x32; K in 4 partitions, 64-channel blocks
-    ("real", "bf16"): [8, 9, 11],      # 32x32, 32x64, 64x64; unsplit K, 128-channel blocks
+    ("real", "bf16"): [8, 9, 11,       # 32x32, 32x64, 64x64; unsplit K, 128-channel blocks
+                       21, 22, 25, 26, 27],   # the same with weights through the LDS ring
 }
 
 

@@ -378,6 +378,31 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
     const int nblk0 = n0 / 16 + wn * NB;
     const Frag* wp = reinterpret_cast<const Frag*>(w_ptr);
 
+    // K-split tiles hold at most one output vector per thread in the
+    // epilogue: its bias and residual are loaded here, before the K loop, so
+    // the epilogue does not wait for them (a vector with a branch mean, or at
+    // the edge of the output, loads what it adds there instead)
+    const int e_idx = tid * 4;
+    const int e_tl = e_idx / BN, e_n4 = n0 + (e_idx - (e_idx / BN) * BN);
+    const bool e_live = WGK > 1 && e_idx < BM * BN && t0 + e_tl < p.F && e_n4 < p.N;
+    f32x4 e_bias = {0.f, 0.f, 0.f, 0.f}, e_res = {0.f, 0.f, 0.f, 0.f};
+    bool e_pre = false;
+    if constexpr (WGK > 1) {
+        static_assert(BM * BN <= 4 * 256, "one output vector per thread");
+        if (e_live) {
+            const int nv = p.N - e_n4 < 4 ? p.N - e_n4 : 4;
+#pragma unroll
+            for (int e = 0; e < 4; e++) e_bias[e] = e < nv ? bias_ptr[e_n4 + e] : 0.f;
+            e_pre = nv == 4 && (p.out_C & 3) == 0 && p.n_mean == 0;
+            if (e_pre && rs.res) {
+                const int rpn = p.u == 1 ? 0 : e_n4 / p.out_C;
+                const int res_s = (int)ring_slot((tau0 + t0) * p.u, rs.res_R);
+                e_res = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(res_s, e_tl * p.u + rpn, rs.res_R)) *
+                                                     p.out_C + e_n4 - rpn * p.out_C);
+            }
+        }
+    }
+
     f32x4 acc[MB][NB];
 #pragma unroll
     for (int i = 0; i < MB; i++)
@@ -589,19 +614,30 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
                 *(f32x4*)(red + (wk * BM + row) * BN + col) = acc[mb][nb];
             }
         __syncthreads();
-        for (int idx = tid * 4; idx < BM * BN; idx += 256 * 4) {
-            const int tl = idx / BN, nl = idx - tl * BN;
-            const int n4 = n0 + nl;
-            if (t0 + tl >= p.F || n4 >= p.N) continue;
-            f32x4 v = *(const f32x4*)(red + idx);
+        if (e_live) {
+            f32x4 v = *(const f32x4*)(red + e_idx);
 #pragma unroll
-            for (int q = 1; q < S; q++) v = v + *(const f32x4*)(red + q * BM * BN + idx);
-            const int nv = p.N - n4 < 4 ? p.N - n4 : 4;
-            f32x4 bias;
+            for (int q = 1; q < S; q++) v = v + *(const f32x4*)(red + q * BM * BN + e_idx);
+            v = v + e_bias;
+            const int rpn = p.u == 1 ? 0 : e_n4 / p.out_C;
+            const int off = e_tl * p.u + rpn, co = e_n4 - rpn * p.out_C;
+            if (e_pre) {   // the vector path of store_out4, with the residual loaded up front
+                if (rs.res) v = e_res + v;
+                if (p.out_act) {
 #pragma unroll
-            for (int e = 0; e < 4; e++) bias[e] = e < nv ? bias_ptr[n4 + e] : 0.f;
-            const int rpn = p.u == 1 ? 0 : n4 / p.out_C;
-            store_out4(p, b, rs, tl * p.u + rpn, n4 - rpn * p.out_C, v + bias, nv);
+                    for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
+                }
+                const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co;
+                if (p.out_elem == kF32) {
+                    *(f32x4*)((float*)rs.out + oo) = v;
+                } else {
+                    typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+                    u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                    *(u32x2*)((uint16_t*)rs.out + oo) = h;
+                }
+            } else {
+                store_out4(p, b, rs, off, co, v, p.N - e_n4 < 4 ? p.N - e_n4 : 4);
+            }
         }
     }
 }
@@ -1019,6 +1055,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     };
     // weight fragments of tap j (channel block of all C channels, one partition)
     const int nblk0 = wn * NB;
+    // both convs' biases of this wave's columns, loaded once for the whole run
+    f32x4 bias1[NB], bias2[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; nb++) {
+        bias1[nb] = *(const f32x4*)(b1 + (nblk0 + nb) * 16 + cg);
+        bias2[nb] = *(const f32x4*)(b2 + (nblk0 + nb) * 16 + cg);
+    }
     auto load_tap = [&](const Frag* wp, int j, Frag (&w)[KCH][NB]) {
         const Frag* wt = wp + (size_t)j * KCH * p.NB16 * 64 + lane;
 #pragma unroll
@@ -1076,9 +1119,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             }
         };
         run_taps(reinterpret_cast<const Frag*>(w1p), tap1, nothing);
-        f32x4 bias1[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; nb++) bias1[nb] = *(const f32x4*)(b1 + (nblk0 + nb) * 16 + cg);
 #pragma unroll
         for (int i = 0; i < R; i++) {
             const int f = fr + 16 * i + fl;
@@ -1142,9 +1182,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         // ---- epilogue: bias, residual z, branch mean; fp32 through the output ring
         const int out_s = (int)ring_slot(tau0 + t, out_R);
         const int mean_s = p.n_mean ? (int)ring_slot(tau0 + t, p.mean_R) : 0;
-        f32x4 bias2[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; nb++) bias2[nb] = *(const f32x4*)(b2 + (nblk0 + nb) * 16 + cg);
         // the residual loads of row block mb + 1 are issued before row block mb
         // is finished (rows past the run read its last frame and store
         // nothing); with a branch mean, each row block loads what it adds

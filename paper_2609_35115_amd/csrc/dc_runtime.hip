@@ -571,6 +571,10 @@ static void build_schedule(dc_state* s)
             return;
         }
         for (int i : m) s->convs[i].variant = s->convs[widest].variant;
+        // members with the most taps first: their blocks are the longest, and
+        // blocks are dispatched in member order (when a launch has more blocks
+        // than the machine holds, the long ones must not start last)
+        std::stable_sort(m.begin(), m.end(), [&](int a, int b) { return s->convs[a].k > s->convs[b].k; });
         s->launches.push_back({L_CONV, m, name});
     };
     const int nconv = (int)s->convs.size();

@@ -36,6 +36,9 @@ class _Arch(ctypes.Structure):
         ("n_dil", ctypes.c_int), ("dil", ctypes.c_int * 8),
         ("head_kernel", ctypes.c_int), ("n_fft", ctypes.c_int), ("hop", ctypes.c_int),
         ("slope", ctypes.c_double),
+        ("n_harmonics", ctypes.c_int),
+        ("sine_amp", ctypes.c_double), ("noise_std", ctypes.c_double),
+        ("voiced_threshold", ctypes.c_double), ("sample_rate", ctypes.c_double),
     ]
 
 
@@ -65,8 +68,15 @@ def _load():
         lib.oc_samples_per_token.argtypes = [ctypes.POINTER(_Arch)]
         lib.oc_samples_per_token.restype = ctypes.c_long
         lib.oc_decode.argtypes = [ctypes.POINTER(_Arch), ctypes.c_int, F, ctypes.c_long, I, ctypes.c_long,
-                                  D, ctypes.c_char_p, D]
+                                  D, ctypes.c_uint64, ctypes.c_uint64, D, ctypes.c_char_p, D]
         lib.oc_decode.restype = ctypes.c_int
+        U64 = ctypes.POINTER(ctypes.c_uint64)
+        lib.oc_philox4x64.argtypes = [U64, U64, U64]
+        lib.oc_u01.argtypes = [ctypes.c_uint64]
+        lib.oc_u01.restype = ctypes.c_double
+        lib.oc_box_muller.argtypes = [ctypes.c_double, ctypes.c_double, D, D]
+        lib.oc_source.argtypes = [ctypes.POINTER(_Arch), D, ctypes.c_long, ctypes.c_uint64, ctypes.c_uint64,
+                                  D, ctypes.c_double, D]
         _lib = lib
     return _lib
 
@@ -96,6 +106,11 @@ def arch_struct(arch: dict) -> _Arch:
         s.dil[i] = d
     s.head_kernel, s.n_fft, s.hop = arch["head_kernel"], arch["n_fft"], arch["hop"]
     s.slope = arch["lrelu_slope"]
+    s.n_harmonics = arch.get("n_harmonics", 0)
+    s.sine_amp = arch.get("sine_amp", 0.0)
+    s.noise_std = arch.get("noise_std", 0.0)
+    s.voiced_threshold = arch.get("voiced_threshold", 0.0)
+    s.sample_rate = arch.get("sample_rate", 1.0)
     return s
 
 
@@ -157,6 +172,40 @@ def round_bf16(x) -> np.ndarray:
     return np.array([lib.oc_round_bf16(float(v)) for v in x.ravel()], dtype=np.float32).reshape(x.shape)
 
 
+def philox4x64(ctr, key) -> np.ndarray:
+    """Philox4x64-10 block of counter ctr (4 x uint64) under key (2 x uint64)."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.empty(4, dtype=np.uint64)
+    _load().oc_philox4x64(_p(c, ctypes.c_uint64), _p(k, ctypes.c_uint64), _p(out, ctypes.c_uint64))
+    return out
+
+
+def u01(x: int) -> float:
+    return _load().oc_u01(int(x))
+
+
+def box_muller(u0: float, u1: float):
+    g0, g1 = ctypes.c_double(), ctypes.c_double()
+    _load().oc_box_muller(u0, u1, ctypes.byref(g0), ctypes.byref(g1))
+    return g0.value, g1.value
+
+
+def source(arch: dict, f0, seed: int, stream: int, merge_w, merge_b: float) -> np.ndarray:
+    """Harmonic-plus-noise excitation of one stream: f0 [F] (Hz, pre-stack
+    frame clock) -> F * prod(up_rate) * hop samples."""
+    s = arch_struct(arch)
+    f0 = _f64(f0).ravel()
+    mw = _f64(merge_w).ravel()
+    S = arch["hop"]
+    for u in arch["up_rate"]:
+        S *= u
+    out = np.empty(f0.size * S, dtype=np.float64)
+    _load().oc_source(ctypes.byref(s), _p(f0, ctypes.c_double), f0.size, seed, stream,
+                      _p(mw, ctypes.c_double), float(merge_b), _p(out, ctypes.c_double))
+    return out
+
+
 def num_threads() -> int:
     return _load().oc_num_threads()
 
@@ -168,18 +217,26 @@ def samples_per_token(arch: dict) -> int:
 
 # ---------------------------------------------------------------- the decoder
 
-def decode(arch: dict, dtype: str, blob: np.ndarray, ids, tap: str | None = None):
+def decode(arch: dict, dtype: str, blob: np.ndarray, ids, tap: str | None = None, f0=None,
+           seed: int = 0, stream: int = 0):
     """Offline decode of one stream from the zero state.
 
     Returns the fp64 PCM (len(ids) * samples_per_token samples), or
     (pcm, tap_values) when `tap` names an intermediate.  dtype "bf16" rounds
-    every parameter to bfloat16 first.
+    every parameter to bfloat16 first.  An architecture with a harmonic
+    source takes f0 (len(ids) * frames_per_token values, Hz) and the
+    generator's (seed, stream) key.
     """
     lib = _load()
     s = arch_struct(arch)
     blob = np.ascontiguousarray(blob, dtype=np.float32)
     ids = np.ascontiguousarray(ids, dtype=np.int32).ravel()
     T = ids.size
+    f0a = None
+    if arch.get("n_harmonics", 0) > 0:
+        f0a = _f64(f0).ravel()
+        if f0a.size != T * arch["frames_per_token"]:
+            raise ValueError("f0 needs len(ids) * frames_per_token values")
     spt = int(lib.oc_samples_per_token(ctypes.byref(s)))
     pcm = np.empty(T * spt, dtype=np.float64)
     tap_buf = None
@@ -187,7 +244,9 @@ def decode(arch: dict, dtype: str, blob: np.ndarray, ids, tap: str | None = None
         frames, ch = _tap_shape(arch, tap, T)
         tap_buf = np.empty((frames, ch), dtype=np.float64)
     rc = lib.oc_decode(ctypes.byref(s), 1 if dtype == "bf16" else 0, _p(blob, ctypes.c_float), blob.size,
-                       _p(ids, ctypes.c_int32), T, _p(pcm, ctypes.c_double),
+                       _p(ids, ctypes.c_int32), T,
+                       _p(f0a, ctypes.c_double) if f0a is not None else None, seed, stream,
+                       _p(pcm, ctypes.c_double),
                        tap.encode() if tap else None,
                        _p(tap_buf, ctypes.c_double) if tap_buf is not None else None)
     if rc != 0:
@@ -199,10 +258,10 @@ def _tap_shape(arch: dict, tap: str, T: int):
     F = T * arch["frames_per_token"]
     if tap == "embed" or tap.startswith("pre"):
         return F, arch["channels"][0]
-    if tap == "head":
+    if tap in ("head", "src"):
         for u in arch["up_rate"]:
             F *= u
-        return F, 2 * (arch["n_fft"] // 2 + 1)
+        return F, 2 * (arch["n_fft"] // 2 + 1) if tap == "head" else arch["hop"]
     s = int(tap[1:tap.index(".")])
     for u in arch["up_rate"][:s + 1]:
         F *= u

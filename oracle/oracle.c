@@ -37,7 +37,13 @@
  *     are not centred, and the overlap-add is divided by the constant
  *     sum_m w^2[n - hop*m] (1.5 for n_fft = 16, hop = 4);
  *   - with bf16 parameters every parameter is rounded to bfloat16 (round to
- *     nearest even) and the arithmetic stays fp64.
+ *     nearest even) and the arithmetic stays fp64;
+ *   - optionally (n_harmonics > 0) a harmonic-plus-noise excitation source,
+ *     the stochastic input of the paper's vocoder (Design, clause (iii)
+ *     effect classification: the harmonic generator draws device randomness
+ *     on every call; the adapter's device-resident constants include the
+ *     sinusoid frequency table and the harmonic multiplier), enters the last
+ *     upsampling stage: see oc_source below.
  */
 #include <math.h>
 #include <stdio.h>
@@ -60,6 +66,9 @@ typedef struct {
     int dil[8];
     int head_kernel, n_fft, hop;
     double slope;
+    /* harmonic source (off when n_harmonics == 0) */
+    int n_harmonics;
+    double sine_amp, noise_std, voiced_threshold, sample_rate;
 } oc_arch;
 
 /* ---------------------------------------------------------------- helpers */
@@ -224,6 +233,125 @@ void oc_istft(int N, int hop, long M, const double* logmag, const double* phase,
     free(frames);
 }
 
+/* ------------------------------------------------------ the source */
+
+/*
+ * Philox4x64-10, the counter-based generator of Salmon, Moraes, Dror and Shaw
+ * ("Parallel random numbers: as easy as 1, 2, 3", SC 2011), written from its
+ * published definition: ten rounds of
+ *   (c0, c1, c2, c3) <- (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0))
+ * with the key advanced by the Weyl constants (W0, W1) before every round but
+ * the first.  The paper's engine admits the vocoder because its generator is
+ * counter-based: what a kernel draws is a function of its counter, not of
+ * hidden host state (Design, clause (iii)).
+ */
+static void mulhilo64(uint64_t a, uint64_t b, uint64_t* hi, uint64_t* lo)
+{
+    unsigned __int128 p = (unsigned __int128)a * b;
+    *hi = (uint64_t)(p >> 64);
+    *lo = (uint64_t)p;
+}
+
+void oc_philox4x64(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4])
+{
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+    uint64_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3], k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; r++) {
+        if (r > 0) {
+            k0 += W0;
+            k1 += W1;
+        }
+        uint64_t hi0, lo0, hi1, lo1;
+        mulhilo64(M0, c0, &hi0, &lo0);
+        mulhilo64(M1, c2, &hi1, &lo1);
+        uint64_t n0 = hi1 ^ c1 ^ k0, n1 = lo1, n2 = hi0 ^ c3 ^ k1, n3 = lo0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* A 64-bit draw -> uniform in (0, 1): the top 53 bits, centred in their cell. */
+double oc_u01(uint64_t x) { return ((double)(x >> 11) + 0.5) * (1.0 / 9007199254740992.0); }
+
+/* Box-Muller: two uniforms -> two independent standard normals. */
+void oc_box_muller(double u0, double u1, double* g0, double* g1)
+{
+    double r = sqrt(-2.0 * log(u0));
+    *g0 = r * cos(2.0 * M_PI * u1);
+    *g1 = r * sin(2.0 * M_PI * u1);
+}
+
+/*
+ * Harmonic-plus-noise excitation of one stream (neural source filter of the
+ * vocoder's harmonic generator; a reading of the paper, which names the
+ * generator and its device-resident sinusoid frequency table and harmonic
+ * multiplier but prints no formula):
+ *   f0[f] >= 0 Hz per frame f of the pre-stack clock, S = prod(up_rate) * hop
+ *   samples per frame, sample t = f*S + r.
+ *   Sinusoid h = 0..H (multiplier h+1): increment inc_h[f] = (h+1) f0[f] / sr
+ *   cycles per sample; phase at the start of frame f
+ *     P_h[0] = phi_h,  P_h[f+1] = frac(P_h[f] + S * inc_h[f])   (frame order),
+ *   phi_0 = 0 and phi_h = u01(Philox(ctr = (0, h, 1, 0))[0]) for h >= 1; the
+ *   phase of sample t is frac(P_h[f] + (r+1) inc_h[f]) (the running sum
+ *   includes sample t).
+ *   Voiced frame: f0[f] > voiced_threshold.  e_h[t] = voiced * A sin(2 pi phase)
+ *   + noise_h[t] * (voiced ? noise_std : A/3).
+ *   Noise: Philox(key = (seed, stream), ctr = (t, g, 0, 0)) for group
+ *   g = 0, 1, ..: its four draws give, by Box-Muller on (u0, u1) and (u2, u3),
+ *   noise_{4g}, noise_{4g+1}, noise_{4g+2}, noise_{4g+3}.
+ *   src[t] = tanh(mb + sum_{h=0..H} mw[h] e_h[t])  (h ascending).
+ * Counters are sample indices since the stream's start, so a chunked decode
+ * draws what an offline one does.  src receives F * S samples.
+ */
+void oc_source(const oc_arch* a, const double* f0, long F, uint64_t seed, uint64_t stream,
+               const double* mw, double mb, double* src)
+{
+    int H1 = a->n_harmonics + 1;
+    long S = a->hop;
+    for (int s = 0; s < a->n_stages; s++) S *= a->up_rate[s];
+    uint64_t key[2] = {seed, stream};
+    double* P = (double*)malloc(sizeof(double) * (size_t)(F + 1) * H1);
+    for (int h = 0; h < H1; h++) {
+        double p0 = 0.0;
+        if (h > 0) {
+            uint64_t ctr[4] = {0, (uint64_t)h, 1, 0}, o[4];
+            oc_philox4x64(ctr, key, o);
+            p0 = oc_u01(o[0]);
+        }
+        P[h] = p0;
+        for (long f = 0; f < F; f++) {
+            double inc = (double)(h + 1) * f0[f] / a->sample_rate;
+            double x = P[(size_t)f * H1 + h] + (double)S * inc;
+            P[(size_t)(f + 1) * H1 + h] = x - floor(x);
+        }
+    }
+    int groups = (H1 + 3) / 4;
+#pragma omp parallel for schedule(static)
+    for (long t = 0; t < F * S; t++) {
+        long f = t / S, r = t - f * S;
+        int voiced = f0[f] > a->voiced_threshold;
+        double noise[64];
+        for (int g = 0; g < groups; g++) {
+            uint64_t ctr[4] = {(uint64_t)t, (uint64_t)g, 0, 0}, o[4];
+            oc_philox4x64(ctr, key, o);
+            oc_box_muller(oc_u01(o[0]), oc_u01(o[1]), &noise[4 * g], &noise[4 * g + 1]);
+            oc_box_muller(oc_u01(o[2]), oc_u01(o[3]), &noise[4 * g + 2], &noise[4 * g + 3]);
+        }
+        double acc = 0.0;
+        for (int h = 0; h < H1; h++) {
+            double inc = (double)(h + 1) * f0[f] / a->sample_rate;
+            double x = P[(size_t)f * H1 + h] + (double)(r + 1) * inc;
+            double ph = x - floor(x);
+            double e = (voiced ? a->sine_amp * sin(2.0 * M_PI * ph) : 0.0) +
+                       noise[h] * (voiced ? a->noise_std : a->sine_amp / 3.0);
+            acc += mw[h] * e;
+        }
+        src[t] = tanh(mb + acc);
+    }
+    free(P);
+}
+
 /* ---------------------------------------------------------- the decoder */
 
 typedef struct {
@@ -252,6 +380,7 @@ long oc_blob_floats(const oc_arch* a)
     }
     long hc = 2 * (a->n_fft / 2 + 1);
     n += hc * a->channels[a->n_stages] * a->head_kernel + hc;
+    if (a->n_harmonics > 0) n += (a->n_harmonics + 1) + 1 + (long)a->channels[a->n_stages] * a->hop + a->channels[a->n_stages];
     return n;
 }
 
@@ -279,16 +408,21 @@ static double* phi_copy(const double* x, size_t n, double slope)
 
 /*
  * Offline decode of one stream of T tokens from the zero state.
- * pcm receives T * samples_per_token samples.  If tap_name names an
- * intermediate ("embed", "pre<l>", "s<s>.y", "s<s>.rb<j>.h<i>",
- * "s<s>.rb<j>.z<i>", "s<s>.x", "head") its [frames][C] values are copied to
- * tap_out.  Returns 0 on success, -1 on a bad argument, -2 if the tap name
- * was given but never produced.
+ * pcm receives T * samples_per_token samples.  With the harmonic source,
+ * f0 holds T * frames_per_token frame values (Hz) and (seed, stream) key its
+ * generator; otherwise f0 may be NULL.  If tap_name names an intermediate
+ * ("embed", "pre<l>", "s<s>.y", "s<s>.rb<j>.h<i>", "s<s>.rb<j>.z<i>",
+ * "s<s>.x", "head", "src" -- the source samples as [frames of the last
+ * stage][hop]) its [frames][C] values are copied to tap_out.  Returns 0 on
+ * success, -1 on a bad argument, -2 if the tap name was given but never
+ * produced.
  */
 int oc_decode(const oc_arch* a, int bf16_params, const float* blob, long blob_n,
-              const int32_t* ids, long T, double* pcm, const char* tap_name, double* tap_out)
+              const int32_t* ids, long T, const double* f0, uint64_t seed, uint64_t stream,
+              double* pcm, const char* tap_name, double* tap_out)
 {
     if (blob_n != oc_blob_floats(a) || T <= 0) return -1;
+    if (a->n_harmonics > 0 && !f0) return -1;
     for (long t = 0; t < T; t++)
         if (ids[t] < 0 || ids[t] >= a->vocab) return -1;
     blob_reader rd = {blob, bf16_params};
@@ -332,6 +466,27 @@ int oc_decode(const oc_arch* a, int bf16_params, const float* blob, long blob_n,
         double* y = (double*)malloc(sizeof(double) * (size_t)Fo * co);
         oc_convt(ci, co, u, F, W, b, xa, y);
         free(W); free(b); free(xa); free(x);
+        if (a->n_harmonics > 0 && s == a->n_stages - 1) {
+            /* the source enters the last stage after its ConvTranspose1d:
+             * y[tau][c] += bd[c] + sum_{j<hop} Wd[c][0][j] * src[tau*hop + j]
+             * (a Conv1d from one channel, kernel = stride = hop) */
+            blob_reader sr = {blob + (blob_n - ((a->n_harmonics + 1) + 1 + (long)co * a->hop + co)), bf16_params};
+            double* mw = take(&sr, (size_t)a->n_harmonics + 1);
+            double* mb = take(&sr, 1);
+            double* Wd = take(&sr, (size_t)co * a->hop);
+            double* bd = take(&sr, (size_t)co);
+            long F0 = T * a->frames_per_token;
+            double* src = (double*)malloc(sizeof(double) * (size_t)Fo * a->hop);
+            oc_source(a, f0, F0, seed, stream, mw, mb[0], src);
+            copy_tap(tap_name, "src", src, (size_t)Fo * a->hop, tap_out, &found);
+            for (long t = 0; t < Fo; t++)
+                for (int o = 0; o < co; o++) {
+                    double sd = bd[o];
+                    for (int j = 0; j < a->hop; j++) sd += Wd[(size_t)o * a->hop + j] * src[(size_t)t * a->hop + j];
+                    y[(size_t)t * co + o] = y[(size_t)t * co + o] + sd;
+                }
+            free(mw); free(mb); free(Wd); free(bd); free(src);
+        }
         snprintf(name, sizeof name, "s%d.y", s);
         copy_tap(tap_name, name, y, (size_t)Fo * co, tap_out, &found);
 
@@ -388,7 +543,8 @@ int oc_decode(const oc_arch* a, int bf16_params, const float* blob, long blob_n,
         }
     oc_istft(a->n_fft, a->hop, F, lm, ph, pcm);
     free(lm); free(ph); free(sh);
-    if (rd.p != blob + blob_n) return -1;
+    long tail = a->n_harmonics > 0 ? (a->n_harmonics + 1) + 1 + (long)C * a->hop + C : 0;
+    if (rd.p != blob + blob_n - tail) return -1;
     if (tap_name && tap_out && !found) return -2;
     return 0;
 }

@@ -21,6 +21,9 @@ layouts):
                      per resblock kernel k_j, per dilation d:
                          W1 [C_s][C_s][k_j], b1 [C_s], W2 [C_s][C_s][k_j], b2 [C_s]
     head:            W [2*(n_fft/2+1)][C_last][head_kernel], b [2*(n_fft/2+1)]
+    harmonic source (architectures with n_harmonics > 0 only):
+                     merge W [n_harmonics+1], merge b [1],
+                     down W [C_last][1][hop], down b [C_last]
 
 Weights are N(0, 1/fan_in) with fan_in = C_in*k for a Conv1d and 2*C_in for a
 ConvTranspose1d with kernel 2u and stride u (each output reads two input
@@ -28,6 +31,14 @@ frames); biases are N(0, 1/fan_in) of their layer; the embedding is N(0, 1).
 All draws come from numpy's PCG64 seeded by SeedSequence([seed, 0]) in blob
 order, in float64, then rounded to float32.  Token ids of stream b come from
 SeedSequence([seed, 1, b]), uniform over the vocabulary.
+
+The harmonic source takes a fundamental frequency per frame of the pre-stack
+clock (f0, Hz; 0 where unvoiced).  Its synthetic contour for stream b comes
+from SeedSequence([seed, 2, b]): alternating unvoiced and voiced runs of
+geometric length (means 8 and 24 frames, i.e. 0.16 s and 0.48 s at 50 Hz),
+voiced frames following a per-stream base pitch in [90, 250] Hz times
+2^(w/12) for a random walk w of N(0, 0.25) semitone steps, clipped to
+[60, 500] Hz -- the range of speech.
 """
 from __future__ import annotations
 
@@ -52,6 +63,13 @@ REAL_ARCH = dict(
     head_kernel=7, n_fft=16, hop=4, lrelu_slope=0.1,
 )
 
+# The same decoders with the harmonic-plus-noise excitation source: the
+# fundamental and n_harmonics overtones, sine amplitude 0.1, noise 0.003 on
+# voiced frames (amplitude / 3 on unvoiced ones), voiced above 10 Hz.
+_SOURCE = dict(sine_amp=0.1, noise_std=0.003, voiced_threshold=10.0, sample_rate=24000.0)
+TINY_NSF_ARCH = dict(TINY_ARCH, n_harmonics=2, **_SOURCE)
+REAL_NSF_ARCH = dict(REAL_ARCH, n_harmonics=8, **_SOURCE)
+
 # Workloads: architecture, arithmetic type, independent streams, tokens per
 # chunk and chunks per measured pass.
 WORKLOADS = {
@@ -62,12 +80,18 @@ WORKLOADS = {
     "real_bf16_b128_n25": dict(arch=REAL_ARCH, dtype="bf16", batch=128, chunk_tokens=25, chunks=40),
 }
 
+# The harmonic source's workloads (f0 given per frame, see make_f0).
+NSF_WORKLOADS = {
+    "real_f32_b1_n25_nsf": dict(arch=REAL_NSF_ARCH, dtype="f32", batch=1, chunk_tokens=25, chunks=20),
+    "real_bf16_b16_n25_nsf": dict(arch=REAL_NSF_ARCH, dtype="bf16", batch=16, chunk_tokens=25, chunks=20),
+}
+
 SAMPLE_RATE = 24000  # output rate of the real architecture (960 samples / 25 Hz token)
 
 
 def workload(name: str) -> dict:
     """Deep copy of a named workload description."""
-    return copy.deepcopy(WORKLOADS[name])
+    return copy.deepcopy(WORKLOADS[name] if name in WORKLOADS else NSF_WORKLOADS[name])
 
 
 def head_channels(arch: dict) -> int:
@@ -102,6 +126,12 @@ def tensor_list(arch: dict):
     kh = arch["head_kernel"]
     out.append(("head.W", (hc, cl, kh), cl * kh))
     out.append(("head.b", (hc,), cl * kh))
+    nh = arch.get("n_harmonics", 0)
+    if nh > 0:
+        out.append(("src.merge.W", (nh + 1,), nh + 1))
+        out.append(("src.merge.b", (1,), nh + 1))
+        out.append(("src.down.W", (cl, 1, arch["hop"]), arch["hop"]))
+        out.append(("src.down.b", (cl,), arch["hop"]))
     return out
 
 
@@ -140,4 +170,31 @@ def make_tokens(arch: dict, batch: int, total_tokens: int, seed: int = 0,
         b = first_stream + r
         rng = np.random.default_rng(np.random.SeedSequence([seed, 1, b]))
         out[r] = rng.integers(0, arch["vocab"], size=total_tokens, dtype=np.int32)
+    return out
+
+
+def frames_per_chunk(arch: dict, tokens: int) -> int:
+    """Frames of the pre-stack clock (the f0 clock) in `tokens` tokens."""
+    return tokens * arch["frames_per_token"]
+
+
+def make_f0(arch: dict, batch: int, total_tokens: int, seed: int = 0, first_stream: int = 0) -> np.ndarray:
+    """float32 [batch][total_tokens * frames_per_token] fundamental frequency
+    per frame (Hz, 0 where unvoiced); stream b uses SeedSequence([seed, 2, b])."""
+    F = frames_per_chunk(arch, total_tokens)
+    out = np.zeros((batch, F), dtype=np.float32)
+    for r in range(batch):
+        b = first_stream + r
+        rng = np.random.default_rng(np.random.SeedSequence([seed, 2, b]))
+        base = rng.uniform(90.0, 250.0)
+        walk = 0.0
+        f, voiced = 0, bool(rng.integers(0, 2))
+        while f < F:
+            run = int(rng.geometric(1.0 / (24.0 if voiced else 8.0)))
+            for _ in range(min(run, F - f)):
+                if voiced:
+                    walk += rng.normal(0.0, 0.25)
+                    out[r, f] = np.clip(base * 2.0 ** (walk / 12.0), 60.0, 500.0)
+                f += 1
+            voiced = not voiced
     return out

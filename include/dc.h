@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define DC_ABI_VERSION 2
+#define DC_ABI_VERSION 3
 #define DC_MAX_STAGES 4
 #define DC_MAX_RB 4
 #define DC_MAX_DIL 4
@@ -92,6 +92,21 @@ typedef struct dc_cfg {
                                             DC_NO_RING */
     int32_t tile_variant;                /* 0: automatic; v > 0 forces tile shape v-1 everywhere
                                             it fits (results are identical by construction)      */
+    /* Harmonic-plus-noise excitation source (the vocoder's stochastic input;
+     * n_harmonics == 0: none, and the fields below are ignored).  Per frame of
+     * the pre-stack clock the caller gives f0 (Hz); the source sums the
+     * fundamental and n_harmonics overtones (amplitude sine_amp, voiced where
+     * f0 > voiced_threshold) and Gaussian noise (noise_std when voiced,
+     * sine_amp / 3 when not) drawn from Philox4x64-10 keyed by (rng_seed,
+     * stream index) with the sample index since the stream's start as
+     * counter, merges them with a learned linear layer and tanh, and adds it
+     * to the last stage through a Conv1d with kernel = stride = hop after the
+     * stage's ConvTranspose1d. */
+    int32_t n_harmonics;                 /* overtones besides the fundamental, 0..31              */
+    float sine_amp, noise_std;           /* sinusoid amplitude, voiced noise standard deviation   */
+    float voiced_threshold;              /* Hz                                                    */
+    float sample_rate;                   /* Hz of the output samples                              */
+    uint64_t rng_seed;                   /* key of the source's counter-based generator           */
     void* hip_stream;                    /* hipStream_t all work is ordered on; NULL: own stream  */
 } dc_cfg;
 
@@ -114,6 +129,7 @@ typedef struct dc_stats {
     int64_t replays_flush;    /* replays of a partial-chunk class (DC_FLUSH_CATALOG)            */
     int32_t graph_classes;    /* captured shape classes: 0, 1 or chunk_tokens                   */
     int32_t reserved;
+    int64_t staged_f0;        /* f0 copies into the fixed f0 buffer (caller not aliased)        */
 } dc_stats;
 
 typedef struct dc_state dc_state;
@@ -125,7 +141,9 @@ typedef struct dc_state dc_state;
  *   per pre layer: W [C0][C0][pre_kernel], b [C0];
  *   per stage s: ConvTranspose1d W [C_s][C_{s+1}][2*u_s], b [C_{s+1}], then per
  *     resblock kernel k_j, per dilation d: W1 [C][C][k_j], b1 [C], W2 [C][C][k_j], b2 [C];
- *   head: W [2*(n_fft/2+1)][C_last][head_kernel], b [2*(n_fft/2+1)].
+ *   head: W [2*(n_fft/2+1)][C_last][head_kernel], b [2*(n_fft/2+1)];
+ *   with a harmonic source (n_harmonics > 0): merge W [n_harmonics+1],
+ *     merge b [1], down W [C_last][1][hop], down b [C_last].
  * The blob is copied (rounded to bfloat16, nearest-even, when dtype is
  * DC_BF16; the head stays fp32 arithmetic on those rounded values) and may be
  * freed on return.  On success *out owns the state, reset to the start of
@@ -157,6 +175,19 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
  */
 dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* audio_out);
 
+/*
+ * dc_decode_chunk for a decoder with a harmonic source (n_harmonics > 0;
+ * dc_decode_chunk refuses such a state with DC_EINVAL, and this call refuses
+ * a state without one).  f0: float32 [batch][n * frames_per_token], Hz per
+ * frame of the pre-stack clock, in the same pointer space as tokens (passing
+ * dc_f0_buffer(s) aliases the fixed buffer).  The source's draws and phases
+ * depend only on each stream's samples since its start, so a chunked decode
+ * equals an offline one bit for bit, and a graph replay equals a direct
+ * launch (Design, clause (iii): the device generator advances along a
+ * declared clock).  Errors as dc_decode_chunk, plus DC_EINVAL for a NULL f0.
+ */
+dc_status dc_decode_chunk_f0(dc_state* s, const int32_t* tokens, const float* f0, int32_t n, float* audio_out);
+
 /* Return every stream to its start: zero every ring in place (addresses are
  * unchanged) and set the clock to 0.  Clears a poisoned state. */
 dc_status dc_reset(dc_state* s);
@@ -181,6 +212,11 @@ int64_t dc_blob_floats(const dc_cfg* cfg);
 int32_t* dc_token_buffer(dc_state* s);
 float* dc_audio_buffer(dc_state* s);
 
+/* The fixed device f0 buffer of a decoder with a harmonic source: float32
+ * [batch][max_tokens * frames_per_token] (read as [batch][n * frames_per_token]);
+ * NULL without a source. */
+float* dc_f0_buffer(dc_state* s);
+
 /* Copy the counters into *out. */
 dc_status dc_get_stats(const dc_state* s, dc_stats* out);
 
@@ -188,7 +224,8 @@ dc_status dc_get_stats(const dc_state* s, dc_stats* out);
  * Inspection of the carried state and intermediates (tests, shadow checks).
  * dc_tap_find returns the index of a named intermediate ("embed", "pre<l>",
  * "s<s>.y", "s<s>.rb<j>.h<i>" (stored as LeakyReLU of h), "s<s>.rb<j>.z<i>",
- * "s<s>.x", "head"), or -1.  dc_tap_read copies, for stream b, the frames
+ * "s<s>.x", "head", and with a harmonic source "src": its samples as frames
+ * of the last stage's clock, hop samples each), or -1.  dc_tap_read copies, for stream b, the frames
  * with absolute index [frame0, frame0 + nframes) of that ring into host
  * memory as float32 [nframes][C]; *channels receives C.  Only frames still held
  * by the ring (the last call's frames and the carried left context) are

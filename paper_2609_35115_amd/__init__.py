@@ -17,7 +17,7 @@ from . import synth  # noqa: F401  (workload shapes and seeded inputs)
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libdc.so")
 
-DC_ABI_VERSION = 2
+DC_ABI_VERSION = 3
 DC_OK, DC_EINVAL, DC_ERANGE, DC_ENOMEM, DC_EDEVICE, DC_ESTATE, DC_EVERSION = 0, -1, -2, -3, -4, -5, -6
 DC_F32, DC_BF16 = 0, 1
 DC_HOST_PTRS, DC_NO_GRAPH, DC_NO_FUSE, DC_FLUSH_CATALOG, DC_NO_RING = 1, 2, 4, 8, 16
@@ -50,6 +50,10 @@ class DcCfg(ctypes.Structure):
         ("max_tokens", ctypes.c_int32),
         ("flags", ctypes.c_uint32),
         ("tile_variant", ctypes.c_int32),
+        ("n_harmonics", ctypes.c_int32),
+        ("sine_amp", ctypes.c_float), ("noise_std", ctypes.c_float),
+        ("voiced_threshold", ctypes.c_float), ("sample_rate", ctypes.c_float),
+        ("rng_seed", ctypes.c_uint64),
         ("hip_stream", ctypes.c_void_p),
     ]
 
@@ -62,7 +66,7 @@ class DcStats(ctypes.Structure):
         ("arena_bytes", ctypes.c_int64), ("weight_bytes", ctypes.c_int64), ("carry_bytes", ctypes.c_int64),
         ("ring_bytes", ctypes.c_int64), ("kernels_per_step", ctypes.c_int32), ("graph_nodes", ctypes.c_int32),
         ("capture_ms", ctypes.c_double), ("replays_flush", ctypes.c_int64), ("graph_classes", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("reserved", ctypes.c_int32), ("staged_f0", ctypes.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -80,6 +84,7 @@ _P = ctypes.c_void_p
 SIGNATURES = {
     "dc_init": ([_P, ctypes.c_size_t, ctypes.POINTER(DcCfg), ctypes.POINTER(_P)], ctypes.c_int),
     "dc_decode_chunk": ([_P, _P, ctypes.c_int32, _P], ctypes.c_int),
+    "dc_decode_chunk_f0": ([_P, _P, _P, ctypes.c_int32, _P], ctypes.c_int),
     "dc_reset": ([_P], ctypes.c_int),
     "dc_reset_stream": ([_P, ctypes.c_int32], ctypes.c_int),
     "dc_sync": ([_P], ctypes.c_int),
@@ -87,6 +92,7 @@ SIGNATURES = {
     "dc_blob_floats": ([ctypes.POINTER(DcCfg)], ctypes.c_int64),
     "dc_token_buffer": ([_P], _P),
     "dc_audio_buffer": ([_P], _P),
+    "dc_f0_buffer": ([_P], _P),
     "dc_get_stats": ([_P, ctypes.POINTER(DcStats)], ctypes.c_int),
     "dc_tap_find": ([_P, ctypes.c_char_p], ctypes.c_int32),
     "dc_tap_read": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _P,
@@ -118,7 +124,7 @@ def lib() -> ctypes.CDLL:
 
 
 def make_cfg(arch: dict, dtype: str, batch: int, chunk_tokens: int, max_tokens: int | None = None,
-             flags: int = 0, tile_variant: int = 0, stream: int | None = None) -> DcCfg:
+             flags: int = 0, tile_variant: int = 0, stream: int | None = None, rng_seed: int = 0) -> DcCfg:
     c = DcCfg()
     c.abi_version = DC_ABI_VERSION
     c.vocab, c.embed, c.frames_per_token = arch["vocab"], arch["embed"], arch["frames_per_token"]
@@ -142,6 +148,12 @@ def make_cfg(arch: dict, dtype: str, batch: int, chunk_tokens: int, max_tokens: 
     c.max_tokens = max_tokens if max_tokens is not None else chunk_tokens
     c.flags = flags
     c.tile_variant = tile_variant
+    c.n_harmonics = arch.get("n_harmonics", 0)
+    c.sine_amp = arch.get("sine_amp", 0.0)
+    c.noise_std = arch.get("noise_std", 0.0)
+    c.voiced_threshold = arch.get("voiced_threshold", 0.0)
+    c.sample_rate = arch.get("sample_rate", 0.0)
+    c.rng_seed = rng_seed
     c.hip_stream = stream
     return c
 
@@ -176,6 +188,13 @@ def dc_decode_chunk(h, tokens, n: int, audio_out) -> int:
                                  _ptr(audio_out) if audio_out is not None else None)
 
 
+def dc_decode_chunk_f0(h, tokens, f0, n: int, audio_out) -> int:
+    """Raw call: returns the status (no exception)."""
+    return lib().dc_decode_chunk_f0(h, _ptr(tokens) if tokens is not None else None,
+                                    _ptr(f0) if f0 is not None else None, n,
+                                    _ptr(audio_out) if audio_out is not None else None)
+
+
 def dc_reset(h) -> int:
     return lib().dc_reset(h)
 
@@ -202,6 +221,10 @@ def dc_token_buffer(h) -> int:
 
 def dc_audio_buffer(h) -> int:
     return lib().dc_audio_buffer(h)
+
+
+def dc_f0_buffer(h) -> int:
+    return lib().dc_f0_buffer(h)
 
 
 def dc_get_stats(h) -> dict:
@@ -256,14 +279,15 @@ class Decoder:
     and a dedicated torch stream that every call is ordered on."""
 
     def __init__(self, arch: dict, dtype: str, blob: np.ndarray, batch: int, chunk_tokens: int,
-                 max_tokens: int | None = None, flags: int = 0, tile_variant: int = 0):
+                 max_tokens: int | None = None, flags: int = 0, tile_variant: int = 0, rng_seed: int = 0):
         import torch
         self.torch = torch
         self.arch, self.dtype, self.batch = arch, dtype, batch
         self.host = bool(flags & DC_HOST_PTRS)
         self.stream = torch.cuda.Stream()
         self.cfg = make_cfg(arch, dtype, batch, chunk_tokens, max_tokens, flags, tile_variant,
-                            self.stream.cuda_stream)
+                            self.stream.cuda_stream, rng_seed)
+        self.has_source = arch.get("n_harmonics", 0) > 0
         self.spt = dc_samples_per_token(self.cfg)
         self.chunk_tokens = chunk_tokens
         self.max_tokens = self.cfg.max_tokens
@@ -280,26 +304,41 @@ class Decoder:
         except Exception:
             pass
 
-    def decode(self, tokens, check: bool = True):
+    def decode(self, tokens, f0=None, check: bool = True):
         """tokens [batch][n] int32 (numpy in host mode, else a device tensor or
-        numpy copied to the device) -> PCM [batch][n*spt] (numpy in host mode,
-        else a device tensor)."""
+        numpy copied to the device), and for a decoder with a harmonic source
+        f0 [batch][n*frames_per_token] float32 likewise -> PCM [batch][n*spt]
+        (numpy in host mode, else a device tensor)."""
         torch = self.torch
         n = tokens.shape[1]
         if self.host:
             tok = np.ascontiguousarray(tokens, dtype=np.int32)
             out = np.empty((self.batch, n * self.spt), dtype=np.float32)
-            st = dc_decode_chunk(self.h, tok, n, out)
+            if self.has_source:
+                st = dc_decode_chunk_f0(self.h, tok, np.ascontiguousarray(f0, dtype=np.float32), n, out)
+            else:
+                st = dc_decode_chunk(self.h, tok, n, out)
         else:
             with torch.cuda.stream(self.stream):
                 if isinstance(tokens, np.ndarray):
                     tok = torch.from_numpy(np.ascontiguousarray(tokens, dtype=np.int32)).to("cuda")
                 else:
                     tok = tokens.contiguous()
+                f0d = None
+                if self.has_source and f0 is not None:
+                    if isinstance(f0, np.ndarray):
+                        f0d = torch.from_numpy(np.ascontiguousarray(f0, dtype=np.float32)).to("cuda")
+                    else:
+                        f0d = f0.contiguous()
                 out = torch.empty((self.batch, n * self.spt), dtype=torch.float32, device="cuda")
             self.stream.wait_stream(torch.cuda.current_stream())
-            st = dc_decode_chunk(self.h, tok, n, out)
+            if self.has_source:
+                st = dc_decode_chunk_f0(self.h, tok, f0d, n, out)
+            else:
+                st = dc_decode_chunk(self.h, tok, n, out)
             tok.record_stream(self.stream)
+            if f0d is not None:
+                f0d.record_stream(self.stream)
             out.record_stream(self.stream)
             torch.cuda.current_stream().wait_stream(self.stream)
         if check:
@@ -339,5 +378,7 @@ def _tap_channels(arch: dict, name: str) -> int:
         return 2 * (arch["n_fft"] // 2 + 1)
     if name == "G":
         return arch["n_fft"]
+    if name == "src":
+        return arch["hop"]
     s = int(name[1:name.index(".")])
     return arch["channels"][s + 1]

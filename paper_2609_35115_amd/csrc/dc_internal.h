@@ -60,6 +60,13 @@ struct ConvParams {
     const int64_t* clock; // tokens decoded before this call
     int64_t in_fpt;       // input-clock frames per token
     float slope;
+    // harmonic source (the last stage's ConvTranspose1d only, else null):
+    // out[frame][c] += sd_b[c] + sum_j sd_w[c][j] * src[frame][j], src a ring
+    // of 4 samples per output frame (out geometry)
+    const float* src;
+    int64_t src_R;
+    const float* sd_w;    // [out_C][4]
+    const float* sd_b;    // [out_C]
 };
 
 // Block of 4 waves: WGM x WGN waves tile the output, each wave MB x NB MFMA
@@ -178,6 +185,28 @@ hipError_t launch_spectrum(const float* head, int64_t head_R, int B, int F, cons
 // G ring -> PCM [B][F*hop] (row stride F*hop), overlap-added in ascending frame order.
 hipError_t launch_ola(Ring g, int B, int F, int hop, int n_fft, float* pcm, const int64_t* clock,
                       int64_t fpt, hipStream_t st);
+
+// Harmonic-plus-noise excitation source of one call.
+struct SourceParams {
+    const float* f0;       // [B][F0] Hz per frame of the pre-stack clock (this call)
+    double* carry;         // [B][2][H1] phase (cycles) at a frame start, two tagged slots
+    int64_t* tags;         // [B][2] the f0 frame each slot's phases belong to
+    double* ptab;          // [B][F0][H1] phase at the start of each frame of this call
+    float* src;            // ring [B][src_R][4]: the samples of each last-stage frame
+    int64_t src_R;
+    const float* mw;       // merge weights [H1]
+    const float* mb;       // merge bias [1]
+    int B, F0, H1;         // streams, frames of this call, sinusoids (fundamental + overtones)
+    int S;                 // samples per f0 frame
+    int64_t fpt0, fptL;    // f0 frames and last-stage frames per token
+    const int64_t* clock;
+    const int64_t* start;  // [B] tokens decoded when each stream last started
+    float amp, noise, thr;
+    double sr;
+    uint64_t seed;
+};
+hipError_t launch_phase(const SourceParams& p, hipStream_t st);
+hipError_t launch_source(const SourceParams& p, hipStream_t st);
 
 hipError_t launch_clock(int64_t* clock, int n, hipStream_t st);
 hipError_t launch_mark_start(int64_t* start, int b, const int64_t* clock, hipStream_t st);

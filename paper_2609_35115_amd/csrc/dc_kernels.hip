@@ -139,7 +139,36 @@ struct OutRef {
     const float* res;
     int out_R, res_R;
     int out_s, res_s, mean_s;
+    int src_s;   // ring slot of the source samples of that frame
 };
+
+// The harmonic source's contribution to output channels co .. co+3 of the
+// frame whose source samples sit at ring slot `slot`:
+//   sd_b[c] + sum_j sd_w[c][j] * src[j], j ascending.
+__device__ __forceinline__ f32x4 src_term4(const ConvParams& p, int b, int slot, int co)
+{
+    const f32x4 x = *(const f32x4*)(p.src + ((size_t)b * p.src_R + slot) * 4);
+    f32x4 v = *(const f32x4*)(p.sd_b + co);
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+        const f32x4 w = *(const f32x4*)(p.sd_w + (size_t)(co + e) * 4);
+        float a = v[e];
+#pragma unroll
+        for (int j = 0; j < 4; j++) a = a + w[j] * x[j];
+        v[e] = a;
+    }
+    return v;
+}
+
+__device__ __forceinline__ float src_term1(const ConvParams& p, int b, int slot, int co)
+{
+    const f32x4 x = *(const f32x4*)(p.src + ((size_t)b * p.src_R + slot) * 4);
+    const f32x4 w = *(const f32x4*)(p.sd_w + (size_t)co * 4);
+    float a = p.sd_b[co];
+#pragma unroll
+    for (int j = 0; j < 4; j++) a = a + w[j] * x[j];
+    return a;
+}
 
 // Slot of a frame `off` frames after a base slot, for 0 <= off < R.
 __device__ __forceinline__ int slot_add(int base, int off, int R)
@@ -152,6 +181,7 @@ __device__ __forceinline__ void store_out(const ConvParams& p, int b, const OutR
                                           float v)
 {
     // off: output frame offset from the block's base frame; co: output channel
+    if (p.src) v = v + src_term1(p, b, slot_add(rs.src_s, off, (int)p.src_R), co);
     if (rs.res) v = rs.res[((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co] + v;
     if (p.n_mean) {
         const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean_s, off, (int)p.mean_R)) * p.out_C + co;
@@ -177,6 +207,7 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Out
         for (int e = 0; e < nv; e++) store_out(p, b, rs, off, co + e, v[e]);
         return;
     }
+    if (p.src) v = v + src_term4(p, b, slot_add(rs.src_s, off, (int)p.src_R), co);
     if (rs.res) v = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co) + v;
     if (p.n_mean) {
         const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean_s, off, (int)p.mean_R)) * p.out_C + co;
@@ -298,6 +329,7 @@ __device__ __forceinline__ void store_tile(const ConvParams& p, const OutRef& rs
 #pragma unroll
             for (int nb = 0; nb < NB; nb++) {
                 f32x4 v = acc[mb][nb] + bias[nb];
+                if (p.src) v = v + src_term4(p, b, slot_add(rs.src_s, off + rp[nb], (int)p.src_R), co[nb]);
                 if (rs.res) v = ld[mb & 1][nb] + v;
                 if (p.out_act) {
 #pragma unroll
@@ -592,6 +624,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
     rs.out_s = (int)ring_slot(tau_out0, rs.out_R);
     rs.res_s = rs.res ? (int)ring_slot(tau_out0, rs.res_R) : 0;
     rs.mean_s = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
+    rs.src_s = p.src ? (int)ring_slot(tau_out0, p.src_R) : 0;
 
     // The weights are the MFMA A operand and the frames the B operand, so lane
     // l holds output channels 4*(l/16) .. +3 of frame l%16 of each 16x16 block:
@@ -622,6 +655,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
             const int rpn = p.u == 1 ? 0 : e_n4 / p.out_C;
             const int off = e_tl * p.u + rpn, co = e_n4 - rpn * p.out_C;
             if (e_pre) {   // the vector path of store_out4, with the residual loaded up front
+                if (p.src) v = v + src_term4(p, b, slot_add(rs.src_s, off, (int)p.src_R), co);
                 if (rs.res) v = e_res + v;
                 if (p.out_act) {
 #pragma unroll
@@ -805,6 +839,7 @@ __global__ __launch_bounds__(256, 2) void wconv_kernel(const ConvGroup g)
     rs.out_s = (int)ring_slot(tau_out0, rs.out_R);
     rs.res_s = rs.res ? (int)ring_slot(tau_out0, rs.res_R) : 0;
     rs.mean_s = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
+    rs.src_s = p.src ? (int)ring_slot(tau_out0, p.src_R) : 0;
     store_tile<MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
 }
 
@@ -943,7 +978,7 @@ static bool same_shape(const ConvParams& a, const ConvParams& b)
            a.N == b.N && a.NB16 == b.NB16 && a.out_C == b.out_C && a.out_elem == b.out_elem &&
            a.out_act == b.out_act && a.u == b.u && a.n_mean == b.n_mean && a.B == b.B && a.F == b.F &&
            a.tiles_t == b.tiles_t && a.clock == b.clock && a.in_fpt == b.in_fpt && a.slope == b.slope &&
-           (a.res == nullptr) == (b.res == nullptr) && (a.n_mean == 0 || (a.mean_R == b.mean_R &&
+           (a.res == nullptr) == (b.res == nullptr) && a.src == b.src && (a.n_mean == 0 || (a.mean_R == b.mean_R &&
            a.mean[0] == b.mean[0] && a.mean[1] == b.mean[1] && a.mean[2] == b.mean[2]));
 }
 
@@ -1437,6 +1472,148 @@ hipError_t launch_ola(Ring g, int B, int F, int hop, int n_fft, float* pcm, cons
     const int64_t total = (int64_t)B * F * hop;
     hipLaunchKernelGGL(ola_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, g, B, F, hop, n_fft,
                        pcm, clock, fpt);
+    return hipGetLastError();
+}
+
+
+// ------------------------------------------------ harmonic-plus-noise source
+//
+// The vocoder's stochastic input: sinusoids at the fundamental f0 and its
+// overtones plus Gaussian noise, merged by a linear layer and tanh.  Every
+// random number is a function of a counter -- the sample index since the
+// stream's start -- so replayed, direct, chunked and offline decodes draw the
+// same values (Design, clause (iii): the device generator advances along a
+// declared clock; here the clock is the stream's own sample clock rather than
+// the call count, which also makes the draws independent of the chunking).
+
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds of two
+// 64x64 -> 128-bit products, the key advanced by two Weyl constants between
+// rounds.
+struct Philox4 {
+    uint64_t v[4];
+};
+__device__ __forceinline__ Philox4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3, uint64_t k0,
+                                                 uint64_t k1)
+{
+    constexpr uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    constexpr uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; r++) {
+        const uint64_t p0_hi = __umul64hi(M0, c0), p0_lo = M0 * c0;
+        const uint64_t p1_hi = __umul64hi(M1, c2), p1_lo = M1 * c2;
+        const uint64_t n0 = p1_hi ^ c1 ^ k0, n2 = p0_hi ^ c3 ^ k1;
+        c0 = n0;
+        c1 = p1_lo;
+        c2 = n2;
+        c3 = p0_lo;
+        k0 += W0;
+        k1 += W1;
+    }
+    return Philox4{{c0, c1, c2, c3}};
+}
+
+// 64 random bits -> uniform in (0, 1): the top 53 bits, centred in their cell.
+__device__ __forceinline__ double to_u01(uint64_t x) { return ((double)(x >> 11) + 0.5) * 0x1.0p-53; }
+
+// Phase of each sinusoid at the start of every frame of this call, carried
+// across calls: one thread per (stream, sinusoid) walks the frames in order,
+// P <- frac(P + S * (h+1) f0 / sr), the fp64 operations of an offline walk.
+// A stream at its first frame starts from its initial phase (0 for the
+// fundamental, a draw of counter (0, h, 1, 0) for overtone h).  The carry
+// has two slots tagged with the f0 frame they hold: a call reads the slot of
+// its first frame and writes the other, so running a call's launch again
+// reproduces it (the carry of a stream is never overwritten in place).
+__global__ __launch_bounds__(64) void phase_kernel(const SourceParams p)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= p.B * p.H1) return;
+    const int b = i / p.H1, h = i - (i / p.H1) * p.H1;
+    const int64_t first = p.clock[0] * p.fpt0;              // f0 frame of this call's start
+    const int sel = p.tags[2 * b] == first ? 0 : 1;
+    double P = p.carry[((size_t)b * 2 + sel) * p.H1 + h];
+    if (p.clock[0] == p.start[b]) {
+        P = 0.0;
+        if (h > 0) P = to_u01(philox4x64_10(0, (uint64_t)h, 1, 0, p.seed, (uint64_t)b).v[0]);
+    }
+    const float* f0 = p.f0 + (size_t)b * p.F0;
+    double* pt = p.ptab + (size_t)b * p.F0 * p.H1 + h;
+    for (int f = 0; f < p.F0; f++) {
+        pt[(size_t)f * p.H1] = P;
+        const double inc = (double)(h + 1) * (double)f0[f] / p.sr;
+        const double x = P + (double)p.S * inc;
+        P = x - floor(x);
+    }
+    p.carry[((size_t)b * 2 + 1 - sel) * p.H1 + h] = P;
+    if (h == 0) p.tags[2 * b + 1 - sel] = first + p.F0;   // (the slot read above keeps its tag)
+}
+
+hipError_t launch_phase(const SourceParams& p, hipStream_t st)
+{
+    const int n = p.B * p.H1;
+    hipLaunchKernelGGL(phase_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64), 0, st, p);
+    return hipGetLastError();
+}
+
+// One thread per (stream, last-stage frame of this call): the frame's 4
+// samples.  Sample t of the call lies in f0 frame t / S at offset r; its
+// sinusoid h has phase frac(P_h[frame] + (r+1) (h+1) f0 / sr).  Noise of
+// sinusoids 4g .. 4g+3 comes from Philox4x64-10 with key (seed, stream) and
+// counter (sample since the stream's start, g, 0, 0), by Box-Muller on its
+// draws (0, 1) and (2, 3).  src = tanh(mb + sum_h mw[h] e_h), h ascending.
+constexpr int kMaxSinusoids = 32;
+
+__global__ __launch_bounds__(256) void source_kernel(const SourceParams p)
+{
+    const int FL = p.F0 / (int)p.fpt0 * (int)p.fptL;   // last-stage frames of this call
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)p.B * FL) return;
+    const int b = (int)(i / FL), tau = (int)(i - (i / FL) * FL);
+    const int64_t tauL = p.clock[0] * p.fptL + tau;                  // absolute last-stage frame
+    const int64_t t_rel0 = (tauL - p.start[b] * p.fptL) * 4;        // sample index since the stream's start
+    const float* f0 = p.f0 + (size_t)b * p.F0;
+    const double* ptab = p.ptab + (size_t)b * p.F0 * p.H1;
+    const int groups = (p.H1 + 3) / 4;
+    f32x4 out;
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+        const int t = tau * 4 + j;                 // sample of this call
+        const int f = t / p.S, r = t - (t / p.S) * p.S;
+        const float fv = f0[f];
+        const bool voiced = fv > p.thr;
+        const float nscale = voiced ? p.noise : p.amp / 3.0f;
+        float acc = 0.f;
+        for (int g = 0; g < groups; g++) {
+            const Philox4 x = philox4x64_10((uint64_t)(t_rel0 + j), (uint64_t)g, 0, 0, p.seed, (uint64_t)b);
+            float nz[4];
+#pragma unroll
+            for (int q = 0; q < 2; q++) {
+                const float rad = (float)sqrt(-2.0 * log(to_u01(x.v[2 * q])));
+                const float ang = (float)(2.0 * M_PI * to_u01(x.v[2 * q + 1]));
+                float sn, cs;
+                sincosf(ang, &sn, &cs);
+                nz[2 * q] = rad * cs;
+                nz[2 * q + 1] = rad * sn;
+            }
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                const int h = 4 * g + q;
+                if (h >= p.H1) break;
+                const double inc = (double)(h + 1) * (double)fv / p.sr;
+                const double ph = ptab[(size_t)f * p.H1 + h] + (double)(r + 1) * inc;
+                const float frac = (float)(ph - floor(ph));
+                const float sine = voiced ? p.amp * sinf(6.28318530717958647692f * frac) : 0.f;
+                acc = acc + p.mw[h] * (sine + nz[q] * nscale);
+            }
+        }
+        out[j] = tanhf(p.mb[0] + acc);
+    }
+    *(f32x4*)(p.src + ((size_t)b * p.src_R + ring_slot(tauL, p.src_R)) * 4) = out;
+}
+
+hipError_t launch_source(const SourceParams& p, hipStream_t st)
+{
+    const int64_t n = (int64_t)p.B * (p.F0 / p.fpt0 * p.fptL);
+    hipLaunchKernelGGL(source_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p);
     return hipGetLastError();
 }
 

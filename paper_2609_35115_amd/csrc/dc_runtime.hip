@@ -48,10 +48,11 @@ struct ConvOp {
     int level_in = 0;
     int stage = -1, branch = -1, dil_i = -1, half = 0;   // resblock position (-1: not a resblock conv)
     int partner = -1;    // fused pair: the other conv of the pair (h stays on chip)
+    int src_ring = -1;   // the last stage's ConvTranspose1d with a harmonic source: its samples
 };
 
 // One kernel launch of a chunk step.
-enum LaunchKind { L_EMBED, L_CONV, L_PAIR, L_SPECTRUM, L_OLA, L_CLOCK };
+enum LaunchKind { L_EMBED, L_CONV, L_PAIR, L_SPECTRUM, L_OLA, L_CLOCK, L_PHASE, L_SOURCE };
 struct Launch {
     LaunchKind kind;
     std::vector<int> convs;   // members of a conv launch (same tile shape; parallel branches);
@@ -96,11 +97,15 @@ struct dc_state {
     std::vector<bool> ring_onchip;   // h of a fused pair: never materialised (R = 0)
     std::vector<ConvOp> convs;
     std::vector<Launch> launches;
-    int ring_E = -1, ring_S = -1, ring_G = -1;
+    int ring_E = -1, ring_S = -1, ring_G = -1, ring_src = -1;
     int levels = 0;
     int64_t fpt[DC_MAX_STAGES + 2] = {};
     int64_t spt = 0;
     size_t emb_off = 0, table_off = 0, tok_off = 0, audio_off = 0, clock_off = 0, start_off = 0, err_off = 0;
+    // harmonic source: merge weights and bias, down-conv weights and bias,
+    // the f0 buffer, the carried phases and the per-call phase table
+    size_t src_w_off = 0, src_down_off = 0, f0_off = 0, phase_off = 0, ptab_off = 0;
+    float* f0 = nullptr;
     size_t ring_begin = 0, ring_end = 0;
     int32_t* tok = nullptr;
     float* audio = nullptr;
@@ -154,8 +159,11 @@ static int64_t blob_floats(const dc_cfg* c)
     }
     int64_t hc = 2 * (c->n_fft / 2 + 1);
     n += hc * c->channels[c->n_stages] * c->head_kernel + hc;
+    if (c->n_harmonics > 0) n += (c->n_harmonics + 1) + 1 + (int64_t)c->channels[c->n_stages] * c->hop + c->channels[c->n_stages];
     return n;
 }
+
+static constexpr int kMaxSinusoidsHost = 32;   // the source kernel's bound on n_harmonics + 1
 
 static std::string validate(const dc_cfg* c)
 {
@@ -186,6 +194,13 @@ static std::string validate(const dc_cfg* c)
         return "unknown flag bits";
     if ((c->flags & DC_FLUSH_CATALOG) && (c->flags & DC_NO_GRAPH)) return "DC_FLUSH_CATALOG needs graphs (not DC_NO_GRAPH)";
     if (c->tile_variant < 0 || c->tile_variant > num_tile_variants()) return "tile_variant out of range";
+    if (c->n_harmonics < 0 || c->n_harmonics >= kMaxSinusoidsHost) return "n_harmonics must be in [0, 31]";
+    if (c->n_harmonics > 0) {
+        if (!(c->sine_amp >= 0.0f && c->sine_amp < 1e6f) || !(c->noise_std >= 0.0f && c->noise_std < 1e6f))
+            return "sine_amp and noise_std must be finite and >= 0";
+        if (!(c->sample_rate > 0.0f && c->sample_rate < 1e9f)) return "sample_rate must be positive";
+        if (!(c->voiced_threshold > -1e30f && c->voiced_threshold < 1e30f)) return "voiced_threshold must be finite";
+    }
     return "";
 }
 
@@ -446,6 +461,8 @@ static void build_network(dc_state* s)
     for (int st = 0; st < c.n_stages; st++) {
         const int ci = c.channels[st], co = c.channels[st + 1], u = c.up_rate[st];
         const std::string sn = "s" + std::to_string(st);
+        const bool src_here = c.n_harmonics > 0 && st == c.n_stages - 1;
+        if (src_here) s->ring_src = add_ring(s, "src", c.hop, kF32, st + 1);   // ctx 0: one call's samples
         const int Y = add_ring(s, sn + ".y", co, kF32, st + 1);
         {
             ConvOp op;
@@ -467,6 +484,7 @@ static void build_network(dc_state* s)
             off += (size_t)ci * co * 2 * u;
             op.blob_b = off;
             off += (size_t)co;
+            if (src_here) op.src_ring = s->ring_src;
             s->convs.push_back(op);
             need_ctx(s, cur, 1);
         }
@@ -556,6 +574,10 @@ static void build_schedule(dc_state* s)
 {
     const dc_cfg& c = s->cfg;
     s->launches.push_back({L_EMBED, {}, "embed"});
+    if (c.n_harmonics > 0) {
+        s->launches.push_back({L_PHASE, {}, "src.phase"});
+        s->launches.push_back({L_SOURCE, {}, "src"});
+    }
     auto add_group = [&](std::vector<int> m, const std::string& name) {
         int widest = m[0];
         for (int i : m)
@@ -692,6 +714,40 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
     p.clock = s->clock;
     p.in_fpt = s->fpt[op.level_in];
     p.slope = c.lrelu_slope;
+    if (op.src_ring >= 0) {
+        p.src = (const float*)s->rings[op.src_ring].ptr;
+        p.src_R = s->rings[op.src_ring].R;
+        p.sd_w = (const float*)(s->arena + s->src_down_off);
+        p.sd_b = p.sd_w + (size_t)op.out_C * c.hop;
+    }
+    return p;
+}
+
+static SourceParams source_params(const dc_state* s, int n)
+{
+    const dc_cfg& c = s->cfg;
+    SourceParams p{};
+    p.f0 = s->f0;
+    p.carry = (double*)(s->arena + s->phase_off);
+    p.tags = (int64_t*)(p.carry + (size_t)c.batch * 2 * (c.n_harmonics + 1));
+    p.ptab = (double*)(s->arena + s->ptab_off);
+    p.src = (float*)s->rings[s->ring_src].ptr;
+    p.src_R = s->rings[s->ring_src].R;
+    p.mw = (const float*)(s->arena + s->src_w_off);
+    p.mb = p.mw + c.n_harmonics + 1;
+    p.B = c.batch;
+    p.F0 = (int)(n * s->fpt[0]);
+    p.H1 = c.n_harmonics + 1;
+    p.S = (int)(s->fpt[c.n_stages] / s->fpt[0] * c.hop);
+    p.fpt0 = s->fpt[0];
+    p.fptL = s->fpt[c.n_stages];
+    p.clock = s->clock;
+    p.start = s->start;
+    p.amp = c.sine_amp;
+    p.noise = c.noise_std;
+    p.thr = c.voiced_threshold;
+    p.sr = (double)c.sample_rate;
+    p.seed = c.rng_seed;
     return p;
 }
 
@@ -763,6 +819,10 @@ static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
         for (int m = 0; m < cnt; m++) ps[m] = pair_params(s, s->convs[la.convs[m]], la.pair_variant, n, cnt);
         return launch_pair(la.pair_variant, ps, cnt, st);
     }
+    case L_PHASE:
+        return launch_phase(source_params(s, n), st);
+    case L_SOURCE:
+        return launch_source(source_params(s, n), st);
     case L_SPECTRUM:
         return launch_spectrum((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL,
                                s->table, s->rings[s->ring_G], s->clock, s->fpt[L], st);
@@ -850,6 +910,11 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
         op.w_off = take(op.w_bytes);
         op.b_off = take((size_t)op.N * sizeof(float));
     }
+    const int CL = c.channels[c.n_stages];
+    if (c.n_harmonics > 0) {
+        s->src_w_off = take((size_t)(c.n_harmonics + 2) * sizeof(float));
+        s->src_down_off = take((size_t)CL * (c.hop + 1) * sizeof(float));
+    }
     const size_t weights_end = off;
     s->ring_begin = off;
     int64_t carry = 0;
@@ -861,7 +926,19 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
         r.ptr = (void*)take((size_t)c.batch * r.R * r.C * es);  // offset for now
         carry += (int64_t)c.batch * r.ctx * r.C * es;
     }
+    if (c.n_harmonics > 0) {
+        // the carried phases sit with the rings: a reset zeroes them (a
+        // stream at its first frame starts from its initial phases anyway)
+        const size_t pb = (size_t)c.batch * 2 * (c.n_harmonics + 1) * sizeof(double) +
+                          (size_t)c.batch * 2 * sizeof(int64_t);
+        s->phase_off = take(pb);
+        carry += (int64_t)pb;
+    }
     s->ring_end = off;
+    if (c.n_harmonics > 0) {
+        s->ptab_off = take((size_t)c.batch * c.max_tokens * s->fpt[0] * (c.n_harmonics + 1) * sizeof(double));
+        s->f0_off = take((size_t)c.batch * c.max_tokens * s->fpt[0] * sizeof(float));
+    }
     s->tok_off = take((size_t)c.batch * c.max_tokens * sizeof(int32_t));
     s->audio_off = take((size_t)c.batch * c.max_tokens * s->spt * sizeof(float));
     s->clock_off = take(sizeof(int64_t));
@@ -882,6 +959,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     s->clock = (int64_t*)(s->arena + s->clock_off);
     s->start = (int64_t*)(s->arena + s->start_off);
     s->err = (int*)(s->arena + s->err_off);
+    if (c.n_harmonics > 0) s->f0 = (float*)(s->arena + s->f0_off);
 
     if (c.hip_stream) {
         s->stream = (hipStream_t)c.hip_stream;
@@ -926,6 +1004,16 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
         pack_weights(op, blob, bf, host.data() + op.w_off);
         float* bias = (float*)(host.data() + op.b_off);
         for (int n = 0; n < op.N; n++) bias[n] = round_param(blob[op.blob_b + (op.transposed ? n % op.out_C : n)], bf);
+    }
+    if (c.n_harmonics > 0) {
+        // merge W [H1], merge b, then down W [CL][hop] and down b [CL]: the
+        // blob's last tensors, in that order
+        const size_t H1 = (size_t)c.n_harmonics + 1;
+        const float* tail = blob + (blob_floats(&c) - (int64_t)(H1 + 1 + (size_t)CL * c.hop + CL));
+        float* mw = (float*)(host.data() + s->src_w_off);
+        for (size_t i = 0; i < H1 + 1; i++) mw[i] = round_param(tail[i], bf);
+        float* dw = (float*)(host.data() + s->src_down_off);
+        for (size_t i = 0; i < (size_t)CL * c.hop + CL; i++) dw[i] = round_param(tail[H1 + 1 + i], bf);
     }
     s->st.weight_bytes = (int64_t)weights_end;
     s->st.arena_bytes = (int64_t)s->arena_bytes;
@@ -981,14 +1069,15 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     return DC_OK;
 }
 
-dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* audio_out)
+// One call: admission, staging of tokens (and f0), replay or direct launch,
+// staging of the PCM.  f0 is non-null exactly for a decoder with a source.
+static dc_status decode_call(dc_state* s, const int32_t* tokens, const float* f0, int32_t n, float* audio_out)
 {
-    if (!s) return DC_EINVAL;
     if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned; call dc_reset");
     const dc_cfg& c = s->cfg;
-    if (!tokens || !audio_out) {
+    if (!tokens || !audio_out || (c.n_harmonics > 0 && !f0)) {
         s->st.rejected++;
-        return fail(s, DC_EINVAL, "tokens or audio_out is NULL");
+        return fail(s, DC_EINVAL, "tokens, f0 or audio_out is NULL");
     }
     if (n <= 0) {
         s->st.rejected++;
@@ -1015,6 +1104,12 @@ dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* 
         if (e != hipSuccess) return device_fail(s, e, "token staging");
         s->st.staged_tokens++;
     }
+    if (c.n_harmonics > 0 && f0 != s->f0) {
+        const size_t f0_bytes = (size_t)c.batch * n * s->fpt[0] * sizeof(float);
+        e = hipMemcpyAsync(s->f0, f0, f0_bytes, host ? hipMemcpyHostToDevice : hipMemcpyDeviceToDevice, s->stream);
+        if (e != hipSuccess) return device_fail(s, e, "f0 staging");
+        s->st.staged_f0++;
+    }
     if (n == c.chunk_tokens && s->exec) {
         e = hipGraphLaunch(s->exec, s->stream);
         if (e != hipSuccess) return device_fail(s, e, "hipGraphLaunch");
@@ -1040,6 +1135,26 @@ dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* 
     }
     if (host) return dc_sync(s);
     return DC_OK;
+}
+
+dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* audio_out)
+{
+    if (!s) return DC_EINVAL;
+    if (s->cfg.n_harmonics > 0) {
+        s->st.rejected++;
+        return fail(s, DC_EINVAL, "this decoder has a harmonic source: call dc_decode_chunk_f0");
+    }
+    return decode_call(s, tokens, nullptr, n, audio_out);
+}
+
+dc_status dc_decode_chunk_f0(dc_state* s, const int32_t* tokens, const float* f0, int32_t n, float* audio_out)
+{
+    if (!s) return DC_EINVAL;
+    if (s->cfg.n_harmonics == 0) {
+        s->st.rejected++;
+        return fail(s, DC_EINVAL, "this decoder has no harmonic source: call dc_decode_chunk");
+    }
+    return decode_call(s, tokens, f0, n, audio_out);
 }
 
 dc_status dc_sync(dc_state* s)
@@ -1088,6 +1203,8 @@ dc_status dc_reset_stream(dc_state* s, int32_t b)
 int32_t* dc_token_buffer(dc_state* s) { return s ? s->tok : nullptr; }
 
 float* dc_audio_buffer(dc_state* s) { return s ? s->audio : nullptr; }
+
+float* dc_f0_buffer(dc_state* s) { return s ? s->f0 : nullptr; }
 
 dc_status dc_get_stats(const dc_state* s, dc_stats* out)
 {
@@ -1201,6 +1318,18 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
                           B * (F + (a.k - 1) * a.d + (a.k - 1)) * a.Ci * 4 + B * F * b2.N * 4 +
                           b2.n_mean * B * F * b2.N * 4;
         }
+        break;
+    }
+    case L_PHASE: {
+        const double F0 = (double)n * s->fpt[0], H1 = c.n_harmonics + 1;
+        set("dc::phase_kernel");
+        out->bytes = B * F0 * 4 + B * F0 * H1 * 8 + 2 * B * H1 * 8;
+        break;
+    }
+    case L_SOURCE: {
+        const double F0 = (double)n * s->fpt[0], H1 = c.n_harmonics + 1;
+        set("dc::source_kernel");
+        out->bytes = B * F0 * 4 + B * F0 * H1 * 8 + B * FL * c.hop * 4;
         break;
     }
     case L_SPECTRUM:

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def declared_functions():
     text = open(os.path.join(ROOT, "include", "dc.h")).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(dc_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(dc_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_and_binding_agree():
@@ -31,10 +31,11 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_sizes_match_header_layout():
-    # dc_cfg: 33 int32 fields + float + uint32 -> padded to 8 before the pointer
-    assert ctypes.sizeof(dc.DcCfg) == 152
-    # dc_stats: 12 int64, 2 int32, a double, then replays_flush and two int32
-    assert ctypes.sizeof(dc.DcStats) == 12 * 8 + 2 * 4 + 8 + 8 + 2 * 4
+    # dc_cfg: 34 int32 fields + float + uint32 (144 bytes), the source's int32
+    # and four floats (164, padded to 168), the uint64 seed and the pointer
+    assert ctypes.sizeof(dc.DcCfg) == 168 + 8 + 8
+    # dc_stats: 12 int64, 2 int32, a double, then replays_flush, two int32 and staged_f0
+    assert ctypes.sizeof(dc.DcStats) == 12 * 8 + 2 * 4 + 8 + 8 + 2 * 4 + 8
 
 
 @pytest.mark.parametrize("name", list(synth.WORKLOADS))
@@ -81,11 +82,25 @@ def test_init_rejects_bad_configs_before_any_device_call():
     c = good()
     assert _init_status(c, blob[:-1])[0] == dc.DC_EINVAL
     assert "blob size" in dc.dc_last_error(None)
+    # the harmonic source: its blob holds the extra tensors, its fields are checked
+    nsf = synth.TINY_NSF_ARCH
+    nblob = synth.make_weights(nsf)
+    c = dc.make_cfg(nsf, "f32", 1, 8, 8)
+    assert dc.dc_blob_floats(c) == synth.blob_floats(nsf) == blob.size + (nsf["n_harmonics"] + 2) + 8 * 5
+    assert _init_status(c, blob)[0] == dc.DC_EINVAL            # the source tensors are missing
+    c.n_harmonics = 40
+    assert _init_status(c, nblob)[0] == dc.DC_EINVAL
+    c = dc.make_cfg(nsf, "f32", 1, 8, 8)
+    c.sample_rate = 0.0
+    assert _init_status(c, nblob)[0] == dc.DC_EINVAL
+    assert "sample_rate" in dc.dc_last_error(None)
 
 
 def test_null_state_calls_fail_closed():
     L = dc.lib()
     assert L.dc_decode_chunk(None, None, 1, None) == dc.DC_EINVAL
+    assert L.dc_decode_chunk_f0(None, None, None, 1, None) == dc.DC_EINVAL
+    assert L.dc_f0_buffer(None) is None
     assert L.dc_reset(None) == dc.DC_EINVAL
     assert L.dc_sync(None) == dc.DC_EINVAL
     assert L.dc_token_buffer(None) is None

@@ -40,6 +40,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 # reads half the bytes the copy moves, WRITE_SIZE all of them.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 DEFAULT_WORKLOAD = "real_f32_b1_n25"
+RNG_SEED = 11   # key of the harmonic source's generator (workloads with a source)
 PEAK = {"hbm": 8000.0, "bf16": 2500.0, "f32": 157.3}   # GB/s, TFLOP/s (MI355X, dense)
 
 
@@ -51,17 +52,21 @@ class _Addr:
         return self.addr
 
 
-def cpu_baseline(arch, dtype, blob, tokens, budget_s: float):
+def cpu_baseline(arch, dtype, blob, tokens, budget_s: float, f0=None):
     """Time the oracle (as it stands) decoding a prefix of stream 0, growing the
     prefix until one run takes budget_s or the workload's tokens run out."""
     import oracle
     from paper_2609_35115_amd import synth
     spt = synth.samples_per_token(arch)
+    fpt = arch["frames_per_token"]
     T_full = tokens.shape[1]
     T = min(T_full, 4)
     while True:
         t0 = time.perf_counter()
-        oracle.decode(arch, dtype, blob, tokens[0, :T])
+        if f0 is None:
+            oracle.decode(arch, dtype, blob, tokens[0, :T])
+        else:
+            oracle.decode(arch, dtype, blob, tokens[0, :T], f0=f0[0, :T * fpt], seed=RNG_SEED, stream=0)
         dt = time.perf_counter() - t0
         if dt >= budget_s or T >= T_full:
             break
@@ -109,20 +114,25 @@ def roofline(layers, us, dtype):
         g["launches"] += 1
     name, g = max(groups.items(), key=lambda kv: kv[1]["us"])
     step_us = sum(us)
-    conv = name.startswith(("dc::conv_kernel", "dc::pair_kernel"))   # MFMA kernels (a fused pair is bf16)
-    op = "bf16" if "<true" in name or name.startswith("dc::pair_kernel") else "f32"
+    conv = name.startswith(("dc::conv_kernel", "dc::wconv_kernel", "dc::pair_kernel"))   # MFMA kernels
+    op = "bf16" if "<true" in name or name.startswith(("dc::pair_kernel", "dc::wconv_kernel")) else "f32"
     if conv and g["flops"] / g["bytes"] > PEAK[op] * 1e12 / (PEAK["hbm"] * 1e9):
         bound, achieved, peak, unit = "mfma", g["flops"] / (g["us"] * 1e-6) / 1e12, PEAK[op], "TFLOP/s"
     else:
         bound, achieved, peak, unit = "hbm", g["bytes"] / (g["us"] * 1e-6) / 1e9, PEAK["hbm"], "GB/s"
     per_kernel = sorted(((k, v["us"] / step_us) for k, v in groups.items()), key=lambda kv: -kv[1])
+    src = None
+    if "dc::source_kernel" in groups:
+        sg, pg = groups["dc::source_kernel"], groups.get("dc::phase_kernel", {"us": 0.0})
+        src = {"source_kernel_us": round(sg["us"], 3), "phase_kernel_us": round(pg["us"], 3),
+               "share_of_step": round((sg["us"] + pg["us"]) / step_us, 4)}
     return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": None,
             "kernel": name, "operand": op, "launches_per_step": g["launches"],
             "mean_launch_us": round(g["us"] / g["launches"], 3),
             "flops_per_launch": g["flops"] / g["launches"], "bytes_per_launch": g["bytes"] / g["launches"],
             "share_of_step": round(g["us"] / step_us, 4),
-            "kernels_by_share": [[k, round(v, 4)] for k, v in per_kernel[:6]]}
+            "kernels_by_share": [[k, round(v, 4)] for k, v in per_kernel[:6]], "source": src}
 
 
 def calibrate_copy():
@@ -290,16 +300,25 @@ def main():
     w = synth.workload(args.workload)
     arch, dtype, B, n, chunks = w["arch"], w["dtype"], w["batch"], w["chunk_tokens"], w["chunks"]
     spt = synth.samples_per_token(arch)
+    fpt = arch["frames_per_token"]
+    has_src = arch.get("n_harmonics", 0) > 0
     torch.cuda.set_device(0)
     blob = synth.make_weights(arch, 0)
     tokens = synth.make_tokens(arch, B, chunks * n)
     tok_dev = torch.from_numpy(np.ascontiguousarray(tokens.reshape(B, chunks, n).transpose(1, 0, 2))).cuda()
-    dec = dc.Decoder(arch, dtype, blob, batch=B, chunk_tokens=n, tile_variant=args.tile_variant)
+    f0 = f0_dev = None
+    if has_src:   # the source's f0 contour, resident like the tokens
+        f0 = synth.make_f0(arch, B, chunks * n)
+        f0_dev = torch.from_numpy(np.ascontiguousarray(f0.reshape(B, chunks, n * fpt).transpose(1, 0, 2))).cuda()
+    dec = dc.Decoder(arch, dtype, blob, batch=B, chunk_tokens=n, tile_variant=args.tile_variant, rng_seed=RNG_SEED)
     audio = _Addr(dc.dc_audio_buffer(dec.h))
     torch.cuda.synchronize()
 
     def step(i):
-        st = dc.dc_decode_chunk(dec.h, tok_dev[i % chunks], n, audio)
+        if has_src:
+            st = dc.dc_decode_chunk_f0(dec.h, tok_dev[i % chunks], f0_dev[i % chunks], n, audio)
+        else:
+            st = dc.dc_decode_chunk(dec.h, tok_dev[i % chunks], n, audio)
         if st != dc.DC_OK:
             raise dc.DcError(st, dc.dc_last_error(dec.h))
 
@@ -344,13 +363,17 @@ def main():
     # host buffers: dc_decode_chunk uploads the tokens, replays the step and
     # returns once the PCM is in host memory
     hdec = dc.Decoder(arch, dtype, blob, batch=B, chunk_tokens=n, flags=dc.DC_HOST_PTRS,
-                      tile_variant=args.tile_variant)
+                      tile_variant=args.tile_variant, rng_seed=RNG_SEED)
     pcm = np.empty((B, n * spt), dtype=np.float32)
     host_tok = [np.ascontiguousarray(tokens[:, c * n:(c + 1) * n]) for c in range(chunks)]
+    host_f0 = [np.ascontiguousarray(f0[:, c * n * fpt:(c + 1) * n * fpt]) for c in range(chunks)] if has_src else None
     lat = []
     for i in range(args.warmup + args.latency_chunks):
         t = time.perf_counter()
-        st = dc.dc_decode_chunk(hdec.h, host_tok[i % chunks], n, pcm)
+        if has_src:
+            st = dc.dc_decode_chunk_f0(hdec.h, host_tok[i % chunks], host_f0[i % chunks], n, pcm)
+        else:
+            st = dc.dc_decode_chunk(hdec.h, host_tok[i % chunks], n, pcm)
         dt = 1000.0 * (time.perf_counter() - t)
         if st != dc.DC_OK:
             raise dc.DcError(st, dc.dc_last_error(hdec.h))
@@ -368,13 +391,14 @@ def main():
 
     cpu = None
     if args.cpu_budget > 0:
-        cpu = cpu_baseline(arch, dtype, blob, tokens, args.cpu_budget)
+        cpu = cpu_baseline(arch, dtype, blob, tokens, args.cpu_budget, f0)
 
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "audio-s/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
-        "data": "synthetic (seeded random-weight decoder and uniform token ids)",
+        "data": "synthetic (seeded random-weight decoder and uniform token ids"
+                + (", synthetic f0 contours)" if has_src else ")"),
         "config": {"workload": args.workload, "arch": "real" if arch["embed"] == 512 else "tiny",
                    "batch": B, "chunk_tokens": n, "chunks_cycled": chunks,
                    "audio_s_per_step": audio_s, "graph_replay": stats["replays"] > 0,

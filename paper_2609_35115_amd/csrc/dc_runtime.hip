@@ -279,8 +279,9 @@ static bool variant_fits(const ConvOp& op, int v)
 }
 
 // Shapes with the weight fragments in an LDS ring (bf16, one K partition),
-// largest first.
-static const int kPreferRing[] = {20, 24, 22, 21, 25, 23, 26};
+// largest first.  (The 64x64 ring shape, 4 MFMAs per wave between barriers,
+// measured slower than the register-weight kernel and is not chosen.)
+static const int kPreferRing[] = {20, 24, 22, 21, 25, 23};
 
 // Tile shape of a conv for this state.  Deterministic: it depends on the
 // layer, the batch and the chunk size only (never on a call's n), so every
@@ -330,14 +331,16 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
         if (kch > kch_all && kch > 1) continue;
         if (wgk == 1 && kch > 4) continue;
         if (wgk == 1 && op.bf16 && !op.split && !(s->cfg.flags & DC_NO_RING)) {
-            // the ring shapes first (split operands read their low halves
-            // unprefetched there: they stay on the register-weight kernel): of those that keep enough blocks, the one
-            // with the least padding in rows and columns (then the largest)
+            // the ring shapes first, for unsplit operands (split ones read their
+            // low halves unprefetched there) and launches that keep the machine
+            // busy for at least two rounds of blocks (two resident per CU; with
+            // fewer the register-weight kernel measured faster): of those, the
+            // one with the least padding in rows and columns (then the largest)
             int bestr = -1;
             double bestr_score = -1.0;
             for (int v : kPreferRing) {
                 const TileShape t = tile_variant(v);
-                if (t.KCH != kch || !variant_fits(op, v) || members * blocks(t) < 512) continue;
+                if (t.KCH != kch || !variant_fits(op, v) || members * blocks(t) < 1024) continue;
                 const int bn = t.BN();
                 const double col = (double)op.N / (double)(((op.N + bn - 1) / bn) * bn);
                 const double score = eff(t) * col;
@@ -596,7 +599,10 @@ static void build_schedule(dc_state* s)
         // members with the most taps first: their blocks are the longest, and
         // blocks are dispatched in member order (when a launch has more blocks
         // than the machine holds, the long ones must not start last)
-        std::stable_sort(m.begin(), m.end(), [&](int a, int b) { return s->convs[a].k > s->convs[b].k; });
+        // (batched tiles only: with K split across waves, at batch 1, the
+        // branch order measured faster)
+        if (tw.WGK == 1)
+            std::stable_sort(m.begin(), m.end(), [&](int a, int b) { return s->convs[a].k > s->convs[b].k; });
         s->launches.push_back({L_CONV, m, name});
     };
     const int nconv = (int)s->convs.size();

@@ -29,7 +29,7 @@ def decode(dec, ids, sizes):
     return np.concatenate(outs, axis=1)
 
 
-@pytest.mark.parametrize("batch,flags", [(8, dc.DC_NO_FUSE), (16, 0), (32, dc.DC_NO_FUSE)])
+@pytest.mark.parametrize("batch,flags", [(8, dc.DC_NO_FUSE), (16, dc.DC_NO_FUSE), (64, 0)])
 def test_ring_equals_register_weights(batch, flags):
     arch = synth.REAL_ARCH
     blob = synth.make_weights(arch, 0)

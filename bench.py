@@ -284,6 +284,8 @@ def main():
     ap.add_argument("--layer-reps", type=int, default=10)
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of one oracle run (0 skips it)")
     ap.add_argument("--tile-variant", type=int, default=0)
+    ap.add_argument("--skip-peaks", action="store_true", help="skip the device copy and GEMM peak runs "
+                    "(for profiler runs; the roofline then has no measured-peak fraction)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested). Streams are "
@@ -381,11 +383,12 @@ def main():
             lat.append(dt)
     hdec.close()
 
-    peaks = measured_peaks()
-    key = "hbm_copy_GBs" if roof["bound"] == "hbm" else f"{roof['operand']}_gemm_TFLOPs"
-    roof["measured_peak"] = peaks[key]
-    roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
-    roof["measured_peaks"] = peaks
+    if not args.skip_peaks:
+        peaks = measured_peaks()
+        key = "hbm_copy_GBs" if roof["bound"] == "hbm" else f"{roof['operand']}_gemm_TFLOPs"
+        roof["measured_peak"] = peaks[key]
+        roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
+        roof["measured_peaks"] = peaks
     print(f"# roofline: {roof['kernel']} {roof['achieved']} {roof['unit']} ({roof['frac']:.1%})",
           file=sys.stderr, flush=True)
 

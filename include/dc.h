@@ -217,6 +217,27 @@ float* dc_audio_buffer(dc_state* s);
  * NULL without a source. */
 float* dc_f0_buffer(dc_state* s);
 
+/*
+ * Carry snapshots: time-multiplexing many sessions over the streams of one
+ * state, and checkpoint/resume (the paper's O(1) carry per session: Design,
+ * state rule, Eq. carry; multi-session bindings).  A snapshot of stream b
+ * holds what its next call reads from the past -- every ring's left context
+ * (the ctx frames before the stream's position), the harmonic source's phases
+ * -- plus the stream's position (tokens since its start) and its source
+ * generator key.  dc_carry_import places a snapshot into stream b of a state
+ * with the same architecture, dtype, source and ring layout (a fused state,
+ * bf16 with batch >= 8, lays its rings out differently from an unfused one):
+ * the frames go to the slots of that state's own clock and the stream's start
+ * is placed `position` tokens back, so the stream continues there bit for bit
+ * as if it had never left.  Other streams are untouched.  Both calls are
+ * synchronous and take a host buffer of exactly dc_carry_bytes(s) bytes.
+ * Errors: DC_EINVAL (bad b, NULL or wrong-size buffer, a snapshot of another
+ * layout), DC_ESTATE (poisoned state), DC_EDEVICE.
+ */
+int64_t dc_carry_bytes(const dc_state* s);
+dc_status dc_carry_export(dc_state* s, int32_t b, void* host_out, size_t bytes);
+dc_status dc_carry_import(dc_state* s, int32_t b, const void* host_in, size_t bytes);
+
 /* Copy the counters into *out. */
 dc_status dc_get_stats(const dc_state* s, dc_stats* out);
 

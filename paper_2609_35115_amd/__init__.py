@@ -94,6 +94,9 @@ SIGNATURES = {
     "dc_audio_buffer": ([_P], _P),
     "dc_f0_buffer": ([_P], _P),
     "dc_get_stats": ([_P, ctypes.POINTER(DcStats)], ctypes.c_int),
+    "dc_carry_bytes": ([_P], ctypes.c_int64),
+    "dc_carry_export": ([_P, ctypes.c_int32, _P, ctypes.c_size_t], ctypes.c_int),
+    "dc_carry_import": ([_P, ctypes.c_int32, _P, ctypes.c_size_t], ctypes.c_int),
     "dc_tap_find": ([_P, ctypes.c_char_p], ctypes.c_int32),
     "dc_tap_read": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _P,
                      ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
@@ -227,6 +230,19 @@ def dc_f0_buffer(h) -> int:
     return lib().dc_f0_buffer(h)
 
 
+def dc_carry_bytes(h) -> int:
+    return lib().dc_carry_bytes(h)
+
+
+def dc_carry_export(h, b: int, buf: np.ndarray) -> int:
+    """Raw call: fills the uint8 buffer buf (dc_carry_bytes long); returns the status."""
+    return lib().dc_carry_export(h, b, buf.ctypes.data, buf.nbytes)
+
+
+def dc_carry_import(h, b: int, buf: np.ndarray) -> int:
+    return lib().dc_carry_import(h, b, buf.ctypes.data, buf.nbytes)
+
+
 def dc_get_stats(h) -> dict:
     s = DcStats()
     _check(lib().dc_get_stats(h, ctypes.byref(s)), h)
@@ -356,6 +372,16 @@ class Decoder:
 
     def stats(self) -> dict:
         return dc_get_stats(self.h)
+
+    def export_carry(self, b: int) -> np.ndarray:
+        """Snapshot of stream b's carry (host bytes)."""
+        buf = np.empty(dc_carry_bytes(self.h), dtype=np.uint8)
+        _check(dc_carry_export(self.h, b, buf), self.h)
+        return buf
+
+    def import_carry(self, b: int, snap: np.ndarray):
+        """Continue the snapshot's stream in stream b of this state."""
+        return _check(dc_carry_import(self.h, b, np.ascontiguousarray(snap, dtype=np.uint8)), self.h)
 
     def layers(self) -> list:
         return [dc_layer_info_get(self.h, i) for i in range(dc_layer_count(self.h))]

@@ -201,6 +201,7 @@ struct SourceParams {
     int64_t fpt0, fptL;    // f0 frames and last-stage frames per token
     const int64_t* clock;
     const int64_t* start;  // [B] tokens decoded when each stream last started
+    const uint64_t* keys;  // [B] each stream's generator key (second key word)
     float amp, noise, thr;
     double sr;
     uint64_t seed;
@@ -209,6 +210,8 @@ hipError_t launch_phase(const SourceParams& p, hipStream_t st);
 hipError_t launch_source(const SourceParams& p, hipStream_t st);
 
 hipError_t launch_clock(int64_t* clock, int n, hipStream_t st);
-hipError_t launch_mark_start(int64_t* start, int b, const int64_t* clock, hipStream_t st);
+hipError_t launch_mark_start(int64_t* start, uint64_t* keys, int b, const int64_t* clock, int64_t back, uint64_t key,
+                             hipStream_t st);
+hipError_t launch_init_keys(uint64_t* keys, int B, hipStream_t st);
 
 }  // namespace dc

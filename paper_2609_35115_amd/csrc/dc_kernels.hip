@@ -1533,7 +1533,7 @@ __global__ __launch_bounds__(64) void phase_kernel(const SourceParams p)
     double P = p.carry[((size_t)b * 2 + sel) * p.H1 + h];
     if (p.clock[0] == p.start[b]) {
         P = 0.0;
-        if (h > 0) P = to_u01(philox4x64_10(0, (uint64_t)h, 1, 0, p.seed, (uint64_t)b).v[0]);
+        if (h > 0) P = to_u01(philox4x64_10(0, (uint64_t)h, 1, 0, p.seed, p.keys[b]).v[0]);
     }
     const float* f0 = p.f0 + (size_t)b * p.F0;
     double* pt = p.ptab + (size_t)b * p.F0 * p.H1 + h;
@@ -1560,6 +1560,8 @@ hipError_t launch_phase(const SourceParams& p, hipStream_t st)
 // sinusoids 4g .. 4g+3 comes from Philox4x64-10 with key (seed, stream) and
 // counter (sample since the stream's start, g, 0, 0), by Box-Muller on its
 // draws (0, 1) and (2, 3).  src = tanh(mb + sum_h mw[h] e_h), h ascending.
+// The stream's key is keys[b]: its index, unless its carry was imported from
+// another slot (dc_carry_import), whose key it keeps.
 constexpr int kMaxSinusoids = 32;
 
 __global__ __launch_bounds__(256) void source_kernel(const SourceParams p)
@@ -1573,6 +1575,7 @@ __global__ __launch_bounds__(256) void source_kernel(const SourceParams p)
     const float* f0 = p.f0 + (size_t)b * p.F0;
     const double* ptab = p.ptab + (size_t)b * p.F0 * p.H1;
     const int groups = (p.H1 + 3) / 4;
+    const uint64_t key = p.keys[b];
     f32x4 out;
 #pragma unroll
     for (int j = 0; j < 4; j++) {
@@ -1583,7 +1586,7 @@ __global__ __launch_bounds__(256) void source_kernel(const SourceParams p)
         const float nscale = voiced ? p.noise : p.amp / 3.0f;
         float acc = 0.f;
         for (int g = 0; g < groups; g++) {
-            const Philox4 x = philox4x64_10((uint64_t)(t_rel0 + j), (uint64_t)g, 0, 0, p.seed, (uint64_t)b);
+            const Philox4 x = philox4x64_10((uint64_t)(t_rel0 + j), (uint64_t)g, 0, 0, p.seed, key);
             float nz[4];
 #pragma unroll
             for (int q = 0; q < 2; q++) {
@@ -1630,15 +1633,35 @@ hipError_t launch_clock(int64_t* clock, int n, hipStream_t st)
     return hipGetLastError();
 }
 
-// start[b] = the clock (in stream order): stream b restarts here.
-__global__ void mark_start_kernel(int64_t* start, int b, const int64_t* clock)
+// start[b] = the clock minus `back` tokens (in stream order): stream b
+// restarted `back` tokens before the next call; keys[b] keys its source
+// generator.
+__global__ void mark_start_kernel(int64_t* start, uint64_t* keys, int b, const int64_t* clock, int64_t back,
+                                  uint64_t key)
 {
-    if (threadIdx.x == 0) start[b] = clock[0];
+    if (threadIdx.x == 0) {
+        start[b] = clock[0] - back;
+        keys[b] = key;
+    }
 }
 
-hipError_t launch_mark_start(int64_t* start, int b, const int64_t* clock, hipStream_t st)
+hipError_t launch_mark_start(int64_t* start, uint64_t* keys, int b, const int64_t* clock, int64_t back, uint64_t key,
+                             hipStream_t st)
 {
-    hipLaunchKernelGGL(mark_start_kernel, dim3(1), dim3(64), 0, st, start, b, clock);
+    hipLaunchKernelGGL(mark_start_kernel, dim3(1), dim3(64), 0, st, start, keys, b, clock, back, key);
+    return hipGetLastError();
+}
+
+// keys[b] = b: every stream keys its source generator with its own index.
+__global__ void init_keys_kernel(uint64_t* keys, int B)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < B) keys[i] = (uint64_t)i;
+}
+
+hipError_t launch_init_keys(uint64_t* keys, int B, hipStream_t st)
+{
+    hipLaunchKernelGGL(init_keys_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, st, keys, B);
     return hipGetLastError();
 }
 

@@ -102,6 +102,7 @@ struct dc_state {
     int64_t fpt[DC_MAX_STAGES + 2] = {};
     int64_t spt = 0;
     size_t emb_off = 0, table_off = 0, tok_off = 0, audio_off = 0, clock_off = 0, start_off = 0, err_off = 0;
+    size_t keys_off = 0;
     // harmonic source: merge weights and bias, down-conv weights and bias,
     // the f0 buffer, the carried phases and the per-call phase table
     size_t src_w_off = 0, src_down_off = 0, f0_off = 0, phase_off = 0, ptab_off = 0;
@@ -111,6 +112,7 @@ struct dc_state {
     float* audio = nullptr;
     int64_t* clock = nullptr;
     int64_t* start = nullptr;   // [B] tokens decoded when each stream last started
+    uint64_t* keys = nullptr;   // [B] each stream's source-generator key
     int* err = nullptr;
     void* emb = nullptr;
     float* table = nullptr;
@@ -749,6 +751,7 @@ static SourceParams source_params(const dc_state* s, int n)
     p.fptL = s->fpt[c.n_stages];
     p.clock = s->clock;
     p.start = s->start;
+    p.keys = s->keys;
     p.amp = c.sine_amp;
     p.noise = c.noise_std;
     p.thr = c.voiced_threshold;
@@ -856,6 +859,8 @@ static hipError_t zero_state(dc_state* s)
     if (e != hipSuccess) return e;
     e = hipMemsetAsync(s->start, 0, (size_t)s->cfg.batch * sizeof(int64_t), s->stream);
     if (e != hipSuccess) return e;
+    e = launch_init_keys(s->keys, s->cfg.batch, s->stream);
+    if (e != hipSuccess) return e;
     return hipMemsetAsync(s->err, 0, sizeof(int), s->stream);
 }
 
@@ -949,6 +954,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     s->audio_off = take((size_t)c.batch * c.max_tokens * s->spt * sizeof(float));
     s->clock_off = take(sizeof(int64_t));
     s->start_off = take((size_t)c.batch * sizeof(int64_t));
+    s->keys_off = take((size_t)c.batch * sizeof(uint64_t));
     s->err_off = take(sizeof(int));
     s->arena_bytes = off;
 
@@ -964,6 +970,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     s->audio = (float*)(s->arena + s->audio_off);
     s->clock = (int64_t*)(s->arena + s->clock_off);
     s->start = (int64_t*)(s->arena + s->start_off);
+    s->keys = (uint64_t*)(s->arena + s->keys_off);
     s->err = (int*)(s->arena + s->err_off);
     if (c.n_harmonics > 0) s->f0 = (float*)(s->arena + s->f0_off);
 
@@ -1201,7 +1208,7 @@ dc_status dc_reset_stream(dc_state* s, int32_t b)
         if (e != hipSuccess) return device_fail(s, e, "dc_reset_stream");
     }
     // fused pairs recompute h of the left context: frames before this point are zeros
-    hipError_t e = launch_mark_start(s->start, b, s->clock, s->stream);
+    hipError_t e = launch_mark_start(s->start, s->keys, b, s->clock, 0, (uint64_t)b, s->stream);
     if (e != hipSuccess) return device_fail(s, e, "dc_reset_stream");
     return DC_OK;
 }
@@ -1211,6 +1218,171 @@ int32_t* dc_token_buffer(dc_state* s) { return s ? s->tok : nullptr; }
 float* dc_audio_buffer(dc_state* s) { return s ? s->audio : nullptr; }
 
 float* dc_f0_buffer(dc_state* s) { return s ? s->f0 : nullptr; }
+
+// ------------------------------------------------------------ carry snapshots
+//
+// One stream's carry as host bytes: what the next call of that stream reads
+// from the past (every ring's ctx frames, the source's phases) plus where the
+// stream is (tokens since its start) and its generator key.  Importing it
+// into any slot of a state with the same layout continues the stream there
+// exactly: the frames go to the slots of the receiving state's own clock,
+// and the stream's start is placed that many tokens back.
+
+namespace {
+
+struct SnapHeader {
+    uint64_t magic;
+    uint64_t fingerprint;
+    int64_t position;   // tokens decoded since the stream's start
+    uint64_t key;       // source-generator key
+    uint64_t bytes;     // whole snapshot
+    uint64_t reserved;
+};
+constexpr uint64_t kSnapMagic = 0x313050414e534344ull;   // "DCSNAP01" as little-endian bytes
+
+// FNV-1a over what a snapshot's meaning depends on: the architecture, the
+// arithmetic, the source, and every ring's geometry (a fused state keeps
+// wider z contexts and no h frames, so its snapshots differ from an unfused
+// one's).
+uint64_t layout_fingerprint(const dc_state* s)
+{
+    uint64_t h = 1469598103934665603ull;
+    auto mix = [&](int64_t v) {
+        for (int i = 0; i < 8; i++) {
+            h ^= (uint64_t)((v >> (8 * i)) & 0xff);
+            h *= 1099511628211ull;
+        }
+    };
+    const dc_cfg& c = s->cfg;
+    mix(DC_ABI_VERSION);
+    mix(c.vocab), mix(c.embed), mix(c.frames_per_token), mix(c.n_pre), mix(c.pre_kernel), mix(c.n_stages);
+    for (int i = 0; i < c.n_stages; i++) mix(c.up_rate[i]);
+    for (int i = 0; i <= c.n_stages; i++) mix(c.channels[i]);
+    mix(c.n_rb);
+    for (int i = 0; i < c.n_rb; i++) mix(c.rb_kernel[i]);
+    mix(c.n_dil);
+    for (int i = 0; i < c.n_dil; i++) mix(c.dil[i]);
+    mix(c.head_kernel), mix(c.n_fft), mix(c.hop), mix(c.dtype), mix(c.n_harmonics);
+    for (const Ring& r : s->rings) mix(r.C), mix(r.elem), mix(r.ctx), mix(r.level);
+    return h;
+}
+
+size_t snapshot_bytes(const dc_state* s)
+{
+    size_t n = sizeof(SnapHeader);
+    for (const Ring& r : s->rings) n += (size_t)r.ctx * r.C * (r.elem == kBF16 ? 2 : 4);
+    n += (size_t)(s->cfg.n_harmonics > 0 ? s->cfg.n_harmonics + 1 : 0) * sizeof(double);
+    return n;
+}
+
+// Copy frames [f0, f0 + nf) of stream b of ring r (host <-> device), as two
+// runs where the ring wraps.
+hipError_t ring_frames(const dc_state* s, const Ring& r, int b, int64_t f0, int nf, char* host, bool to_host)
+{
+    const size_t es = r.elem == kBF16 ? 2 : 4, row = (size_t)r.C * es;
+    int64_t slot = f0 % r.R;
+    if (slot < 0) slot += r.R;
+    int done = 0;
+    while (done < nf) {
+        const int run = (int)std::min<int64_t>(nf - done, r.R - slot);
+        char* dev = (char*)r.ptr + ((size_t)b * r.R + slot) * row;
+        const hipError_t e = to_host ? hipMemcpy(host + done * row, dev, run * row, hipMemcpyDeviceToHost)
+                                     : hipMemcpy(dev, host + done * row, run * row, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return e;
+        done += run;
+        slot = 0;
+    }
+    return hipSuccess;
+}
+
+}  // namespace
+
+int64_t dc_carry_bytes(const dc_state* s) { return s ? (int64_t)snapshot_bytes(s) : 0; }
+
+dc_status dc_carry_export(dc_state* s, int32_t b, void* host_out, size_t bytes)
+{
+    if (!s) return DC_EINVAL;
+    if (b < 0 || b >= s->cfg.batch || !host_out) return fail(s, DC_EINVAL, "bad stream index or buffer");
+    if (bytes != snapshot_bytes(s)) return fail(s, DC_EINVAL, "buffer size differs from dc_carry_bytes");
+    if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned; call dc_reset");
+    hipError_t e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) return device_fail(s, e, "dc_carry_export");
+    int64_t start = 0;
+    uint64_t key = 0;
+    e = hipMemcpy(&start, s->start + b, sizeof start, hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(&key, s->keys + b, sizeof key, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return device_fail(s, e, "dc_carry_export");
+    char* out = (char*)host_out;
+    SnapHeader hd{kSnapMagic, layout_fingerprint(s), s->clock_host - start, key, (uint64_t)bytes, 0};
+    std::memcpy(out, &hd, sizeof hd);
+    size_t off = sizeof hd;
+    for (const Ring& r : s->rings) {
+        if (r.ctx == 0) continue;
+        const int64_t end = s->clock_host * s->fpt[r.level];
+        e = ring_frames(s, r, b, end - r.ctx, r.ctx, out + off, true);
+        if (e != hipSuccess) return device_fail(s, e, "dc_carry_export");
+        off += (size_t)r.ctx * r.C * (r.elem == kBF16 ? 2 : 4);
+    }
+    if (s->cfg.n_harmonics > 0) {
+        // the phases of the next call's first f0 frame: the slot tagged with it
+        const int H1 = s->cfg.n_harmonics + 1;
+        const double* carry = (const double*)(s->arena + s->phase_off);
+        const int64_t* tags = (const int64_t*)(carry + (size_t)s->cfg.batch * 2 * H1);
+        int64_t tg[2];
+        e = hipMemcpy(tg, tags + 2 * b, sizeof tg, hipMemcpyDeviceToHost);
+        const int sel = tg[0] == s->clock_host * s->fpt[0] ? 0 : 1;
+        if (e == hipSuccess)
+            e = hipMemcpy(out + off, carry + ((size_t)b * 2 + sel) * H1, H1 * sizeof(double), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return device_fail(s, e, "dc_carry_export");
+        off += H1 * sizeof(double);
+    }
+    return DC_OK;
+}
+
+dc_status dc_carry_import(dc_state* s, int32_t b, const void* host_in, size_t bytes)
+{
+    if (!s) return DC_EINVAL;
+    if (b < 0 || b >= s->cfg.batch || !host_in) return fail(s, DC_EINVAL, "bad stream index or buffer");
+    if (bytes != snapshot_bytes(s)) return fail(s, DC_EINVAL, "snapshot size differs from dc_carry_bytes");
+    SnapHeader hd;
+    std::memcpy(&hd, host_in, sizeof hd);
+    if (hd.magic != kSnapMagic || hd.bytes != bytes) return fail(s, DC_EINVAL, "not a carry snapshot");
+    if (hd.fingerprint != layout_fingerprint(s))
+        return fail(s, DC_EINVAL, "snapshot of a different architecture, dtype or ring layout");
+    if (hd.position < 0) return fail(s, DC_EINVAL, "bad snapshot position");
+    if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned; call dc_reset");
+    hipError_t e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) return device_fail(s, e, "dc_carry_import");
+    // the stream's rings start clean, then take the carried frames
+    for (const Ring& r : s->rings) {
+        const size_t per = (size_t)r.R * r.C * (r.elem == kBF16 ? 2 : 4);
+        if (per) e = hipMemset((char*)r.ptr + (size_t)b * per, 0, per);
+        if (e != hipSuccess) return device_fail(s, e, "dc_carry_import");
+    }
+    const char* in = (const char*)host_in;
+    size_t off = sizeof hd;
+    for (const Ring& r : s->rings) {
+        if (r.ctx == 0) continue;
+        const int64_t end = s->clock_host * s->fpt[r.level];
+        e = ring_frames(s, r, b, end - r.ctx, r.ctx, const_cast<char*>(in + off), false);
+        if (e != hipSuccess) return device_fail(s, e, "dc_carry_import");
+        off += (size_t)r.ctx * r.C * (r.elem == kBF16 ? 2 : 4);
+    }
+    if (s->cfg.n_harmonics > 0) {
+        const int H1 = s->cfg.n_harmonics + 1;
+        double* carry = (double*)(s->arena + s->phase_off);
+        int64_t* tags = (int64_t*)(carry + (size_t)s->cfg.batch * 2 * H1);
+        const int64_t tg[2] = {s->clock_host * s->fpt[0], -1};
+        e = hipMemcpy(carry + (size_t)b * 2 * H1, in + off, H1 * sizeof(double), hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMemcpy(tags + 2 * b, tg, sizeof tg, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return device_fail(s, e, "dc_carry_import");
+    }
+    // the stream started `position` tokens before this state's next call
+    e = launch_mark_start(s->start, s->keys, b, s->clock, hd.position, hd.key, s->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) return device_fail(s, e, "dc_carry_import");
+    return DC_OK;
+}
 
 dc_status dc_get_stats(const dc_state* s, dc_stats* out)
 {

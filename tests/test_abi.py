@@ -101,6 +101,9 @@ def test_null_state_calls_fail_closed():
     assert L.dc_decode_chunk(None, None, 1, None) == dc.DC_EINVAL
     assert L.dc_decode_chunk_f0(None, None, None, 1, None) == dc.DC_EINVAL
     assert L.dc_f0_buffer(None) is None
+    assert L.dc_carry_bytes(None) == 0
+    assert L.dc_carry_export(None, 0, None, 0) == dc.DC_EINVAL
+    assert L.dc_carry_import(None, 0, None, 0) == dc.DC_EINVAL
     assert L.dc_reset(None) == dc.DC_EINVAL
     assert L.dc_sync(None) == dc.DC_EINVAL
     assert L.dc_token_buffer(None) is None

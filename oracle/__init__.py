@@ -14,6 +14,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
+_SRCS = [_SRC, os.path.join(_HERE, "flow.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
@@ -22,7 +23,7 @@ def build() -> str:
     """Compile the oracle (plain C, fp64, OpenMP over output frames)."""
     tmp = _LIB + ".tmp"
     subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-std=gnu11",
-                    "-o", tmp, _SRC, "-lm"], check=True)
+                    "-o", tmp, *_SRCS, "-lm"], check=True)
     os.replace(tmp, _LIB)
     return _LIB
 
@@ -45,7 +46,7 @@ class _Arch(ctypes.Structure):
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(f) for f in _SRCS):
             build()
         lib = ctypes.CDLL(_LIB)
         D = ctypes.POINTER(ctypes.c_double)
@@ -77,8 +78,42 @@ def _load():
         lib.oc_box_muller.argtypes = [ctypes.c_double, ctypes.c_double, D, D]
         lib.oc_source.argtypes = [ctypes.POINTER(_Arch), D, ctypes.c_long, ctypes.c_uint64, ctypes.c_uint64,
                                   D, ctypes.c_double, D]
+        FP = ctypes.POINTER(_FlowArch)
+        V = ctypes.c_void_p
+        lib.ocf_blob_floats.argtypes = [FP]
+        lib.ocf_blob_floats.restype = ctypes.c_long
+        lib.ocf_open.argtypes = [FP, ctypes.c_int, F, ctypes.c_long, ctypes.c_uint64, ctypes.c_uint64]
+        lib.ocf_open.restype = V
+        lib.ocf_close.argtypes = [V]
+        lib.ocf_prompt.argtypes = [V, ctypes.c_int, D, D, D, D]
+        lib.ocf_prompt.restype = ctypes.c_int
+        lib.ocf_chunk.argtypes = [V, ctypes.c_int, D, D]
+        lib.ocf_chunk.restype = ctypes.c_int
+        lib.ocf_carry.argtypes = [V, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, D]
+        lib.ocf_carry.restype = ctypes.c_int
+        lib.ocf_position.argtypes = [V]
+        lib.ocf_position.restype = ctypes.c_int64
+        lib.ocf_get_times.argtypes = [V, D]
+        lib.ocf_get_mods.argtypes = [V, ctypes.c_int, ctypes.c_int, D]
+        lib.ocf_times.argtypes = [ctypes.c_int, D]
+        lib.ocf_time_embedding.argtypes = [ctypes.c_int, ctypes.c_double, D]
+        lib.ocf_gelu.argtypes = [ctypes.c_double]
+        lib.ocf_gelu.restype = ctypes.c_double
+        lib.ocf_lnmod.argtypes = [ctypes.c_int, D, D, D, D]
+        lib.ocf_attention.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, D, D, D, ctypes.c_int, D]
+        lib.ocf_noise.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_uint64, ctypes.c_uint64,
+                                  ctypes.c_int64, ctypes.c_int, D]
         _lib = lib
     return _lib
+
+
+class _FlowArch(ctypes.Structure):
+    _fields_ = [
+        ("n_mel", ctypes.c_int), ("dim", ctypes.c_int), ("heads", ctypes.c_int), ("depth", ctypes.c_int),
+        ("mlp", ctypes.c_int), ("t_dim", ctypes.c_int), ("n_steps", ctypes.c_int),
+        ("f_prompt", ctypes.c_int), ("f_retained", ctypes.c_int), ("f_chunk", ctypes.c_int),
+        ("f_call", ctypes.c_int), ("cfg_rate", ctypes.c_double), ("temperature", ctypes.c_double),
+    ]
 
 
 def _p(a: np.ndarray, ct):
@@ -266,3 +301,117 @@ def _tap_shape(arch: dict, tap: str, T: int):
     for u in arch["up_rate"][:s + 1]:
         F *= u
     return F, arch["channels"][s + 1]
+
+
+# ------------------------------------------------------------ the flow decoder
+
+def flow_arch_struct(arch: dict) -> _FlowArch:
+    s = _FlowArch()
+    for name, _ in _FlowArch._fields_:
+        setattr(s, name, arch[name])
+    return s
+
+
+def flow_times(n: int) -> np.ndarray:
+    t = np.empty(n + 1, dtype=np.float64)
+    _load().ocf_times(n, _p(t, ctypes.c_double))
+    return t
+
+
+def flow_time_embedding(t_dim: int, t: float) -> np.ndarray:
+    e = np.empty(t_dim, dtype=np.float64)
+    _load().ocf_time_embedding(t_dim, float(t), _p(e, ctypes.c_double))
+    return e
+
+
+def gelu(v: float) -> float:
+    return _load().ocf_gelu(float(v))
+
+
+def lnmod(h, shift, scale) -> np.ndarray:
+    h, shift, scale = _f64(h).ravel(), _f64(shift).ravel(), _f64(scale).ravel()
+    out = np.empty_like(h)
+    _load().ocf_lnmod(h.size, _p(h, ctypes.c_double), _p(shift, ctypes.c_double), _p(scale, ctypes.c_double),
+                      _p(out, ctypes.c_double))
+    return out
+
+
+def attention(q, k, v) -> np.ndarray:
+    """One head: q [nq][hd], k, v [nk][hd] -> [nq][hd]."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    out = np.empty_like(q)
+    _load().ocf_attention(q.shape[0], k.shape[0], q.shape[1], _p(q, ctypes.c_double), _p(k, ctypes.c_double),
+                          _p(v, ctypes.c_double), q.shape[1], _p(out, ctypes.c_double))
+    return out
+
+
+def flow_noise(n_mel: int, temperature: float, seed: int, key: int, tau0: int, frames: int) -> np.ndarray:
+    out = np.empty((frames, n_mel), dtype=np.float64)
+    _load().ocf_noise(n_mel, temperature, seed, key, tau0, frames, _p(out, ctypes.c_double))
+    return out
+
+
+class FlowStream:
+    """One stream of the flow decoder in fp64: prompt(), then chunk() calls.
+
+    dtype "bf16" rounds the per-step Linear weights to bfloat16 first.
+    """
+
+    def __init__(self, arch: dict, dtype: str, blob: np.ndarray, seed: int = 0, key: int = 0):
+        self.arch = dict(arch)
+        self._a = flow_arch_struct(arch)
+        self._blob = np.ascontiguousarray(blob, dtype=np.float32)
+        self._lib = _load()
+        self._h = self._lib.ocf_open(ctypes.byref(self._a), 1 if dtype == "bf16" else 0,
+                                     _p(self._blob, ctypes.c_float), self._blob.size, seed, key)
+        if not self._h:
+            raise ValueError("bad flow architecture or blob size")
+
+    def close(self):
+        if self._h:
+            self._lib.ocf_close(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.close()
+
+    def prompt(self, mu, cond, spk) -> np.ndarray:
+        mu, cond, spk = _f64(mu), _f64(cond), _f64(spk).ravel()
+        P = mu.shape[0]
+        mel = np.empty((P, self.arch["n_mel"]), dtype=np.float64)
+        if self._lib.ocf_prompt(self._h, P, _p(mu, ctypes.c_double), _p(cond, ctypes.c_double),
+                                _p(spk, ctypes.c_double), _p(mel, ctypes.c_double)) != 0:
+            raise ValueError("prompt length out of range")
+        return mel
+
+    def chunk(self, mu) -> np.ndarray:
+        mu = _f64(mu)
+        n = mu.shape[0]
+        mel = np.empty((n, self.arch["n_mel"]), dtype=np.float64)
+        self.extent = self._lib.ocf_chunk(self._h, n, _p(mu, ctypes.c_double), _p(mel, ctypes.c_double))
+        if self.extent < 0:
+            raise ValueError("chunk before a prompt, or frame count out of range")
+        return mel
+
+    def carry(self, step: int, layer: int, branch: int, kv: int) -> np.ndarray:
+        n = self._lib.ocf_carry(self._h, step, layer, branch, kv, None)
+        out = np.empty((n, self.arch["dim"]), dtype=np.float64)
+        self._lib.ocf_carry(self._h, step, layer, branch, kv, _p(out, ctypes.c_double))
+        return out
+
+    @property
+    def position(self) -> int:
+        return int(self._lib.ocf_position(self._h))
+
+    def times(self) -> np.ndarray:
+        t = np.empty(self.arch["n_steps"] + 1, dtype=np.float64)
+        self._lib.ocf_get_times(self._h, _p(t, ctypes.c_double))
+        return t
+
+    def mods(self, step: int, layer: int) -> np.ndarray:
+        """[6][dim] modulation of block `layer` at solver step `step` ([2][dim] for layer == depth)."""
+        D = self.arch["dim"]
+        k = 6 if layer < self.arch["depth"] else 2
+        out = np.empty(k * D, dtype=np.float64)
+        self._lib.ocf_get_mods(self._h, step, layer, _p(out, ctypes.c_double))
+        return out.reshape(k, D)

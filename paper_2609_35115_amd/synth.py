@@ -88,10 +88,55 @@ NSF_WORKLOADS = {
 
 SAMPLE_RATE = 24000  # output rate of the real architecture (960 samples / 25 Hz token)
 
+# ---------------------------------------------------------------------------
+# Flow decoder (conditional flow matching with a DiT velocity estimator), the
+# stage before the vocoder in the Token2Wav pipeline.  The clock quantities
+# are the paper's adapter declaration (Design, "Adapter"; Table S11):
+# f_prompt = 302, f_retained = 100, f_chunk = 50 and f_call = 56 frames,
+# n_steps = 10 solver steps, each evaluating the estimator on the
+# conditional and the unconditional input (classifier-free guidance x2).
+# The paper gives no layer shapes; it gives the stacked carry's declared
+# live size, 0.125 MiB per frame in fp32 (Table 2), which a 16-block DiT of
+# width 512 with both guidance branches holds exactly: 16 blocks x (K, V) x
+# 512 x 2 branches x 4 bytes.  The rest (8 heads of 64, MLP 2048, 80 mel
+# bins, a 256-wide sinusoidal time embedding) is the common DiT shape.
+#
+# Weight blob (float32, PyTorch Linear layouts [out][in], back to back):
+#
+#     t.W1 [dim][t_dim], t.b1 [dim], t.W2 [dim][dim], t.b2 [dim]
+#     in.W [dim][4*n_mel], in.b [dim]          (input = x | mu | spk | cond)
+#     per block l: ada.W [6*dim][dim], ada.b [6*dim],
+#                  qkv.W [3*dim][dim], qkv.b [3*dim], o.W [dim][dim], o.b [dim],
+#                  fc1.W [mlp][dim], fc1.b [mlp], fc2.W [dim][mlp], fc2.b [dim]
+#     final:       ada.W [2*dim][dim], ada.b [2*dim], out.W [n_mel][dim], out.b [n_mel]
+#
+# drawn like the vocoder's blob (N(0, 1/fan_in), fan_in = in-features, from
+# SeedSequence([seed, 0]) in blob order).
+TINY_FLOW_ARCH = dict(
+    n_mel=16, dim=128, heads=2, depth=2, mlp=256, t_dim=32, n_steps=4,
+    f_prompt=20, f_retained=16, f_chunk=8, f_call=11, cfg_rate=0.7, temperature=1.0,
+)
+REAL_FLOW_ARCH = dict(
+    n_mel=80, dim=512, heads=8, depth=16, mlp=2048, t_dim=256, n_steps=10,
+    f_prompt=302, f_retained=100, f_chunk=50, f_call=56, cfg_rate=0.7, temperature=1.0,
+)
+
+# Flow workloads: architecture, arithmetic type, streams, chunks per pass.
+# Every call presents f_call frames (f_chunk retained plus the lookahead).
+FLOW_WORKLOADS = {
+    "flow_tiny_f32_b2": dict(arch=TINY_FLOW_ARCH, dtype="f32", batch=2, chunks=6),
+    "flow_real_f32_b1": dict(arch=REAL_FLOW_ARCH, dtype="f32", batch=1, chunks=6),
+    "flow_real_bf16_b1": dict(arch=REAL_FLOW_ARCH, dtype="bf16", batch=1, chunks=6),
+    "flow_real_bf16_b16": dict(arch=REAL_FLOW_ARCH, dtype="bf16", batch=16, chunks=6),
+}
+
 
 def workload(name: str) -> dict:
     """Deep copy of a named workload description."""
-    return copy.deepcopy(WORKLOADS[name] if name in WORKLOADS else NSF_WORKLOADS[name])
+    for table in (WORKLOADS, NSF_WORKLOADS, FLOW_WORKLOADS):
+        if name in table:
+            return copy.deepcopy(table[name])
+    raise KeyError(name)
 
 
 def head_channels(arch: dict) -> int:
@@ -197,4 +242,71 @@ def make_f0(arch: dict, batch: int, total_tokens: int, seed: int = 0, first_stre
                     out[r, f] = np.clip(base * 2.0 ** (walk / 12.0), 60.0, 500.0)
                 f += 1
             voiced = not voiced
+    return out
+
+
+# ------------------------------------------------------------- flow decoder
+
+def flow_tensor_list(arch: dict):
+    """(name, shape, fan_in) for every tensor of the flow decoder's blob, in blob order."""
+    D, M, T, H = arch["dim"], arch["n_mel"], arch["t_dim"], arch["mlp"]
+    out = [("t.W1", (D, T), T), ("t.b1", (D,), T), ("t.W2", (D, D), D), ("t.b2", (D,), D),
+           ("in.W", (D, 4 * M), 4 * M), ("in.b", (D,), 4 * M)]
+    for l in range(arch["depth"]):
+        out += [(f"b{l}.ada.W", (6 * D, D), D), (f"b{l}.ada.b", (6 * D,), D),
+                (f"b{l}.qkv.W", (3 * D, D), D), (f"b{l}.qkv.b", (3 * D,), D),
+                (f"b{l}.o.W", (D, D), D), (f"b{l}.o.b", (D,), D),
+                (f"b{l}.fc1.W", (H, D), D), (f"b{l}.fc1.b", (H,), D),
+                (f"b{l}.fc2.W", (D, H), H), (f"b{l}.fc2.b", (D,), H)]
+    out += [("f.ada.W", (2 * D, D), D), ("f.ada.b", (2 * D,), D),
+            ("out.W", (M, D), D), ("out.b", (M,), D)]
+    return out
+
+
+def flow_blob_floats(arch: dict) -> int:
+    return sum(math.prod(shape) for _, shape, _ in flow_tensor_list(arch))
+
+
+def make_flow_weights(arch: dict, seed: int = 0) -> np.ndarray:
+    """The float32 weight blob of the flow decoder `arch` drawn from `seed`."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 0]))
+    parts = []
+    for _name, shape, fan_in in flow_tensor_list(arch):
+        parts.append((rng.standard_normal(math.prod(shape)) / math.sqrt(fan_in)).astype(np.float32))
+    return np.concatenate(parts)
+
+
+def split_flow_weights(arch: dict, blob: np.ndarray) -> dict:
+    """Views of the flow blob by tensor name."""
+    out, off = {}, 0
+    for name, shape, _ in flow_tensor_list(arch):
+        n = math.prod(shape)
+        out[name] = blob[off:off + n].reshape(shape)
+        off += n
+    assert off == blob.size
+    return out
+
+
+def make_flow_prompt(arch: dict, frames: int, seed: int = 0, stream: int = 0):
+    """One turn's prompt of stream `stream`: (mu [frames][n_mel], cond [frames][n_mel],
+    spk [n_mel]) float32 from SeedSequence([seed, 4, stream]).  mu and spk are N(0, 1)
+    features (the token encoder's output, the speaker embedding); cond stands in for
+    the prompt's log-mel spectrogram, N(-5, 2^2)."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 4, stream]))
+    M = arch["n_mel"]
+    mu = rng.standard_normal((frames, M)).astype(np.float32)
+    cond = (-5.0 + 2.0 * rng.standard_normal((frames, M))).astype(np.float32)
+    spk = rng.standard_normal(M).astype(np.float32)
+    return mu, cond, spk
+
+
+def make_flow_mu(arch: dict, batch: int, frames: int, seed: int = 0, first_stream: int = 0) -> np.ndarray:
+    """float32 [batch][frames][n_mel] encoder features of the frames after the prompt
+    (frame 0 = the first frame of the first chunk), N(0, 1); stream b uses
+    SeedSequence([seed, 3, b]).  A call over frames [p, p + n) takes rows p .. p + n - 1,
+    so a lookahead frame gets the same features in both calls that present it."""
+    out = np.empty((batch, frames, arch["n_mel"]), dtype=np.float32)
+    for r in range(batch):
+        rng = np.random.default_rng(np.random.SeedSequence([seed, 3, first_stream + r]))
+        out[r] = rng.standard_normal((frames, arch["n_mel"]))
     return out

@@ -8,7 +8,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdc.so")
-SOURCES = ["dc_runtime.hip", "dc_kernels.hip"]
+SOURCES = ["dc_runtime.hip", "dc_kernels.hip", "flow_runtime.hip", "flow_kernels.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -1,6 +1,7 @@
-"""The C-ABI library on the host: it loads, exports every symbol include/dc.h
-declares, and its host-only logic (sizes, configuration checks) fails closed
-before touching the device.  No GPU needed."""
+"""The C-ABI library on the host: it loads, exports every symbol that
+include/dc.h and include/dc_flow.h declare, and its host-only logic (sizes,
+configuration checks) fails closed before touching the device.  No GPU
+needed."""
 import ctypes
 import os
 import re
@@ -9,19 +10,26 @@ import numpy as np
 import pytest
 
 import paper_2609_35115_amd as dc
-from paper_2609_35115_amd import synth
+from paper_2609_35115_amd import flow, synth
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def declared_functions():
-    text = open(os.path.join(ROOT, "include", "dc.h")).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(dc_[a-z0-9_]+)\s*\(", text)))
+def declared_functions(header: str | None = None):
+    names = set()
+    for h in ([header] if header else sorted(os.listdir(os.path.join(ROOT, "include")))):
+        if not h.endswith(".h"):
+            continue
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(dc_[a-z0-9_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_header_and_binding_agree():
-    assert declared_functions() == sorted(dc.SIGNATURES)
+    assert declared_functions("dc.h") == sorted(dc.SIGNATURES)
+    assert declared_functions("dc_flow.h") == sorted(flow.FLOW_SIGNATURES)
+    assert declared_functions() == sorted(set(dc.SIGNATURES) | set(flow.FLOW_SIGNATURES))
 
 
 def test_library_exports_every_declared_symbol():
@@ -109,3 +117,55 @@ def test_null_state_calls_fail_closed():
     assert L.dc_token_buffer(None) is None
     assert L.dc_tap_find(None, b"embed") == -1
     L.dc_free(None)
+
+
+# ------------------------------------------------------------ flow decoder
+
+def test_flow_struct_sizes_match_header_layout():
+    # 14 int32 + uint32 flags + two floats (68, padded to 72), the seed, the stream
+    assert ctypes.sizeof(flow.DcFlowCfg) == 72 + 8 + 8
+    # 9 int64, 2 int32, a double
+    assert ctypes.sizeof(flow.DcFlowStats) == 9 * 8 + 2 * 4 + 8
+
+
+@pytest.mark.parametrize("arch", [synth.TINY_FLOW_ARCH, synth.REAL_FLOW_ARCH])
+def test_flow_blob_size_agrees_with_generator(arch):
+    assert flow.dc_flow_blob_floats(flow.make_flow_cfg(arch, "bf16", 4)) == synth.flow_blob_floats(arch)
+
+
+def _flow_init_status(cfg, blob):
+    blob = np.ascontiguousarray(blob, dtype=np.float32)
+    h = ctypes.c_void_p()
+    st = flow.flib().dc_flow_init(blob.ctypes.data, blob.nbytes, ctypes.byref(cfg), ctypes.byref(h))
+    return st, h.value
+
+
+def test_flow_init_rejects_bad_configs_before_any_device_call():
+    arch = synth.TINY_FLOW_ARCH
+    blob = synth.make_flow_weights(arch)
+    good = lambda: flow.make_flow_cfg(arch, "f32", 2)
+    c = good()
+    c.abi_version = 7
+    assert _flow_init_status(c, blob) == (dc.DC_EVERSION, None)
+    for field, value, words in [("heads", 3, "dim"), ("n_mel", 12, "n_mel"), ("mlp", 100, "mlp"),
+                                ("f_call", 7, "f_chunk"), ("f_retained", 12, "f_retained"),
+                                ("dtype", 5, "dtype"), ("flags", 64, "flags"), ("batch", 0, "batch"),
+                                ("t_dim", 3, "t_dim")]:
+        c = good()
+        setattr(c, field, value)
+        assert _flow_init_status(c, blob)[0] == dc.DC_EINVAL, field
+        assert words in flow.dc_flow_last_error(None), (field, flow.dc_flow_last_error(None))
+        assert flow.dc_flow_blob_floats(c) == 0
+    assert _flow_init_status(good(), blob[:-1])[0] == dc.DC_EINVAL
+    assert "blob size" in flow.dc_flow_last_error(None)
+
+
+def test_flow_null_state_calls_fail_closed():
+    L = flow.flib()
+    assert L.dc_flow_prompt(None, 0, None, None, None, 1) == dc.DC_EINVAL
+    assert L.dc_flow_decode_chunk(None, None, 1, None) == dc.DC_EINVAL
+    assert L.dc_flow_sync(None) == dc.DC_EINVAL
+    assert L.dc_flow_carry_read(None, 0, 0, 0, 0, 0, None, None) == dc.DC_EINVAL
+    assert L.dc_flow_get_stats(None, None) == dc.DC_EINVAL
+    assert L.dc_flow_blob_floats(None) == 0
+    L.dc_flow_free(None)

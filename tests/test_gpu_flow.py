@@ -1,0 +1,215 @@
+"""Flow-decoder chunk step on the GPU against the fp64 oracle, through the C ABI.
+
+Parity: every chunk's mel frames within 1e-4 (fp32) / 2e-2 (bf16) of the
+oracle's, as max-abs-error / RMS; the carry the kernels wrote in place,
+read back in Eq. carry's order, within the same bound of the oracle's
+concatenated carry (the shadow audit); exact invariants (graph replay equals
+direct launches, a stream's result does not depend on the batch, a flush
+changes no state, a new turn starts from the prompt alone).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_35115_amd import synth
+from tests.gpu_common import TOL, bits_equal, err_stats, say
+
+pytestmark = pytest.mark.gpu
+
+TINY = synth.TINY_FLOW_ARCH
+SEED = 5
+
+
+def _flow():
+    import torch
+    assert torch.cuda.is_available()
+    from paper_2609_35115_amd import flow
+    return flow
+
+
+def _prompts(arch, B, P, seed=0):
+    return [synth.make_flow_prompt(arch, P, seed=seed, stream=b) for b in range(B)]
+
+
+def _run_gpu(arch, dtype, blob, B, P, calls, flags=0, prompts=None, mu=None):
+    """Prompt every stream, then the calls (frame counts); returns the decoder,
+    the per-call mel outputs (numpy [B][n][n_mel]) and the features."""
+    flow = _flow()
+    dec = flow.FlowDecoder(arch, dtype, blob, B, flags=flags, rng_seed=SEED)
+    prompts = prompts or _prompts(arch, B, P)
+    for b in range(B):
+        dec.prompt(b, *prompts[b])
+    total = sum(n for n in calls if n >= arch["f_chunk"]) + arch["f_call"]
+    mu = synth.make_flow_mu(arch, B, total) if mu is None else mu
+    outs, p = [], 0
+    for n in calls:
+        outs.append(dec.decode(mu[:, p:p + n]).cpu().numpy())
+        if n >= arch["f_chunk"]:
+            p += arch["f_chunk"]
+    dec.sync()
+    return dec, outs, mu, prompts
+
+
+def _run_oracle(arch, dtype, blob, b, prompt, mu_b, calls):
+    s = oracle.FlowStream(arch, dtype, blob, seed=SEED, key=b)
+    s.prompt(*prompt)
+    outs, p = [], 0
+    for n in calls:
+        outs.append(s.chunk(mu_b[p:p + n]))
+        if n >= arch["f_chunk"]:
+            p += arch["f_chunk"]
+    return s, outs
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tiny_chunks_match_oracle(dtype):
+    a = TINY
+    blob = synth.make_flow_weights(a, 0)
+    B, P = 2, a["f_prompt"]
+    calls = [a["f_call"]] * 5
+    say(f"flow tiny {dtype} B={B} calls={calls}")
+    dec, outs, mu, prompts = _run_gpu(a, dtype, blob, B, P, calls)
+    st = dec.stats()
+    assert st["replays"] == 5 and st["direct"] == 0, st
+    worst = 0.0
+    for b in range(B):
+        s, ref = _run_oracle(a, dtype, blob, b, prompts[b], mu[b], calls)
+        for k, (g, r) in enumerate(zip(outs, ref)):
+            e, _ = err_stats(g[b], r)
+            worst = max(worst, e)
+            assert e <= TOL[dtype], f"stream {b} call {k}: {e:.3e}"
+        # shadow audit: the carry read back in Eq. carry's order
+        for (i, l, c, kv) in [(0, 0, 0, 0), (a["n_steps"] - 1, a["depth"] - 1, 1, 1), (1, 0, 1, 0)]:
+            got = dec.carry(b, i, l, c, kv)
+            want = s.carry(i, l, c, kv)
+            assert got.shape == want.shape
+            e, _ = err_stats(got, want)
+            assert e <= TOL[dtype], f"carry {(b, i, l, c, kv)}: {e:.3e}"
+    say(f"  worst max-abs/RMS {worst:.3e}")
+    dec.close()
+
+
+def test_partial_calls_and_flush_match_oracle():
+    """Calls of other sizes run kernel by kernel: f_chunk frames (no lookahead),
+    a call between f_chunk and f_call, and a flush of fewer than f_chunk frames
+    that leaves the state unchanged."""
+    a = TINY
+    blob = synth.make_flow_weights(a, 0)
+    fc = a["f_chunk"]
+    calls = [a["f_call"], fc, fc + 1, 3, a["f_call"], fc]
+    dec, outs, mu, prompts = _run_gpu(a, "f32", blob, 2, 13, calls, prompts=_prompts(a, 2, 13, seed=1))
+    st = dec.stats()
+    assert st["replays"] == 2 and st["direct"] == 4, st
+    for b in range(2):
+        _s, ref = _run_oracle(a, "f32", blob, b, prompts[b], mu[b], calls)
+        for k, (g, r) in enumerate(zip(outs, ref)):
+            e, _ = err_stats(g[b], r)
+            assert e <= TOL["f32"], f"stream {b} call {k} (n={calls[k]}): {e:.3e}"
+    dec.close()
+
+
+def test_graph_replay_equals_direct_launches():
+    flow = _flow()
+    a = TINY
+    blob = synth.make_flow_weights(a, 2)
+    calls = [a["f_call"]] * 4
+    _d1, o1, _mu, _p = _run_gpu(a, "bf16", blob, 3, a["f_prompt"], calls)
+    _d2, o2, _mu, _p = _run_gpu(a, "bf16", blob, 3, a["f_prompt"], calls, flags=flow.DC_NO_GRAPH)
+    assert _d2.stats()["replays"] == 0
+    for x, y in zip(o1, o2):
+        assert bits_equal(x, y)
+
+
+def test_result_does_not_depend_on_the_batch():
+    """Stream 0 decoded alone and beside four other streams: bit for bit."""
+    a = TINY
+    blob = synth.make_flow_weights(a, 3)
+    calls = [a["f_call"]] * 3
+    prompts = _prompts(a, 5, a["f_prompt"])
+    _d5, o5, mu, _p = _run_gpu(a, "f32", blob, 5, a["f_prompt"], calls, prompts=prompts)
+    _d1, o1, _mu, _p = _run_gpu(a, "f32", blob, 1, a["f_prompt"], calls, prompts=prompts[:1], mu=mu[:1])
+    for x, y in zip(o5, o1):
+        assert bits_equal(x[0], y[0])
+
+
+def test_new_turn_starts_from_the_prompt_alone():
+    """A prompt pass in the middle of a stream's life resets its history: the
+    next chunks equal those of a fresh state given the same prompt."""
+    a = TINY
+    blob = synth.make_flow_weights(a, 0)
+    flow = _flow()
+    prompts = _prompts(a, 1, a["f_prompt"], seed=4)
+    dec, _outs, mu, _p = _run_gpu(a, "f32", blob, 1, a["f_prompt"], [a["f_call"]] * 3)
+    dec.prompt(0, *prompts[0])
+    again = [dec.decode(mu[:, k * a["f_chunk"]:k * a["f_chunk"] + a["f_call"]]).cpu().numpy() for k in range(2)]
+    fresh = flow.FlowDecoder(a, "f32", blob, 1, rng_seed=SEED)
+    fresh.prompt(0, *prompts[0])
+    ref = [fresh.decode(mu[:, k * a["f_chunk"]:k * a["f_chunk"] + a["f_call"]]).cpu().numpy() for k in range(2)]
+    for x, y in zip(again, ref):
+        assert bits_equal(x, y)
+    assert dec.carry(0, 0, 0, 0, 0).shape[0] == a["f_prompt"] + 2 * a["f_chunk"]
+
+
+def test_extents_follow_the_papers_catalog():
+    """The clock quantities of the paper (302, 100, 50, 56) at a small width:
+    carried extents 302, 352, 402, 402 (Eq. catalog)."""
+    a = dict(TINY, f_prompt=302, f_retained=100, f_chunk=50, f_call=56, n_steps=2, depth=1, dim=64, heads=1,
+             mlp=64, n_mel=8, t_dim=8)
+    blob = synth.make_flow_weights(a, 0)
+    flow = _flow()
+    dec = flow.FlowDecoder(a, "bf16", blob, 2, rng_seed=SEED)
+    for b in range(2):
+        dec.prompt(b, *synth.make_flow_prompt(a, 302, stream=b))
+    mu = synth.make_flow_mu(a, 2, 400)
+    seen = [dec.carry(1, 0, 0, 0, 0).shape[0]]
+    for k in range(3):
+        dec.decode(mu[:, 50 * k:50 * k + 56])
+        seen.append(dec.carry(1, 1, 0, 1, 1).shape[0])
+    assert seen == [302, 352, 402, 402]
+    dec.close()
+
+
+def test_rejects_bad_calls():
+    flow = _flow()
+    a = TINY
+    blob = synth.make_flow_weights(a, 0)
+    dec = flow.FlowDecoder(a, "f32", blob, 2, rng_seed=SEED)
+    mu = synth.make_flow_mu(a, 2, a["f_call"])
+    st = dec.decode(mu, check=False)
+    assert dec.stats()["rejected"] == 1                     # no turn yet
+    dec.prompt(0, *synth.make_flow_prompt(a, a["f_prompt"]))
+    dec.decode(mu, check=False)
+    assert dec.stats()["rejected"] == 2                     # stream 1 still has none
+    dec.prompt(1, *synth.make_flow_prompt(a, a["f_prompt"], stream=1))
+    too_long = synth.make_flow_mu(a, 2, a["f_call"] + 1)
+    with pytest.raises(Exception):
+        dec.decode(too_long)
+    big = synth.make_flow_prompt(a, a["f_prompt"] + 1)
+    with pytest.raises(Exception):
+        dec.prompt(0, *big)
+    out = dec.decode(mu)                                     # still usable
+    assert np.isfinite(out.cpu().numpy()).all()
+    del st
+    dec.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_real_shape_matches_oracle(dtype):
+    """The paper-shaped decoder (16 blocks of width 512, 10 solver steps,
+    f_call 56, f_chunk 50) with a 64-frame prompt: three calls (extents 64,
+    114, 164) against the oracle."""
+    a = synth.REAL_FLOW_ARCH
+    blob = synth.make_flow_weights(a, 0)
+    P = 64
+    calls = [a["f_call"]] * 2
+    say(f"flow real {dtype} B=1 P={P} calls={calls}")
+    dec, outs, mu, prompts = _run_gpu(a, dtype, blob, 1, P, calls)
+    s, ref = _run_oracle(a, dtype, blob, 0, prompts[0], mu[0], calls)
+    for k, (g, r) in enumerate(zip(outs, ref)):
+        e, er = err_stats(g[0], r)
+        say(f"  call {k}: max-abs/RMS {e:.3e}, RMS err/RMS {er:.3e}")
+        assert e <= TOL[dtype], f"call {k}: {e:.3e}"
+    for (i, l, c, kv) in [(9, 15, 0, 1), (0, 7, 1, 0)]:
+        e, _ = err_stats(dec.carry(0, i, l, c, kv), s.carry(i, l, c, kv))
+        assert e <= TOL[dtype], f"carry {(i, l, c, kv)}: {e:.3e}"
+    dec.close()

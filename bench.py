@@ -4,7 +4,11 @@
 
 A step is one chunk step of the whole decode path (embedding, pre-stack,
 upsampling stages with their resblocks, head, inverse STFT) for every stream
-of the workload, replayed as one HIP graph through the C ABI.  Token chunks
+of the workload, replayed as one HIP graph through the C ABI.  For a flow
+workload (--workload flow_*) a step is one flow-decoder call of f_call frames
+for every stream (n_steps guided Euler steps of the DiT estimator over the
+carried attention state), also one graph replay; it yields f_chunk new frames
+per stream, f_chunk / 50 seconds of audio at the 50 Hz frame clock.  Token chunks
 are resident in HBM before the timed region; each step stages its chunk into
 the state's token buffer (counted in the step) and leaves the PCM in the
 state's audio buffer.  Prints one JSON line:
@@ -77,17 +81,21 @@ def cpu_baseline(arch, dtype, blob, tokens, budget_s: float, f0=None):
                       f"{' on bf16-rounded weights' if dtype == 'bf16' else ''}, {dt:.1f} s wall"}
 
 
-def kernel_source_hash() -> str:
+FLOW_FRAME_RATE = 50.0   # frames per second of audio: 2 frames per 25 Hz token
+FLOW_SOURCES = ("flow_kernels.hip", "flow_internal.h")
+
+
+def kernel_source_hash(files=("dc_kernels.hip", "dc_internal.h")) -> str:
     """Hash of the kernel sources: a traffic figure taken on other sources is stale."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("dc_kernels.hip", "dc_internal.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2609_35115_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def traffic_from_profiles(workload: str, kernel: str):
+def traffic_from_profiles(workload: str, kernel: str, files=("dc_kernels.hip", "dc_internal.h")):
     """HBM bytes per launch of `kernel` recorded under profiles/ for this workload
     with the current kernel sources, else None."""
     path = os.path.join(PROFILES, f"traffic_{workload}.txt")
@@ -98,7 +106,7 @@ def traffic_from_profiles(workload: str, kernel: str):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             rec[k.strip()] = v.strip()
-    if rec.get("kernel_source_hash") != kernel_source_hash() or rec.get("kernel") != kernel:
+    if rec.get("kernel_source_hash") != kernel_source_hash(files) or rec.get("kernel") != kernel:
         return None
     return float(rec["hbm_bytes_per_launch"])
 
@@ -266,6 +274,168 @@ def summarize_mfma(prof_dir: str, workload: str, out: str, command: str):
     print("\n".join(lines))
 
 
+FLOW_KERNEL = {   # role -> the kernel template that runs it (dtype filled in)
+    "gemm:in": "gemm_kernel<{b}, 0>", "gemm:qkv": "gemm_kernel<{b}, 1>", "gemm:o": "gemm_kernel<{b}, 2>",
+    "gemm:fc2": "gemm_kernel<{b}, 2>", "gemm:fc1": "gemm_kernel<{b}, 3>", "gemm:out": "gemm_kernel<{b}, 4>",
+    "attn": "attn_kernel<{b}>", "lnmod": "lnmod_kernel<{b}>", "assemble": "assemble_kernel<{b}>",
+    "euler": "euler_kernel<{b}>",
+}
+
+
+def flow_roofline(prof, dtype):
+    """The role with the most device time per call, against its bound."""
+    step_us = sum(r["us"] for r in prof)
+    top = max(prof, key=lambda r: r["us"])
+    op = "bf16" if dtype == "bf16" else "f32"
+    if top["mfma"] and top["flops"] / top["bytes"] > PEAK[op] * 1e12 / (PEAK["hbm"] * 1e9):
+        bound, achieved, peak, unit = "mfma", top["flops"] / (top["us"] * 1e-6) / 1e12, PEAK[op], "TFLOP/s"
+    else:
+        bound, achieved, peak, unit = "hbm", top["bytes"] / (top["us"] * 1e-6) / 1e9, PEAK["hbm"], "GB/s"
+    kern = "dcf::" + FLOW_KERNEL.get(top["name"], top["name"]).format(b="true" if dtype == "bf16" else "false")
+    return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": None, "kernel": kern, "role": top["name"],
+            "operand": op, "launches_per_step": top["launches"],
+            "mean_launch_us": round(top["us"] / top["launches"], 3),
+            "flops_per_launch": top["flops"] / top["launches"], "bytes_per_launch": top["bytes"] / top["launches"],
+            "share_of_step": round(top["us"] / step_us, 4),
+            "kernels_by_share": [[r["name"], round(r["us"] / step_us, 4)]
+                                 for r in sorted(prof, key=lambda r: -r["us"])[:6]],
+            "step_us_launch_by_launch": round(step_us, 2)}
+
+
+def flow_cpu_baseline(arch, dtype, blob, budget_s: float, prompt_frames: int = 64):
+    """The oracle on stream 0: a short prompt (untimed), then chunk calls of
+    f_call frames until one budget's worth of time has passed."""
+    import oracle
+    from paper_2609_35115_amd import synth
+    fc, fcall = arch["f_chunk"], arch["f_call"]
+    P = min(prompt_frames, arch["f_prompt"])
+    s = oracle.FlowStream(arch, dtype, blob, seed=RNG_SEED, key=0)
+    s.prompt(*synth.make_flow_prompt(arch, P))
+    mu = synth.make_flow_mu(arch, 1, 64 * fc + fcall)[0]
+    calls, t0 = 0, time.perf_counter()
+    while True:
+        s.chunk(mu[calls * fc:calls * fc + fcall])
+        calls += 1
+        dt = time.perf_counter() - t0
+        if dt >= budget_s or calls >= 64:
+            break
+    return {"value": calls * fc / FLOW_FRAME_RATE / dt, "unit": "audio-s/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"stream 0, {calls} chunk calls of {fcall} frames after a {P}-frame prompt (untimed), "
+                      f"fp64{' on bf16-rounded weights' if dtype == 'bf16' else ''}, {dt:.1f} s wall"}
+
+
+def bench_flow(args):
+    import numpy as np
+    import torch
+
+    from paper_2609_35115_amd import flow, synth
+
+    w = synth.workload(args.workload)
+    arch, dtype, B, chunks = w["arch"], w["dtype"], w["batch"], w["chunks"]
+    fc, fcall, P, M = arch["f_chunk"], arch["f_call"], arch["f_prompt"], arch["n_mel"]
+    torch.cuda.set_device(0)
+    blob = synth.make_flow_weights(arch, 0)
+    prompts = [synth.make_flow_prompt(arch, P, stream=b) for b in range(B)]
+    mu = synth.make_flow_mu(arch, B, chunks * fc + fcall)
+    mu_dev = torch.from_numpy(np.ascontiguousarray(np.stack([mu[:, k * fc:k * fc + fcall] for k in range(chunks)]))).cuda()
+    mel = torch.empty((B, fcall, M), dtype=torch.float32, device="cuda")
+    dec = flow.FlowDecoder(arch, dtype, blob, B, rng_seed=RNG_SEED)
+    for b in range(B):
+        dec.prompt(b, *prompts[b])
+    dec.sync()
+    torch.cuda.synchronize()
+
+    def step(d, i):
+        st = flow.dc_flow_decode_chunk(d.h, mu_dev[i % chunks], fcall, mel)
+        if st != 0:
+            raise RuntimeError(flow.dc_flow_last_error(d.h))
+
+    print(f"# workload {args.workload}: batch {B}, f_call {fcall}, f_chunk {fc}, {dtype}; warmup {args.warmup}, "
+          f"steps {args.steps}", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(dec, i)
+    dec.sync()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(dec, args.warmup + i)
+    dec.stream.synchronize()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dec.sync()
+    ms_per_step = 1000.0 * wall / args.steps
+    audio_s = B * fc / FLOW_FRAME_RATE
+    value = audio_s * args.steps / wall
+    print(f"# timed {args.steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
+
+    lat_dev, lat_ev = [], []
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for i in range(args.latency_chunks):
+        t = time.perf_counter()
+        ev[0].record(dec.stream)
+        step(dec, i)
+        ev[1].record(dec.stream)
+        dec.stream.synchronize()
+        lat_dev.append(1000.0 * (time.perf_counter() - t))
+        lat_ev.append(ev[0].elapsed_time(ev[1]))
+    prof = dec.profile(args.layer_reps)
+    roof = flow_roofline(prof, dtype)
+    roof["traffic"] = traffic_from_profiles(args.workload, roof["kernel"], FLOW_SOURCES)
+    stats = dec.stats()
+    dec.close()
+
+    hdec = flow.FlowDecoder(arch, dtype, blob, B, flags=flow.DC_HOST_PTRS, rng_seed=RNG_SEED)
+    for b in range(B):
+        hdec.prompt(b, *prompts[b])
+    host_mu = [np.ascontiguousarray(mu[:, k * fc:k * fc + fcall]) for k in range(chunks)]
+    out = np.empty((B, fcall, M), dtype=np.float32)
+    lat = []
+    for i in range(min(args.warmup, 5) + args.latency_chunks):
+        t = time.perf_counter()
+        st = flow.dc_flow_decode_chunk(hdec.h, host_mu[i % chunks], fcall, out)
+        dt = 1000.0 * (time.perf_counter() - t)
+        if st != 0:
+            raise RuntimeError(flow.dc_flow_last_error(hdec.h))
+        if i >= min(args.warmup, 5):
+            lat.append(dt)
+    hdec.close()
+
+    if not args.skip_peaks:
+        peaks = measured_peaks()
+        key = "hbm_copy_GBs" if roof["bound"] == "hbm" else f"{roof['operand']}_gemm_TFLOPs"
+        roof["measured_peak"] = peaks[key]
+        roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
+        roof["measured_peaks"] = peaks
+    print(f"# roofline: {roof['kernel']} ({roof['role']}) {roof['achieved']} {roof['unit']} ({roof['frac']:.1%})",
+          file=sys.stderr, flush=True)
+    cpu = flow_cpu_baseline(arch, dtype, blob, args.cpu_budget) if args.cpu_budget > 0 else None
+    res = {
+        "metric": METRIC, "value": round(value, 3), "unit": "audio-s/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+        "data": "synthetic (seeded random-weight DiT flow decoder, N(0,1) encoder features, synthetic prompts)",
+        "config": {"workload": args.workload, "stage": "flow decoder",
+                   "arch": "real" if arch["dim"] == 512 else "tiny", "batch": B, "f_call": fcall, "f_chunk": fc,
+                   "f_prompt": P, "f_retained": arch["f_retained"], "n_steps": arch["n_steps"],
+                   "chunks_cycled": chunks, "audio_s_per_step": audio_s, "graph_replay": stats["replays"] > 0,
+                   "kernels_per_step": stats["kernels_per_call"],
+                   "flops_per_step": sum(r["flops"] for r in prof),
+                   "carry_bytes": stats["carry_bytes"], "carry_live_bytes": stats["carry_live_bytes"]},
+        "p50_chunk_ms": round(float(np.percentile(lat, 50)), 4),
+        "p99_chunk_ms": round(float(np.percentile(lat, 99)), 4),
+        "latency_path": "host mu in, host mel out, synchronous dc_flow_decode_chunk",
+        "p50_chunk_ms_device_buffers": round(float(np.percentile(lat_dev, 50)), 4),
+        "p99_chunk_ms_device_buffers": round(float(np.percentile(lat_dev, 99)), 4),
+        "p50_replay_ms_hip_events": round(float(np.percentile(lat_ev, 50)), 4),
+        "capture_ms": round(stats["capture_ms"], 3),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize-mfma":
         return summarize_mfma(*sys.argv[2:6])
@@ -292,6 +462,9 @@ def main():
               "independent, so a multi-GPU deployment runs one state per GPU with no collectives; "
               "run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload.startswith("flow_"):
+        return bench_flow(args)
 
     import numpy as np
     import torch

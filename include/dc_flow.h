@@ -21,8 +21,8 @@
  * capture placement", Eq. granularity: binding at the chunk clock divides
  * host launches by n_steps).
  *
- * Shapes fixed by the kernels: head width dim / heads = 64; dim, mlp and
- * 4 n_mel multiples of 32; n_mel even and <= 256.
+ * Shapes fixed by the kernels: head width dim / heads = 64 and dim <= 1024;
+ * mlp a multiple of 32; n_mel a multiple of 8, <= 1024; t_dim even, <= 1024.
  *
  * Conventions are those of dc.h: functions return a dc_status (0 on
  * success); dc_flow_last_error() explains the last failure; a state is not
@@ -78,6 +78,17 @@ typedef struct dc_flow_stats {
     double capture_ms;        /* dc_flow_init wall time: upload, constants, warm-up, capture     */
 } dc_flow_stats;
 
+/* Device time of one kernel role in one call (dc_flow_profile). */
+typedef struct dc_flow_kernel_stat {
+    char name[48];            /* role: "assemble", "gemm:in", "lnmod", "gemm:qkv", "attn", "gemm:o",
+                                 "gemm:fc1", "gemm:fc2", "gemm:out", "euler"                           */
+    int32_t launches;         /* launches of this role per call                                      */
+    int32_t mfma;             /* 1: the role is a matrix-core contraction                            */
+    double us;                /* device time per call, summed over its launches (HIP events)        */
+    double flops;             /* algorithmic floating-point operations per call                      */
+    double bytes;             /* algorithmic HBM bytes per call: operands read once, results written */
+} dc_flow_kernel_stat;
+
 typedef struct dc_flow_state dc_flow_state;
 
 /* Number of float32 values the weight blob of cfg must hold (0 for NULL).  The
@@ -132,6 +143,14 @@ dc_status dc_flow_carry_read(dc_flow_state* s, int32_t b, int32_t step, int32_t 
                              float* host_out, int32_t* frames);
 
 dc_status dc_flow_get_stats(const dc_flow_state* s, dc_flow_stats* out);
+
+/* Time an f_call-frame call launch by launch, `reps` times (mean per call),
+ * with HIP events on the state's stream, grouped by kernel role into out[0 ..
+ * *count) (at most max entries; out = NULL queries the count).  The streams'
+ * state does not advance and no retained frame changes: the call writes only
+ * the slot that the next call overwrites.  Every stream needs a turn.  For
+ * measurement; synchronous.  Errors: DC_EINVAL, DC_ESTATE, DC_EDEVICE. */
+dc_status dc_flow_profile(dc_flow_state* s, int32_t reps, dc_flow_kernel_stat* out, int32_t max, int32_t* count);
 
 /* Text of the last error of s (of the last failed dc_flow_init when s is NULL). */
 const char* dc_flow_last_error(const dc_flow_state* s);

@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <cstdio>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -159,9 +160,20 @@ CarryRef carry_ref(const dc_flow_state* s, int i, int l)
     return r;
 }
 
+// Per-launch timing: events recorded around each launch of a profiled call.
+struct Recorder {
+    std::vector<std::string> role;
+    std::vector<double> flops, bytes;
+    std::vector<int> mfma;
+    std::vector<hipEvent_t> ev;   // two per launch
+    size_t at = 0;
+};
+
 // The launches of one call over Bc streams from b0 with n frames per stream.
+// With a recorder, each launch is bracketed by events and described (role,
+// algorithmic flops and bytes), and the state advance is left out.
 hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, const float* mu, const float* cond,
-                        float* mel, hipStream_t st, int* count)
+                        float* mel, hipStream_t st, int* count, Recorder* rec = nullptr)
 {
     const dc_flow_cfg& c = s->cfg;
     const int bf = s->bf ? 1 : 0;
@@ -169,14 +181,49 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
     const int rows = Bc * 2 * n, Fq = round_up(n, 64);
     int k = 0;
     hipError_t e;
-#define DCF_TRY(x)                        \
-    do {                                  \
-        e = (x);                          \
-        if (e != hipSuccess) return e;    \
-        k++;                              \
+    const double es = (double)s->esz;
+    const int64_t ext_keys = [&] {   // keys attended by all the call's queries, summed over its streams
+        int64_t t = 0;
+        if (!rec) return t;
+        for (int b = b0; b < b0 + Bc; b++)
+            t += prompt ? n : std::min<int64_t>(s->hist_host[b], s->R) * c.f_chunk + s->plen_host[b] + n;
+        return t;
+    }();
+    std::string role;
+    double fl = 0, by = 0;
+    int mf = 0;
+    auto describe = [&](const char* r, double f, double b, int m) {
+        role = r;
+        fl = f;
+        by = b;
+        mf = m;
+    };
+    auto gemm_cost = [&](const char* r, int N, int K, double out_es, bool reads_h) {
+        describe(r, 2.0 * rows * N * K, (double)rows * K * es + (double)N * K * es + (double)N * 4 +
+                                            (double)rows * N * out_es * (reads_h ? 2 : 1), 1);
+    };
+#define DCF_TRY(x)                                                           \
+    do {                                                                     \
+        if (rec) {                                                           \
+            e = hipEventRecord(rec->ev[2 * rec->at], st);                    \
+            if (e != hipSuccess) return e;                                   \
+        }                                                                    \
+        e = (x);                                                             \
+        if (e != hipSuccess) return e;                                       \
+        if (rec) {                                                           \
+            e = hipEventRecord(rec->ev[2 * rec->at + 1], st);                \
+            if (e != hipSuccess) return e;                                   \
+            rec->role[rec->at] = role;                                       \
+            rec->flops[rec->at] = fl;                                        \
+            rec->bytes[rec->at] = by;                                        \
+            rec->mfma[rec->at] = mf;                                         \
+            rec->at++;                                                       \
+        }                                                                    \
+        k++;                                                                 \
     } while (0)
 
     AssembleParams ap{mu, cond, s->spk, s->x, s->xin, s->pos, s->keys, c.rng_seed, c.temperature, n, b0, Bc, M};
+    describe("assemble", 0, (double)Bc * n * M * 4 * (cond ? 2 : 1) + (double)rows * 4 * M * es + (double)Bc * n * M * 4, 0);
     DCF_TRY(launch_assemble(ap, bf, st));
     for (int i = 0; i < NS; i++) {
         GemmParams g{};
@@ -195,10 +242,12 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
         g.N = D;
         g.K = 4 * M;
         g.h = s->h;
+        gemm_cost("gemm:in", D, 4 * M, 4, false);
         DCF_TRY(launch_gemm(g, E_H, bf, st));
         for (int l = 0; l < NL; l++) {
             const float* md = s->mods + ((size_t)i * NL + l) * 6 * D;
             LnParams ln{s->h, s->a, md, md + D, rows, D};
+            describe("lnmod", 8.0 * rows * D, (double)rows * D * (4 + es) + 2.0 * D * 4, 0);
             DCF_TRY(launch_lnmod(ln, bf, st));
             const CarryRef cr = carry_ref(s, i, l);
             g.A = s->a;
@@ -207,8 +256,12 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
             g.N = 3 * D;
             g.K = D;
             g.carry = cr;
+            gemm_cost("gemm:qkv", 3 * D, D, es, false);
             DCF_TRY(launch_gemm(g, E_QKV, bf, st));
             AttnParams at{s->q, Fq, cr, s->o, prompt, n, b0, c.heads, D, c.f_chunk};
+            // per (stream, branch, head): n queries x its keys x 64, twice (scores, values)
+            describe("attn", 4.0 * 2 * c.heads * 64 * (double)n * ext_keys,
+                     2.0 * 2 * c.heads * 64 * (double)ext_keys * es + 2.0 * rows * D * es, 1);
             DCF_TRY(launch_attn(at, Bc, bf, st));
             g.A = s->o;
             g.W = s->w_o[l];
@@ -216,8 +269,10 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
             g.N = D;
             g.K = D;
             g.gate = md + 2 * D;
+            gemm_cost("gemm:o", D, D, 4, true);
             DCF_TRY(launch_gemm(g, E_RES, bf, st));
             LnParams ln2{s->h, s->a, md + 3 * D, md + 4 * D, rows, D};
+            describe("lnmod", 8.0 * rows * D, (double)rows * D * (4 + es) + 2.0 * D * 4, 0);
             DCF_TRY(launch_lnmod(ln2, bf, st));
             g.A = s->a;
             g.W = s->w_fc1[l];
@@ -225,6 +280,7 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
             g.N = c.mlp;
             g.K = D;
             g.out = s->u;
+            gemm_cost("gemm:fc1", c.mlp, D, es, false);
             DCF_TRY(launch_gemm(g, E_GELU, bf, st));
             g.A = s->u;
             g.W = s->w_fc2[l];
@@ -232,10 +288,12 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
             g.N = D;
             g.K = c.mlp;
             g.gate = md + 5 * D;
+            gemm_cost("gemm:fc2", D, c.mlp, 4, true);
             DCF_TRY(launch_gemm(g, E_RES, bf, st));
         }
         const float* fm = s->fmods + (size_t)i * 2 * D;
         LnParams lf{s->h, s->a, fm, fm + D, rows, D};
+        describe("lnmod", 8.0 * rows * D, (double)rows * D * (4 + es) + 2.0 * D * 4, 0);
         DCF_TRY(launch_lnmod(lf, bf, st));
         g.A = s->a;
         g.W = s->w_out;
@@ -243,11 +301,15 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
         g.N = M;
         g.K = D;
         g.out = s->v;
+        gemm_cost("gemm:out", M, D, 4, false);
         DCF_TRY(launch_gemm(g, E_VEL, bf, st));
         EulerParams ep{s->v, s->x, s->xin, i == NS - 1 ? mel : nullptr, s->dt + i, c.cfg_rate, n, Bc, M};
+        describe("euler", 5.0 * Bc * n * M, (double)rows * M * 4 + 2.0 * Bc * n * M * 4 + (double)rows * M * es, 0);
         DCF_TRY(launch_euler(ep, bf, st));
     }
-    if (!prompt && n >= c.f_chunk) DCF_TRY(launch_advance(s->hist, s->pos, s->plen, 2, 0, 0, c.batch, c.f_chunk, st));
+    describe("advance", 0, 0, 0);
+    if (!prompt && n >= c.f_chunk && !rec)
+        DCF_TRY(launch_advance(s->hist, s->pos, s->plen, 2, 0, 0, c.batch, c.f_chunk, st));
 #undef DCF_TRY
     if (count) *count = k;
     return hipSuccess;
@@ -289,6 +351,8 @@ dc_status dc_flow_init(const void* weights_blob, size_t blob_bytes, const dc_flo
     s->esz = s->bf ? 2 : 4;
     const int D = c.dim, M = c.n_mel, NL = c.depth, NS = c.n_steps, B = c.batch;
     const float* blob = (const float*)weights_blob;
+    s->plen_host.assign(B, 0);   // no stream has a turn
+    s->hist_host.assign(B, 0);
 
     // carry geometry: prompt region and slots padded to 4 frames (aligned
     // 4-key value groups), R history slots plus the one a call writes
@@ -492,8 +556,6 @@ dc_status dc_flow_init(const void* weights_blob, size_t blob_bytes, const dc_flo
         dc_flow_free(s);
         return fail(nullptr, DC_EDEVICE, m);
     }
-    s->plen_host.assign(B, 0);
-    s->hist_host.assign(B, 0);
     s->st.weight_bytes = (int64_t)consts_end;
     s->st.carry_bytes = (int64_t)(carry_end - o_carry);
     s->st.carry_live_bytes = (int64_t)B * NS * NL * 4 * (int64_t)(c.f_retained + c.f_prompt) * D * (int64_t)es;
@@ -602,6 +664,60 @@ dc_status dc_flow_carry_read(dc_flow_state* s, int32_t b, int32_t step, int32_t 
         e = hipMemcpyAsync(host_out, s->gather, (size_t)ext * c.dim * 4, hipMemcpyDeviceToHost, s->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
     if (e != hipSuccess) return device_fail(s, e, "carry read");
+    return DC_OK;
+}
+
+dc_status dc_flow_profile(dc_flow_state* s, int32_t reps, dc_flow_kernel_stat* out, int32_t max, int32_t* count)
+{
+    if (!s || !count || reps < 1 || (out && max < 0)) return DC_EINVAL;
+    if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned");
+    const dc_flow_cfg& c = s->cfg;
+    for (int b = 0; b < c.batch; b++)
+        if (s->plen_host[b] == 0) return fail(s, DC_ESTATE, "a stream has no turn: call dc_flow_prompt first");
+    const int nl = s->st.kernels_per_call;
+    Recorder rec;
+    rec.role.assign(nl, "");
+    rec.flops.assign(nl, 0.0);
+    rec.bytes.assign(nl, 0.0);
+    rec.mfma.assign(nl, 0);
+    rec.ev.assign(2 * (size_t)nl, nullptr);
+    hipError_t e = hipSuccess;
+    for (auto& ev : rec.ev)
+        if (e == hipSuccess) e = hipEventCreate(&ev);
+    std::vector<double> us(nl, 0.0);
+    int launched = 0;
+    for (int r = 0; r < reps && e == hipSuccess; r++) {
+        rec.at = 0;
+        e = enqueue_call(s, 0, c.batch, c.f_call, 0, s->mu_in, nullptr, s->mel_out, s->stream, &launched, &rec);
+        if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+        for (size_t i = 0; i < rec.at && e == hipSuccess; i++) {
+            float ms = 0.f;
+            e = hipEventElapsedTime(&ms, rec.ev[2 * i], rec.ev[2 * i + 1]);
+            us[i] += 1000.0 * ms / reps;
+        }
+    }
+    for (auto& ev : rec.ev)
+        if (ev) (void)hipEventDestroy(ev);
+    if (e != hipSuccess) return device_fail(s, e, "profile");
+    std::vector<dc_flow_kernel_stat> groups;
+    for (size_t i = 0; i < rec.at; i++) {
+        auto it = std::find_if(groups.begin(), groups.end(),
+                               [&](const dc_flow_kernel_stat& g) { return rec.role[i] == g.name; });
+        if (it == groups.end()) {
+            dc_flow_kernel_stat g{};
+            std::snprintf(g.name, sizeof(g.name), "%s", rec.role[i].c_str());
+            g.mfma = rec.mfma[i];
+            groups.push_back(g);
+            it = groups.end() - 1;
+        }
+        it->launches++;
+        it->us += us[i];
+        it->flops += rec.flops[i];
+        it->bytes += rec.bytes[i];
+    }
+    *count = (int32_t)groups.size();
+    if (out)
+        for (int i = 0; i < (int)groups.size() && i < max; i++) out[i] = groups[i];
     return DC_OK;
 }
 

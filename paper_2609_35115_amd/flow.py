@@ -37,6 +37,13 @@ class DcFlowStats(ctypes.Structure):
     ]
 
 
+class DcFlowKernelStat(ctypes.Structure):
+    _fields_ = [
+        ("name", ctypes.c_char * 48), ("launches", ctypes.c_int32), ("mfma", ctypes.c_int32),
+        ("us", ctypes.c_double), ("flops", ctypes.c_double), ("bytes", ctypes.c_double),
+    ]
+
+
 FLOW_SIGNATURES = {
     "dc_flow_blob_floats": ([ctypes.POINTER(DcFlowCfg)], ctypes.c_int64),
     "dc_flow_init": ([_P, ctypes.c_size_t, ctypes.POINTER(DcFlowCfg), ctypes.POINTER(_P)], ctypes.c_int),
@@ -46,6 +53,8 @@ FLOW_SIGNATURES = {
     "dc_flow_carry_read": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P,
                             ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
     "dc_flow_get_stats": ([_P, ctypes.POINTER(DcFlowStats)], ctypes.c_int),
+    "dc_flow_profile": ([_P, ctypes.c_int32, ctypes.POINTER(DcFlowKernelStat), ctypes.c_int32,
+                         ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
     "dc_flow_last_error": ([_P], ctypes.c_char_p),
     "dc_flow_free": ([_P], None),
 }
@@ -136,6 +145,16 @@ def dc_flow_get_stats(h) -> dict:
     return {name: getattr(s, name) for name, _ in DcFlowStats._fields_}
 
 
+def dc_flow_profile(h, reps: int) -> list:
+    """Per-role device time of one f_call-frame call (dicts, in launch order of first use)."""
+    n = ctypes.c_int32()
+    _check(flib().dc_flow_profile(h, reps, None, 0, ctypes.byref(n)), h)
+    arr = (DcFlowKernelStat * n.value)()
+    _check(flib().dc_flow_profile(h, reps, arr, n.value, ctypes.byref(n)), h)
+    return [{"name": a.name.decode(), "launches": a.launches, "mfma": bool(a.mfma), "us": a.us,
+             "flops": a.flops, "bytes": a.bytes} for a in arr]
+
+
 def dc_flow_free(h) -> None:
     flib().dc_flow_free(h)
 
@@ -216,3 +235,6 @@ class FlowDecoder:
 
     def stats(self) -> dict:
         return dc_flow_get_stats(self.h)
+
+    def profile(self, reps: int = 5) -> list:
+        return dc_flow_profile(self.h, reps)

@@ -126,6 +126,8 @@ def test_flow_struct_sizes_match_header_layout():
     assert ctypes.sizeof(flow.DcFlowCfg) == 72 + 8 + 8
     # 9 int64, 2 int32, a double
     assert ctypes.sizeof(flow.DcFlowStats) == 9 * 8 + 2 * 4 + 8
+    # a 48-byte name, 2 int32, 3 doubles
+    assert ctypes.sizeof(flow.DcFlowKernelStat) == 48 + 8 + 24
 
 
 @pytest.mark.parametrize("arch", [synth.TINY_FLOW_ARCH, synth.REAL_FLOW_ARCH])
@@ -168,4 +170,5 @@ def test_flow_null_state_calls_fail_closed():
     assert L.dc_flow_carry_read(None, 0, 0, 0, 0, 0, None, None) == dc.DC_EINVAL
     assert L.dc_flow_get_stats(None, None) == dc.DC_EINVAL
     assert L.dc_flow_blob_floats(None) == 0
+    assert L.dc_flow_profile(None, 1, None, 0, None) == dc.DC_EINVAL
     L.dc_flow_free(None)

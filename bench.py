@@ -274,15 +274,24 @@ def summarize_mfma(prof_dir: str, workload: str, out: str, command: str):
     print("\n".join(lines))
 
 
-FLOW_KERNEL = {   # role -> the kernel template that runs it (dtype filled in)
-    "gemm:in": "gemm_kernel<{b}, 0>", "gemm:qkv": "gemm_kernel<{b}, 1>", "gemm:o": "gemm_kernel<{b}, 2>",
-    "gemm:fc2": "gemm_kernel<{b}, 2>", "gemm:fc1": "gemm_kernel<{b}, 3>", "gemm:out": "gemm_kernel<{b}, 4>",
-    "attn": "attn_kernel<{b}>", "lnmod": "lnmod_kernel<{b}>", "assemble": "assemble_kernel<{b}>",
-    "euler": "euler_kernel<{b}>",
+FLOW_GEMM = {   # role -> (epilogue, LayerNorm operand) of the GEMM that runs it
+    "gemm:in": (0, False), "gemm:qkv": (1, True), "gemm:o": (2, False), "gemm:fc2": (2, False),
+    "gemm:fc1": (3, True), "gemm:out": (4, True),
 }
+SKINNY_ROWS = 512   # calls of at most this many rows (2 per stream and frame) run the skinny GEMM
 
 
-def flow_roofline(prof, dtype):
+def flow_kernel_name(role: str, dtype: str, rows: int) -> str:
+    b = "true" if dtype == "bf16" else "false"
+    if role in FLOW_GEMM:
+        epi, ln = FLOW_GEMM[role]
+        if rows <= SKINNY_ROWS:
+            return f"dcf::skinny_kernel<{b}, {epi}, {'true' if ln else 'false'}>"
+        return f"dcf::gemm_kernel<{b}, {epi}, false>"
+    return f"dcf::{role}_kernel<{b}>" if role in ("attn", "assemble", "euler") else role
+
+
+def flow_roofline(prof, dtype, rows):
     """The role with the most device time per call, against its bound."""
     step_us = sum(r["us"] for r in prof)
     top = max(prof, key=lambda r: r["us"])
@@ -291,7 +300,7 @@ def flow_roofline(prof, dtype):
         bound, achieved, peak, unit = "mfma", top["flops"] / (top["us"] * 1e-6) / 1e12, PEAK[op], "TFLOP/s"
     else:
         bound, achieved, peak, unit = "hbm", top["bytes"] / (top["us"] * 1e-6) / 1e9, PEAK["hbm"], "GB/s"
-    kern = "dcf::" + FLOW_KERNEL.get(top["name"], top["name"]).format(b="true" if dtype == "bf16" else "false")
+    kern = flow_kernel_name(top["name"], dtype, rows)
     return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": None, "kernel": kern, "role": top["name"],
             "operand": op, "launches_per_step": top["launches"],
@@ -381,7 +390,7 @@ def bench_flow(args):
         lat_dev.append(1000.0 * (time.perf_counter() - t))
         lat_ev.append(ev[0].elapsed_time(ev[1]))
     prof = dec.profile(args.layer_reps)
-    roof = flow_roofline(prof, dtype)
+    roof = flow_roofline(prof, dtype, B * 2 * fcall)
     roof["traffic"] = traffic_from_profiles(args.workload, roof["kernel"], FLOW_SOURCES)
     stats = dec.stats()
     dec.close()

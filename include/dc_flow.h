@@ -16,12 +16,12 @@
  * Eq. carry: new frames in front, the immutable prompt tail behind, extent
  * capped at L = f_retained + f_prompt; the attended extents are f_prompt,
  * f_prompt + f_chunk, ..., L, Eq. catalog).  The whole call for f_call frames
- * -- n_steps x (input projection, depth x 7 kernels, output projection,
+ * -- n_steps x (input projection, depth x 5 kernels, output projection,
  * guided Euler update) -- is one HIP graph replay (Design, "Granularity and
  * capture placement", Eq. granularity: binding at the chunk clock divides
  * host launches by n_steps).
  *
- * Shapes fixed by the kernels: head width dim / heads = 64 and dim <= 1024;
+ * Shapes fixed by the kernels: head width dim / heads = 64 and dim <= 512;
  * mlp a multiple of 32; n_mel a multiple of 8, <= 1024; t_dim even, <= 1024.
  *
  * Conventions are those of dc.h: functions return a dc_status (0 on
@@ -80,7 +80,7 @@ typedef struct dc_flow_stats {
 
 /* Device time of one kernel role in one call (dc_flow_profile). */
 typedef struct dc_flow_kernel_stat {
-    char name[48];            /* role: "assemble", "gemm:in", "lnmod", "gemm:qkv", "attn", "gemm:o",
+    char name[48];            /* role: "assemble", "gemm:in", "gemm:qkv", "attn", "gemm:o",
                                  "gemm:fc1", "gemm:fc2", "gemm:out", "euler"                           */
     int32_t launches;         /* launches of this role per call                                      */
     int32_t mfma;             /* 1: the role is a matrix-core contraction                            */

@@ -38,9 +38,15 @@ struct CarryRef {
     const int* plen;         // [B] prompt frames of the turn
 };
 
-// out[row][col] = epilogue(sum_k A[row][k] W[col][k] + bias[col])
+// out[row][col] = epilogue(sum_k A[row][k] W[col][k] + bias[col]); with
+// ln_h set, A[row][k] = LN(ln_h[row])[k] * (1 + ln_scale[k]) + ln_shift[k]
+// (the modulated LayerNorm of the fp32 residual stream, K <= 512): normalised
+// while staged for calls of few rows, else written to A by a launch of its own.
 struct GemmParams {
-    const void* A;           // [M][K] operand type
+    const void* A;           // [M][K] operand type (with ln_h: where the normalised operand may be written)
+    const float* ln_h;       // [M][K] or null
+    const float* ln_shift;   // [K]
+    const float* ln_scale;   // [K]
     const void* W;           // [N][K] operand type
     const float* bias;       // [N]
     int M, N, K;
@@ -61,14 +67,6 @@ struct AttnParams {
     void* o;                 // [M][dim] operand type
     int prompt;              // 1: the keys are the call's own frames only
     int n, b0, heads, dim, f_chunk;
-};
-
-struct LnParams {
-    const float* h;          // [M][dim]
-    void* out;               // [M][dim] operand type
-    const float* shift;      // [dim]
-    const float* scale;      // [dim]
-    int M, dim;
 };
 
 struct AssembleParams {
@@ -111,7 +109,6 @@ struct ConstParams {
 hipError_t launch_consts(const ConstParams& p, hipStream_t st);
 hipError_t launch_assemble(const AssembleParams& p, int bf16, hipStream_t st);
 hipError_t launch_gemm(const GemmParams& p, int epi, int bf16, hipStream_t st);
-hipError_t launch_lnmod(const LnParams& p, int bf16, hipStream_t st);
 hipError_t launch_attn(const AttnParams& p, int Bc, int bf16, hipStream_t st);
 hipError_t launch_euler(const EulerParams& p, int bf16, hipStream_t st);
 // Per-stream state: mode 0 begins a turn of stream b (no history, position

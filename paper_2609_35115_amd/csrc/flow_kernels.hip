@@ -69,13 +69,115 @@ __device__ __forceinline__ int own_base(const CarryRef& c, int prompt, int b)
 
 // ------------------------------------------------------------------- GEMM
 //
-// Tile 64 rows x 64 columns, 4 waves as 2 x 2, each 32 x 32 = 2 x 2 MFMA
-// blocks of 16 x 16.  K runs in chunks of 32: the next chunk's operands are
-// loaded into registers while the current one is multiplied out of LDS.  The
-// weight is the MFMA's A operand (a lane's four results are four consecutive
-// output columns of one row), the activation row the B operand.
+// Both GEMM kernels take the weight as the MFMA's A operand (a lane's four
+// results are four consecutive output columns of one row) and the activation
+// row as the B operand, and hand every 4-column group of a row to the same
+// epilogue.  With a LayerNorm operand (p.ln_h set) the activation is
+// LN(h) * (1 + scale) + shift of the fp32 residual stream h, normalised while
+// it is staged: mean and variance per row from sums shifted by the row's
+// first value, eps 1e-6.
+
+// The epilogue's operands of one 4-column group (bias; for E_RES also the
+// gate and the residual row), loaded apart from their use so that a kernel
+// can fetch them before its main loop.
+struct EpiPre {
+    f32x4 bias, gate, h;
+};
+template <int EPI>
+__device__ __forceinline__ EpiPre epi_prefetch(const GemmParams& p, int row, int col)
+{
+    EpiPre e;
+    e.bias = *(const f32x4*)(p.bias + col);
+    if constexpr (EPI == E_RES) {
+        e.gate = *(const f32x4*)(p.gate + col);
+        e.h = *(const f32x4*)(p.h + (size_t)row * p.N + col);
+    }
+    return e;
+}
 
 template <bool BF16, int EPI>
+__device__ __forceinline__ void epilogue4(const GemmParams& p, int row, int col, f32x4 acc, const EpiPre& e)
+{
+    const f32x4 y = acc + e.bias;
+    if constexpr (EPI == E_H) {
+        *(f32x4*)(p.h + (size_t)row * p.N + col) = y;
+    } else if constexpr (EPI == E_RES) {
+        f32x4 hv = e.h;
+#pragma unroll
+        for (int r = 0; r < 4; r++) hv[r] = hv[r] + e.gate[r] * y[r];
+        *(f32x4*)(p.h + (size_t)row * p.N + col) = hv;
+    } else if constexpr (EPI == E_GELU) {
+        f32x4 z;
+#pragma unroll
+        for (int r = 0; r < 4; r++) z[r] = gelu_tanh(y[r]);
+        store4<BF16>(p.out, (size_t)row * p.N + col, z);
+    } else if constexpr (EPI == E_VEL) {
+        *(f32x4*)((float*)p.out + (size_t)row * p.N + col) = y;
+    } else {   // E_QKV
+        const int part = col / p.dim, hd = (col % p.dim) >> 6, d = col & 63;
+        const int bp = row / (2 * p.n), c = (row / p.n) & 1, f = row % p.n;
+        if (part == 0) {
+            store4<BF16>(p.q, ((((size_t)bp * 2 + c) * p.heads + hd) * p.Fq + f) * 64 + d, y);
+        } else {
+            const int b = p.b0 + bp;
+            const int frame = own_base(p.carry, p.prompt, b) + f;
+            const size_t region = (size_t)b * p.carry.stream_stride +
+                                  ((size_t)((c * 2 + (part - 1)) * p.heads + hd)) * p.carry.Fr * 64;
+            if (part == 1) {
+                store4<BF16>(p.carry.base, region + (size_t)frame * 64 + d, y);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; r++) store1<BF16>(p.carry.base, region + (size_t)(d + r) * p.carry.Fr + frame, y[r]);
+            }
+        }
+    }
+}
+
+// LayerNorm statistics of rows m0 .. m0 + 255 / TPR of h [M][K] (K <= 512):
+// TPR adjacent threads share a row, thread t taking row t / TPR and columns
+// [(t % TPR) K / TPR, (t % TPR + 1) K / TPR).  Returns the row's mean and
+// 1 / sqrt(var + eps); the thread's values stay in v.  Mean and variance come
+// from sums shifted by the row's first value.
+struct LnRow {
+    float mean, rstd;
+};
+template <int TPR, int NV>
+__device__ __forceinline__ LnRow ln_row_stats(const float* h, int M, int K, int m0, f32x4 (&v)[NV])
+{
+    const int tid = threadIdx.x, lane = tid & 63, q = tid % TPR;
+    const int row = min(m0 + tid / TPR, M - 1);
+    const int kq = K / TPR, nv = kq >> 2;
+    const f32x4* hr = (const f32x4*)(h + (size_t)row * K + q * kq);
+    // every load is issued (clamped into the thread's columns) before any is used
+#pragma unroll
+    for (int i = 0; i < NV; i++) v[i] = hr[min(i, nv - 1)];
+    const float x0 = __shfl(v[0][0], lane & ~(TPR - 1), 64);
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; i++) {
+        const float live = i < nv ? 1.0f : 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            const float d = (v[i][e] - x0) * live;
+            s1 += d;
+            s2 += d * d;
+        }
+    }
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) {
+        s1 += __shfl_xor(s1, o, 64);
+        s2 += __shfl_xor(s2, o, 64);
+    }
+    const float md = s1 / (float)K;
+    const float var = fmaxf(s2 / (float)K - md * md, 0.f);
+    return LnRow{x0 + md, 1.0f / sqrtf(var + 1e-6f)};
+}
+
+// Tiled GEMM for many rows: tile 64 x 64, 4 waves as 2 x 2, each 32 x 32 =
+// 2 x 2 MFMA blocks.  K runs in chunks of 32: the next chunk's operands are
+// loaded into registers while the current one is multiplied out of LDS.
+
+template <bool BF16, int EPI, bool LN>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
 {
     using T = typename std::conditional<BF16, uint16_t, float>::type;
@@ -86,28 +188,63 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
     constexpr int NV = BM * VPR / 256;               // vectors per thread per operand
     __shared__ __attribute__((aligned(16))) T As[BM * LD];
     __shared__ __attribute__((aligned(16))) T Bs[BN * LD];
+    __shared__ float st_mean[BM], st_rstd[BM];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
     const T* A = (const T*)p.A;
     const T* W = (const T*)p.W;
 
+    if constexpr (LN) {
+        f32x4 v[32];
+        const LnRow st = ln_row_stats<4, 32>(p.ln_h, p.M, p.K, m0, v);
+        if ((tid & 3) == 0) {
+            st_mean[tid >> 2] = st.mean;
+            st_rstd[tid >> 2] = st.rstd;
+        }
+        __syncthreads();
+    }
+
     u32x4 ra[NV], rb[NV];
+    f32x4 rh[NV][VE / 4];
     auto gload = [&](int k0) {
 #pragma unroll
         for (int v = 0; v < NV; v++) {
             const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
-            const int row = m0 + r, col = n0 + r;
-            ra[v] = row < p.M ? *(const u32x4*)(A + (size_t)row * p.K + k0 + kv) : u32x4{0, 0, 0, 0};
+            const int row = min(m0 + r, p.M - 1), col = n0 + r;
+            if constexpr (LN) {
+#pragma unroll
+                for (int e = 0; e < VE / 4; e++) rh[v][e] = *(const f32x4*)(p.ln_h + (size_t)row * p.K + k0 + kv + 4 * e);
+            } else {
+                ra[v] = *(const u32x4*)(A + (size_t)row * p.K + k0 + kv);
+            }
             rb[v] = col < p.N ? *(const u32x4*)(W + (size_t)col * p.K + k0 + kv) : u32x4{0, 0, 0, 0};
         }
     };
-    auto lstore = [&]() {
+    auto lstore = [&](int k0) {
 #pragma unroll
         for (int v = 0; v < NV; v++) {
             const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
-            *(u32x4*)(As + r * LD + kv) = ra[v];
+            if constexpr (LN) {
+                const float mean = st_mean[r], rs = st_rstd[r];
+                float a[VE];
+#pragma unroll
+                for (int e = 0; e < VE / 4; e++) {
+                    const f32x4 sc = *(const f32x4*)(p.ln_scale + k0 + kv + 4 * e);
+                    const f32x4 sh = *(const f32x4*)(p.ln_shift + k0 + kv + 4 * e);
+#pragma unroll
+                    for (int u = 0; u < 4; u++) a[4 * e + u] = (rh[v][e][u] - mean) * rs * (1.0f + sc[u]) + sh[u];
+                }
+                if constexpr (BF16) {
+                    u32x4 w = {pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(a[4], a[5]), pack2(a[6], a[7])};
+                    *(u32x4*)(As + r * LD + kv) = w;
+                } else {
+                    *(f32x4*)(As + r * LD + kv) = f32x4{a[0], a[1], a[2], a[3]};
+                }
+            } else {
+                *(u32x4*)(As + r * LD + kv) = ra[v];
+            }
             *(u32x4*)(Bs + r * LD + kv) = rb[v];
         }
     };
@@ -122,7 +259,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
     const int nk = p.K / KC;
     gload(0);
     for (int kc = 0; kc < nk; kc++) {
-        lstore();
+        lstore(kc * KC);
         __syncthreads();
         if (kc + 1 < nk) gload((kc + 1) * KC);
         if constexpr (BF16) {
@@ -160,185 +297,391 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
     for (int i = 0; i < 2; i++) {
         const int col = n0 + wn * 32 + 16 * i + 4 * g;
         if (col >= p.N) continue;
-        const f32x4 bias = *(const f32x4*)(p.bias + col);
 #pragma unroll
         for (int j = 0; j < 2; j++) {
             const int row = m0 + wm * 32 + 16 * j + l16;
-            if (row >= p.M) continue;
-            const f32x4 y = acc[i][j] + bias;
-            if constexpr (EPI == E_H) {
-                *(f32x4*)(p.h + (size_t)row * p.N + col) = y;
-            } else if constexpr (EPI == E_RES) {
-                float* hp = p.h + (size_t)row * p.N + col;
-                const f32x4 gt = *(const f32x4*)(p.gate + col);
-                f32x4 hv = *(const f32x4*)hp;
+            if (row < p.M) epilogue4<BF16, EPI>(p, row, col, acc[i][j], epi_prefetch<EPI>(p, row, col));
+        }
+    }
+}
+
+// Skinny GEMM for few rows (a call of a handful of streams): block = 64 rows
+// x 16 columns, 8 waves that split K into contiguous eighths of whole MFMA
+// steps; each wave loads its weight and activation fragments for up to 4
+// steps at once, so a block costs few memory round trips.  The weight loads
+// of the first batch and the epilogue's operands are issued before anything
+// waits.  The eight partial tiles are summed through LDS in wave order.
+// With a LayerNorm operand the block first normalises its 64 rows into LDS
+// (operand type, all K).
+#ifndef DCF_SKINNY_WAVES
+#define DCF_SKINNY_WAVES 4
+#endif
+constexpr int kSkinnyWaves = DCF_SKINNY_WAVES;
+
+template <bool BF16, int EPI, bool LN>
+__global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(const GemmParams p)
+{
+    using T = typename std::conditional<BF16, uint16_t, float>::type;
+    constexpr int KQ = BF16 ? 32 : 16;               // K of one MFMA step group (one 16-byte load per lane)
+    constexpr int BATCH = 4;
+    constexpr int PAD = BF16 ? 8 : 4;
+    constexpr int NW = kSkinnyWaves;
+    extern __shared__ __align__(16) unsigned char smem[];
+    T* As = (T*)smem;                                 // LN: [64][K + PAD], then scale and shift
+    f32x4* red = (f32x4*)smem;                        // after the main loop: [NW waves][4 row blocks][64 lanes]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, g = lane >> 4;
+    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 16;
+    const int LDA = p.K + PAD;
+    const T* A = (const T*)p.A;
+    const T* W = (const T*)p.W;
+
+    const int ng = p.K / KQ;
+    const int q0 = wave * ng / NW, q1 = (wave + 1) * ng / NW;
+    const int col = min(n0 + l16, p.N - 1);
+    // the first batch's weight fragments (they do not wait for the LayerNorm)
+    u32x4 wf[BATCH];
 #pragma unroll
-                for (int r = 0; r < 4; r++) hv[r] = hv[r] + gt[r] * y[r];
-                *(f32x4*)hp = hv;
-            } else if constexpr (EPI == E_GELU) {
-                f32x4 z;
+    for (int b = 0; b < BATCH; b++)
+        wf[b] = *(const u32x4*)(W + (size_t)col * p.K + min(q0 + b, max(q1 - 1, 0)) * KQ + (BF16 ? 8 : 4) * g);
+    // the epilogue's operands (waves 0-3 finalise row blocks 0-3)
+    const int erow = min(m0 + 16 * (wave & 3) + l16, p.M - 1), ecol = min(n0 + 4 * g, p.N - 4);
+    const EpiPre pre = epi_prefetch<EPI>(p, erow, ecol);
+
+    if constexpr (LN) {
+        float* ss = (float*)(smem + (size_t)64 * LDA * sizeof(T));
+        for (int k4 = tid; k4 < (p.K >> 2); k4 += 64 * NW) {
+            ((f32x4*)ss)[k4] = ((const f32x4*)p.ln_scale)[k4];
+            ((f32x4*)(ss + p.K))[k4] = ((const f32x4*)p.ln_shift)[k4];
+        }
+        // NW threads per row, K / NW columns each
+        f32x4 v[128 / NW];
+        const LnRow st = ln_row_stats<NW, 128 / NW>(p.ln_h, p.M, p.K, m0, v);
+        __syncthreads();
+        const int r = tid / NW, kq = p.K / NW, nv = kq >> 2, kb = (tid % NW) * kq;
 #pragma unroll
-                for (int r = 0; r < 4; r++) z[r] = gelu_tanh(y[r]);
-                store4<BF16>(p.out, (size_t)row * p.N + col, z);
-            } else if constexpr (EPI == E_VEL) {
-                *(f32x4*)((float*)p.out + (size_t)row * p.N + col) = y;
-            } else {   // E_QKV
-                const int part = col / p.dim, hd = (col % p.dim) >> 6, d = col & 63;
-                const int bp = row / (2 * p.n), c = (row / p.n) & 1, f = row % p.n;
-                if (part == 0) {
-                    store4<BF16>(p.q, ((((size_t)bp * 2 + c) * p.heads + hd) * p.Fq + f) * 64 + d, y);
+        for (int i = 0; i < 128 / NW; i++)
+            if (i < nv) {
+                const int k = kb + 4 * i;
+                const f32x4 sc = *(const f32x4*)(ss + k), sh = *(const f32x4*)(ss + p.K + k);
+                f32x4 a;
+#pragma unroll
+                for (int u = 0; u < 4; u++) a[u] = (v[i][u] - st.mean) * st.rstd * (1.0f + sc[u]) + sh[u];
+                store4<BF16>(As, (size_t)r * LDA + k, a);
+            }
+        __syncthreads();
+    }
+
+    int xr[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) xr[i] = min(m0 + 16 * i + l16, p.M - 1);
+    f32x4 acc[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int q = q0; q < q1; q += BATCH) {
+        // all loads of the batch first; a step past the wave's range reloads
+        // its last one with a zero weight fragment, so the loop has no branch
+        // (its products add exact zeros: the activations are finite)
+        u32x4 xf[BATCH][4];
+        if (q != q0) {
+#pragma unroll
+            for (int b = 0; b < BATCH; b++)
+                wf[b] = *(const u32x4*)(W + (size_t)col * p.K + min(q + b, q1 - 1) * KQ + (BF16 ? 8 : 4) * g);
+        }
+#pragma unroll
+        for (int b = 0; b < BATCH; b++) {
+            const int k = min(q + b, q1 - 1) * KQ + (BF16 ? 8 : 4) * g;
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                if constexpr (LN) xf[b][i] = *(const u32x4*)(As + (16 * i + l16) * LDA + k);
+                else xf[b][i] = *(const u32x4*)(A + (size_t)xr[i] * p.K + k);
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < BATCH; b++) {
+            const bool live = q + b < q1;
+            u32x4 w = wf[b];
+#pragma unroll
+            for (int e = 0; e < 4; e++) w[e] = live ? w[e] : 0u;
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                if constexpr (BF16) {
+                    acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w),
+                                                                     __builtin_bit_cast(bf16x8_t, xf[b][i]), acc[i], 0, 0,
+                                                                     0);
                 } else {
-                    const int b = p.b0 + bp;
-                    const int frame = own_base(p.carry, p.prompt, b) + f;
-                    const size_t region =
-                        (size_t)b * p.carry.stream_stride +
-                        ((size_t)((c * 2 + (part - 1)) * p.heads + hd)) * p.carry.Fr * 64;
-                    if (part == 1) {
-                        store4<BF16>(p.carry.base, region + (size_t)frame * 64 + d, y);
-                    } else {
+                    const f32x4 wv = __builtin_bit_cast(f32x4, w), xv = __builtin_bit_cast(f32x4, xf[b][i]);
 #pragma unroll
-                        for (int r = 0; r < 4; r++)
-                            store1<BF16>(p.carry.base, region + (size_t)(d + r) * p.carry.Fr + frame, y[r]);
-                    }
+                    for (int u = 0; u < 4; u++) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[u], xv[u], acc[i], 0, 0, 0);
                 }
             }
         }
     }
-}
-
-hipError_t launch_gemm(const GemmParams& p, int epi, int bf16, hipStream_t st)
-{
-    const dim3 grid((p.N + 63) / 64, (p.M + 63) / 64);
-#define DCF_GEMM(B, E)                                                              \
-    if (bf16 == B && epi == E) {                                                    \
-        hipLaunchKernelGGL((gemm_kernel<B, E>), grid, dim3(256), 0, st, p);         \
-        return hipGetLastError();                                                   \
-    }
-    DCF_GEMM(1, E_H) DCF_GEMM(1, E_QKV) DCF_GEMM(1, E_RES) DCF_GEMM(1, E_GELU) DCF_GEMM(1, E_VEL)
-    DCF_GEMM(0, E_H) DCF_GEMM(0, E_QKV) DCF_GEMM(0, E_RES) DCF_GEMM(0, E_GELU) DCF_GEMM(0, E_VEL)
-#undef DCF_GEMM
-    return hipErrorInvalidValue;
+    if constexpr (LN) __syncthreads();   // the LDS tile becomes the reduction buffer
+#pragma unroll
+    for (int i = 0; i < 4; i++) red[(wave * 4 + i) * 64 + lane] = acc[i];
+    __syncthreads();
+    if (wave >= 4) return;
+    // wave w sums row block w over the waves, in wave order
+    f32x4 y = red[(0 * 4 + wave) * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < NW; w++) y += red[(w * 4 + wave) * 64 + lane];
+    const int row = m0 + 16 * wave + l16, c4 = n0 + 4 * g;
+    if (row < p.M && c4 < p.N) epilogue4<BF16, EPI>(p, row, c4, y, pre);
 }
 
 // ------------------------------------------------------- modulated LayerNorm
 //
-// One wave per row: mean, then the centred second moment (two passes over
-// the row held in registers), eps 1e-6, then * (1 + scale) + shift.
+// For calls of many rows: out = LN(h) * (1 + scale) + shift, one wave per
+// row, the row's values in registers (dim <= 512), mean and variance from
+// sums shifted by the row's first value, eps 1e-6; the operand of the
+// following tiled GEMM.
 template <bool BF16>
-__global__ __launch_bounds__(256) void lnmod_kernel(const LnParams p)
+__global__ __launch_bounds__(256) void lnmod_kernel(const float* h, void* out, const float* shift, const float* scale,
+                                                    int M, int dim)
 {
-    constexpr int MAXV = 16;   // dim <= 1024
     const int lane = threadIdx.x & 63;
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= p.M) return;
-    const int nv = p.dim / 64;
-    const float* hr = p.h + (size_t)row * p.dim;
-    float v[MAXV];
-    float s = 0.f;
+    if (row >= M) return;
+    const int nv = dim >> 6;
+    const float* hr = h + (size_t)row * dim;
+    float v[8], sc[8], sh[8];
 #pragma unroll
-    for (int k = 0; k < MAXV; k++)
-        if (k < nv) {
-            v[k] = hr[lane + 64 * k];
-            s += v[k];
-        }
-    const float mean = wave_sum(s) / (float)p.dim;
-    float q = 0.f;
+    for (int k = 0; k < 8; k++) {
+        const int col = lane + 64 * min(k, nv - 1);
+        v[k] = hr[col];
+        sc[k] = scale[col];
+        sh[k] = shift[col];
+    }
+    const float x0 = __shfl(v[0], 0, 64);
+    float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-    for (int k = 0; k < MAXV; k++)
-        if (k < nv) {
-            const float d = v[k] - mean;
-            q += d * d;
-        }
-    const float inv = 1.0f / sqrtf(wave_sum(q) / (float)p.dim + 1e-6f);
+    for (int k = 0; k < 8; k++) {
+        const float d = (v[k] - x0) * (k < nv ? 1.0f : 0.0f);
+        s1 += d;
+        s2 += d * d;
+    }
+    s1 = wave_sum(s1);
+    s2 = wave_sum(s2);
+    const float md = s1 / (float)dim;
+    const float mean = x0 + md;
+    const float rs = 1.0f / sqrtf(fmaxf(s2 / (float)dim - md * md, 0.f) + 1e-6f);
 #pragma unroll
-    for (int k = 0; k < MAXV; k++)
-        if (k < nv) {
-            const int col = lane + 64 * k;
-            store1<BF16>(p.out, (size_t)row * p.dim + col, (v[k] - mean) * inv * (1.0f + p.scale[col]) + p.shift[col]);
-        }
+    for (int k = 0; k < 8; k++)
+        if (k < nv) store1<BF16>(out, (size_t)row * dim + lane + 64 * k, (v[k] - mean) * rs * (1.0f + sc[k]) + sh[k]);
 }
 
-hipError_t launch_lnmod(const LnParams& p, int bf16, hipStream_t st)
+// Rows up to which a call uses the skinny kernel.
+constexpr int kSkinnyRows = 512;
+
+size_t skinny_lds_bytes(const GemmParams& p, int bf16)
 {
-    const dim3 grid((p.M + 3) / 4);
-    if (bf16) hipLaunchKernelGGL((lnmod_kernel<true>), grid, dim3(256), 0, st, p);
-    else hipLaunchKernelGGL((lnmod_kernel<false>), grid, dim3(256), 0, st, p);
+    const size_t red = (size_t)kSkinnyWaves * 4 * 64 * 16;
+    if (!p.ln_h) return red;
+    // the normalised tile, then scale and shift
+    const size_t a = (size_t)64 * (p.K + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4) + (size_t)2 * p.K * 4;
+    return a > red ? a : red;
+}
+
+template <bool BF16, int EPI, bool LN>
+hipError_t launch_one(const GemmParams& p, hipStream_t st)
+{
+    if (p.M <= kSkinnyRows) {
+        const size_t lds = skinny_lds_bytes(p, BF16);
+        static size_t set = 0;
+        if (lds > 65536 && lds > set) {
+            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<BF16, EPI, LN>),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+            set = lds;
+        }
+        hipLaunchKernelGGL((skinny_kernel<BF16, EPI, LN>), dim3((p.N + 15) / 16, (p.M + 63) / 64), dim3(64 * kSkinnyWaves),
+                           lds, st, p);
+    } else if (LN) {
+        // the normalised operand is written once to p.A by its own launch
+        hipLaunchKernelGGL((lnmod_kernel<BF16>), dim3((p.M + 3) / 4), dim3(256), 0, st, p.ln_h, const_cast<void*>(p.A),
+                           p.ln_shift, p.ln_scale, p.M, p.K);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        GemmParams q = p;
+        q.ln_h = nullptr;
+        hipLaunchKernelGGL((gemm_kernel<BF16, EPI, false>), dim3((p.N + 63) / 64, (p.M + 63) / 64), dim3(256), 0, st, q);
+    } else {
+        hipLaunchKernelGGL((gemm_kernel<BF16, EPI, false>), dim3((p.N + 63) / 64, (p.M + 63) / 64), dim3(256), 0, st, p);
+    }
     return hipGetLastError();
+}
+
+hipError_t launch_gemm(const GemmParams& p, int epi, int bf16, hipStream_t st)
+{
+    const bool ln = p.ln_h != nullptr;
+#define DCF_GEMM(B, E, L)                                     \
+    if (bf16 == B && epi == E && ln == L) return launch_one<B, E, L>(p, st);
+    DCF_GEMM(1, E_H, false) DCF_GEMM(1, E_QKV, true) DCF_GEMM(1, E_RES, false) DCF_GEMM(1, E_GELU, true)
+    DCF_GEMM(1, E_VEL, true)
+    DCF_GEMM(0, E_H, false) DCF_GEMM(0, E_QKV, true) DCF_GEMM(0, E_RES, false) DCF_GEMM(0, E_GELU, true)
+    DCF_GEMM(0, E_VEL, true)
+#undef DCF_GEMM
+    return hipErrorInvalidValue;
 }
 
 // --------------------------------------------------------------- attention
 //
-// Block = (stream, branch, head) x 64 queries; wave w takes queries
-// 16 w .. 16 w + 15.  Keys are walked in Eq. carry's logical order -- the
-// retained chunks newest first, the prompt, then the call's own frames -- in
-// tiles of 32, with a running maximum (online softmax).  Per tile:
+// Block = (stream, branch, head) x up to 64 queries, 8 waves.  The keys, in
+// Eq. carry's logical order (the retained chunks newest first, the prompt,
+// the call's own frames), are cut into tiles of 32 inside each segment; wave
+// w takes tiles w, w + 8, ... for all the block's queries (4 groups of 16),
+// loading the next tile while it works on the current one, with a running
+// maximum per query (online softmax); the waves' partial results are merged
+// through LDS in wave order.  Per tile and query group:
 //   S^T (keys x queries) = K Q^T        : A = key rows, B = query rows
 //   O^T (dims x queries) += V^T P^T     : A = value columns (stored [dim][frame]),
 //                                         B = the lane's own probabilities
 // In S^T a lane holds keys 4g .. 4g+3 and 16+4g .. 16+4g+3 of the tile for
 // query l16 (g = lane / 16); those eight keys, in that order, are the lane's
 // K slice of the second product, so P never leaves its registers, and the
-// running maximum, sum and rescale of O^T all stay per lane.
+// running maximum, sum and rescale of O^T stay per lane.
+constexpr int kMaxSegments = 8;
+#ifndef DCF_ATTN_WAVES
+#define DCF_ATTN_WAVES 8
+#endif
+constexpr int kAttnWaves = DCF_ATTN_WAVES;
+constexpr int kAttnLd = 68;   // padded row of the merge buffer (floats)
+
+size_t attn_lds_bytes() { return (size_t)kAttnWaves * 64 * kAttnLd * 4 + (size_t)2 * kAttnWaves * 64 * 4; }
 
 template <bool BF16>
-__global__ __launch_bounds__(256) void attn_kernel(const AttnParams p)
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams p)
 {
     using T = typename std::conditional<BF16, uint16_t, float>::type;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int NW = kAttnWaves;
+    extern __shared__ __align__(16) unsigned char smem[];
+    float* Os = (float*)smem;                          // [NW waves][64 queries][kAttnLd]
+    float* Ms = Os + NW * 64 * kAttnLd;                // [NW][64]
+    float* Ls = Ms + NW * 64;                          // [NW][64]
+
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int l16 = lane & 15, g = lane >> 4;
     const int bh = blockIdx.x;
     const int bp = bh / (2 * p.heads), c = (bh / p.heads) & 1, hd = bh % p.heads;
     const int b = p.b0 + bp;
-    const int q0 = blockIdx.y * 64 + wave * 16;
-    if (q0 >= p.n) return;
-    const int fq = q0 + l16;   // this lane's query (rows past n are computed and dropped)
-
-    const T* qp = (const T*)p.q + ((((size_t)bp * 2 + c) * p.heads + hd) * p.Fq + fq) * 64;
+    const int qb0 = blockIdx.y * 64;
     const CarryRef& cr = p.carry;
     const T* Kb = (const T*)cr.base + (size_t)b * cr.stream_stride + ((size_t)((c * 2 + 0) * p.heads + hd)) * cr.Fr * 64;
     const T* Vb = (const T*)cr.base + (size_t)b * cr.stream_stride + ((size_t)((c * 2 + 1) * p.heads + hd)) * cr.Fr * 64;
+    const T* qp = (const T*)p.q + (((size_t)bp * 2 + c) * p.heads + hd) * p.Fq * 64;
 
-    // query fragments (B operand of S^T)
-    bf16x8_t qb[2];
-    f32x4 qf[4];
-    if constexpr (BF16) {
+    // segments (frame base, length, first global tile) in logical order
+    int sb[kMaxSegments], sl[kMaxSegments], st0[kMaxSegments + 1], ns = 0;
+    if (!p.prompt) {
+        const int64_t hist = cr.hist[b];
+        const int nh = hist < cr.R ? (int)hist : cr.R;
+        for (int r = 0; r < nh; r++) {
+            sb[ns] = cr.Pr + (int)((hist - 1 - r) % (cr.R + 1)) * cr.Sl;
+            sl[ns++] = p.f_chunk;
+        }
+        sb[ns] = 0;
+        sl[ns++] = cr.plen[b];
+    }
+    sb[ns] = own_base(cr, p.prompt, b);
+    sl[ns++] = p.n;
+    st0[0] = 0;
+    for (int i = 0; i < ns; i++) st0[i + 1] = st0[i] + ((sl[i] + 31) >> 5);
+    const int total = st0[ns];
+    auto locate = [&](int t, int& base, int& len, int& t0) {
+        int i = 0;
+        while (i + 1 < ns && t >= st0[i + 1]) i++;
+        base = sb[i];
+        len = sl[i];
+        t0 = 32 * (t - st0[i]);
+    };
+
+    // query fragments of the four groups (B operand of S^T)
+    bf16x8_t qb[4][2];
+    f32x4 qf[4][4];
 #pragma unroll
-        for (int s = 0; s < 2; s++) qb[s] = *(const bf16x8_t*)(qp + 32 * s + 8 * g);
-    } else {
+    for (int qg = 0; qg < 4; qg++) {
+        const T* qr = qp + (size_t)(qb0 + 16 * qg + l16) * 64;   // rows past n are computed and dropped
+        if constexpr (BF16) {
 #pragma unroll
-        for (int s = 0; s < 4; s++) qf[s] = *(const f32x4*)(qp + 16 * s + 4 * g);
+            for (int s2 = 0; s2 < 2; s2++) qb[qg][s2] = *(const bf16x8_t*)(qr + 32 * s2 + 8 * g);
+        } else {
+#pragma unroll
+            for (int s4 = 0; s4 < 4; s4++) qf[qg][s4] = *(const f32x4*)(qr + 16 * s4 + 4 * g);
+        }
     }
 
-    float m = -INFINITY, lsum = 0.f;
-    f32x4 O[4];
-#pragma unroll
-    for (int db = 0; db < 4; db++) O[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    auto run = [&](int base, int len) {
+    // one tile's operands: keys (two blocks of 16) and the value groups
+    struct Tile {
+        u32x4 kf[2][4];
+        u32x4 va[4], vb[4];
+    };
+    auto load = [&](int t, Tile& tl) {
+        int base, len, t0;
+        locate(t, base, len, t0);
         const int last4 = (len - 1) & ~3;
-        for (int t0 = 0; t0 < len; t0 += 32) {
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+            const T* kr = Kb + (size_t)(base + min(t0 + 16 * j + l16, len - 1)) * 64;
+            if constexpr (BF16) {
+#pragma unroll
+                for (int s2 = 0; s2 < 2; s2++) tl.kf[j][s2] = *(const u32x4*)(kr + 32 * s2 + 8 * g);
+            } else {
+#pragma unroll
+                for (int s4 = 0; s4 < 4; s4++) tl.kf[j][s4] = *(const u32x4*)(kr + 16 * s4 + 4 * g);
+            }
+        }
+        // value groups: keys t0 + 4 g (+16) .. +3, clamped into the segment's storage
+        const int ga = min(t0 + 4 * g, last4), gb2 = min(t0 + 16 + 4 * g, last4);
+#pragma unroll
+        for (int db = 0; db < 4; db++) {
+            const T* vr = Vb + (size_t)(16 * db + l16) * cr.Fr + base;
+            if constexpr (BF16) {
+                const u32x2 x = *(const u32x2*)(vr + ga), y = *(const u32x2*)(vr + gb2);
+                tl.va[db] = u32x4{x[0], x[1], y[0], y[1]};
+            } else {
+                tl.va[db] = *(const u32x4*)(vr + ga);
+                tl.vb[db] = *(const u32x4*)(vr + gb2);
+            }
+        }
+    };
+
+    float m[4], lsum[4];
+    f32x4 O[4][4];
+#pragma unroll
+    for (int qg = 0; qg < 4; qg++) {
+        m[qg] = -INFINITY;
+        lsum[qg] = 0.f;
+#pragma unroll
+        for (int db = 0; db < 4; db++) O[qg][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    auto work = [&](int t, const Tile& cur) {
+        int base, len, t0;
+        locate(t, base, len, t0);
+#pragma unroll
+        for (int qg = 0; qg < 4; qg++) {
             f32x4 st[2];
 #pragma unroll
             for (int j = 0; j < 2; j++) {
                 st[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-                const int key = min(t0 + 16 * j + l16, len - 1);
-                const T* kr = Kb + (size_t)(base + key) * 64;
                 if constexpr (BF16) {
 #pragma unroll
-                    for (int s = 0; s < 2; s++)
-                        st[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8_t*)(kr + 32 * s + 8 * g), qb[s],
-                                                                        st[j], 0, 0, 0);
+                    for (int s2 = 0; s2 < 2; s2++)
+                        st[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, cur.kf[j][s2]),
+                                                                        qb[qg][s2], st[j], 0, 0, 0);
                 } else {
 #pragma unroll
-                    for (int s = 0; s < 4; s++) {
-                        const f32x4 kf = *(const f32x4*)(kr + 16 * s + 4 * g);
+                    for (int s4 = 0; s4 < 4; s4++) {
+                        const f32x4 kv = __builtin_bit_cast(f32x4, cur.kf[j][s4]);
 #pragma unroll
-                        for (int q = 0; q < 4; q++)
-                            st[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[q], qf[s][q], st[j], 0, 0, 0);
+                        for (int u = 0; u < 4; u++)
+                            st[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[u], qf[qg][s4][u], st[j], 0, 0, 0);
                     }
                 }
             }
-            // scores of keys t0 + 16 j + 4 g + r; keys past the segment do not exist
             float mt = -INFINITY;
 #pragma unroll
             for (int j = 0; j < 2; j++)
@@ -350,9 +693,9 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnParams p)
                 }
             mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
             mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-            const float mn = fmaxf(m, mt);
-            const float alpha = expf(m - mn);
-            m = mn;
+            const float mn = fmaxf(m[qg], mt);
+            const float alpha = expf(m[qg] - mn);
+            m[qg] = mn;
             float ps = 0.f;
 #pragma unroll
             for (int j = 0; j < 2; j++)
@@ -361,59 +704,106 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnParams p)
                     st[j][r] = expf(st[j][r] - mn);
                     ps += st[j][r];
                 }
-            lsum = lsum * alpha + ps;
+            lsum[qg] = lsum[qg] * alpha + ps;
 #pragma unroll
-            for (int db = 0; db < 4; db++) O[db] *= alpha;
-            // value groups: keys t0 + 4 g (+16) .. +3, clamped into the segment's storage
-            const int ga = min(t0 + 4 * g, last4), gb = min(t0 + 16 + 4 * g, last4);
+            for (int db = 0; db < 4; db++) O[qg][db] *= alpha;
             if constexpr (BF16) {
-                u32x4 pw = {pack2(st[0][0], st[0][1]), pack2(st[0][2], st[0][3]), pack2(st[1][0], st[1][1]),
-                            pack2(st[1][2], st[1][3])};
+                const u32x4 pw = {pack2(st[0][0], st[0][1]), pack2(st[0][2], st[0][3]), pack2(st[1][0], st[1][1]),
+                                  pack2(st[1][2], st[1][3])};
                 const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
 #pragma unroll
-                for (int db = 0; db < 4; db++) {
-                    const T* vr = Vb + (size_t)(16 * db + l16) * cr.Fr + base;
-                    const u32x2 va = *(const u32x2*)(vr + ga), vb = *(const u32x2*)(vr + gb);
-                    const u32x4 vw = {va[0], va[1], vb[0], vb[1]};
-                    O[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vw), pf, O[db], 0, 0, 0);
-                }
+                for (int db = 0; db < 4; db++)
+                    O[qg][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, cur.va[db]), pf,
+                                                                        O[qg][db], 0, 0, 0);
             } else {
 #pragma unroll
                 for (int db = 0; db < 4; db++) {
-                    const T* vr = Vb + (size_t)(16 * db + l16) * cr.Fr + base;
-                    const f32x4 va = *(const f32x4*)(vr + ga), vb = *(const f32x4*)(vr + gb);
+                    const f32x4 va = __builtin_bit_cast(f32x4, cur.va[db]), vb = __builtin_bit_cast(f32x4, cur.vb[db]);
 #pragma unroll
-                    for (int q = 0; q < 4; q++) O[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(va[q], st[0][q], O[db], 0, 0, 0);
+                    for (int u = 0; u < 4; u++)
+                        O[qg][db] = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u], st[0][u], O[qg][db], 0, 0, 0);
 #pragma unroll
-                    for (int q = 0; q < 4; q++) O[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(vb[q], st[1][q], O[db], 0, 0, 0);
+                    for (int u = 0; u < 4; u++)
+                        O[qg][db] = __builtin_amdgcn_mfma_f32_16x16x4f32(vb[u], st[1][u], O[qg][db], 0, 0, 0);
                 }
             }
         }
     };
-
-    if (!p.prompt) {
-        const int64_t hist = cr.hist[b];
-        const int nh = hist < cr.R ? (int)hist : cr.R;
-        for (int r = 0; r < nh; r++) run(cr.Pr + (int)((hist - 1 - r) % (cr.R + 1)) * cr.Sl, p.f_chunk);
-        run(0, cr.plen[b]);
+#ifndef DCF_ATTN_PREFETCH
+#define DCF_ATTN_PREFETCH 1
+#endif
+    if constexpr (BF16 && DCF_ATTN_PREFETCH) {
+        // the next tile (or this one again) is in flight while one is worked on
+        Tile cur;
+        load(min(wave, total - 1), cur);
+        for (int t = wave; t < total; t += NW) {
+            Tile nxt;
+            load(min(t + NW, total - 1), nxt);
+            work(t, cur);
+            cur = nxt;
+        }
+    } else {   // fp32 tiles are twice the registers: one at a time
+        for (int t = wave; t < total; t += NW) {
+            Tile cur;
+            load(t, cur);
+            work(t, cur);
+        }
     }
-    run(own_base(cr, p.prompt, b), p.n);
 
-    float l1 = lsum + __shfl_xor(lsum, 16, 64);
-    l1 = l1 + __shfl_xor(l1, 32, 64);
-    const float inv = 1.0f / l1;
+    // this wave's partial results: O^T lane (l16, g) holds dims 16 db + 4 g + r of query l16
+#pragma unroll
+    for (int qg = 0; qg < 4; qg++) {
+        float l1 = lsum[qg] + __shfl_xor(lsum[qg], 16, 64);
+        l1 += __shfl_xor(l1, 32, 64);
+        const int qq = 16 * qg + l16;
+#pragma unroll
+        for (int db = 0; db < 4; db++) *(f32x4*)(Os + ((size_t)wave * 64 + qq) * kAttnLd + 16 * db + 4 * g) = O[qg][db];
+        if (g == 0) {
+            Ms[wave * 64 + qq] = m[qg];
+            Ls[wave * 64 + qq] = l1;
+        }
+    }
+    __syncthreads();
+    if (wave >= 4) return;
+    // wave w merges queries 16 w .. 16 w + 15 over the waves, in wave order
+    const int qq = 16 * wave + l16;
+    float mx = Ms[qq];
+#pragma unroll
+    for (int w = 1; w < NW; w++) mx = fmaxf(mx, Ms[w * 64 + qq]);
+    float L = 0.f;
+    f32x4 acc[4];
+#pragma unroll
+    for (int db = 0; db < 4; db++) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < NW; w++) {
+        const float sc = expf(Ms[w * 64 + qq] - mx);
+        L += sc * Ls[w * 64 + qq];
+#pragma unroll
+        for (int db = 0; db < 4; db++) acc[db] += sc * *(const f32x4*)(Os + ((size_t)w * 64 + qq) * kAttnLd + 16 * db + 4 * g);
+    }
+    const float inv = 1.0f / L;
+    const int fq = qb0 + qq;
     if (fq < p.n) {
         const size_t row = ((size_t)bp * 2 + c) * p.n + fq;
 #pragma unroll
-        for (int db = 0; db < 4; db++) store4<BF16>(p.o, row * p.dim + hd * 64 + 16 * db + 4 * g, O[db] * inv);
+        for (int db = 0; db < 4; db++) store4<BF16>(p.o, row * p.dim + hd * 64 + 16 * db + 4 * g, acc[db] * inv);
     }
 }
 
 hipError_t launch_attn(const AttnParams& p, int Bc, int bf16, hipStream_t st)
 {
     const dim3 grid(Bc * 2 * p.heads, (p.n + 63) / 64);
-    if (bf16) hipLaunchKernelGGL((attn_kernel<true>), grid, dim3(256), 0, st, p);
-    else hipLaunchKernelGGL((attn_kernel<false>), grid, dim3(256), 0, st, p);
+    const size_t lds = attn_lds_bytes();
+    static bool set[2] = {false, false};
+    if (!set[bf16 ? 1 : 0]) {
+        const void* fn = bf16 ? reinterpret_cast<const void*>(&attn_kernel<true>)
+                              : reinterpret_cast<const void*>(&attn_kernel<false>);
+        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        set[bf16 ? 1 : 0] = true;
+    }
+    if (bf16) hipLaunchKernelGGL((attn_kernel<true>), grid, dim3(64 * kAttnWaves), lds, st, p);
+    else hipLaunchKernelGGL((attn_kernel<false>), grid, dim3(64 * kAttnWaves), lds, st, p);
     return hipGetLastError();
 }
 

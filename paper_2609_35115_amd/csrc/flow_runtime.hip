@@ -74,13 +74,14 @@ std::string validate(const dc_flow_cfg* c)
 {
     if (c->n_mel < 8 || c->n_mel % 8 != 0 || c->n_mel > 1024) return "n_mel must be a multiple of 8 in [8, 1024]";
     if (c->heads < 1 || c->dim != 64 * c->heads) return "dim must be 64 * heads";
-    if (c->dim > 1024) return "dim must be <= 1024";
+    if (c->dim > 512) return "dim must be <= 512";
     if (c->depth < 1) return "depth must be >= 1";
     if (c->mlp < 32 || c->mlp % 32 != 0) return "mlp must be a positive multiple of 32";
     if (c->t_dim < 2 || c->t_dim % 2 != 0 || c->t_dim > 1024) return "t_dim must be even, in [2, 1024]";
     if (c->n_steps < 1 || c->n_steps > 1000) return "n_steps must be in [1, 1000]";
     if (c->f_chunk < 1 || c->f_call < c->f_chunk) return "need 1 <= f_chunk <= f_call";
     if (c->f_retained < 0 || c->f_retained % c->f_chunk != 0) return "f_retained must be a multiple of f_chunk";
+    if (c->f_retained / c->f_chunk > 6) return "f_retained / f_chunk must be <= 6";
     if (c->f_prompt < 1) return "f_prompt must be >= 1";
     if (c->f_call > 4096 || c->f_prompt > 4096) return "f_call and f_prompt must be <= 4096";
     if (c->batch < 1 || c->batch > 4096) return "batch must be in [1, 4096]";
@@ -198,8 +199,8 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
         by = b;
         mf = m;
     };
-    auto gemm_cost = [&](const char* r, int N, int K, double out_es, bool reads_h) {
-        describe(r, 2.0 * rows * N * K, (double)rows * K * es + (double)N * K * es + (double)N * 4 +
+    auto gemm_cost = [&](const char* r, int N, int K, double a_es, double out_es, bool reads_h) {
+        describe(r, 2.0 * rows * N * K, (double)rows * K * a_es + (double)N * K * es + (double)N * 4 +
                                             (double)rows * N * out_es * (reads_h ? 2 : 1), 1);
     };
 #define DCF_TRY(x)                                                           \
@@ -235,73 +236,75 @@ hipError_t enqueue_call(dc_flow_state* s, int b0, int Bc, int n, int prompt, con
         g.Fq = Fq;
         g.prompt = prompt;
         g.q = s->q;
+        auto plain = [&](const void* A) {
+            g.A = A;
+            g.ln_h = nullptr;
+            g.ln_shift = g.ln_scale = nullptr;
+        };
+        auto normed = [&](const float* shift, const float* scale) {   // A = LN(h) * (1 + scale) + shift
+            g.A = s->a;                                                // written there for calls of many rows
+            g.ln_h = s->h;
+            g.ln_shift = shift;
+            g.ln_scale = scale;
+        };
         // input projection
-        g.A = s->xin;
+        plain(s->xin);
         g.W = s->w_in;
         g.bias = s->b_in;
         g.N = D;
         g.K = 4 * M;
         g.h = s->h;
-        gemm_cost("gemm:in", D, 4 * M, 4, false);
+        gemm_cost("gemm:in", D, 4 * M, es, 4, false);
         DCF_TRY(launch_gemm(g, E_H, bf, st));
         for (int l = 0; l < NL; l++) {
             const float* md = s->mods + ((size_t)i * NL + l) * 6 * D;
-            LnParams ln{s->h, s->a, md, md + D, rows, D};
-            describe("lnmod", 8.0 * rows * D, (double)rows * D * (4 + es) + 2.0 * D * 4, 0);
-            DCF_TRY(launch_lnmod(ln, bf, st));
             const CarryRef cr = carry_ref(s, i, l);
-            g.A = s->a;
+            normed(md, md + D);
             g.W = s->w_qkv[l];
             g.bias = s->b_qkv[l];
             g.N = 3 * D;
             g.K = D;
             g.carry = cr;
-            gemm_cost("gemm:qkv", 3 * D, D, es, false);
+            gemm_cost("gemm:qkv", 3 * D, D, 4, es, false);
             DCF_TRY(launch_gemm(g, E_QKV, bf, st));
             AttnParams at{s->q, Fq, cr, s->o, prompt, n, b0, c.heads, D, c.f_chunk};
             // per (stream, branch, head): n queries x its keys x 64, twice (scores, values)
             describe("attn", 4.0 * 2 * c.heads * 64 * (double)n * ext_keys,
                      2.0 * 2 * c.heads * 64 * (double)ext_keys * es + 2.0 * rows * D * es, 1);
             DCF_TRY(launch_attn(at, Bc, bf, st));
-            g.A = s->o;
+            plain(s->o);
             g.W = s->w_o[l];
             g.bias = s->b_o[l];
             g.N = D;
             g.K = D;
             g.gate = md + 2 * D;
-            gemm_cost("gemm:o", D, D, 4, true);
+            gemm_cost("gemm:o", D, D, es, 4, true);
             DCF_TRY(launch_gemm(g, E_RES, bf, st));
-            LnParams ln2{s->h, s->a, md + 3 * D, md + 4 * D, rows, D};
-            describe("lnmod", 8.0 * rows * D, (double)rows * D * (4 + es) + 2.0 * D * 4, 0);
-            DCF_TRY(launch_lnmod(ln2, bf, st));
-            g.A = s->a;
+            normed(md + 3 * D, md + 4 * D);
             g.W = s->w_fc1[l];
             g.bias = s->b_fc1[l];
             g.N = c.mlp;
             g.K = D;
             g.out = s->u;
-            gemm_cost("gemm:fc1", c.mlp, D, es, false);
+            gemm_cost("gemm:fc1", c.mlp, D, 4, es, false);
             DCF_TRY(launch_gemm(g, E_GELU, bf, st));
-            g.A = s->u;
+            plain(s->u);
             g.W = s->w_fc2[l];
             g.bias = s->b_fc2[l];
             g.N = D;
             g.K = c.mlp;
             g.gate = md + 5 * D;
-            gemm_cost("gemm:fc2", D, c.mlp, 4, true);
+            gemm_cost("gemm:fc2", D, c.mlp, es, 4, true);
             DCF_TRY(launch_gemm(g, E_RES, bf, st));
         }
         const float* fm = s->fmods + (size_t)i * 2 * D;
-        LnParams lf{s->h, s->a, fm, fm + D, rows, D};
-        describe("lnmod", 8.0 * rows * D, (double)rows * D * (4 + es) + 2.0 * D * 4, 0);
-        DCF_TRY(launch_lnmod(lf, bf, st));
-        g.A = s->a;
+        normed(fm, fm + D);
         g.W = s->w_out;
         g.bias = s->b_out;
         g.N = M;
         g.K = D;
         g.out = s->v;
-        gemm_cost("gemm:out", M, D, 4, false);
+        gemm_cost("gemm:out", M, D, 4, 4, false);
         DCF_TRY(launch_gemm(g, E_VEL, bf, st));
         EulerParams ep{s->v, s->x, s->xin, i == NS - 1 ? mel : nullptr, s->dt + i, c.cfg_rate, n, Bc, M};
         describe("euler", 5.0 * Bc * n * M, (double)rows * M * 4 + 2.0 * Bc * n * M * 4 + (double)rows * M * es, 0);

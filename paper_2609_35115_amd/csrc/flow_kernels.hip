@@ -174,21 +174,21 @@ __device__ __forceinline__ LnRow ln_row_stats(const float* h, int M, int K, int 
 }
 
 // Tiled GEMM for many rows: tile 64 x 64, 4 waves as 2 x 2, each 32 x 32 =
-// 2 x 2 MFMA blocks.  K runs in chunks of 32: the next chunk's operands are
-// loaded into registers while the current one is multiplied out of LDS.
-
-template <bool BF16, int EPI, bool LN>
+// 2 x 2 MFMA blocks.  K runs in chunks of 128 (bf16) or 64 (fp32) through two
+// LDS buffers: the next chunk is loaded into registers while the current one
+// is multiplied, then stored into the other buffer; one barrier per chunk.
+template <bool BF16, int EPI>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
 {
     using T = typename std::conditional<BF16, uint16_t, float>::type;
-    constexpr int BM = 64, BN = 64, KC = 32;
+    constexpr int BM = 64, BN = 64, KC = BF16 ? 128 : 64;
     constexpr int LD = KC + (BF16 ? 8 : 4);          // padded LDS row: conflict-free 16-byte reads
     constexpr int VE = 16 / (int)sizeof(T);          // elements per 16-byte vector
     constexpr int VPR = KC / VE;                     // vectors per tile row
     constexpr int NV = BM * VPR / 256;               // vectors per thread per operand
-    __shared__ __attribute__((aligned(16))) T As[BM * LD];
-    __shared__ __attribute__((aligned(16))) T Bs[BN * LD];
-    __shared__ float st_mean[BM], st_rstd[BM];
+    constexpr int KQ = BF16 ? 32 : 16;               // K of one MFMA step group
+    __shared__ __attribute__((aligned(16))) T As[2][BM * LD];
+    __shared__ __attribute__((aligned(16))) T Bs[2][BN * LD];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
@@ -196,56 +196,21 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
     const T* A = (const T*)p.A;
     const T* W = (const T*)p.W;
 
-    if constexpr (LN) {
-        f32x4 v[32];
-        const LnRow st = ln_row_stats<4, 32>(p.ln_h, p.M, p.K, m0, v);
-        if ((tid & 3) == 0) {
-            st_mean[tid >> 2] = st.mean;
-            st_rstd[tid >> 2] = st.rstd;
-        }
-        __syncthreads();
-    }
-
     u32x4 ra[NV], rb[NV];
-    f32x4 rh[NV][VE / 4];
     auto gload = [&](int k0) {
 #pragma unroll
         for (int v = 0; v < NV; v++) {
             const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
-            const int row = min(m0 + r, p.M - 1), col = n0 + r;
-            if constexpr (LN) {
-#pragma unroll
-                for (int e = 0; e < VE / 4; e++) rh[v][e] = *(const f32x4*)(p.ln_h + (size_t)row * p.K + k0 + kv + 4 * e);
-            } else {
-                ra[v] = *(const u32x4*)(A + (size_t)row * p.K + k0 + kv);
-            }
-            rb[v] = col < p.N ? *(const u32x4*)(W + (size_t)col * p.K + k0 + kv) : u32x4{0, 0, 0, 0};
+            ra[v] = *(const u32x4*)(A + (size_t)min(m0 + r, p.M - 1) * p.K + k0 + kv);
+            rb[v] = *(const u32x4*)(W + (size_t)min(n0 + r, p.N - 1) * p.K + k0 + kv);
         }
     };
-    auto lstore = [&](int k0) {
+    auto lstore = [&](int buf) {
 #pragma unroll
         for (int v = 0; v < NV; v++) {
             const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
-            if constexpr (LN) {
-                const float mean = st_mean[r], rs = st_rstd[r];
-                float a[VE];
-#pragma unroll
-                for (int e = 0; e < VE / 4; e++) {
-                    const f32x4 sc = *(const f32x4*)(p.ln_scale + k0 + kv + 4 * e);
-                    const f32x4 sh = *(const f32x4*)(p.ln_shift + k0 + kv + 4 * e);
-#pragma unroll
-                    for (int u = 0; u < 4; u++) a[4 * e + u] = (rh[v][e][u] - mean) * rs * (1.0f + sc[u]) + sh[u];
-                }
-                if constexpr (BF16) {
-                    u32x4 w = {pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(a[4], a[5]), pack2(a[6], a[7])};
-                    *(u32x4*)(As + r * LD + kv) = w;
-                } else {
-                    *(f32x4*)(As + r * LD + kv) = f32x4{a[0], a[1], a[2], a[3]};
-                }
-            } else {
-                *(u32x4*)(As + r * LD + kv) = ra[v];
-            }
-            *(u32x4*)(Bs + r * LD + kv) = rb[v];
+            *(u32x4*)(&As[buf][r * LD + kv]) = ra[v];
+            *(u32x4*)(&Bs[buf][r * LD + kv]) = rb[v];
         }
     };
 
@@ -256,30 +221,46 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
         for (int j = 0; j < 2; j++) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int l16 = lane & 15, g = lane >> 4;
-    const int nk = p.K / KC;
-    gload(0);
+    const int nk = (p.K + KC - 1) / KC;   // K is a multiple of 32; a last partial chunk reads zeros past K
+    const int kfull = p.K / KC;
+    auto gload_chunk = [&](int kc) {
+        if (kc < kfull) {
+            gload(kc * KC);
+        } else {   // partial last chunk: vectors past K are zero
+#pragma unroll
+            for (int v = 0; v < NV; v++) {
+                const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
+                const int k = kc * KC + kv;
+                ra[v] = k < p.K ? *(const u32x4*)(A + (size_t)min(m0 + r, p.M - 1) * p.K + k) : u32x4{0, 0, 0, 0};
+                rb[v] = k < p.K ? *(const u32x4*)(W + (size_t)min(n0 + r, p.N - 1) * p.K + k) : u32x4{0, 0, 0, 0};
+            }
+        }
+    };
+    gload_chunk(0);
+    lstore(0);
+    __syncthreads();
     for (int kc = 0; kc < nk; kc++) {
-        lstore(kc * KC);
-        __syncthreads();
-        if (kc + 1 < nk) gload((kc + 1) * KC);
-        if constexpr (BF16) {
-            bf16x8_t wf[2], xf[2];
+        const int buf = kc & 1;
+        if (kc + 1 < nk) gload_chunk(kc + 1);
 #pragma unroll
-            for (int i = 0; i < 2; i++) wf[i] = *(const bf16x8_t*)(Bs + (wn * 32 + 16 * i + l16) * LD + 8 * g);
+        for (int s = 0; s < KC / KQ; s++) {
+            if constexpr (BF16) {
+                bf16x8_t wf[2], xf[2];
 #pragma unroll
-            for (int j = 0; j < 2; j++) xf[j] = *(const bf16x8_t*)(As + (wm * 32 + 16 * j + l16) * LD + 8 * g);
+                for (int i = 0; i < 2; i++) wf[i] = *(const bf16x8_t*)(&Bs[buf][(wn * 32 + 16 * i + l16) * LD + KQ * s + 8 * g]);
 #pragma unroll
-            for (int i = 0; i < 2; i++)
+                for (int j = 0; j < 2; j++) xf[j] = *(const bf16x8_t*)(&As[buf][(wm * 32 + 16 * j + l16) * LD + KQ * s + 8 * g]);
 #pragma unroll
-                for (int j = 0; j < 2; j++) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], xf[j], acc[i][j], 0, 0, 0);
-        } else {
+                for (int i = 0; i < 2; i++)
 #pragma unroll
-            for (int s = 0; s < 2; s++) {
+                    for (int j = 0; j < 2; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], xf[j], acc[i][j], 0, 0, 0);
+            } else {
                 f32x4 wf[2], xf[2];
 #pragma unroll
-                for (int i = 0; i < 2; i++) wf[i] = *(const f32x4*)(Bs + (wn * 32 + 16 * i + l16) * LD + 16 * s + 4 * g);
+                for (int i = 0; i < 2; i++) wf[i] = *(const f32x4*)(&Bs[buf][(wn * 32 + 16 * i + l16) * LD + KQ * s + 4 * g]);
 #pragma unroll
-                for (int j = 0; j < 2; j++) xf[j] = *(const f32x4*)(As + (wm * 32 + 16 * j + l16) * LD + 16 * s + 4 * g);
+                for (int j = 0; j < 2; j++) xf[j] = *(const f32x4*)(&As[buf][(wm * 32 + 16 * j + l16) * LD + KQ * s + 4 * g]);
 #pragma unroll
                 for (int q = 0; q < 4; q++)
 #pragma unroll
@@ -289,6 +270,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
                             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(wf[i][q], xf[j][q], acc[i][j], 0, 0, 0);
             }
         }
+        if (kc + 1 < nk) lstore(buf ^ 1);
         __syncthreads();
     }
 
@@ -507,9 +489,9 @@ hipError_t launch_one(const GemmParams& p, hipStream_t st)
         if (e != hipSuccess) return e;
         GemmParams q = p;
         q.ln_h = nullptr;
-        hipLaunchKernelGGL((gemm_kernel<BF16, EPI, false>), dim3((p.N + 63) / 64, (p.M + 63) / 64), dim3(256), 0, st, q);
+        hipLaunchKernelGGL((gemm_kernel<BF16, EPI>), dim3((p.N + 63) / 64, (p.M + 63) / 64), dim3(256), 0, st, q);
     } else {
-        hipLaunchKernelGGL((gemm_kernel<BF16, EPI, false>), dim3((p.N + 63) / 64, (p.M + 63) / 64), dim3(256), 0, st, p);
+        hipLaunchKernelGGL((gemm_kernel<BF16, EPI>), dim3((p.N + 63) / 64, (p.M + 63) / 64), dim3(256), 0, st, p);
     }
     return hipGetLastError();
 }

@@ -213,3 +213,21 @@ def test_real_shape_matches_oracle(dtype):
         e, _ = err_stats(dec.carry(0, i, l, c, kv), s.carry(i, l, c, kv))
         assert e <= TOL[dtype], f"carry {(i, l, c, kv)}: {e:.3e}"
     dec.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_many_rows_take_the_tiled_path_and_match_oracle(dtype):
+    """24 streams: a call of 528 rows runs the tiled GEMMs with a standalone
+    LayerNorm (calls of at most 512 rows take the skinny GEMMs)."""
+    a = TINY
+    blob = synth.make_flow_weights(a, 5)
+    B = 24
+    calls = [a["f_call"]] * 3
+    say(f"flow tiny {dtype} B={B} (tiled path)")
+    dec, outs, mu, prompts = _run_gpu(a, dtype, blob, B, a["f_prompt"], calls)
+    for b in (0, 11, 23):
+        _s, ref = _run_oracle(a, dtype, blob, b, prompts[b], mu[b], calls)
+        for k, (g, r) in enumerate(zip(outs, ref)):
+            e, _ = err_stats(g[b], r)
+            assert e <= TOL[dtype], f"stream {b} call {k}: {e:.3e}"
+    dec.close()

@@ -195,12 +195,17 @@ def _csv(path):
         return list(csv.DictReader(fh))
 
 
+def _sources_for(path: str):
+    """The kernel sources a profile of this workload covers (flow workloads: the flow kernels)."""
+    return FLOW_SOURCES if "flow_" in os.path.basename(path) else ("dc_kernels.hip", "dc_internal.h")
+
+
 def summarize_stats(prof_dir: str, out: str, command: str):
     """Text summary of a rocprofv3 --kernel-trace --stats --output-format csv run."""
     import glob
     rows = _csv(glob.glob(os.path.join(prof_dir, "**", "*kernel_stats.csv"), recursive=True)[0])
     lines = [f"# rocprofv3 kernel statistics", f"# command: {command}",
-             f"# kernel sources: {kernel_source_hash()}", "",
+             f"# kernel sources: {kernel_source_hash(_sources_for(out))}", "",
              f"{'kernel':64s} {'calls':>7s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'total_ms':>9s} {'pct':>6s}"]
     for r in rows:
         name = r["Name"].replace("void ", "")
@@ -230,7 +235,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, workload: str, kernel: str
     lines = ["# HBM traffic per launch from rocprofv3 PMC counters", f"# command: {command}",
              f"# FETCH_SIZE x {FETCH_SCALE} + WRITE_SIZE x {WRITE_SCALE} (KiB per dispatch; scale factors from a "
              "plain 256 MiB device copy: python3 bench.py --calibrate-copy)",
-             f"workload: {workload}", f"kernel: {kernel}", f"kernel_source_hash: {kernel_source_hash()}",
+             f"workload: {workload}", f"kernel: {kernel}", f"kernel_source_hash: {kernel_source_hash(_sources_for(out))}",
              f"dispatches: {nf} / {nw}", f"fetch_kib_per_dispatch: {f:.1f}", f"write_kib_per_dispatch: {w:.1f}",
              f"hbm_bytes_per_launch: {hbm:.0f}"]
     open(out, "w").write("\n".join(lines) + "\n")
@@ -246,14 +251,14 @@ def summarize_mfma(prof_dir: str, workload: str, out: str, command: str):
     for r in rows:
         name = r["Kernel_Name"].replace("void ", "")
         name = name[:name.index("(")] if "(" in name else name
-        if not name.startswith("dc::"):
+        if not name.startswith(("dc::", "dcf::")):
             continue
         d = per.setdefault(name, {}).setdefault(r["Dispatch_Id"], {})
         d[r["Counter_Name"]] = float(r["Counter_Value"])
         d["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
     xcds, simds = 8, 1024
     lines = ["# MFMA counters per kernel from rocprofv3 PMC counters", f"# command: {command}",
-             f"# workload: {workload}", f"# kernel sources: {kernel_source_hash()}",
+             f"# workload: {workload}", f"# kernel sources: {kernel_source_hash(_sources_for(out))}",
              "# mfma_flops = (SQ_INSTS_VALU_MFMA_MOPS_BF16 + SQ_INSTS_VALU_MFMA_MOPS_F32) * 512 per dispatch",
              "# mfma_util  = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs * 1024 SIMDs); for dispatches "
              "of a few microseconds GRBM_GUI_ACTIVE also counts the collection window, so it reads low there",
@@ -287,7 +292,7 @@ def flow_kernel_name(role: str, dtype: str, rows: int) -> str:
         epi, ln = FLOW_GEMM[role]
         if rows <= SKINNY_ROWS:
             return f"dcf::skinny_kernel<{b}, {epi}, {'true' if ln else 'false'}>"
-        return f"dcf::gemm_kernel<{b}, {epi}, false>"
+        return f"dcf::gemm_kernel<{b}, {epi}>"
     return f"dcf::{role}_kernel<{b}>" if role in ("attn", "assemble", "euler") else role
 
 
@@ -378,6 +383,11 @@ def bench_flow(args):
     audio_s = B * fc / FLOW_FRAME_RATE
     value = audio_s * args.steps / wall
     print(f"# timed {args.steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
+    if args.only_steps:
+        dec.close()
+        print(json.dumps({"workload": args.workload, "steps": args.steps, "ms_per_step": round(ms_per_step, 4)}),
+              flush=True)
+        return
 
     lat_dev, lat_ev = [], []
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -465,6 +475,8 @@ def main():
     ap.add_argument("--tile-variant", type=int, default=0)
     ap.add_argument("--skip-peaks", action="store_true", help="skip the device copy and GEMM peak runs "
                     "(for profiler runs; the roofline then has no measured-peak fraction)")
+    ap.add_argument("--only-steps", action="store_true", help="flow workloads: run the warmup and timed steps only "
+                    "and print their timing (for hardware-counter runs, which serialise every dispatch)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested). Streams are "

@@ -580,21 +580,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams 
         t0 = 32 * (t - st0[i]);
     };
 
-    // query fragments of the four groups (B operand of S^T)
-    bf16x8_t qb[4][2];
-    f32x4 qf[4][4];
-#pragma unroll
-    for (int qg = 0; qg < 4; qg++) {
-        const T* qr = qp + (size_t)(qb0 + 16 * qg + l16) * 64;   // rows past n are computed and dropped
-        if constexpr (BF16) {
-#pragma unroll
-            for (int s2 = 0; s2 < 2; s2++) qb[qg][s2] = *(const bf16x8_t*)(qr + 32 * s2 + 8 * g);
-        } else {
-#pragma unroll
-            for (int s4 = 0; s4 < 4; s4++) qf[qg][s4] = *(const f32x4*)(qr + 16 * s4 + 4 * g);
-        }
-    }
-
     // one tile's operands: keys (two blocks of 16) and the value groups
     struct Tile {
         u32x4 kf[2][4];
@@ -630,120 +615,162 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams 
         }
     };
 
-    float m[4], lsum[4];
-    f32x4 O[4][4];
+    // query fragments of one group of 16 queries (B operand of S^T)
+    struct QFrag {
+        bf16x8_t b[2];
+        f32x4 f[4];
+    };
+    auto load_q = [&](int qg, QFrag& qfr) {
+        const T* qr = qp + (size_t)(qb0 + 16 * qg + l16) * 64;   // rows past n are computed and dropped
+        if constexpr (BF16) {
 #pragma unroll
-    for (int qg = 0; qg < 4; qg++) {
-        m[qg] = -INFINITY;
-        lsum[qg] = 0.f;
+            for (int s2 = 0; s2 < 2; s2++) qfr.b[s2] = *(const bf16x8_t*)(qr + 32 * s2 + 8 * g);
+        } else {
 #pragma unroll
-        for (int db = 0; db < 4; db++) O[qg][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-
-    auto work = [&](int t, const Tile& cur) {
-        int base, len, t0;
-        locate(t, base, len, t0);
+            for (int s4 = 0; s4 < 4; s4++) qfr.f[s4] = *(const f32x4*)(qr + 16 * s4 + 4 * g);
+        }
+    };
+    // one tile for one query group: scores, running maximum and sum, O^T update
+    auto step = [&](const Tile& cur, int t0, int len, const QFrag& qfr, float& m, float& lsum, f32x4 (&O)[4]) {
+        f32x4 st[2];
 #pragma unroll
-        for (int qg = 0; qg < 4; qg++) {
-            f32x4 st[2];
-#pragma unroll
-            for (int j = 0; j < 2; j++) {
-                st[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-                if constexpr (BF16) {
-#pragma unroll
-                    for (int s2 = 0; s2 < 2; s2++)
-                        st[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, cur.kf[j][s2]),
-                                                                        qb[qg][s2], st[j], 0, 0, 0);
-                } else {
-#pragma unroll
-                    for (int s4 = 0; s4 < 4; s4++) {
-                        const f32x4 kv = __builtin_bit_cast(f32x4, cur.kf[j][s4]);
-#pragma unroll
-                        for (int u = 0; u < 4; u++)
-                            st[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[u], qf[qg][s4][u], st[j], 0, 0, 0);
-                    }
-                }
-            }
-            float mt = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < 2; j++)
-#pragma unroll
-                for (int r = 0; r < 4; r++) {
-                    const bool live = t0 + 16 * j + 4 * g + r < len;
-                    st[j][r] = live ? st[j][r] * 0.125f : -INFINITY;
-                    mt = fmaxf(mt, st[j][r]);
-                }
-            mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-            mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-            const float mn = fmaxf(m[qg], mt);
-            const float alpha = expf(m[qg] - mn);
-            m[qg] = mn;
-            float ps = 0.f;
-#pragma unroll
-            for (int j = 0; j < 2; j++)
-#pragma unroll
-                for (int r = 0; r < 4; r++) {
-                    st[j][r] = expf(st[j][r] - mn);
-                    ps += st[j][r];
-                }
-            lsum[qg] = lsum[qg] * alpha + ps;
-#pragma unroll
-            for (int db = 0; db < 4; db++) O[qg][db] *= alpha;
+        for (int j = 0; j < 2; j++) {
+            st[j] = f32x4{0.f, 0.f, 0.f, 0.f};
             if constexpr (BF16) {
-                const u32x4 pw = {pack2(st[0][0], st[0][1]), pack2(st[0][2], st[0][3]), pack2(st[1][0], st[1][1]),
-                                  pack2(st[1][2], st[1][3])};
-                const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
 #pragma unroll
-                for (int db = 0; db < 4; db++)
-                    O[qg][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, cur.va[db]), pf,
-                                                                        O[qg][db], 0, 0, 0);
+                for (int s2 = 0; s2 < 2; s2++)
+                    st[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, cur.kf[j][s2]),
+                                                                    qfr.b[s2], st[j], 0, 0, 0);
             } else {
 #pragma unroll
-                for (int db = 0; db < 4; db++) {
-                    const f32x4 va = __builtin_bit_cast(f32x4, cur.va[db]), vb = __builtin_bit_cast(f32x4, cur.vb[db]);
+                for (int s4 = 0; s4 < 4; s4++) {
+                    const f32x4 kv = __builtin_bit_cast(f32x4, cur.kf[j][s4]);
 #pragma unroll
                     for (int u = 0; u < 4; u++)
-                        O[qg][db] = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u], st[0][u], O[qg][db], 0, 0, 0);
-#pragma unroll
-                    for (int u = 0; u < 4; u++)
-                        O[qg][db] = __builtin_amdgcn_mfma_f32_16x16x4f32(vb[u], st[1][u], O[qg][db], 0, 0, 0);
+                        st[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[u], qfr.f[s4][u], st[j], 0, 0, 0);
                 }
+            }
+        }
+        float mt = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                const bool live = t0 + 16 * j + 4 * g + r < len;
+                st[j][r] = live ? st[j][r] * 0.125f : -INFINITY;
+                mt = fmaxf(mt, st[j][r]);
+            }
+        mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        const float mn = fmaxf(m, mt);
+        const float alpha = expf(m - mn);
+        m = mn;
+        float ps = 0.f;
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                st[j][r] = expf(st[j][r] - mn);
+                ps += st[j][r];
+            }
+        lsum = lsum * alpha + ps;
+#pragma unroll
+        for (int db = 0; db < 4; db++) O[db] *= alpha;
+        if constexpr (BF16) {
+            const u32x4 pw = {pack2(st[0][0], st[0][1]), pack2(st[0][2], st[0][3]), pack2(st[1][0], st[1][1]),
+                              pack2(st[1][2], st[1][3])};
+            const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
+#pragma unroll
+            for (int db = 0; db < 4; db++)
+                O[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, cur.va[db]), pf, O[db], 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int db = 0; db < 4; db++) {
+                const f32x4 va = __builtin_bit_cast(f32x4, cur.va[db]), vb = __builtin_bit_cast(f32x4, cur.vb[db]);
+#pragma unroll
+                for (int u = 0; u < 4; u++) O[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(va[u], st[0][u], O[db], 0, 0, 0);
+#pragma unroll
+                for (int u = 0; u < 4; u++) O[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(vb[u], st[1][u], O[db], 0, 0, 0);
             }
         }
     };
-#ifndef DCF_ATTN_PREFETCH
-#define DCF_ATTN_PREFETCH 1
-#endif
-    if constexpr (BF16 && DCF_ATTN_PREFETCH) {
-        // the next tile (or this one again) is in flight while one is worked on
-        Tile cur;
-        load(min(wave, total - 1), cur);
-        for (int t = wave; t < total; t += NW) {
-            Tile nxt;
-            load(min(t + NW, total - 1), nxt);
-            work(t, cur);
-            cur = nxt;
-        }
-    } else {   // fp32 tiles are twice the registers: one at a time
-        for (int t = wave; t < total; t += NW) {
-            Tile cur;
-            load(t, cur);
-            work(t, cur);
-        }
-    }
-
-    // this wave's partial results: O^T lane (l16, g) holds dims 16 db + 4 g + r of query l16
-#pragma unroll
-    for (int qg = 0; qg < 4; qg++) {
-        float l1 = lsum[qg] + __shfl_xor(lsum[qg], 16, 64);
+    // this wave's partial result of one group: O^T lane (l16, g) holds dims 16 db + 4 g + r of query l16
+    auto put = [&](int qg, float m, float lsum, const f32x4 (&O)[4]) {
+        float l1 = lsum + __shfl_xor(lsum, 16, 64);
         l1 += __shfl_xor(l1, 32, 64);
         const int qq = 16 * qg + l16;
 #pragma unroll
-        for (int db = 0; db < 4; db++) *(f32x4*)(Os + ((size_t)wave * 64 + qq) * kAttnLd + 16 * db + 4 * g) = O[qg][db];
+        for (int db = 0; db < 4; db++) *(f32x4*)(Os + ((size_t)wave * 64 + qq) * kAttnLd + 16 * db + 4 * g) = O[db];
         if (g == 0) {
-            Ms[wave * 64 + qq] = m[qg];
+            Ms[wave * 64 + qq] = m;
             Ls[wave * 64 + qq] = l1;
         }
+    };
+
+#ifndef DCF_ATTN_PREFETCH
+#define DCF_ATTN_PREFETCH 1
+#endif
+#ifndef DCF_ATTN_QG_ROLLED
+#define DCF_ATTN_QG_ROLLED 0
+#endif
+    if constexpr (DCF_ATTN_QG_ROLLED) {
+        // one query group at a time over the wave's tiles (the tiles are
+        // read once per group, from L1/L2 after the first): a fourth of the code
+#pragma unroll 1
+        for (int qg = 0; qg < 4; qg++) {
+            QFrag qfr;
+            load_q(qg, qfr);
+            float m = -INFINITY, lsum = 0.f;
+            f32x4 O[4];
+#pragma unroll
+            for (int db = 0; db < 4; db++) O[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int t = wave; t < total; t += NW) {
+                Tile cur;
+                load(t, cur);
+                int base, len, t0;
+                locate(t, base, len, t0);
+                step(cur, t0, len, qfr, m, lsum, O);
+            }
+            put(qg, m, lsum, O);
+        }
+    } else {
+        QFrag qfr[4];
+#pragma unroll
+        for (int qg = 0; qg < 4; qg++) load_q(qg, qfr[qg]);
+        float m[4], lsum[4];
+        f32x4 O[4][4];
+#pragma unroll
+        for (int qg = 0; qg < 4; qg++) {
+            m[qg] = -INFINITY;
+            lsum[qg] = 0.f;
+#pragma unroll
+            for (int db = 0; db < 4; db++) O[qg][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        auto work = [&](int t, const Tile& cur) {
+            int base, len, t0;
+            locate(t, base, len, t0);
+#pragma unroll
+            for (int qg = 0; qg < 4; qg++) step(cur, t0, len, qfr[qg], m[qg], lsum[qg], O[qg]);
+        };
+        if constexpr (BF16 && DCF_ATTN_PREFETCH) {
+            // the next tile (or this one again) is in flight while one is worked on
+            Tile cur;
+            load(min(wave, total - 1), cur);
+            for (int t = wave; t < total; t += NW) {
+                Tile nxt;
+                load(min(t + NW, total - 1), nxt);
+                work(t, cur);
+                cur = nxt;
+            }
+        } else {   // fp32 tiles are twice the registers: one at a time
+            for (int t = wave; t < total; t += NW) {
+                Tile cur;
+                load(t, cur);
+                work(t, cur);
+            }
+        }
+#pragma unroll
+        for (int qg = 0; qg < 4; qg++) put(qg, m[qg], lsum[qg], O[qg]);
     }
     __syncthreads();
     if (wave >= 4) return;

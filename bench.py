@@ -286,17 +286,22 @@ FLOW_GEMM = {   # role -> (epilogue, LayerNorm operand) of the GEMM that runs it
 SKINNY_ROWS = 512   # calls of at most this many rows (2 per stream and frame) run the skinny GEMM
 
 
-def flow_kernel_name(role: str, dtype: str, rows: int) -> str:
+ATTN_WIDE_BLOCKS = 64   # (stream, branch, head) x 64-query blocks from which attention takes its wide shape
+
+
+def flow_kernel_name(role: str, dtype: str, rows: int, attn_blocks: int = 0) -> str:
     b = "true" if dtype == "bf16" else "false"
+    if role == "attn":
+        return f"dcf::attn_kernel<{b}, 4, 8>" if attn_blocks >= ATTN_WIDE_BLOCKS else f"dcf::attn_kernel<{b}, 1, 4>"
     if role in FLOW_GEMM:
         epi, ln = FLOW_GEMM[role]
         if rows <= SKINNY_ROWS:
             return f"dcf::skinny_kernel<{b}, {epi}, {'true' if ln else 'false'}>"
         return f"dcf::gemm_kernel<{b}, {epi}>"
-    return f"dcf::{role}_kernel<{b}>" if role in ("attn", "assemble", "euler") else role
+    return f"dcf::{role}_kernel<{b}>" if role in ("assemble", "euler") else role
 
 
-def flow_roofline(prof, dtype, rows):
+def flow_roofline(prof, dtype, rows, attn_blocks):
     """The role with the most device time per call, against its bound."""
     step_us = sum(r["us"] for r in prof)
     top = max(prof, key=lambda r: r["us"])
@@ -305,7 +310,7 @@ def flow_roofline(prof, dtype, rows):
         bound, achieved, peak, unit = "mfma", top["flops"] / (top["us"] * 1e-6) / 1e12, PEAK[op], "TFLOP/s"
     else:
         bound, achieved, peak, unit = "hbm", top["bytes"] / (top["us"] * 1e-6) / 1e9, PEAK["hbm"], "GB/s"
-    kern = flow_kernel_name(top["name"], dtype, rows)
+    kern = flow_kernel_name(top["name"], dtype, rows, attn_blocks)
     return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": None, "kernel": kern, "role": top["name"],
             "operand": op, "launches_per_step": top["launches"],
@@ -400,7 +405,7 @@ def bench_flow(args):
         lat_dev.append(1000.0 * (time.perf_counter() - t))
         lat_ev.append(ev[0].elapsed_time(ev[1]))
     prof = dec.profile(args.layer_reps)
-    roof = flow_roofline(prof, dtype, B * 2 * fcall)
+    roof = flow_roofline(prof, dtype, B * 2 * fcall, B * 2 * arch["heads"] * ((fcall + 63) // 64))
     roof["traffic"] = traffic_from_profiles(args.workload, roof["kernel"], FLOW_SOURCES)
     stats = dec.stats()
     dec.close()

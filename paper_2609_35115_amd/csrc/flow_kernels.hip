@@ -526,19 +526,22 @@ hipError_t launch_gemm(const GemmParams& p, int epi, int bf16, hipStream_t st)
 // K slice of the second product, so P never leaves its registers, and the
 // running maximum, sum and rescale of O^T stay per lane.
 constexpr int kMaxSegments = 8;
-#ifndef DCF_ATTN_WAVES
-#define DCF_ATTN_WAVES 8
-#endif
-constexpr int kAttnWaves = DCF_ATTN_WAVES;
+// Two block shapes: 4 query groups (64 queries) over 8 waves when the call
+// has enough (stream, branch, head) blocks to fill the device, else one
+// query group (16 queries) over 4 waves, which gives a small call four times
+// the blocks.  The shape fixes the order of the softmax merge, so results of
+// the two shapes differ in rounding only.
 constexpr int kAttnLd = 68;   // padded row of the merge buffer (floats)
+constexpr int kAttnWideBlocks = 64;   // blocks of 64 queries below which the narrow shape is used
 
-size_t attn_lds_bytes() { return (size_t)kAttnWaves * 64 * kAttnLd * 4 + (size_t)2 * kAttnWaves * 64 * 4; }
+size_t attn_lds_bytes(int nw) { return (size_t)nw * 64 * kAttnLd * 4 + (size_t)2 * nw * 64 * 4; }
 
-template <bool BF16>
-__global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams p)
+template <bool BF16, int QG, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_kernel(const AttnParams p)
 {
     using T = typename std::conditional<BF16, uint16_t, float>::type;
-    constexpr int NW = kAttnWaves;
+    static_assert((QG == 1 || QG == 2 || QG == 4) && QG <= NW,
+                  "16 * QG divides the 64-row query padding; a merge wave per query group");
     extern __shared__ __align__(16) unsigned char smem[];
     float* Os = (float*)smem;                          // [NW waves][64 queries][kAttnLd]
     float* Ms = Os + NW * 64 * kAttnLd;                // [NW][64]
@@ -549,7 +552,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams 
     const int bh = blockIdx.x;
     const int bp = bh / (2 * p.heads), c = (bh / p.heads) & 1, hd = bh % p.heads;
     const int b = p.b0 + bp;
-    const int qb0 = blockIdx.y * 64;
+    const int qb0 = blockIdx.y * 16 * QG;
     const CarryRef& cr = p.carry;
     const T* Kb = (const T*)cr.base + (size_t)b * cr.stream_stride + ((size_t)((c * 2 + 0) * p.heads + hd)) * cr.Fr * 64;
     const T* Vb = (const T*)cr.base + (size_t)b * cr.stream_stride + ((size_t)((c * 2 + 1) * p.heads + hd)) * cr.Fr * 64;
@@ -717,7 +720,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams 
         // one query group at a time over the wave's tiles (the tiles are
         // read once per group, from L1/L2 after the first): a fourth of the code
 #pragma unroll 1
-        for (int qg = 0; qg < 4; qg++) {
+        for (int qg = 0; qg < QG; qg++) {
             QFrag qfr;
             load_q(qg, qfr);
             float m = -INFINITY, lsum = 0.f;
@@ -734,13 +737,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams 
             put(qg, m, lsum, O);
         }
     } else {
-        QFrag qfr[4];
+        QFrag qfr[QG];
 #pragma unroll
-        for (int qg = 0; qg < 4; qg++) load_q(qg, qfr[qg]);
-        float m[4], lsum[4];
-        f32x4 O[4][4];
+        for (int qg = 0; qg < QG; qg++) load_q(qg, qfr[qg]);
+        float m[QG], lsum[QG];
+        f32x4 O[QG][4];
 #pragma unroll
-        for (int qg = 0; qg < 4; qg++) {
+        for (int qg = 0; qg < QG; qg++) {
             m[qg] = -INFINITY;
             lsum[qg] = 0.f;
 #pragma unroll
@@ -750,7 +753,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams 
             int base, len, t0;
             locate(t, base, len, t0);
 #pragma unroll
-            for (int qg = 0; qg < 4; qg++) step(cur, t0, len, qfr[qg], m[qg], lsum[qg], O[qg]);
+            for (int qg = 0; qg < QG; qg++) step(cur, t0, len, qfr[qg], m[qg], lsum[qg], O[qg]);
         };
         if constexpr (BF16 && DCF_ATTN_PREFETCH) {
             // the next tile (or this one again) is in flight while one is worked on
@@ -770,10 +773,10 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams 
             }
         }
 #pragma unroll
-        for (int qg = 0; qg < 4; qg++) put(qg, m[qg], lsum[qg], O[qg]);
+        for (int qg = 0; qg < QG; qg++) put(qg, m[qg], lsum[qg], O[qg]);
     }
     __syncthreads();
-    if (wave >= 4) return;
+    if (wave >= QG) return;
     // wave w merges queries 16 w .. 16 w + 15 over the waves, in wave order
     const int qq = 16 * wave + l16;
     float mx = Ms[qq];
@@ -799,21 +802,27 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_kernel(const AttnParams 
     }
 }
 
+template <bool BF16, int QG, int NW>
+hipError_t launch_attn_shape(const AttnParams& p, int Bc, hipStream_t st)
+{
+    const dim3 grid(Bc * 2 * p.heads, (p.n + 16 * QG - 1) / (16 * QG));
+    const size_t lds = attn_lds_bytes(NW);
+    static bool set = false;
+    if (!set) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<BF16, QG, NW>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        set = true;
+    }
+    hipLaunchKernelGGL((attn_kernel<BF16, QG, NW>), grid, dim3(64 * NW), lds, st, p);
+    return hipGetLastError();
+}
+
 hipError_t launch_attn(const AttnParams& p, int Bc, int bf16, hipStream_t st)
 {
-    const dim3 grid(Bc * 2 * p.heads, (p.n + 63) / 64);
-    const size_t lds = attn_lds_bytes();
-    static bool set[2] = {false, false};
-    if (!set[bf16 ? 1 : 0]) {
-        const void* fn = bf16 ? reinterpret_cast<const void*>(&attn_kernel<true>)
-                              : reinterpret_cast<const void*>(&attn_kernel<false>);
-        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        set[bf16 ? 1 : 0] = true;
-    }
-    if (bf16) hipLaunchKernelGGL((attn_kernel<true>), grid, dim3(64 * kAttnWaves), lds, st, p);
-    else hipLaunchKernelGGL((attn_kernel<false>), grid, dim3(64 * kAttnWaves), lds, st, p);
-    return hipGetLastError();
+    const bool wide = Bc * 2 * p.heads * ((p.n + 63) / 64) >= kAttnWideBlocks;
+    if (bf16) return wide ? launch_attn_shape<true, 4, 8>(p, Bc, st) : launch_attn_shape<true, 1, 4>(p, Bc, st);
+    return wide ? launch_attn_shape<false, 4, 8>(p, Bc, st) : launch_attn_shape<false, 1, 4>(p, Bc, st);
 }
 
 // ------------------------------------------------------ inputs and the solver

@@ -288,48 +288,52 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
 }
 
 // Skinny GEMM for few rows (a call of a handful of streams): block = 64 rows
-// x 16 columns, 8 waves that split K into contiguous eighths of whole MFMA
-// steps; each wave loads its weight and activation fragments for up to 4
+// x 16 NBLK columns, NW waves that split K into contiguous ranges of whole
+// MFMA steps; each wave loads its weight and activation fragments for 4
 // steps at once, so a block costs few memory round trips.  The weight loads
 // of the first batch and the epilogue's operands are issued before anything
-// waits.  The eight partial tiles are summed through LDS in wave order.
-// With a LayerNorm operand the block first normalises its 64 rows into LDS
+// waits.  The partial tiles are summed through LDS in wave order.  With a
+// LayerNorm operand the block first normalises its 64 rows into LDS
 // (operand type, all K).
-#ifndef DCF_SKINNY_WAVES
-#define DCF_SKINNY_WAVES 4
-#endif
-constexpr int kSkinnyWaves = DCF_SKINNY_WAVES;
-
-template <bool BF16, int EPI, bool LN>
-__global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(const GemmParams p)
+template <bool BF16, int EPI, bool LN, int NW, int NBLK>
+__global__ __launch_bounds__(64 * NW) void skinny_kernel(const GemmParams p)
 {
     using T = typename std::conditional<BF16, uint16_t, float>::type;
     constexpr int KQ = BF16 ? 32 : 16;               // K of one MFMA step group (one 16-byte load per lane)
     constexpr int BATCH = 4;
     constexpr int PAD = BF16 ? 8 : 4;
-    constexpr int NW = kSkinnyWaves;
+    constexpr int NPAIR = 4 * NBLK;                  // (column block, row block) output tiles of 16 x 16
+    constexpr int PPW = (NPAIR + NW - 1) / NW;       // tiles each wave finalises
     extern __shared__ __align__(16) unsigned char smem[];
     T* As = (T*)smem;                                 // LN: [64][K + PAD], then scale and shift
-    f32x4* red = (f32x4*)smem;                        // after the main loop: [NW waves][4 row blocks][64 lanes]
+    f32x4* red = (f32x4*)smem;                        // after the main loop: [NW waves][NPAIR][64 lanes]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, g = lane >> 4;
-    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 16;
+    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 16 * NBLK;
     const int LDA = p.K + PAD;
     const T* A = (const T*)p.A;
     const T* W = (const T*)p.W;
 
     const int ng = p.K / KQ;
     const int q0 = wave * ng / NW, q1 = (wave + 1) * ng / NW;
-    const int col = min(n0 + l16, p.N - 1);
+    int col[NBLK];
+#pragma unroll
+    for (int j = 0; j < NBLK; j++) col[j] = min(n0 + 16 * j + l16, p.N - 1);
     // the first batch's weight fragments (they do not wait for the LayerNorm)
-    u32x4 wf[BATCH];
+    u32x4 wf[BATCH][NBLK];
 #pragma unroll
     for (int b = 0; b < BATCH; b++)
-        wf[b] = *(const u32x4*)(W + (size_t)col * p.K + min(q0 + b, max(q1 - 1, 0)) * KQ + (BF16 ? 8 : 4) * g);
-    // the epilogue's operands (waves 0-3 finalise row blocks 0-3)
-    const int erow = min(m0 + 16 * (wave & 3) + l16, p.M - 1), ecol = min(n0 + 4 * g, p.N - 4);
-    const EpiPre pre = epi_prefetch<EPI>(p, erow, ecol);
+#pragma unroll
+        for (int j = 0; j < NBLK; j++)
+            wf[b][j] = *(const u32x4*)(W + (size_t)col[j] * p.K + min(q0 + b, max(q1 - 1, 0)) * KQ + (BF16 ? 8 : 4) * g);
+    // the epilogue's operands of the tiles this wave finalises
+    EpiPre pre[PPW];
+#pragma unroll
+    for (int u = 0; u < PPW; u++) {
+        const int pp = min(wave + u * NW, NPAIR - 1), j = pp >> 2, i = pp & 3;
+        pre[u] = epi_prefetch<EPI>(p, min(m0 + 16 * i + l16, p.M - 1), min(n0 + 16 * j + 4 * g, p.N - 4));
+    }
 
     if constexpr (LN) {
         float* ss = (float*)(smem + (size_t)64 * LDA * sizeof(T));
@@ -358,9 +362,11 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(const GemmPar
     int xr[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) xr[i] = min(m0 + 16 * i + l16, p.M - 1);
-    f32x4 acc[4];
+    f32x4 acc[NBLK][4];
 #pragma unroll
-    for (int i = 0; i < 4; i++) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NBLK; j++)
+#pragma unroll
+        for (int i = 0; i < 4; i++) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     for (int q = q0; q < q1; q += BATCH) {
         // all loads of the batch first; a step past the wave's range reloads
@@ -370,7 +376,9 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(const GemmPar
         if (q != q0) {
 #pragma unroll
             for (int b = 0; b < BATCH; b++)
-                wf[b] = *(const u32x4*)(W + (size_t)col * p.K + min(q + b, q1 - 1) * KQ + (BF16 ? 8 : 4) * g);
+#pragma unroll
+                for (int j = 0; j < NBLK; j++)
+                    wf[b][j] = *(const u32x4*)(W + (size_t)col[j] * p.K + min(q + b, q1 - 1) * KQ + (BF16 ? 8 : 4) * g);
         }
 #pragma unroll
         for (int b = 0; b < BATCH; b++) {
@@ -384,34 +392,45 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(const GemmPar
 #pragma unroll
         for (int b = 0; b < BATCH; b++) {
             const bool live = q + b < q1;
-            u32x4 w = wf[b];
 #pragma unroll
-            for (int e = 0; e < 4; e++) w[e] = live ? w[e] : 0u;
+            for (int j = 0; j < NBLK; j++) {
+                u32x4 w = wf[b][j];
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
-                if constexpr (BF16) {
-                    acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w),
-                                                                     __builtin_bit_cast(bf16x8_t, xf[b][i]), acc[i], 0, 0,
-                                                                     0);
-                } else {
-                    const f32x4 wv = __builtin_bit_cast(f32x4, w), xv = __builtin_bit_cast(f32x4, xf[b][i]);
+                for (int e = 0; e < 4; e++) w[e] = live ? w[e] : 0u;
 #pragma unroll
-                    for (int u = 0; u < 4; u++) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[u], xv[u], acc[i], 0, 0, 0);
+                for (int i = 0; i < 4; i++) {
+                    if constexpr (BF16) {
+                        acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w),
+                                                                            __builtin_bit_cast(bf16x8_t, xf[b][i]),
+                                                                            acc[j][i], 0, 0, 0);
+                    } else {
+                        const f32x4 wv = __builtin_bit_cast(f32x4, w), xv = __builtin_bit_cast(f32x4, xf[b][i]);
+#pragma unroll
+                        for (int u = 0; u < 4; u++)
+                            acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[u], xv[u], acc[j][i], 0, 0, 0);
+                    }
                 }
             }
         }
     }
     if constexpr (LN) __syncthreads();   // the LDS tile becomes the reduction buffer
 #pragma unroll
-    for (int i = 0; i < 4; i++) red[(wave * 4 + i) * 64 + lane] = acc[i];
-    __syncthreads();
-    if (wave >= 4) return;
-    // wave w sums row block w over the waves, in wave order
-    f32x4 y = red[(0 * 4 + wave) * 64 + lane];
+    for (int j = 0; j < NBLK; j++)
 #pragma unroll
-    for (int w = 1; w < NW; w++) y += red[(w * 4 + wave) * 64 + lane];
-    const int row = m0 + 16 * wave + l16, c4 = n0 + 4 * g;
-    if (row < p.M && c4 < p.N) epilogue4<BF16, EPI>(p, row, c4, y, pre);
+        for (int i = 0; i < 4; i++) red[(wave * NPAIR + 4 * j + i) * 64 + lane] = acc[j][i];
+    __syncthreads();
+    // wave w sums its tiles over the waves, in wave order
+#pragma unroll
+    for (int u = 0; u < PPW; u++) {
+        const int pp = wave + u * NW;
+        if (pp >= NPAIR) break;
+        f32x4 y = red[pp * 64 + lane];
+#pragma unroll
+        for (int w = 1; w < NW; w++) y += red[(w * NPAIR + pp) * 64 + lane];
+        const int j = pp >> 2, i = pp & 3;
+        const int row = m0 + 16 * i + l16, c4 = n0 + 16 * j + 4 * g;
+        if (row < p.M && c4 < p.N) epilogue4<BF16, EPI>(p, row, c4, y, pre[u]);
+    }
 }
 
 // ------------------------------------------------------- modulated LayerNorm
@@ -458,29 +477,56 @@ __global__ __launch_bounds__(256) void lnmod_kernel(const float* h, void* out, c
 // Rows up to which a call uses the skinny kernel.
 constexpr int kSkinnyRows = 512;
 
-size_t skinny_lds_bytes(const GemmParams& p, int bf16)
+// Skinny shapes: waves and 16-column blocks per block, by operand kind.
+#ifndef DCF_SK_LN_NBLK
+#define DCF_SK_LN_NBLK 1
+#endif
+#ifndef DCF_SK_PLAIN_NBLK
+#define DCF_SK_PLAIN_NBLK 1
+#endif
+#ifndef DCF_SK_BIGK_WAVES
+#define DCF_SK_BIGK_WAVES 8
+#endif
+#ifndef DCF_SK_PLAIN_WAVES
+#define DCF_SK_PLAIN_WAVES 4
+#endif
+#ifndef DCF_SK_LN_WAVES
+#define DCF_SK_LN_WAVES 4
+#endif
+constexpr int kSkinnyBigK = 1024;   // K from which the plain skinny GEMM uses DCF_SK_BIGK_WAVES waves
+
+size_t skinny_lds_bytes(const GemmParams& p, int bf16, int nw, int nblk)
 {
-    const size_t red = (size_t)kSkinnyWaves * 4 * 64 * 16;
+    const size_t red = (size_t)nw * 4 * nblk * 64 * 16;
     if (!p.ln_h) return red;
     // the normalised tile, then scale and shift
     const size_t a = (size_t)64 * (p.K + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4) + (size_t)2 * p.K * 4;
     return a > red ? a : red;
 }
 
+template <bool BF16, int EPI, bool LN, int NW, int NBLK>
+hipError_t launch_skinny(const GemmParams& p, hipStream_t st)
+{
+    const size_t lds = skinny_lds_bytes(p, BF16, NW, NBLK);
+    static size_t set = 0;
+    if (lds > 65536 && lds > set) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<BF16, EPI, LN, NW, NBLK>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        set = lds;
+    }
+    hipLaunchKernelGGL((skinny_kernel<BF16, EPI, LN, NW, NBLK>), dim3((p.N + 16 * NBLK - 1) / (16 * NBLK), (p.M + 63) / 64),
+                       dim3(64 * NW), lds, st, p);
+    return hipGetLastError();
+}
+
 template <bool BF16, int EPI, bool LN>
 hipError_t launch_one(const GemmParams& p, hipStream_t st)
 {
     if (p.M <= kSkinnyRows) {
-        const size_t lds = skinny_lds_bytes(p, BF16);
-        static size_t set = 0;
-        if (lds > 65536 && lds > set) {
-            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<BF16, EPI, LN>),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) return e;
-            set = lds;
-        }
-        hipLaunchKernelGGL((skinny_kernel<BF16, EPI, LN>), dim3((p.N + 15) / 16, (p.M + 63) / 64), dim3(64 * kSkinnyWaves),
-                           lds, st, p);
+        if constexpr (LN) return launch_skinny<BF16, EPI, true, DCF_SK_LN_WAVES, DCF_SK_LN_NBLK>(p, st);
+        else if (p.K >= kSkinnyBigK) return launch_skinny<BF16, EPI, false, DCF_SK_BIGK_WAVES, DCF_SK_PLAIN_NBLK>(p, st);
+        else return launch_skinny<BF16, EPI, false, DCF_SK_PLAIN_WAVES, DCF_SK_PLAIN_NBLK>(p, st);
     } else if (LN) {
         // the normalised operand is written once to p.A by its own launch
         hipLaunchKernelGGL((lnmod_kernel<BF16>), dim3((p.M + 3) / 4), dim3(256), 0, st, p.ln_h, const_cast<void*>(p.A),

@@ -289,19 +289,30 @@ SKINNY_ROWS = 512   # calls of at most this many rows (2 per stream and frame) r
 ATTN_WIDE_BLOCKS = 64   # (stream, branch, head) x 64-query blocks from which attention takes its wide shape
 
 
-def flow_kernel_name(role: str, dtype: str, rows: int, attn_blocks: int = 0) -> str:
+TILE_BIG_BLOCKS = 1024   # 64 x 64 tiles of a GEMM from which the tiled kernel takes 128 x 128
+TILE_MID_BLOCKS = 256    # ... and from which it takes 128 rows x 64 columns
+
+
+def flow_kernel_name(role: str, dtype: str, rows: int, attn_blocks: int = 0, arch: dict | None = None) -> str:
     b = "true" if dtype == "bf16" else "false"
     if role == "attn":
         return f"dcf::attn_kernel<{b}, 4, 8>" if attn_blocks >= ATTN_WIDE_BLOCKS else f"dcf::attn_kernel<{b}, 1, 4>"
     if role in FLOW_GEMM:
         epi, ln = FLOW_GEMM[role]
+        D = arch["dim"] if arch else 512
+        N, K = {"gemm:in": (D, 4 * (arch["n_mel"] if arch else 80)), "gemm:qkv": (3 * D, D), "gemm:o": (D, D),
+                "gemm:fc1": (arch["mlp"] if arch else 2048, D), "gemm:fc2": (D, arch["mlp"] if arch else 2048),
+                "gemm:out": (arch["n_mel"] if arch else 80, D)}[role]
         if rows <= SKINNY_ROWS:
-            return f"dcf::skinny_kernel<{b}, {epi}, {'true' if ln else 'false'}>"
-        return f"dcf::gemm_kernel<{b}, {epi}>"
+            waves = 8 if (not ln and K >= 1024) else 4
+            return f"dcf::skinny_kernel<{b}, {epi}, {'true' if ln else 'false'}, {waves}, 1>"
+        blocks = ((N + 63) // 64) * ((rows + 63) // 64)
+        tile = "4, 4" if blocks >= TILE_BIG_BLOCKS else "4, 2" if blocks >= TILE_MID_BLOCKS else "2, 2"
+        return f"dcf::gemm_kernel<{b}, {epi}, {tile}>"
     return f"dcf::{role}_kernel<{b}>" if role in ("assemble", "euler") else role
 
 
-def flow_roofline(prof, dtype, rows, attn_blocks):
+def flow_roofline(prof, dtype, rows, attn_blocks, arch):
     """The role with the most device time per call, against its bound."""
     step_us = sum(r["us"] for r in prof)
     top = max(prof, key=lambda r: r["us"])
@@ -310,7 +321,7 @@ def flow_roofline(prof, dtype, rows, attn_blocks):
         bound, achieved, peak, unit = "mfma", top["flops"] / (top["us"] * 1e-6) / 1e12, PEAK[op], "TFLOP/s"
     else:
         bound, achieved, peak, unit = "hbm", top["bytes"] / (top["us"] * 1e-6) / 1e9, PEAK["hbm"], "GB/s"
-    kern = flow_kernel_name(top["name"], dtype, rows, attn_blocks)
+    kern = flow_kernel_name(top["name"], dtype, rows, attn_blocks, arch)
     return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": None, "kernel": kern, "role": top["name"],
             "operand": op, "launches_per_step": top["launches"],
@@ -405,7 +416,7 @@ def bench_flow(args):
         lat_dev.append(1000.0 * (time.perf_counter() - t))
         lat_ev.append(ev[0].elapsed_time(ev[1]))
     prof = dec.profile(args.layer_reps)
-    roof = flow_roofline(prof, dtype, B * 2 * fcall, B * 2 * arch["heads"] * ((fcall + 63) // 64))
+    roof = flow_roofline(prof, dtype, B * 2 * fcall, B * 2 * arch["heads"] * ((fcall + 63) // 64), arch)
     roof["traffic"] = traffic_from_profiles(args.workload, roof["kernel"], FLOW_SOURCES)
     stats = dec.stats()
     dec.close()

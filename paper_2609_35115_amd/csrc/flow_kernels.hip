@@ -173,22 +173,25 @@ __device__ __forceinline__ LnRow ln_row_stats(const float* h, int M, int K, int 
     return LnRow{x0 + md, 1.0f / sqrtf(var + 1e-6f)};
 }
 
-// Tiled GEMM for many rows: tile 64 x 64, 4 waves as 2 x 2, each 32 x 32 =
-// 2 x 2 MFMA blocks.  K runs in chunks of 128 (bf16) or 64 (fp32) through two
-// LDS buffers: the next chunk is loaded into registers while the current one
-// is multiplied, then stored into the other buffer; one barrier per chunk.
-template <bool BF16, int EPI>
+// Tiled GEMM for many rows: 4 waves as 2 x 2, each 16 MB rows x 16 NB
+// columns of MFMA blocks, so a block computes 32 MB x 32 NB.  K runs in
+// chunks of KC through two LDS buffers: the next chunk is loaded into
+// registers while the current one is multiplied, then stored into the other
+// buffer; one barrier per chunk.
+template <bool BF16, int EPI, int MB, int NB>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
 {
     using T = typename std::conditional<BF16, uint16_t, float>::type;
-    constexpr int BM = 64, BN = 64, KC = BF16 ? 128 : 64;
+    constexpr int BM = 32 * MB, BN = 32 * NB;
+    constexpr int KC = (MB * NB <= 4 ? 128 : 64) / (BF16 ? 1 : 2);
     constexpr int LD = KC + (BF16 ? 8 : 4);          // padded LDS row: conflict-free 16-byte reads
     constexpr int VE = 16 / (int)sizeof(T);          // elements per 16-byte vector
     constexpr int VPR = KC / VE;                     // vectors per tile row
-    constexpr int NV = BM * VPR / 256;               // vectors per thread per operand
+    constexpr int NVA = BM * VPR / 256, NVB = BN * VPR / 256;   // vectors per thread per operand
     constexpr int KQ = BF16 ? 32 : 16;               // K of one MFMA step group
-    __shared__ __attribute__((aligned(16))) T As[2][BM * LD];
-    __shared__ __attribute__((aligned(16))) T Bs[2][BN * LD];
+    extern __shared__ __align__(16) unsigned char smem[];
+    T* As = (T*)smem;                                // [2][BM * LD]
+    T* Bs = As + 2 * BM * LD;                        // [2][BN * LD]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
@@ -196,77 +199,87 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
     const T* A = (const T*)p.A;
     const T* W = (const T*)p.W;
 
-    u32x4 ra[NV], rb[NV];
-    auto gload = [&](int k0) {
-#pragma unroll
-        for (int v = 0; v < NV; v++) {
-            const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
-            ra[v] = *(const u32x4*)(A + (size_t)min(m0 + r, p.M - 1) * p.K + k0 + kv);
-            rb[v] = *(const u32x4*)(W + (size_t)min(n0 + r, p.N - 1) * p.K + k0 + kv);
-        }
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-        for (int v = 0; v < NV; v++) {
-            const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
-            *(u32x4*)(&As[buf][r * LD + kv]) = ra[v];
-            *(u32x4*)(&Bs[buf][r * LD + kv]) = rb[v];
-        }
-    };
-
-    f32x4 acc[2][2];
-#pragma unroll
-    for (int i = 0; i < 2; i++)
-#pragma unroll
-        for (int j = 0; j < 2; j++) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int l16 = lane & 15, g = lane >> 4;
-    const int nk = (p.K + KC - 1) / KC;   // K is a multiple of 32; a last partial chunk reads zeros past K
+    u32x4 ra[NVA], rb[NVB];
     const int kfull = p.K / KC;
-    auto gload_chunk = [&](int kc) {
+    auto gload = [&](int kc) {
         if (kc < kfull) {
-            gload(kc * KC);
-        } else {   // partial last chunk: vectors past K are zero
 #pragma unroll
-            for (int v = 0; v < NV; v++) {
+            for (int v = 0; v < NVA; v++) {
                 const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
-                const int k = kc * KC + kv;
+                ra[v] = *(const u32x4*)(A + (size_t)min(m0 + r, p.M - 1) * p.K + kc * KC + kv);
+            }
+#pragma unroll
+            for (int v = 0; v < NVB; v++) {
+                const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
+                rb[v] = *(const u32x4*)(W + (size_t)min(n0 + r, p.N - 1) * p.K + kc * KC + kv);
+            }
+        } else {   // a last partial chunk reads zeros past K
+#pragma unroll
+            for (int v = 0; v < NVA; v++) {
+                const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE, k = kc * KC + kv;
                 ra[v] = k < p.K ? *(const u32x4*)(A + (size_t)min(m0 + r, p.M - 1) * p.K + k) : u32x4{0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int v = 0; v < NVB; v++) {
+                const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE, k = kc * KC + kv;
                 rb[v] = k < p.K ? *(const u32x4*)(W + (size_t)min(n0 + r, p.N - 1) * p.K + k) : u32x4{0, 0, 0, 0};
             }
         }
     };
-    gload_chunk(0);
+    auto lstore = [&](int buf) {
+#pragma unroll
+        for (int v = 0; v < NVA; v++) {
+            const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
+            *(u32x4*)(As + (size_t)buf * BM * LD + r * LD + kv) = ra[v];
+        }
+#pragma unroll
+        for (int v = 0; v < NVB; v++) {
+            const int idx = tid + 256 * v, r = idx / VPR, kv = (idx % VPR) * VE;
+            *(u32x4*)(Bs + (size_t)buf * BN * LD + r * LD + kv) = rb[v];
+        }
+    };
+
+    f32x4 acc[NB][MB];
+#pragma unroll
+    for (int i = 0; i < NB; i++)
+#pragma unroll
+        for (int j = 0; j < MB; j++) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int l16 = lane & 15, g = lane >> 4;
+    const int nk = (p.K + KC - 1) / KC;
+    gload(0);
     lstore(0);
     __syncthreads();
     for (int kc = 0; kc < nk; kc++) {
         const int buf = kc & 1;
-        if (kc + 1 < nk) gload_chunk(kc + 1);
+        if (kc + 1 < nk) gload(kc + 1);
+        const T* Ab = As + (size_t)buf * BM * LD;
+        const T* Bb = Bs + (size_t)buf * BN * LD;
 #pragma unroll
         for (int s = 0; s < KC / KQ; s++) {
             if constexpr (BF16) {
-                bf16x8_t wf[2], xf[2];
+                bf16x8_t wf[NB], xf[MB];
 #pragma unroll
-                for (int i = 0; i < 2; i++) wf[i] = *(const bf16x8_t*)(&Bs[buf][(wn * 32 + 16 * i + l16) * LD + KQ * s + 8 * g]);
+                for (int i = 0; i < NB; i++) wf[i] = *(const bf16x8_t*)(Bb + (wn * 16 * NB + 16 * i + l16) * LD + KQ * s + 8 * g);
 #pragma unroll
-                for (int j = 0; j < 2; j++) xf[j] = *(const bf16x8_t*)(&As[buf][(wm * 32 + 16 * j + l16) * LD + KQ * s + 8 * g]);
+                for (int j = 0; j < MB; j++) xf[j] = *(const bf16x8_t*)(Ab + (wm * 16 * MB + 16 * j + l16) * LD + KQ * s + 8 * g);
 #pragma unroll
-                for (int i = 0; i < 2; i++)
+                for (int i = 0; i < NB; i++)
 #pragma unroll
-                    for (int j = 0; j < 2; j++)
+                    for (int j = 0; j < MB; j++)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], xf[j], acc[i][j], 0, 0, 0);
             } else {
-                f32x4 wf[2], xf[2];
+                f32x4 wf[NB], xf[MB];
 #pragma unroll
-                for (int i = 0; i < 2; i++) wf[i] = *(const f32x4*)(&Bs[buf][(wn * 32 + 16 * i + l16) * LD + KQ * s + 4 * g]);
+                for (int i = 0; i < NB; i++) wf[i] = *(const f32x4*)(Bb + (wn * 16 * NB + 16 * i + l16) * LD + KQ * s + 4 * g);
 #pragma unroll
-                for (int j = 0; j < 2; j++) xf[j] = *(const f32x4*)(&As[buf][(wm * 32 + 16 * j + l16) * LD + KQ * s + 4 * g]);
+                for (int j = 0; j < MB; j++) xf[j] = *(const f32x4*)(Ab + (wm * 16 * MB + 16 * j + l16) * LD + KQ * s + 4 * g);
 #pragma unroll
                 for (int q = 0; q < 4; q++)
 #pragma unroll
-                    for (int i = 0; i < 2; i++)
+                    for (int i = 0; i < NB; i++)
 #pragma unroll
-                        for (int j = 0; j < 2; j++)
+                        for (int j = 0; j < MB; j++)
                             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(wf[i][q], xf[j][q], acc[i][j], 0, 0, 0);
             }
         }
@@ -274,17 +287,58 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p)
         __syncthreads();
     }
 
-    // acc[i][j][r]: row m0 + wm*32 + 16 j + l16, column n0 + wn*32 + 16 i + 4 g + r
+    // acc[i][j][r]: row m0 + wm*16 MB + 16 j + l16, column n0 + wn*16 NB + 16 i + 4 g + r
 #pragma unroll
-    for (int i = 0; i < 2; i++) {
-        const int col = n0 + wn * 32 + 16 * i + 4 * g;
+    for (int i = 0; i < NB; i++) {
+        const int col = n0 + wn * 16 * NB + 16 * i + 4 * g;
         if (col >= p.N) continue;
 #pragma unroll
-        for (int j = 0; j < 2; j++) {
-            const int row = m0 + wm * 32 + 16 * j + l16;
+        for (int j = 0; j < MB; j++) {
+            const int row = m0 + wm * 16 * MB + 16 * j + l16;
             if (row < p.M) epilogue4<BF16, EPI>(p, row, col, acc[i][j], epi_prefetch<EPI>(p, row, col));
         }
     }
+}
+
+template <bool BF16, int MB, int NB>
+constexpr size_t tiled_lds_bytes()
+{
+    constexpr int KC = (MB * NB <= 4 ? 128 : 64) / (BF16 ? 1 : 2);
+    return (size_t)2 * (32 * MB + 32 * NB) * (KC + (BF16 ? 8 : 4)) * (BF16 ? 2 : 4);
+}
+
+template <bool BF16, int EPI, int MB, int NB>
+hipError_t launch_tiled(const GemmParams& p, hipStream_t st)
+{
+    constexpr size_t lds = tiled_lds_bytes<BF16, MB, NB>();
+    static bool set = false;
+    if (lds > 65536 && !set) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<BF16, EPI, MB, NB>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        set = true;
+    }
+    hipLaunchKernelGGL((gemm_kernel<BF16, EPI, MB, NB>), dim3((p.N + 32 * NB - 1) / (32 * NB), (p.M + 32 * MB - 1) / (32 * MB)),
+                       dim3(256), lds, st, p);
+    return hipGetLastError();
+}
+
+// 64 x 64 tiles unless the call has at least DCF_TILE_BIG_BLOCKS of them (then
+// 128 x 128) or DCF_TILE_MID_BLOCKS (then 128 rows x 64 columns).
+#ifndef DCF_TILE_BIG_BLOCKS
+#define DCF_TILE_BIG_BLOCKS 1024
+#endif
+#ifndef DCF_TILE_MID_BLOCKS
+#define DCF_TILE_MID_BLOCKS 256
+#endif
+
+template <bool BF16, int EPI>
+hipError_t launch_tiled_any(const GemmParams& p, hipStream_t st)
+{
+    const long small_blocks = (long)((p.N + 63) / 64) * ((p.M + 63) / 64);
+    if (small_blocks >= DCF_TILE_BIG_BLOCKS) return launch_tiled<BF16, EPI, 4, 4>(p, st);
+    if (small_blocks >= DCF_TILE_MID_BLOCKS) return launch_tiled<BF16, EPI, 4, 2>(p, st);
+    return launch_tiled<BF16, EPI, 2, 2>(p, st);
 }
 
 // Skinny GEMM for few rows (a call of a handful of streams): block = 64 rows
@@ -535,11 +589,9 @@ hipError_t launch_one(const GemmParams& p, hipStream_t st)
         if (e != hipSuccess) return e;
         GemmParams q = p;
         q.ln_h = nullptr;
-        hipLaunchKernelGGL((gemm_kernel<BF16, EPI>), dim3((p.N + 63) / 64, (p.M + 63) / 64), dim3(256), 0, st, q);
-    } else {
-        hipLaunchKernelGGL((gemm_kernel<BF16, EPI>), dim3((p.N + 63) / 64, (p.M + 63) / 64), dim3(256), 0, st, p);
+        return launch_tiled_any<BF16, EPI>(q, st);
     }
-    return hipGetLastError();
+    return launch_tiled_any<BF16, EPI>(p, st);
 }
 
 hipError_t launch_gemm(const GemmParams& p, int epi, int bf16, hipStream_t st)

@@ -128,6 +128,7 @@ FLOW_WORKLOADS = {
     "flow_real_f32_b1": dict(arch=REAL_FLOW_ARCH, dtype="f32", batch=1, chunks=6),
     "flow_real_bf16_b1": dict(arch=REAL_FLOW_ARCH, dtype="bf16", batch=1, chunks=6),
     "flow_real_bf16_b16": dict(arch=REAL_FLOW_ARCH, dtype="bf16", batch=16, chunks=6),
+    "flow_real_bf16_b128": dict(arch=REAL_FLOW_ARCH, dtype="bf16", batch=128, chunks=6),
 }
 
 

@@ -231,3 +231,20 @@ def test_many_rows_take_the_tiled_path_and_match_oracle(dtype):
             e, _ = err_stats(g[b], r)
             assert e <= TOL[dtype], f"stream {b} call {k}: {e:.3e}"
     dec.close()
+
+
+def test_real_shape_batch20_every_tile_size():
+    """20 paper-shaped streams in bf16: 2,240 rows per call, so the MLP-up GEMM
+    takes 128 x 128 tiles, the QKV GEMM 128 x 64 and the others 64 x 64."""
+    a = synth.REAL_FLOW_ARCH
+    blob = synth.make_flow_weights(a, 0)
+    B, P = 20, 64
+    calls = [a["f_call"]]
+    say(f"flow real bf16 B={B} P={P}")
+    dec, outs, mu, prompts = _run_gpu(a, "bf16", blob, B, P, calls)
+    for b in (0, 19):
+        _s, ref = _run_oracle(a, "bf16", blob, b, prompts[b], mu[b], calls)
+        e, er = err_stats(outs[0][b], ref[0])
+        say(f"  stream {b}: max-abs/RMS {e:.3e}, RMS err/RMS {er:.3e}")
+        assert e <= TOL["bf16"], f"stream {b}: {e:.3e}"
+    dec.close()

@@ -21,6 +21,9 @@
 
 namespace dcf {
 
+// Calls of at most this many rows (2 per stream and frame) run the skinny GEMM.
+constexpr int kSkinnyRows = 512;
+
 enum Epi : int {
     E_H = 0,     // h = acc + bias                        (fp32)
     E_QKV = 1,   // q -> q buffer, k, v -> the carry      (operand type)

@@ -528,8 +528,6 @@ __global__ __launch_bounds__(256) void lnmod_kernel(const float* h, void* out, c
         if (k < nv) store1<BF16>(out, (size_t)row * dim + lane + 64 * k, (v[k] - mean) * rs * (1.0f + sc[k]) + sh[k]);
 }
 
-// Rows up to which a call uses the skinny kernel.
-constexpr int kSkinnyRows = 512;
 
 // Skinny shapes: waves and 16-column blocks per block, by operand kind.
 #ifndef DCF_SK_LN_NBLK
@@ -599,10 +597,12 @@ hipError_t launch_gemm(const GemmParams& p, int epi, int bf16, hipStream_t st)
     const bool ln = p.ln_h != nullptr;
 #define DCF_GEMM(B, E, L)                                     \
     if (bf16 == B && epi == E && ln == L) return launch_one<B, E, L>(p, st);
-    DCF_GEMM(1, E_H, false) DCF_GEMM(1, E_QKV, true) DCF_GEMM(1, E_RES, false) DCF_GEMM(1, E_GELU, true)
-    DCF_GEMM(1, E_VEL, true)
-    DCF_GEMM(0, E_H, false) DCF_GEMM(0, E_QKV, true) DCF_GEMM(0, E_RES, false) DCF_GEMM(0, E_GELU, true)
-    DCF_GEMM(0, E_VEL, true)
+    // the LayerNorm operand exists for the GEMMs that follow one; every
+    // GEMM can take a plain operand
+    DCF_GEMM(1, E_H, false) DCF_GEMM(1, E_QKV, true) DCF_GEMM(1, E_QKV, false) DCF_GEMM(1, E_RES, false)
+    DCF_GEMM(1, E_GELU, true) DCF_GEMM(1, E_GELU, false) DCF_GEMM(1, E_VEL, true) DCF_GEMM(1, E_VEL, false)
+    DCF_GEMM(0, E_H, false) DCF_GEMM(0, E_QKV, true) DCF_GEMM(0, E_QKV, false) DCF_GEMM(0, E_RES, false)
+    DCF_GEMM(0, E_GELU, true) DCF_GEMM(0, E_GELU, false) DCF_GEMM(0, E_VEL, true) DCF_GEMM(0, E_VEL, false)
 #undef DCF_GEMM
     return hipErrorInvalidValue;
 }
@@ -630,6 +630,9 @@ constexpr int kMaxSegments = 8;
 // the blocks.  The shape fixes the order of the softmax merge, so results of
 // the two shapes differ in rounding only.
 constexpr int kAttnLd = 68;   // padded row of the merge buffer (floats)
+// Scores in base 2: q.k / sqrt(64) * log2(e), so the softmax's exponentials are
+// plain exp2 (the maximum and the merge work in the same units).
+constexpr float kScoreLog2 = 0.125f * 1.4426950408889634f;
 constexpr int kAttnWideBlocks = 64;   // blocks of 64 queries below which the narrow shape is used
 
 size_t attn_lds_bytes(int nw) { return (size_t)nw * 64 * kAttnLd * 4 + (size_t)2 * nw * 64 * 4; }
@@ -758,20 +761,20 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const AttnParams p)
 #pragma unroll
             for (int r = 0; r < 4; r++) {
                 const bool live = t0 + 16 * j + 4 * g + r < len;
-                st[j][r] = live ? st[j][r] * 0.125f : -INFINITY;
+                st[j][r] = live ? st[j][r] * kScoreLog2 : -INFINITY;
                 mt = fmaxf(mt, st[j][r]);
             }
         mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
         const float mn = fmaxf(m, mt);
-        const float alpha = expf(m - mn);
+        const float alpha = exp2f(m - mn);
         m = mn;
         float ps = 0.f;
 #pragma unroll
         for (int j = 0; j < 2; j++)
 #pragma unroll
             for (int r = 0; r < 4; r++) {
-                st[j][r] = expf(st[j][r] - mn);
+                st[j][r] = exp2f(st[j][r] - mn);
                 ps += st[j][r];
             }
         lsum = lsum * alpha + ps;
@@ -886,7 +889,7 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const AttnParams p)
     for (int db = 0; db < 4; db++) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int w = 0; w < NW; w++) {
-        const float sc = expf(Ms[w * 64 + qq] - mx);
+        const float sc = exp2f(Ms[w * 64 + qq] - mx);
         L += sc * Ls[w * 64 + qq];
 #pragma unroll
         for (int db = 0; db < 4; db++) acc[db] += sc * *(const f32x4*)(Os + ((size_t)w * 64 + qq) * kAttnLd + 16 * db + 4 * g);

@@ -50,6 +50,22 @@ def _run_gpu(arch, dtype, blob, B, P, calls, flags=0, prompts=None, mu=None):
     return dec, outs, mu, prompts
 
 
+def _carry_ok(got, want, dtype):
+    """The carry audit's bound.  fp32: max-abs-error / RMS as for the output.
+    bf16: the carry is stored in bf16, so an element's own rounding is up to
+    2^-9 of its magnitude, which against the RMS alone can approach the
+    output's 2e-2 for the largest keys; the audit bounds the worst element
+    against the largest magnitude and the bulk by the RMS error, both 2e-2."""
+    got = np.asarray(got, dtype=np.float64)
+    if dtype == "f32":
+        e, _ = err_stats(got, want)
+        return e <= TOL["f32"], e
+    d = np.abs(got - want)
+    e1 = d.max() / np.abs(want).max()
+    e2 = np.sqrt(np.mean(d ** 2)) / np.sqrt(np.mean(want ** 2))
+    return max(e1, e2) <= TOL["bf16"], max(e1, e2)
+
+
 def _run_oracle(arch, dtype, blob, b, prompt, mu_b, calls):
     s = oracle.FlowStream(arch, dtype, blob, seed=SEED, key=b)
     s.prompt(*prompt)
@@ -83,8 +99,8 @@ def test_tiny_chunks_match_oracle(dtype):
             got = dec.carry(b, i, l, c, kv)
             want = s.carry(i, l, c, kv)
             assert got.shape == want.shape
-            e, _ = err_stats(got, want)
-            assert e <= TOL[dtype], f"carry {(b, i, l, c, kv)}: {e:.3e}"
+            ok, e = _carry_ok(got, want, dtype)
+            assert ok, f"carry {(b, i, l, c, kv)}: {e:.3e}"
     say(f"  worst max-abs/RMS {worst:.3e}")
     dec.close()
 
@@ -210,8 +226,9 @@ def test_real_shape_matches_oracle(dtype):
         say(f"  call {k}: max-abs/RMS {e:.3e}, RMS err/RMS {er:.3e}")
         assert e <= TOL[dtype], f"call {k}: {e:.3e}"
     for (i, l, c, kv) in [(9, 15, 0, 1), (0, 7, 1, 0)]:
-        e, _ = err_stats(dec.carry(0, i, l, c, kv), s.carry(i, l, c, kv))
-        assert e <= TOL[dtype], f"carry {(i, l, c, kv)}: {e:.3e}"
+        ok, e = _carry_ok(dec.carry(0, i, l, c, kv), s.carry(i, l, c, kv), dtype)
+        say(f"  carry {(i, l, c, kv)}: {e:.3e}")
+        assert ok, f"carry {(i, l, c, kv)}: {e:.3e}"
     dec.close()
 
 

@@ -265,3 +265,24 @@ def test_real_shape_batch20_every_tile_size():
         say(f"  stream {b}: max-abs/RMS {e:.3e}, RMS err/RMS {er:.3e}")
         assert e <= TOL["bf16"], f"stream {b}: {e:.3e}"
     dec.close()
+
+
+def test_host_pointer_mode_equals_device_mode():
+    """DC_HOST_PTRS: host prompts, features and mel (synchronous calls) give the
+    bits of the device-pointer path."""
+    flow = _flow()
+    a = TINY
+    blob = synth.make_flow_weights(a, 1)
+    calls = [a["f_call"], a["f_call"], a["f_chunk"] - 2]
+    _d, dev_out, mu, prompts = _run_gpu(a, "bf16", blob, 2, a["f_prompt"], calls)
+    h = flow.FlowDecoder(a, "bf16", blob, 2, flags=flow.DC_HOST_PTRS, rng_seed=SEED)
+    for b in range(2):
+        h.prompt(b, *prompts[b])
+    p = 0
+    for k, n in enumerate(calls):
+        out = h.decode(np.ascontiguousarray(mu[:, p:p + n]))
+        assert isinstance(out, np.ndarray)
+        assert bits_equal(out, dev_out[k])
+        if n >= a["f_chunk"]:
+            p += a["f_chunk"]
+    h.close()

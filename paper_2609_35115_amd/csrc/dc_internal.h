@@ -7,8 +7,12 @@
 
 namespace dc {
 
-// Element type of a ring buffer or of a conv operand.
-enum Elem : int { kF32 = 0, kBF16 = 1 };
+// Element type of a ring buffer or of a conv operand.  kF16 (IEEE binary16)
+// holds the fp32-accumulated residual stream of a bf16 decoder: values of
+// order one keep 11 significant bits at half the bytes of fp32.
+enum Elem : int { kF32 = 0, kBF16 = 1, kF16 = 2 };
+
+inline int elem_bytes(int e) { return e == kF32 ? 4 : 2; }
 
 // A ring of frames for B streams: frame with absolute index tau of stream b
 // lives at ptr + ((b * R) + (tau mod R)) * C elements.  R >= ctx + frames of
@@ -50,9 +54,9 @@ struct ConvParams {
     int out_elem;
     int out_act;          // apply LeakyReLU before the store
     int u;                // 1 for a conv, stride u for a transposed conv
-    const float* res;     // residual ring (fp32, out geometry) or null
+    const void* res;      // residual ring (element type out_elem, out geometry) or null
     int64_t res_R;
-    const float* mean[3]; // earlier branch results (fp32 rings, out geometry)
+    const void* mean[3];  // earlier branch results (rings of element type out_elem, out geometry)
     int64_t mean_R;
     int n_mean;           // >0: out = (mean[0] + ... + mean[n_mean-1] + z) / (n_mean + 1)
     int B, F;             // streams, input frames of this call
@@ -87,7 +91,7 @@ struct ConvMember {
     const float* bias;
     void* out;
     int64_t out_R;
-    const float* res;
+    const void* res;
     int64_t res_R;
     int k;
 };
@@ -104,26 +108,26 @@ struct TileShape {
     int S() const { return WGK; }
 };
 
-// One fused resblock pair (bf16 operands): h = LeakyReLU(conv_k,d(LeakyReLU(z)) + b1)
-// stays in LDS, and out = z + conv_k,1(h) + b2 (optionally averaged with
+// One fused resblock pair (bf16 operands, fp16 residual stream):
+// h = LeakyReLU(conv_k,d(LeakyReLU(z)) + b1) stays in LDS, and out = z + conv_k,1(h) + b2 (optionally averaged with
 // earlier branch results).  A block owns one stream's frames
 // [seg * seg_t * BM, (seg + 1) * seg_t * BM) x all C channels and walks them
 // in sub-tiles of BM frames, keeping LeakyReLU(z) and h in LDS windows that
 // slide with the sub-tile: the first sub-tile computes the k - 1 frames of h
 // left of the run, later ones only their own BM frames.
 struct PairParams {
-    const float* z;       // fp32 ring: the first conv's input and the residual
+    const uint16_t* z;    // fp16 ring: the first conv's input and the residual
     int64_t z_R;
     const void* w1;       // packed like a conv with channel block C (one partition)
     const float* b1;
     const void* w2;
     const float* b2;
-    float* out;           // fp32 ring
+    uint16_t* out;        // fp16 ring
     int64_t out_R;
     int k, d;             // taps; dilation of the first conv (the second has 1)
     int C;                // channels in and out of both convs
     int NB16;             // C / 16
-    const float* mean[3]; // earlier branch results (fp32 rings, out geometry)
+    const uint16_t* mean[3]; // earlier branch results (fp16 rings, out geometry)
     int64_t mean_R;
     int n_mean;
     int B, F, tiles_t;    // tiles_t = ceil(F / BM) sub-tiles per stream
@@ -134,13 +138,13 @@ struct PairParams {
     float slope;
 };
 struct PairMember {
-    const float* z;
+    const uint16_t* z;
     int64_t z_R;
     const void* w1;
     const float* b1;
     const void* w2;
     const float* b2;
-    float* out;
+    uint16_t* out;
     int64_t out_R;
     int k;
 };

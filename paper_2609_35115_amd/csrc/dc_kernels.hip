@@ -27,6 +27,7 @@ namespace dc {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
 
 // ------------------------------------------------------------------ helpers
 
@@ -50,6 +51,56 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
 }
 
 __device__ __forceinline__ float lrelu(float v, float s) { return v >= 0.0f ? v : v * s; }
+
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
+
+// IEEE binary16 bits -> float (exact), and two floats -> a packed binary16
+// pair (round to nearest even).
+__device__ __forceinline__ float h2f(uint32_t h) { return (float)__builtin_bit_cast(_Float16, (uint16_t)h); }
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi)
+{
+    const f16x2_t v = {(_Float16)lo, (_Float16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// Ring element access by element type (kF32, kBF16 or kF16; a compile-time
+// constant on the hot paths, so the selection folds away): four consecutive
+// elements at a 4-element-aligned offset, or one.
+__device__ __forceinline__ f32x4 load4(const void* base, int elem, size_t off)
+{
+    if (elem == kF32) return *(const f32x4*)((const float*)base + off);
+    const u32x2 w = *(const u32x2*)((const uint16_t*)base + off);
+    if (elem == kF16) return f32x4{h2f(w[0] & 0xffffu), h2f(w[0] >> 16), h2f(w[1] & 0xffffu), h2f(w[1] >> 16)};
+    return f32x4{bf2f(w[0] & 0xffffu), bf2f(w[0] >> 16), bf2f(w[1] & 0xffffu), bf2f(w[1] >> 16)};
+}
+
+__device__ __forceinline__ float load1(const void* base, int elem, size_t off)
+{
+    if (elem == kF32) return ((const float*)base)[off];
+    const uint32_t h = ((const uint16_t*)base)[off];
+    return elem == kF16 ? h2f(h) : bf2f(h);
+}
+
+__device__ __forceinline__ void store4(void* base, int elem, size_t off, f32x4 v)
+{
+    if (elem == kF32) {
+        *(f32x4*)((float*)base + off) = v;
+    } else if (elem == kF16) {
+        *(u32x2*)((uint16_t*)base + off) = u32x2{pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3])};
+    } else {
+        *(u32x2*)((uint16_t*)base + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+    }
+}
+
+__device__ __forceinline__ void store1(void* base, int elem, size_t off, float v)
+{
+    if (elem == kF32)
+        ((float*)base)[off] = v;
+    else if (elem == kF16)
+        ((uint16_t*)base)[off] = __builtin_bit_cast(uint16_t, (_Float16)v);
+    else
+        ((uint16_t*)base)[off] = (uint16_t)f2bf(v);
+}
 
 __device__ __forceinline__ int64_t ring_slot(int64_t tau, int64_t R)
 {
@@ -78,7 +129,7 @@ template <> struct OpT<false> {
     static constexpr int PAD = 4;
 };
 
-// Load 8 channels of one frame as floats (zeros when absent).
+// Load 8 channels of one frame as floats.
 __device__ __forceinline__ void load8(const void* base, int elem, size_t off, float v[8])
 {
     if (elem == kF32) {
@@ -86,6 +137,13 @@ __device__ __forceinline__ void load8(const void* base, int elem, size_t off, fl
         f32x4 a = p[0], b = p[1];
         v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
         v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
+    } else if (elem == kF16) {
+        u32x4 a = *(const u32x4*)((const uint16_t*)base + off);
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            v[2 * e] = h2f(a[e] & 0xffffu);
+            v[2 * e + 1] = h2f(a[e] >> 16);
+        }
     } else {
         u32x4 a = *(const u32x4*)((const uint16_t*)base + off);
 #pragma unroll
@@ -137,7 +195,7 @@ __device__ __forceinline__ void store8_lds(float* dst, const float v[8])
 // slots of its output frame at block row 0, phase 0.
 struct OutRef {
     void* out;
-    const float* res;
+    const void* res;     // element type out_elem, as are the branch-mean rings
     int out_R, res_R;
     int out_s, res_s, mean_s;
     int src_s;   // ring slot of the source samples of that frame
@@ -183,20 +241,17 @@ __device__ __forceinline__ void store_out(const ConvParams& p, int b, const OutR
 {
     // off: output frame offset from the block's base frame; co: output channel
     if (p.src) v = v + src_term1(p, b, slot_add(rs.src_s, off, (int)p.src_R), co);
-    if (rs.res) v = rs.res[((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co] + v;
+    const int oe = p.out_elem;
+    if (rs.res) v = load1(rs.res, oe, ((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co) + v;
     if (p.n_mean) {
         const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean_s, off, (int)p.mean_R)) * p.out_C + co;
-        float x = p.mean[0][mo];
-        for (int i = 1; i < p.n_mean; i++) x = x + p.mean[i][mo];
+        float x = load1(p.mean[0], oe, mo);
+        for (int i = 1; i < p.n_mean; i++) x = x + load1(p.mean[i], oe, mo);
         x = x + v;
         v = x / (float)(p.n_mean + 1);
     }
     if (p.out_act) v = lrelu(v, p.slope);
-    const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co;
-    if (p.out_elem == kF32)
-        ((float*)rs.out)[oo] = v;
-    else
-        ((uint16_t*)rs.out)[oo] = (uint16_t)f2bf(v);
+    store1(rs.out, oe, ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co, v);
 }
 
 // Four consecutive output channels co .. co+3 of one frame (nv < 4 at the
@@ -209,11 +264,12 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Out
         return;
     }
     if (p.src) v = v + src_term4(p, b, slot_add(rs.src_s, off, (int)p.src_R), co);
-    if (rs.res) v = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co) + v;
+    const int oe = p.out_elem;
+    if (rs.res) v = load4(rs.res, oe, ((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co) + v;
     if (p.n_mean) {
         const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean_s, off, (int)p.mean_R)) * p.out_C + co;
-        f32x4 x = *(const f32x4*)(p.mean[0] + mo);
-        for (int i = 1; i < p.n_mean; i++) x = x + *(const f32x4*)(p.mean[i] + mo);
+        f32x4 x = load4(p.mean[0], oe, mo);
+        for (int i = 1; i < p.n_mean; i++) x = x + load4(p.mean[i], oe, mo);
         x = x + v;
         const float J = (float)(p.n_mean + 1);
         v = f32x4{x[0] / J, x[1] / J, x[2] / J, x[3] / J};
@@ -222,14 +278,7 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Out
 #pragma unroll
         for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
     }
-    const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co;
-    if (p.out_elem == kF32) {
-        *(f32x4*)((float*)rs.out + oo) = v;
-    } else {
-        typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
-        u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-        *(u32x2*)((uint16_t*)rs.out + oo) = h;
-    }
+    store4(rs.out, oe, ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co, v);
 }
 
 // Operand rows [t0 - halo, t0 - halo + rows) of channel block cb of stream b,
@@ -289,10 +338,10 @@ __device__ __forceinline__ void load_bias(const ConvParams& p, const float* bias
 // are the MFMA A operand and the frames the B operand, so lane l holds output
 // channels 4*(l/16) .. +3 of frame l%16 of each block: four consecutive
 // channels of one frame, stored as one vector.
-template <int MB, int NB>
-__device__ __forceinline__ void store_tile(const ConvParams& p, const OutRef& rs, const f32x4 (&acc)[MB][NB],
-                                           const f32x4 (&bias)[NB], int b, int t0, int n0, int row0, int colblk0,
-                                           int lane)
+template <int MB, int NB, int OE>
+__device__ __forceinline__ void store_tile_e(const ConvParams& p, const OutRef& rs, const f32x4 (&acc)[MB][NB],
+                                             const f32x4 (&bias)[NB], int b, int t0, int n0, int row0, int colblk0,
+                                             int lane)
 {
     const int fl = lane & 15, cg = (lane >> 4) * 4;
     int rp[NB], co[NB], nv[NB];
@@ -318,8 +367,8 @@ __device__ __forceinline__ void store_tile(const ConvParams& p, const OutRef& rs
             const int off = off_of(mb);
 #pragma unroll
             for (int nb = 0; nb < NB; nb++)
-                q[nb] = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(rs.res_s, off + rp[nb], rs.res_R)) *
-                                                     p.out_C + co[nb]);
+                q[nb] = load4(rs.res, OE, ((size_t)b * rs.res_R + slot_add(rs.res_s, off + rp[nb], rs.res_R)) *
+                                              p.out_C + co[nb]);
         };
         if (rs.res) issue(0, ld[0]);
 #pragma unroll
@@ -337,14 +386,8 @@ __device__ __forceinline__ void store_tile(const ConvParams& p, const OutRef& rs
                     for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
                 }
                 if (!live) continue;
-                const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off + rp[nb], rs.out_R)) * p.out_C + co[nb];
-                if (p.out_elem == kF32) {
-                    *(f32x4*)((float*)rs.out + oo) = v;
-                } else {
-                    typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
-                    u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-                    *(u32x2*)((uint16_t*)rs.out + oo) = h;
-                }
+                store4(rs.out, OE, ((size_t)b * rs.out_R + slot_add(rs.out_s, off + rp[nb], rs.out_R)) * p.out_C + co[nb],
+                       v);
             }
         }
     } else {
@@ -360,6 +403,20 @@ __device__ __forceinline__ void store_tile(const ConvParams& p, const OutRef& rs
             }
         }
     }
+}
+
+// store_tile_e for the output's element type (fp32 operands write fp32 only).
+template <bool BF16, int MB, int NB>
+__device__ __forceinline__ void store_tile(const ConvParams& p, const OutRef& rs, const f32x4 (&acc)[MB][NB],
+                                           const f32x4 (&bias)[NB], int b, int t0, int n0, int row0, int colblk0,
+                                           int lane)
+{
+    if (!BF16 || p.out_elem == kF32)
+        store_tile_e<MB, NB, kF32>(p, rs, acc, bias, b, t0, n0, row0, colblk0, lane);
+    else if (p.out_elem == kF16)
+        store_tile_e<MB, NB, kF16>(p, rs, acc, bias, b, t0, n0, row0, colblk0, lane);
+    else
+        store_tile_e<MB, NB, kBF16>(p, rs, acc, bias, b, t0, n0, row0, colblk0, lane);
 }
 
 template <bool BF16, int MB, int NB, int WGM, int WGN, int WGK, int KCH>
@@ -430,8 +487,8 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
             if (e_pre && rs.res) {
                 const int rpn = p.u == 1 ? 0 : e_n4 / p.out_C;
                 const int res_s = (int)ring_slot((tau0 + t0) * p.u, rs.res_R);
-                e_res = *(const f32x4*)(rs.res + ((size_t)b * rs.res_R + slot_add(res_s, e_tl * p.u + rpn, rs.res_R)) *
-                                                     p.out_C + e_n4 - rpn * p.out_C);
+                e_res = load4(rs.res, p.out_elem, ((size_t)b * rs.res_R + slot_add(res_s, e_tl * p.u + rpn, rs.res_R)) *
+                                                      p.out_C + e_n4 - rpn * p.out_C);
             }
         }
     }
@@ -634,7 +691,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
     if constexpr (WGK == 1) {
         f32x4 bias[NB];
         load_bias<NB>(p, bias_ptr, n0, wn * NB, lane, bias);
-        store_tile<MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
+        store_tile<BF16, MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
     } else {
         // partial sums of every partition through LDS, added in partition order
         __syncthreads();
@@ -662,14 +719,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
 #pragma unroll
                     for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
                 }
-                const size_t oo = ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co;
-                if (p.out_elem == kF32) {
-                    *(f32x4*)((float*)rs.out + oo) = v;
-                } else {
-                    typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
-                    u32x2 h = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-                    *(u32x2*)((uint16_t*)rs.out + oo) = h;
-                }
+                store4(rs.out, p.out_elem, ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co, v);
             } else {
                 store_out4(p, b, rs, off, co, v, p.N - e_n4 < 4 ? p.N - e_n4 : 4);
             }
@@ -841,7 +891,7 @@ __global__ __launch_bounds__(256, 2) void wconv_kernel(const ConvGroup g)
     rs.res_s = rs.res ? (int)ring_slot(tau_out0, rs.res_R) : 0;
     rs.mean_s = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
     rs.src_s = p.src ? (int)ring_slot(tau_out0, p.src_R) : 0;
-    store_tile<MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
+    store_tile<true, MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
 }
 
 // ------------------------------------------------------------- tile table
@@ -1012,7 +1062,7 @@ hipError_t launch_conv(int v, bool bf16, const ConvParams* ps, int count, hipStr
 // Per sub-tile: the first conv writes h for its BM frames (the first sub-tile
 // of the segment also the 16 frames left of it, of which the second conv reads
 // the last k - 1); after a barrier the second conv reads Hs and the epilogue
-// adds b2, the fp32 residual z and the branch mean; then the next sub-tile's
+// adds b2, the residual z and the branch mean; then the next sub-tile's
 // BM z frames go to Zs, replacing frames older than any the next first conv
 // reads.  Both convs use one K partition and a channel block of all C
 // channels, i.e. the arithmetic of the unfused launches with those
@@ -1022,13 +1072,13 @@ template <int MB, int NB, int WGM, int WGN, int KCH, int LZ, int LH>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void pair_kernel(const PairGroup g)
 {
     const PairParams& p = g.p;
-    const float* z = p.z;
+    const uint16_t* z = p.z;
     int z_R = (int)p.z_R;
     const void* w1p = p.w1;
     const float* b1 = p.b1;
     const void* w2p = p.w2;
     const float* b2 = p.b2;
-    float* out = p.out;
+    uint16_t* out = p.out;
     int out_R = (int)p.out_R;
     int k = p.k;
     if (blockIdx.z > 0) {
@@ -1066,7 +1116,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     const int64_t tau0 = p.clock[0] * p.in_fpt;
     const int64_t start_f = p.start[b] * p.in_fpt;   // this stream's first frame since its reset
     const int fl = lane & 15, cg = (lane >> 4) * 4;
-    const float* zb = z + (size_t)b * z_R * C;
+    const uint16_t* zb = z + (size_t)b * z_R * C;
     const int zs0 = (int)ring_slot(tau0 + f0 - H, z_R);   // ring slot of frame f0 - H
     // ring slot of frame f of this chunk, for f0 - H <= f < f0 - H + z_R
     auto zslot = [&](int f) { return slot_add(zs0, f - (f0 - H), z_R); };
@@ -1078,12 +1128,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             const int f = fa + r;
             float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
             if (f < p.F) {
-                const f32x4* q = (const f32x4*)(zb + (size_t)zslot(f) * C + c8);
-                const f32x4 a0 = q[0], a1 = q[1];
+                const u32x4 a = *(const u32x4*)(zb + (size_t)zslot(f) * C + c8);
 #pragma unroll
                 for (int e = 0; e < 4; e++) {
-                    x[e] = lrelu(a0[e], p.slope);
-                    x[4 + e] = lrelu(a1[e], p.slope);
+                    x[2 * e] = lrelu(h2f(a[e] & 0xffffu), p.slope);
+                    x[2 * e + 1] = lrelu(h2f(a[e] >> 16), p.slope);
                 }
             }
             store8_lds(Zs + (f & ZM) * LDW + c8, x);
@@ -1215,7 +1264,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         };
         run_taps(reinterpret_cast<const Frag*>(w2p), tap2, nothing);
 
-        // ---- epilogue: bias, residual z, branch mean; fp32 through the output ring
+        // ---- epilogue: bias, residual z, branch mean; fp16 through the output ring
         const int out_s = (int)ring_slot(tau0 + t, out_R);
         const int mean_s = p.n_mean ? (int)ring_slot(tau0 + t, p.mean_R) : 0;
         // the residual loads of row block mb + 1 are issued before row block mb
@@ -1228,14 +1277,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         auto store = [&](int mb, int nb, f32x4 v) {
             const int tl = wm * 16 * MB + mb * 16 + fl;
             if (t + tl < f1)
-                *(f32x4*)(out + ((size_t)b * out_R + slot_add(out_s, tl, out_R)) * C + (nblk0 + nb) * 16 + cg) = v;
+                store4(out, kF16, ((size_t)b * out_R + slot_add(out_s, tl, out_R)) * C + (nblk0 + nb) * 16 + cg, v);
         };
         if (p.n_mean == 0) {
             f32x4 ld[2][NB];
             auto issue = [&](int mb, f32x4 (&q)[NB]) {
-                const float* zr = zb + (size_t)zslot(t + tl_of(mb)) * C + nblk0 * 16 + cg;
+                const uint16_t* zr = zb + (size_t)zslot(t + tl_of(mb)) * C + nblk0 * 16 + cg;
 #pragma unroll
-                for (int nb = 0; nb < NB; nb++) q[nb] = *(const f32x4*)(zr + nb * 16);
+                for (int nb = 0; nb < NB; nb++) q[nb] = load4(zr, kF16, nb * 16);
             };
             issue(0, ld[0]);
 #pragma unroll
@@ -1249,15 +1298,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
 #pragma unroll
             for (int mb = 0; mb < MB; mb++) {
                 const int tl = tl_of(mb);
-                const float* zr = zb + (size_t)zslot(t + tl) * C + nblk0 * 16 + cg;
+                const uint16_t* zr = zb + (size_t)zslot(t + tl) * C + nblk0 * 16 + cg;
                 const size_t mo = ((size_t)b * mean_R + slot_add(mean_s, tl, mean_R)) * C + nblk0 * 16 + cg;
                 f32x4 r[NB], m[3][NB];
 #pragma unroll
                 for (int nb = 0; nb < NB; nb++) {
-                    r[nb] = *(const f32x4*)(zr + nb * 16);
+                    r[nb] = load4(zr, kF16, nb * 16);
 #pragma unroll
                     for (int i = 0; i < 3; i++)
-                        if (i < p.n_mean) m[i][nb] = *(const f32x4*)(p.mean[i] + mo + nb * 16);
+                        if (i < p.n_mean) m[i][nb] = load4(p.mean[i], kF16, mo + nb * 16);
                 }
 #pragma unroll
                 for (int nb = 0; nb < NB; nb++) {

@@ -19,6 +19,7 @@
 #include <algorithm>
 #include <chrono>
 #include <cmath>
+#include <limits>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -79,6 +80,15 @@ float host_bf2f(uint16_t h)
     float f;
     std::memcpy(&f, &u, 4);
     return f;
+}
+
+// IEEE binary16 bits -> float.
+float host_h2f(uint16_t h)
+{
+    const int e = (h >> 10) & 31, m = h & 1023;
+    const float sgn = (h & 0x8000) ? -1.f : 1.f;
+    if (e == 31) return m ? std::numeric_limits<float>::quiet_NaN() : sgn * std::numeric_limits<float>::infinity();
+    return sgn * std::ldexp((float)(e ? (1024 + m) : m), (e ? e : 1) - 25);
 }
 
 float round_param(float x, bool bf16) { return bf16 ? host_bf2f(host_f2bf(x)) : x; }
@@ -429,6 +439,9 @@ static void build_network(dc_state* s)
     const dc_cfg& c = s->cfg;
     const bool bf = c.dtype == DC_BF16;
     const int opE = bf ? kBF16 : kF32;
+    // the stages' residual stream (upsample output, resblock sums, stage
+    // output): fp16 next to bf16 operands, fp32 otherwise
+    const int opR = bf ? kF16 : kF32;
     size_t off = (size_t)c.vocab * c.embed;  // blob float offset after the embedding
     auto conv = [&](const std::string& name, int in, int out, int Ci, int N, int k, int d, int level) -> ConvOp& {
         ConvOp op;
@@ -468,7 +481,7 @@ static void build_network(dc_state* s)
         const std::string sn = "s" + std::to_string(st);
         const bool src_here = c.n_harmonics > 0 && st == c.n_stages - 1;
         if (src_here) s->ring_src = add_ring(s, "src", c.hop, kF32, st + 1);   // ctx 0: one call's samples
-        const int Y = add_ring(s, sn + ".y", co, kF32, st + 1);
+        const int Y = add_ring(s, sn + ".y", co, opR, st + 1);
         {
             ConvOp op;
             op.name = sn + ".up";
@@ -520,9 +533,9 @@ static void build_network(dc_state* s)
                 const bool last = i == c.n_dil - 1;
                 int Z;
                 if (last && j == c.n_rb - 1)
-                    Z = X = add_ring(s, sn + ".x", co, kF32, st + 1);
+                    Z = X = add_ring(s, sn + ".x", co, opR, st + 1);
                 else
-                    Z = add_ring(s, pn + ".z" + std::to_string(i), co, kF32, st + 1);
+                    Z = add_ring(s, pn + ".z" + std::to_string(i), co, opR, st + 1);
                 ConvOp& op = conv(pn + ".d" + std::to_string(i) + ".c2", H, Z, co, co, kj, 1, st + 1);
                 op.res = zin;
                 op.stage = st;
@@ -708,12 +721,12 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
     p.out_act = op.out_act;
     p.u = op.u;
     if (op.res >= 0) {
-        p.res = (const float*)s->rings[op.res].ptr;
+        p.res = s->rings[op.res].ptr;
         p.res_R = s->rings[op.res].R;
     }
     p.n_mean = op.n_mean;
     for (int m = 0; m < op.n_mean; m++) {
-        p.mean[m] = (const float*)s->rings[op.mean[m]].ptr;
+        p.mean[m] = s->rings[op.mean[m]].ptr;
         p.mean_R = s->rings[op.mean[m]].R;
     }
     p.B = c.batch;
@@ -770,13 +783,13 @@ static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n
     const Ring& z = s->rings[c1.in];
     const Ring& o = s->rings[c2.out];
     PairParams p{};
-    p.z = (const float*)z.ptr;
+    p.z = (const uint16_t*)z.ptr;
     p.z_R = z.R;
     p.w1 = s->arena + c1.w_off;
     p.b1 = (const float*)(s->arena + c1.b_off);
     p.w2 = s->arena + c2.w_off;
     p.b2 = (const float*)(s->arena + c2.b_off);
-    p.out = (float*)o.ptr;
+    p.out = (uint16_t*)o.ptr;
     p.out_R = o.R;
     p.k = c1.k;
     p.d = c1.d;
@@ -784,7 +797,7 @@ static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n
     p.NB16 = c1.NB16;
     p.n_mean = c2.n_mean;
     for (int m = 0; m < c2.n_mean; m++) {
-        p.mean[m] = (const float*)s->rings[c2.mean[m]].ptr;
+        p.mean[m] = (const uint16_t*)s->rings[c2.mean[m]].ptr;
         p.mean_R = s->rings[c2.mean[m]].R;
     }
     p.B = c.batch;
@@ -933,7 +946,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
         Ring& r = s->rings[i];
         r.ctx = s->ring_onchip[i] ? 0 : s->ring_ctx[i];
         r.R = s->ring_onchip[i] ? 0 : r.ctx + (int64_t)c.max_tokens * s->fpt[r.level];
-        const size_t es = r.elem == kBF16 ? 2 : 4;
+        const size_t es = elem_bytes(r.elem);
         r.ptr = (void*)take((size_t)c.batch * r.R * r.C * es);  // offset for now
         carry += (int64_t)c.batch * r.ctx * r.C * es;
     }
@@ -1202,7 +1215,7 @@ dc_status dc_reset_stream(dc_state* s, int32_t b)
     if (!s) return DC_EINVAL;
     if (b < 0 || b >= s->cfg.batch) return fail(s, DC_EINVAL, "stream index out of range");
     for (const Ring& r : s->rings) {
-        const size_t es = r.elem == kBF16 ? 2 : 4;
+        const size_t es = elem_bytes(r.elem);
         const size_t per = (size_t)r.R * r.C * es;
         hipError_t e = hipMemsetAsync((char*)r.ptr + (size_t)b * per, 0, per, s->stream);
         if (e != hipSuccess) return device_fail(s, e, "dc_reset_stream");
@@ -1270,7 +1283,7 @@ uint64_t layout_fingerprint(const dc_state* s)
 size_t snapshot_bytes(const dc_state* s)
 {
     size_t n = sizeof(SnapHeader);
-    for (const Ring& r : s->rings) n += (size_t)r.ctx * r.C * (r.elem == kBF16 ? 2 : 4);
+    for (const Ring& r : s->rings) n += (size_t)r.ctx * r.C * (elem_bytes(r.elem));
     n += (size_t)(s->cfg.n_harmonics > 0 ? s->cfg.n_harmonics + 1 : 0) * sizeof(double);
     return n;
 }
@@ -1279,7 +1292,7 @@ size_t snapshot_bytes(const dc_state* s)
 // runs where the ring wraps.
 hipError_t ring_frames(const dc_state* s, const Ring& r, int b, int64_t f0, int nf, char* host, bool to_host)
 {
-    const size_t es = r.elem == kBF16 ? 2 : 4, row = (size_t)r.C * es;
+    const size_t es = elem_bytes(r.elem), row = (size_t)r.C * es;
     int64_t slot = f0 % r.R;
     if (slot < 0) slot += r.R;
     int done = 0;
@@ -1321,7 +1334,7 @@ dc_status dc_carry_export(dc_state* s, int32_t b, void* host_out, size_t bytes)
         const int64_t end = s->clock_host * s->fpt[r.level];
         e = ring_frames(s, r, b, end - r.ctx, r.ctx, out + off, true);
         if (e != hipSuccess) return device_fail(s, e, "dc_carry_export");
-        off += (size_t)r.ctx * r.C * (r.elem == kBF16 ? 2 : 4);
+        off += (size_t)r.ctx * r.C * (elem_bytes(r.elem));
     }
     if (s->cfg.n_harmonics > 0) {
         // the phases of the next call's first f0 frame: the slot tagged with it
@@ -1355,7 +1368,7 @@ dc_status dc_carry_import(dc_state* s, int32_t b, const void* host_in, size_t by
     if (e != hipSuccess) return device_fail(s, e, "dc_carry_import");
     // the stream's rings start clean, then take the carried frames
     for (const Ring& r : s->rings) {
-        const size_t per = (size_t)r.R * r.C * (r.elem == kBF16 ? 2 : 4);
+        const size_t per = (size_t)r.R * r.C * (elem_bytes(r.elem));
         if (per) e = hipMemset((char*)r.ptr + (size_t)b * per, 0, per);
         if (e != hipSuccess) return device_fail(s, e, "dc_carry_import");
     }
@@ -1366,7 +1379,7 @@ dc_status dc_carry_import(dc_state* s, int32_t b, const void* host_in, size_t by
         const int64_t end = s->clock_host * s->fpt[r.level];
         e = ring_frames(s, r, b, end - r.ctx, r.ctx, const_cast<char*>(in + off), false);
         if (e != hipSuccess) return device_fail(s, e, "dc_carry_import");
-        off += (size_t)r.ctx * r.C * (r.elem == kBF16 ? 2 : 4);
+        off += (size_t)r.ctx * r.C * (elem_bytes(r.elem));
     }
     if (s->cfg.n_harmonics > 0) {
         const int H1 = s->cfg.n_harmonics + 1;
@@ -1412,7 +1425,7 @@ dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32
     if (frame0 < end - r.R || frame0 + nframes > end) return fail(s, DC_ERANGE, "frames not held by the ring");
     hipError_t e = hipStreamSynchronize(s->stream);
     if (e != hipSuccess) return device_fail(s, e, "dc_tap_read");
-    const size_t es = r.elem == kBF16 ? 2 : 4;
+    const size_t es = elem_bytes(r.elem);
     std::vector<char> row((size_t)r.C * es);
     for (int32_t f = 0; f < nframes; f++) {
         int64_t slot = (frame0 + f) % r.R;
@@ -1422,7 +1435,9 @@ dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32
         if (e != hipSuccess) return device_fail(s, e, "dc_tap_read copy");
         for (int ch = 0; ch < r.C; ch++)
             host_out[(size_t)f * r.C + ch] =
-                r.elem == kBF16 ? host_bf2f(((uint16_t*)row.data())[ch]) : ((float*)row.data())[ch];
+                r.elem == kF32    ? ((float*)row.data())[ch]
+                : r.elem == kF16 ? host_h2f(((uint16_t*)row.data())[ch])
+                                 : host_bf2f(((uint16_t*)row.data())[ch]);
     }
     return DC_OK;
 }
@@ -1446,7 +1461,7 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
     switch (la.kind) {
     case L_EMBED: {
         const Ring& E = s->rings[s->ring_E];
-        const double es = E.elem == kBF16 ? 2 : 4;
+        const double es = elem_bytes(E.elem);
         const double F = (double)n * c.frames_per_token;
         set("dc::embed_kernel");
         out->bytes = B * n * 4 + B * n * c.embed * es + B * F * c.embed * es;
@@ -1472,10 +1487,10 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
             out->depth += (int64_t)op.k * op.Ci;
             out->flops += 2.0 * B * F * op.N * op.Ci * op.k;
             const double wes = op.bf16 ? 2 : 4;
-            const double ies = in.elem == kBF16 ? 2 : 4, oes = o.elem == kBF16 ? 2 : 4;
+            const double ies = elem_bytes(in.elem), oes = elem_bytes(o.elem);
             const double Fo = F * op.u;
             out->bytes += (double)op.N * op.Ci * op.k * wes + B * (F + (op.k - 1) * op.d) * op.Ci * ies +
-                          B * Fo * o.C * oes + (op.res >= 0 ? B * Fo * o.C * 4 : 0) + op.n_mean * B * Fo * o.C * 4;
+                          B * Fo * o.C * oes + (op.res >= 0 ? B * Fo * o.C * oes : 0) + op.n_mean * B * Fo * o.C * oes;
         }
         break;
     }
@@ -1484,7 +1499,7 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
         set("dc::pair_kernel<" + std::to_string(t.MB) + ", " + std::to_string(t.NB) + ", " + std::to_string(t.WGM) +
             ", " + std::to_string(t.WGN) + ", " + std::to_string(t.KCH) + ", " + std::to_string(t.LZ) + ", " +
             std::to_string(t.LH) + ">");
-        for (int ci : la.convs) {   // both convs' work; z once, the output once, both weights
+        for (int ci : la.convs) {   // both convs' work; z once, the output once, both weights (fp16 rings)
             const ConvOp& a = s->convs[ci];
             const ConvOp& b2 = s->convs[a.partner];
             const double F = (double)n * s->fpt[a.level_in];
@@ -1493,8 +1508,8 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
             out->depth += (int64_t)a.k * a.Ci + (int64_t)b2.k * b2.Ci;
             out->flops += 2.0 * B * F * a.N * a.Ci * a.k + 2.0 * B * F * b2.N * b2.Ci * b2.k;
             out->bytes += 2.0 * ((double)a.N * a.Ci * a.k + (double)b2.N * b2.Ci * b2.k) +
-                          B * (F + (a.k - 1) * a.d + (a.k - 1)) * a.Ci * 4 + B * F * b2.N * 4 +
-                          b2.n_mean * B * F * b2.N * 4;
+                          B * (F + (a.k - 1) * a.d + (a.k - 1)) * a.Ci * 2 + B * F * b2.N * 2 +
+                          b2.n_mean * B * F * b2.N * 2;
         }
         break;
     }

@@ -1138,6 +1138,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             store8_lds(Zs + (f & ZM) * LDW + c8, x);
         }
     };
+    // the same for the BM frames of the next sub-tile in two halves: fetch
+    // issues the loads (frames past F read frame F - 1, so every lane loads
+    // and nothing waits on a branch), commit converts and writes Zs after
+    // the second conv has run in their shadow.  At C = 128 the registers the
+    // loads hold would spill: there the next frames are staged after the
+    // epilogue instead.
+    constexpr bool PF = KCH <= 2;
+    constexpr int PV = BM * VPR / 256;
+    static_assert(BM * VPR % 256 == 0, "pair staging vectors");
+    auto fetch = [&](int fa, u32x4 (&q)[PV]) {
+#pragma unroll
+        for (int i = 0; i < PV; i++) {
+            const int v = tid + 256 * i, r = v / VPR, c8 = (v - r * VPR) * 8;
+            const int f = min(fa + r, p.F - 1);
+            q[i] = *(const u32x4*)(zb + (size_t)zslot(f) * C + c8);
+        }
+    };
+    auto commit = [&](int fa, const u32x4 (&q)[PV]) {
+#pragma unroll
+        for (int i = 0; i < PV; i++) {
+            const int v = tid + 256 * i, r = v / VPR, c8 = (v - r * VPR) * 8;
+            const int f = fa + r;
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                x[2 * e] = f < p.F ? lrelu(h2f(q[i][e] & 0xffffu), p.slope) : 0.f;
+                x[2 * e + 1] = f < p.F ? lrelu(h2f(q[i][e] >> 16), p.slope) : 0.f;
+            }
+            store8_lds(Zs + (f & ZM) * LDW + c8, x);
+        }
+    };
     // weight fragments of tap j (channel block of all C channels, one partition)
     const int nblk0 = wn * NB;
     // both convs' biases of this wave's columns, loaded once for the whole run
@@ -1230,6 +1261,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         else
             conv1(std::integral_constant<int, MB>{}, t + wm * 16 * MB);
         __syncthreads();
+        // the next sub-tile's z frames, loaded while the second conv runs
+        u32x4 zq[PV];
+        if constexpr (PF) {
+            if (t + BM < f1) fetch(t + BM, zq);
+        }
 
         // ---- second conv: output frames t + wm*16*MB + 16 mb + fl, h from Hs
         f32x4 acc[MB][NB];
@@ -1320,9 +1356,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
                 }
             }
         }
-        // the next sub-tile's z frames (the frames they replace are older than
-        // any the next first conv reads)
-        if (t + BM < f1) stage(t + BM, BM);
+        // the next sub-tile's z frames to Zs (the frames they replace are
+        // older than any the next first conv reads)
+        if (t + BM < f1) {
+            if constexpr (PF)
+                commit(t + BM, zq);
+            else
+                stage(t + BM, BM);
+        }
         __syncthreads();
     }
 }

@@ -284,6 +284,7 @@ FLOW_GEMM = {   # role -> (epilogue, LayerNorm operand) of the GEMM that runs it
     "gemm:fc1": (3, True), "gemm:out": (4, True),
 }
 SKINNY_ROWS = 512   # calls of at most this many rows (2 per stream and frame) run the skinny GEMM
+SKINNY_LN = (8, 2, 1)   # LayerNorm-operand skinny GEMM: waves, 16-column blocks, 16-row blocks per block
 
 
 ATTN_WIDE_BLOCKS = 64   # (stream, branch, head) x 64-query blocks from which attention takes its wide shape
@@ -304,8 +305,11 @@ def flow_kernel_name(role: str, dtype: str, rows: int, attn_blocks: int = 0, arc
                 "gemm:fc1": (arch["mlp"] if arch else 2048, D), "gemm:fc2": (D, arch["mlp"] if arch else 2048),
                 "gemm:out": (arch["n_mel"] if arch else 80, D)}[role]
         if rows <= SKINNY_ROWS:
-            waves = 8 if (not ln and K >= 1024) else 4
-            return f"dcf::skinny_kernel<{b}, {epi}, {'true' if ln else 'false'}, {waves}, 1>"
+            if ln:
+                waves, nblk, rb = SKINNY_LN if K % (16 * SKINNY_LN[0] // SKINNY_LN[2]) == 0 else (4, SKINNY_LN[1], 1)
+            else:
+                waves, nblk, rb = (8 if K >= 1024 else 4), 1, 1
+            return f"dcf::skinny_kernel<{b}, {epi}, {'true' if ln else 'false'}, {waves}, {nblk}, {rb}>"
         blocks = ((N + 63) // 64) * ((rows + 63) // 64)
         tile = "4, 4" if blocks >= TILE_BIG_BLOCKS else "4, 2" if blocks >= TILE_MID_BLOCKS else "2, 2"
         return f"dcf::gemm_kernel<{b}, {epi}, {tile}>"

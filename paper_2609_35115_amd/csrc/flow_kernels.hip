@@ -341,30 +341,32 @@ hipError_t launch_tiled_any(const GemmParams& p, hipStream_t st)
     return launch_tiled<BF16, EPI, 2, 2>(p, st);
 }
 
-// Skinny GEMM for few rows (a call of a handful of streams): block = 64 rows
-// x 16 NBLK columns, NW waves that split K into contiguous ranges of whole
+// Skinny GEMM for few rows (a call of a handful of streams): block = 16 RB
+// rows x 16 NBLK columns, NW waves that split K into contiguous ranges of whole
 // MFMA steps; each wave loads its weight and activation fragments for 4
 // steps at once, so a block costs few memory round trips.  The weight loads
 // of the first batch and the epilogue's operands are issued before anything
 // waits.  The partial tiles are summed through LDS in wave order.  With a
-// LayerNorm operand the block first normalises its 64 rows into LDS
+// LayerNorm operand the block first normalises its 16 RB rows into LDS
 // (operand type, all K).
-template <bool BF16, int EPI, bool LN, int NW, int NBLK>
+template <bool BF16, int EPI, bool LN, int NW, int NBLK, int RB>
 __global__ __launch_bounds__(64 * NW) void skinny_kernel(const GemmParams p)
 {
     using T = typename std::conditional<BF16, uint16_t, float>::type;
     constexpr int KQ = BF16 ? 32 : 16;               // K of one MFMA step group (one 16-byte load per lane)
     constexpr int BATCH = 4;
     constexpr int PAD = BF16 ? 8 : 4;
-    constexpr int NPAIR = 4 * NBLK;                  // (column block, row block) output tiles of 16 x 16
+    constexpr int NPAIR = RB * NBLK;                 // (column block, row block) output tiles of 16 x 16
+    constexpr int TPR = 4 * NW / RB;                 // LayerNorm: threads per row
+    static_assert(TPR >= 1 && (TPR & (TPR - 1)) == 0 && TPR * 16 * RB == 64 * NW, "skinny shape");
     constexpr int PPW = (NPAIR + NW - 1) / NW;       // tiles each wave finalises
     extern __shared__ __align__(16) unsigned char smem[];
-    T* As = (T*)smem;                                 // LN: [64][K + PAD], then scale and shift
+    T* As = (T*)smem;                                 // LN: [16 RB][K + PAD], then scale and shift
     f32x4* red = (f32x4*)smem;                        // after the main loop: [NW waves][NPAIR][64 lanes]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, g = lane >> 4;
-    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 16 * NBLK;
+    const int m0 = blockIdx.y * 16 * RB, n0 = blockIdx.x * 16 * NBLK;
     const int LDA = p.K + PAD;
     const T* A = (const T*)p.A;
     const T* W = (const T*)p.W;
@@ -385,23 +387,23 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(const GemmParams p)
     EpiPre pre[PPW];
 #pragma unroll
     for (int u = 0; u < PPW; u++) {
-        const int pp = min(wave + u * NW, NPAIR - 1), j = pp >> 2, i = pp & 3;
+        const int pp = min(wave + u * NW, NPAIR - 1), j = pp / RB, i = pp % RB;
         pre[u] = epi_prefetch<EPI>(p, min(m0 + 16 * i + l16, p.M - 1), min(n0 + 16 * j + 4 * g, p.N - 4));
     }
 
     if constexpr (LN) {
-        float* ss = (float*)(smem + (size_t)64 * LDA * sizeof(T));
+        float* ss = (float*)(smem + (size_t)16 * RB * LDA * sizeof(T));
         for (int k4 = tid; k4 < (p.K >> 2); k4 += 64 * NW) {
             ((f32x4*)ss)[k4] = ((const f32x4*)p.ln_scale)[k4];
             ((f32x4*)(ss + p.K))[k4] = ((const f32x4*)p.ln_shift)[k4];
         }
-        // NW threads per row, K / NW columns each
-        f32x4 v[128 / NW];
-        const LnRow st = ln_row_stats<NW, 128 / NW>(p.ln_h, p.M, p.K, m0, v);
+        // TPR threads per row, K / TPR columns each
+        f32x4 v[128 / TPR];
+        const LnRow st = ln_row_stats<TPR, 128 / TPR>(p.ln_h, p.M, p.K, m0, v);
         __syncthreads();
-        const int r = tid / NW, kq = p.K / NW, nv = kq >> 2, kb = (tid % NW) * kq;
+        const int r = tid / TPR, kq = p.K / TPR, nv = kq >> 2, kb = (tid % TPR) * kq;
 #pragma unroll
-        for (int i = 0; i < 128 / NW; i++)
+        for (int i = 0; i < 128 / TPR; i++)
             if (i < nv) {
                 const int k = kb + 4 * i;
                 const f32x4 sc = *(const f32x4*)(ss + k), sh = *(const f32x4*)(ss + p.K + k);
@@ -413,20 +415,20 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(const GemmParams p)
         __syncthreads();
     }
 
-    int xr[4];
+    int xr[RB];
 #pragma unroll
-    for (int i = 0; i < 4; i++) xr[i] = min(m0 + 16 * i + l16, p.M - 1);
-    f32x4 acc[NBLK][4];
+    for (int i = 0; i < RB; i++) xr[i] = min(m0 + 16 * i + l16, p.M - 1);
+    f32x4 acc[NBLK][RB];
 #pragma unroll
     for (int j = 0; j < NBLK; j++)
 #pragma unroll
-        for (int i = 0; i < 4; i++) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < RB; i++) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     for (int q = q0; q < q1; q += BATCH) {
         // all loads of the batch first; a step past the wave's range reloads
         // its last one with a zero weight fragment, so the loop has no branch
         // (its products add exact zeros: the activations are finite)
-        u32x4 xf[BATCH][4];
+        u32x4 xf[BATCH][RB];
         if (q != q0) {
 #pragma unroll
             for (int b = 0; b < BATCH; b++)
@@ -438,7 +440,7 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(const GemmParams p)
         for (int b = 0; b < BATCH; b++) {
             const int k = min(q + b, q1 - 1) * KQ + (BF16 ? 8 : 4) * g;
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
+            for (int i = 0; i < RB; i++) {
                 if constexpr (LN) xf[b][i] = *(const u32x4*)(As + (16 * i + l16) * LDA + k);
                 else xf[b][i] = *(const u32x4*)(A + (size_t)xr[i] * p.K + k);
             }
@@ -452,7 +454,7 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(const GemmParams p)
 #pragma unroll
                 for (int e = 0; e < 4; e++) w[e] = live ? w[e] : 0u;
 #pragma unroll
-                for (int i = 0; i < 4; i++) {
+                for (int i = 0; i < RB; i++) {
                     if constexpr (BF16) {
                         acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w),
                                                                             __builtin_bit_cast(bf16x8_t, xf[b][i]),
@@ -471,7 +473,7 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(const GemmParams p)
 #pragma unroll
     for (int j = 0; j < NBLK; j++)
 #pragma unroll
-        for (int i = 0; i < 4; i++) red[(wave * NPAIR + 4 * j + i) * 64 + lane] = acc[j][i];
+        for (int i = 0; i < RB; i++) red[(wave * NPAIR + RB * j + i) * 64 + lane] = acc[j][i];
     __syncthreads();
     // wave w sums its tiles over the waves, in wave order
 #pragma unroll
@@ -481,7 +483,7 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(const GemmParams p)
         f32x4 y = red[pp * 64 + lane];
 #pragma unroll
         for (int w = 1; w < NW; w++) y += red[(w * NPAIR + pp) * 64 + lane];
-        const int j = pp >> 2, i = pp & 3;
+        const int j = pp / RB, i = pp % RB;
         const int row = m0 + 16 * i + l16, c4 = n0 + 16 * j + 4 * g;
         if (row < p.M && c4 < p.N) epilogue4<BF16, EPI>(p, row, c4, y, pre[u]);
     }
@@ -531,7 +533,7 @@ __global__ __launch_bounds__(256) void lnmod_kernel(const float* h, void* out, c
 
 // Skinny shapes: waves and 16-column blocks per block, by operand kind.
 #ifndef DCF_SK_LN_NBLK
-#define DCF_SK_LN_NBLK 1
+#define DCF_SK_LN_NBLK 2
 #endif
 #ifndef DCF_SK_PLAIN_NBLK
 #define DCF_SK_PLAIN_NBLK 1
@@ -543,31 +545,39 @@ __global__ __launch_bounds__(256) void lnmod_kernel(const float* h, void* out, c
 #define DCF_SK_PLAIN_WAVES 4
 #endif
 #ifndef DCF_SK_LN_WAVES
-#define DCF_SK_LN_WAVES 4
+#define DCF_SK_LN_WAVES 8
+#endif
+// 16-row blocks per skinny block, by operand kind
+#ifndef DCF_SK_LN_RB
+#define DCF_SK_LN_RB 1
+#endif
+#ifndef DCF_SK_PLAIN_RB
+#define DCF_SK_PLAIN_RB 1
 #endif
 constexpr int kSkinnyBigK = 1024;   // K from which the plain skinny GEMM uses DCF_SK_BIGK_WAVES waves
 
-size_t skinny_lds_bytes(const GemmParams& p, int bf16, int nw, int nblk)
+size_t skinny_lds_bytes(const GemmParams& p, int bf16, int nw, int nblk, int rb)
 {
-    const size_t red = (size_t)nw * 4 * nblk * 64 * 16;
+    const size_t red = (size_t)nw * rb * nblk * 64 * 16;
     if (!p.ln_h) return red;
     // the normalised tile, then scale and shift
-    const size_t a = (size_t)64 * (p.K + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4) + (size_t)2 * p.K * 4;
+    const size_t a = (size_t)16 * rb * (p.K + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4) + (size_t)2 * p.K * 4;
     return a > red ? a : red;
 }
 
-template <bool BF16, int EPI, bool LN, int NW, int NBLK>
+template <bool BF16, int EPI, bool LN, int NW, int NBLK, int RB>
 hipError_t launch_skinny(const GemmParams& p, hipStream_t st)
 {
-    const size_t lds = skinny_lds_bytes(p, BF16, NW, NBLK);
+    const size_t lds = skinny_lds_bytes(p, BF16, NW, NBLK, RB);
     static size_t set = 0;
     if (lds > 65536 && lds > set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<BF16, EPI, LN, NW, NBLK>),
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<BF16, EPI, LN, NW, NBLK, RB>),
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         set = lds;
     }
-    hipLaunchKernelGGL((skinny_kernel<BF16, EPI, LN, NW, NBLK>), dim3((p.N + 16 * NBLK - 1) / (16 * NBLK), (p.M + 63) / 64),
+    hipLaunchKernelGGL((skinny_kernel<BF16, EPI, LN, NW, NBLK, RB>),
+                       dim3((p.N + 16 * NBLK - 1) / (16 * NBLK), (p.M + 16 * RB - 1) / (16 * RB)),
                        dim3(64 * NW), lds, st, p);
     return hipGetLastError();
 }
@@ -576,9 +586,17 @@ template <bool BF16, int EPI, bool LN>
 hipError_t launch_one(const GemmParams& p, hipStream_t st)
 {
     if (p.M <= kSkinnyRows) {
-        if constexpr (LN) return launch_skinny<BF16, EPI, true, DCF_SK_LN_WAVES, DCF_SK_LN_NBLK>(p, st);
-        else if (p.K >= kSkinnyBigK) return launch_skinny<BF16, EPI, false, DCF_SK_BIGK_WAVES, DCF_SK_PLAIN_NBLK>(p, st);
-        else return launch_skinny<BF16, EPI, false, DCF_SK_PLAIN_WAVES, DCF_SK_PLAIN_NBLK>(p, st);
+        if constexpr (LN) {
+            // the LayerNorm staging gives each of a row's 4 NW / RB threads a
+            // whole number of 4-column vectors; 4 waves suffice for K = 64
+            if (p.K % (16 * DCF_SK_LN_WAVES / DCF_SK_LN_RB) == 0)
+                return launch_skinny<BF16, EPI, true, DCF_SK_LN_WAVES, DCF_SK_LN_NBLK, DCF_SK_LN_RB>(p, st);
+            return launch_skinny<BF16, EPI, true, 4, DCF_SK_LN_NBLK, 1>(p, st);
+        }
+        else if (p.K >= kSkinnyBigK)
+            return launch_skinny<BF16, EPI, false, DCF_SK_BIGK_WAVES, DCF_SK_PLAIN_NBLK, DCF_SK_PLAIN_RB>(p, st);
+        else
+            return launch_skinny<BF16, EPI, false, DCF_SK_PLAIN_WAVES, DCF_SK_PLAIN_NBLK, DCF_SK_PLAIN_RB>(p, st);
     } else if (LN) {
         // the normalised operand is written once to p.A by its own launch
         hipLaunchKernelGGL((lnmod_kernel<BF16>), dim3((p.M + 3) / 4), dim3(256), 0, st, p.ln_h, const_cast<void*>(p.A),

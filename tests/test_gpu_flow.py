@@ -79,14 +79,24 @@ def _run_oracle(arch, dtype, blob, b, prompt, mu_b, calls):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_tiny_chunks_match_oracle(dtype):
-    a = TINY
+    _chunks_match_oracle(TINY, dtype, 5)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_one_head_matches_oracle(dtype):
+    """dim = 64 (a single head): the LayerNorm-operand GEMMs take their 4-wave
+    shape, whose rows are split over fewer threads."""
+    _chunks_match_oracle(dict(TINY, dim=64, heads=1), dtype, 3)
+
+
+def _chunks_match_oracle(a, dtype, ncalls):
     blob = synth.make_flow_weights(a, 0)
     B, P = 2, a["f_prompt"]
-    calls = [a["f_call"]] * 5
-    say(f"flow tiny {dtype} B={B} calls={calls}")
+    calls = [a["f_call"]] * ncalls
+    say(f"flow tiny dim {a['dim']} {dtype} B={B} calls={calls}")
     dec, outs, mu, prompts = _run_gpu(a, dtype, blob, B, P, calls)
     st = dec.stats()
-    assert st["replays"] == 5 and st["direct"] == 0, st
+    assert st["replays"] == ncalls and st["direct"] == 0, st
     worst = 0.0
     for b in range(B):
         s, ref = _run_oracle(a, dtype, blob, b, prompts[b], mu[b], calls)

@@ -311,7 +311,7 @@ def flow_kernel_name(role: str, dtype: str, rows: int, attn_blocks: int = 0, arc
                 waves, nblk, rb = (8 if K >= 1024 else 4), 1, 1
             return f"dcf::skinny_kernel<{b}, {epi}, {'true' if ln else 'false'}, {waves}, {nblk}, {rb}>"
         blocks = ((N + 63) // 64) * ((rows + 63) // 64)
-        tile = "4, 4" if blocks >= TILE_BIG_BLOCKS else "4, 2" if blocks >= TILE_MID_BLOCKS else "2, 2"
+        tile = "4, 4" if blocks >= TILE_BIG_BLOCKS else "4, 2" if blocks >= TILE_MID_BLOCKS else "1, 1"
         return f"dcf::gemm_kernel<{b}, {epi}, {tile}>"
     return f"dcf::{role}_kernel<{b}>" if role in ("assemble", "euler") else role
 

@@ -323,8 +323,10 @@ hipError_t launch_tiled(const GemmParams& p, hipStream_t st)
     return hipGetLastError();
 }
 
-// 64 x 64 tiles unless the call has at least DCF_TILE_BIG_BLOCKS of them (then
-// 128 x 128) or DCF_TILE_MID_BLOCKS (then 128 rows x 64 columns).
+// Tile size by the number of 64 x 64 tiles the call would have: at least
+// DCF_TILE_BIG_BLOCKS -> 128 x 128, at least DCF_TILE_MID_BLOCKS -> 128 rows x
+// 64 columns, fewer -> 32 x 32 (more blocks for calls that would not fill the
+// machine).
 #ifndef DCF_TILE_BIG_BLOCKS
 #define DCF_TILE_BIG_BLOCKS 1024
 #endif
@@ -338,7 +340,7 @@ hipError_t launch_tiled_any(const GemmParams& p, hipStream_t st)
     const long small_blocks = (long)((p.N + 63) / 64) * ((p.M + 63) / 64);
     if (small_blocks >= DCF_TILE_BIG_BLOCKS) return launch_tiled<BF16, EPI, 4, 4>(p, st);
     if (small_blocks >= DCF_TILE_MID_BLOCKS) return launch_tiled<BF16, EPI, 4, 2>(p, st);
-    return launch_tiled<BF16, EPI, 2, 2>(p, st);
+    return launch_tiled<BF16, EPI, 1, 1>(p, st);
 }
 
 // Skinny GEMM for few rows (a call of a handful of streams): block = 16 RB

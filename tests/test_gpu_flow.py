@@ -262,7 +262,8 @@ def test_many_rows_take_the_tiled_path_and_match_oracle(dtype):
 
 def test_real_shape_batch20_every_tile_size():
     """20 paper-shaped streams in bf16: 2,240 rows per call, so the MLP-up GEMM
-    takes 128 x 128 tiles, the QKV GEMM 128 x 64 and the others 64 x 64."""
+    takes 128 x 128 tiles, the input, QKV, attention-output and MLP-down GEMMs
+    128 x 64, and the 80-column output projection 32 x 32."""
     a = synth.REAL_FLOW_ARCH
     blob = synth.make_flow_weights(a, 0)
     B, P = 20, 64
@@ -296,3 +297,24 @@ def test_host_pointer_mode_equals_device_mode():
         if n >= a["f_chunk"]:
             p += a["f_chunk"]
     h.close()
+
+
+@pytest.mark.parametrize("name,streams", [("flow_real_bf16_b16", (0, 15)), ("flow_real_bf16_b128", (0, 127))])
+def test_batched_bench_workloads_match_oracle(name, streams):
+    """The batched benchmark configurations in the benchmark's launch shapes
+    (all streams, a replayed f_call-frame call); sampled streams against the
+    oracle.  Prompts of 64 frames keep the oracle's share short (the batch-1
+    configurations are the real-shape test above)."""
+    w = synth.workload(name)
+    a, dtype, B = w["arch"], w["dtype"], w["batch"]
+    blob = synth.make_flow_weights(a, 0)
+    P = 64
+    say(f"{name}: B={B} prompt {P}, one call of {a['f_call']} frames")
+    dec, outs, mu, prompts = _run_gpu(a, dtype, blob, B, P, [a["f_call"]])
+    assert dec.stats()["replays"] == 1
+    for b in streams:
+        _s, ref = _run_oracle(a, dtype, blob, b, prompts[b], mu[b], [a["f_call"]])
+        e, er = err_stats(outs[0][b], ref[0])
+        say(f"  stream {b}: max-abs/RMS {e:.3e}, RMS err/RMS {er:.3e}")
+        assert e <= TOL[dtype], f"stream {b}: {e:.3e}"
+    dec.close()

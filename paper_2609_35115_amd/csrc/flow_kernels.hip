@@ -655,7 +655,8 @@ constexpr int kAttnLd = 68;   // padded row of the merge buffer (floats)
 constexpr float kScoreLog2 = 0.125f * 1.4426950408889634f;
 constexpr int kAttnWideBlocks = 64;   // blocks of 64 queries below which the narrow shape is used
 
-size_t attn_lds_bytes(int nw) { return (size_t)nw * 64 * kAttnLd * 4 + (size_t)2 * nw * 64 * 4; }
+// per wave: the partial O of its block's 16 QG queries, their running maxima and sums
+size_t attn_lds_bytes(int nw, int qg) { return (size_t)nw * 16 * qg * (kAttnLd + 2) * 4; }
 
 template <bool BF16, int QG, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_kernel(const AttnParams p)
@@ -664,9 +665,10 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const AttnParams p)
     static_assert((QG == 1 || QG == 2 || QG == 4) && QG <= NW,
                   "16 * QG divides the 64-row query padding; a merge wave per query group");
     extern __shared__ __align__(16) unsigned char smem[];
-    float* Os = (float*)smem;                          // [NW waves][64 queries][kAttnLd]
-    float* Ms = Os + NW * 64 * kAttnLd;                // [NW][64]
-    float* Ls = Ms + NW * 64;                          // [NW][64]
+    constexpr int QB = 16 * QG;                        // queries of the block
+    float* Os = (float*)smem;                          // [NW waves][QB queries][kAttnLd]
+    float* Ms = Os + NW * QB * kAttnLd;                // [NW][QB]
+    float* Ls = Ms + NW * QB;                          // [NW][QB]
 
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int l16 = lane & 15, g = lane >> 4;
@@ -824,10 +826,10 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const AttnParams p)
         l1 += __shfl_xor(l1, 32, 64);
         const int qq = 16 * qg + l16;
 #pragma unroll
-        for (int db = 0; db < 4; db++) *(f32x4*)(Os + ((size_t)wave * 64 + qq) * kAttnLd + 16 * db + 4 * g) = O[db];
+        for (int db = 0; db < 4; db++) *(f32x4*)(Os + ((size_t)wave * QB + qq) * kAttnLd + 16 * db + 4 * g) = O[db];
         if (g == 0) {
-            Ms[wave * 64 + qq] = m;
-            Ls[wave * 64 + qq] = l1;
+            Ms[wave * QB + qq] = m;
+            Ls[wave * QB + qq] = l1;
         }
     };
 
@@ -902,17 +904,17 @@ __global__ __launch_bounds__(64 * NW) void attn_kernel(const AttnParams p)
     const int qq = 16 * wave + l16;
     float mx = Ms[qq];
 #pragma unroll
-    for (int w = 1; w < NW; w++) mx = fmaxf(mx, Ms[w * 64 + qq]);
+    for (int w = 1; w < NW; w++) mx = fmaxf(mx, Ms[w * QB + qq]);
     float L = 0.f;
     f32x4 acc[4];
 #pragma unroll
     for (int db = 0; db < 4; db++) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int w = 0; w < NW; w++) {
-        const float sc = exp2f(Ms[w * 64 + qq] - mx);
-        L += sc * Ls[w * 64 + qq];
+        const float sc = exp2f(Ms[w * QB + qq] - mx);
+        L += sc * Ls[w * QB + qq];
 #pragma unroll
-        for (int db = 0; db < 4; db++) acc[db] += sc * *(const f32x4*)(Os + ((size_t)w * 64 + qq) * kAttnLd + 16 * db + 4 * g);
+        for (int db = 0; db < 4; db++) acc[db] += sc * *(const f32x4*)(Os + ((size_t)w * QB + qq) * kAttnLd + 16 * db + 4 * g);
     }
     const float inv = 1.0f / L;
     const int fq = qb0 + qq;
@@ -927,7 +929,7 @@ template <bool BF16, int QG, int NW>
 hipError_t launch_attn_shape(const AttnParams& p, int Bc, hipStream_t st)
 {
     const dim3 grid(Bc * 2 * p.heads, (p.n + 16 * QG - 1) / (16 * QG));
-    const size_t lds = attn_lds_bytes(NW);
+    const size_t lds = attn_lds_bytes(NW, QG);
     static bool set = false;
     if (!set) {
         const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<BF16, QG, NW>),

@@ -146,7 +146,10 @@ typedef struct dc_state dc_state;
  *     merge b [1], down W [C_last][1][hop], down b [C_last].
  * The blob is copied (rounded to bfloat16, nearest-even, when dtype is
  * DC_BF16; the head stays fp32 arithmetic on those rounded values) and may be
- * freed on return.  On success *out owns the state, reset to the start of
+ * freed on return.  A DC_BF16 state stores the stages' residual stream (the
+ * "s<s>.y", "s<s>.rb<j>.z<i>" and "s<s>.x" intermediates) as IEEE binary16:
+ * activations of order one keep 11 significant bits; magnitudes beyond
+ * 65504 do not fit (a DC_F32 state has no such limit).  On success *out owns the state, reset to the start of
  * every stream, with the chunk graph captured unless DC_NO_GRAPH.
  * Errors: DC_EVERSION, DC_EINVAL (cfg or blob size), DC_ENOMEM, DC_EDEVICE;
  * *out is NULL then.

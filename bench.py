@@ -222,21 +222,29 @@ def summarize_traffic(fetch_dir: str, write_dir: str, workload: str, kernel: str
     import glob
     def mean_kib(d, counter):
         rows = _csv(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0])
-        vals = {}
+        vals, grid = {}, {}
         for r in rows:
             name = r["Kernel_Name"].replace("void ", "")
             name = name[:name.index("(")] if "(" in name else name
             if name == kernel and r["Counter_Name"] == counter:
-                vals[r["Dispatch_Id"]] = vals.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
-        return sum(vals.values()) / len(vals), len(vals)
-    f, nf = mean_kib(fetch_dir, "FETCH_SIZE")
-    w, nw = mean_kib(write_dir, "WRITE_SIZE")
+                i = int(r["Dispatch_Id"])
+                vals[i] = vals.get(i, 0.0) + float(r["Counter_Value"])
+                grid[i] = int(r["Grid_Size"])
+        if workload.startswith("flow_"):
+            # the timed calls' launches only: the prompt passes that set up
+            # the streams run the same kernels over other row counts
+            g_last = grid[max(grid)]
+            vals = {i: v for i, v in vals.items() if grid[i] == g_last}
+        return sum(vals.values()) / len(vals), len(vals), grid[max(grid)]
+    f, nf, g = mean_kib(fetch_dir, "FETCH_SIZE")
+    w, nw, _ = mean_kib(write_dir, "WRITE_SIZE")
     hbm = (f * FETCH_SCALE + w * WRITE_SCALE) * 1024.0
     lines = ["# HBM traffic per launch from rocprofv3 PMC counters", f"# command: {command}",
              f"# FETCH_SIZE x {FETCH_SCALE} + WRITE_SIZE x {WRITE_SCALE} (KiB per dispatch; scale factors from a "
              "plain 256 MiB device copy: python3 bench.py --calibrate-copy)",
              f"workload: {workload}", f"kernel: {kernel}", f"kernel_source_hash: {kernel_source_hash(_sources_for(out))}",
-             f"dispatches: {nf} / {nw}", f"fetch_kib_per_dispatch: {f:.1f}", f"write_kib_per_dispatch: {w:.1f}",
+             f"dispatches: {nf} / {nw}" + (f" (grid size {g}: the timed calls' launches)" if workload.startswith("flow_") else ""),
+             f"fetch_kib_per_dispatch: {f:.1f}", f"write_kib_per_dispatch: {w:.1f}",
              f"hbm_bytes_per_launch: {hbm:.0f}"]
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))

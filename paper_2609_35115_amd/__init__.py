@@ -290,6 +290,74 @@ def dc_free(h) -> None:
 
 # --------------------------------------------------------------- convenience
 
+def _shape_dtype_device(x):
+    """(shape, dtype name, device index or None for host memory) of a numpy
+    array or a torch tensor."""
+    if isinstance(x, np.ndarray):
+        return tuple(x.shape), str(x.dtype), None
+    dev = x.device
+    return tuple(x.shape), str(x.dtype).replace("torch.", ""), (dev.index if dev.type == "cuda" else None)
+
+
+def check_decode_args(tokens, f0, batch: int, max_tokens: int, fpt: int, has_source: bool, host: bool,
+                      device: int | None = 0) -> int:
+    """Validate the arguments of Decoder.decode and return n.
+
+    tokens must be [batch][n] with 1 <= n <= max_tokens.  In host mode it is
+    a numpy int32 array; in device mode an int32 tensor on the state's device,
+    or a numpy array of any integer type whose values fit int32 (copied).  A
+    decoder with a harmonic source needs f0 [batch][n * fpt] float32 in the
+    same form (numpy float arrays are converted).  Anything else raises
+    DcError: DC_ERANGE for n > max_tokens (the status the C call gives), else
+    DC_EINVAL.  The C call reads tokens as int32 and trusts the row count, so
+    an int64 tensor or a short one would otherwise be misread silently."""
+    if tokens is None:
+        raise DcError(DC_EINVAL, "tokens is None")
+    shape, dt, dev = _shape_dtype_device(tokens)
+    if len(shape) != 2 or shape[0] != batch:
+        raise DcError(DC_EINVAL, f"tokens must be [batch={batch}][n], got shape {shape}")
+    n = shape[1]
+    if n < 1:
+        raise DcError(DC_EINVAL, f"n = {n} tokens per stream; at least 1 is needed")
+    if n > max_tokens:
+        raise DcError(DC_ERANGE, f"n = {n} tokens per stream exceeds max_tokens = {max_tokens}")
+    if isinstance(tokens, np.ndarray):
+        if host and dt != "int32":
+            raise DcError(DC_EINVAL, f"host-mode tokens must be int32, got {dt}")
+        if not np.issubdtype(tokens.dtype, np.integer):
+            raise DcError(DC_EINVAL, f"tokens must be integers, got {dt}")
+        if tokens.size and (int(tokens.min()) < -2 ** 31 or int(tokens.max()) >= 2 ** 31):
+            raise DcError(DC_EINVAL, "token ids do not fit int32")
+    else:
+        if host:
+            raise DcError(DC_EINVAL, "host-mode tokens must be a numpy int32 array")
+        if dt != "int32":
+            raise DcError(DC_EINVAL, f"device tokens must be an int32 tensor, got {dt}")
+        if dev is None or (device is not None and dev != device):
+            raise DcError(DC_EINVAL, f"device tokens must live on cuda:{device}, got {tokens.device}")
+    if has_source:
+        if f0 is None:
+            raise DcError(DC_EINVAL, "a decoder with a harmonic source needs f0")
+        fshape, fdt, fdev = _shape_dtype_device(f0)
+        if fshape != (batch, n * fpt):
+            raise DcError(DC_EINVAL, f"f0 must be [batch={batch}][n*frames_per_token={n * fpt}], got {fshape}")
+        if isinstance(f0, np.ndarray):
+            if host and fdt != "float32":
+                raise DcError(DC_EINVAL, f"host-mode f0 must be float32, got {fdt}")
+            if not np.issubdtype(f0.dtype, np.floating):
+                raise DcError(DC_EINVAL, f"f0 must be floating point, got {fdt}")
+        else:
+            if host:
+                raise DcError(DC_EINVAL, "host-mode f0 must be a numpy float32 array")
+            if fdt != "float32":
+                raise DcError(DC_EINVAL, f"device f0 must be a float32 tensor, got {fdt}")
+            if fdev is None or (device is not None and fdev != device):
+                raise DcError(DC_EINVAL, f"device f0 must live on cuda:{device}, got {f0.device}")
+    elif f0 is not None:
+        raise DcError(DC_EINVAL, "f0 given to a decoder without a harmonic source")
+    return n
+
+
 class Decoder:
     """One dc_state on the current GPU, with torch-ROCm tensors for device memory
     and a dedicated torch stream that every call is ordered on."""
@@ -324,9 +392,12 @@ class Decoder:
         """tokens [batch][n] int32 (numpy in host mode, else a device tensor or
         numpy copied to the device), and for a decoder with a harmonic source
         f0 [batch][n*frames_per_token] float32 likewise -> PCM [batch][n*spt]
-        (numpy in host mode, else a device tensor)."""
+        (numpy in host mode, else a device tensor).  Arguments that the C call
+        would misread (another dtype, rank, row count or device) raise DcError
+        before anything is launched; see check_decode_args."""
         torch = self.torch
-        n = tokens.shape[1]
+        n = check_decode_args(tokens, f0, self.batch, self.max_tokens, self.arch["frames_per_token"],
+                              self.has_source, self.host, torch.cuda.current_device())
         if self.host:
             tok = np.ascontiguousarray(tokens, dtype=np.int32)
             out = np.empty((self.batch, n * self.spt), dtype=np.float32)

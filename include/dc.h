@@ -15,8 +15,16 @@
  * Correctness contract (Design, Definition 2, strict trace equivalence): for
  * every stream, decoding a token sequence chunk by chunk yields bit-for-bit the
  * PCM of decoding the concatenation in one call, and graph replay yields
- * bit-for-bit the PCM of direct launches.  Results never depend on the batch
- * size, the chunk size or the tile shapes chosen for the hardware.
+ * bit-for-bit the PCM of direct launches.  This holds within one state and
+ * across states that share the architecture, dtype and batch class: with the
+ * automatic tile choice (tile_variant 0) the reduction order of every output
+ * sample depends on the layer, the dtype and whether batch < 8 (the streaming
+ * class: K split in four partitions) or batch >= 8 (the batched class: one
+ * partition, bf16 resblock pairs fused), never on chunk_tokens, max_tokens,
+ * the call's n or the stream's index in the batch.  A fresh state whose
+ * chunk_tokens covers a whole utterance therefore decodes it to the bits of a
+ * chunked decode on a state of the same class.  Across classes the PCM
+ * agrees within the rounding tolerance of the dtype, not bit for bit.
  *
  * Conventions for every function:
  *   - the return value is a dc_status (0 on success, negative on error); no
@@ -90,8 +98,9 @@ typedef struct dc_cfg {
     int32_t max_tokens;                  /* largest n accepted by dc_decode_chunk                 */
     uint32_t flags;                      /* DC_HOST_PTRS | DC_NO_GRAPH | DC_NO_FUSE | DC_FLUSH_CATALOG |
                                             DC_NO_RING */
-    int32_t tile_variant;                /* 0: automatic; v > 0 forces tile shape v-1 everywhere
-                                            it fits (results are identical by construction)      */
+    int32_t tile_variant;                /* 0: automatic; v > 0 forces tile shape v-1, and with it
+                                            its K partitions and channel block, everywhere it fits
+                                            (shapes that share those two give identical results) */
     /* Harmonic-plus-noise excitation source (the vocoder's stochastic input;
      * n_harmonics == 0: none, and the fields below are ignored).  Per frame of
      * the pre-stack clock the caller gives f0 (Hz); the source sums the
@@ -192,15 +201,24 @@ dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* 
 dc_status dc_decode_chunk_f0(dc_state* s, const int32_t* tokens, const float* f0, int32_t n, float* audio_out);
 
 /* Return every stream to its start: zero every ring in place (addresses are
- * unchanged) and set the clock to 0.  Clears a poisoned state. */
+ * unchanged) and set the clock to 0.  Clears a poisoned state.  This is the
+ * state rule's reset, which writes the base state into the contract-owned
+ * carry in place rather than reallocating it (Design, "State rule: demand
+ * sizing and the carry"; the representation invariant that every replay sees
+ * the same addresses). */
 dc_status dc_reset(dc_state* s);
 
 /* Return stream b (0 <= b < batch) to its start in place; other streams keep
- * their carry.  DC_EINVAL for a bad b. */
+ * their carry (the state rule's in-place reset applied to one session's slice
+ * of the carry, as a turn boundary of one session of a multi-session binding
+ * needs).  DC_EINVAL for a bad b. */
 dc_status dc_reset_stream(dc_state* s, int32_t b);
 
 /* Wait for all work of the state; report DC_ERANGE for a bad token id seen on
- * the device, DC_EDEVICE for a HIP error (both poison the state). */
+ * the device, DC_EDEVICE for a HIP error (both poison the state).  A failure
+ * found here is the device side of the fail-closed admission: the call that
+ * raised it produced no trusted output (Design, "Granularity and capture
+ * placement", local fail-closed admission). */
 dc_status dc_sync(dc_state* s);
 
 /* frames_per_token * prod(up_rate) * hop for cfg (0 for a NULL cfg). */
@@ -211,7 +229,13 @@ int64_t dc_blob_floats(const dc_cfg* cfg);
 
 /* The fixed device buffers that dc_decode_chunk stages through:
  * int32 [batch][max_tokens] and float32 [batch][max_tokens * samples_per_token]
- * (read as [batch][n] and [batch][n * spt] for a call with n tokens). */
+ * (read as [batch][n] and [batch][n * spt] for a call with n tokens).  A
+ * caller that writes its tokens here and reads its PCM from here is aliased
+ * with the contract's own inputs and outputs, so no staging copy is made on
+ * that side (Design, clause (ii) address stability: contract-owned inputs are
+ * aliased and skip per-call staging; Proposition 2, mutual enabling, and Eq.
+ * enabling: an aliased input needs no class-specific staging storage).  Owned by the state; valid until
+ * dc_free. */
 int32_t* dc_token_buffer(dc_state* s);
 float* dc_audio_buffer(dc_state* s);
 

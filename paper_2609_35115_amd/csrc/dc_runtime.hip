@@ -267,6 +267,12 @@ static void pack_weights(const ConvOp& op, const float* blob, bool round_bf16, c
                     }
 }
 
+// The batch class: from this many streams a state runs every conv with one K
+// partition (and, for bf16, the resblock pairs fused); below it, 4.
+#ifndef DC_BATCHED_MIN
+#define DC_BATCHED_MIN 8
+#endif
+
 // Unsplit tile shapes in order of preference (ids of the kernel's shape
 // table).  Layers that read a residual and write fp32 -- and every layer of
 // the 64-channel stage -- move more bytes per FLOP and run best on 64x64
@@ -298,8 +304,12 @@ static const int kPreferRing[] = {20, 24, 22, 21, 25, 23};
 // Tile shape of a conv for this state.  Deterministic: it depends on the
 // layer, the batch and the chunk size only (never on a call's n), so every
 // call of a state -- replayed or direct, chunked or offline -- runs the same
-// arithmetic.  First the K partitions: 4 (waves split K) when even 32x32
-// output tiles leave fewer than 512 blocks, else 1.  Then the channel block:
+// arithmetic.  The arithmetic itself (K partitions, channel block) depends on
+// the layer and the batch class only, never on the chunk size: a state built
+// for another chunk size, or an offline state holding a whole utterance,
+// computes the same bits.  First the K partitions: 4 (waves split K) for the
+// streaming class (batch below DC_BATCHED_MIN), whose calls leave too few
+// output tiles to fill the machine, else 1.  Then the channel block:
 // as wide as the layer's channels (capped at 4 chunks for unsplit tiles),
 // so no K step is padding.  Then the tile: for split K the one that best
 // fills the machine, otherwise the first in preference order that keeps
@@ -335,8 +345,7 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
     };
     const int kq = op.bf16 ? 32 : 16;
     const int kch_all = (op.Ci + kq - 1) / kq;      // chunks covering every input channel
-    const TileShape t32 = {1, 1, 2, 2, 1, 1};
-    const int wgk = blocks(t32) < 512 ? 4 : 1;
+    const int wgk = B < DC_BATCHED_MIN ? 4 : 1;
     // channel-block candidates, widest first: no wider than the channels
     // (nor than 4 chunks when waves do not split K)
     for (int kch = 32; kch >= 1; kch /= 2) {
@@ -418,12 +427,9 @@ static void need_ctx(dc_state* s, int ring, int ctx)
 // Resblock pairs of a stage run fused (h on chip) for bf16 with enough
 // streams to fill the machine, at the channel counts the fused kernel has
 // shapes for, unless the caller forces a tile shape or asks for no fusion.
-#ifndef DC_FUSE_MIN_BATCH
-#define DC_FUSE_MIN_BATCH 8
-#endif
 static bool fuse_stage(const dc_cfg& c, int channels)
 {
-    if (c.dtype != DC_BF16 || (c.flags & DC_NO_FUSE) || c.tile_variant != 0 || c.batch < DC_FUSE_MIN_BATCH)
+    if (c.dtype != DC_BF16 || (c.flags & DC_NO_FUSE) || c.tile_variant != 0 || c.batch < DC_BATCHED_MIN)
         return false;
     int k_max = 1, d_max = 1;
     for (int j = 0; j < c.n_rb; j++) k_max = c.rb_kernel[j] > k_max ? c.rb_kernel[j] : k_max;

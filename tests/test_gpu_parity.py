@@ -167,6 +167,40 @@ def test_stream_in_batch_equals_stream_alone(dtype):
     assert bits_equal(pb[2:3], p1)
 
 
+# Automatic tile choice (tile_variant 0): the arithmetic depends on the layer,
+# the dtype and the batch class only.  A fresh state whose chunk holds the
+# whole utterance decodes it to the bits of a chunked decode, and a stream's
+# bits do not depend on the batch it shares (within one class).
+@pytest.mark.parametrize("dtype,batch", [("f32", 1), ("bf16", 1), ("bf16", 16)])
+def test_whole_utterance_state_equals_chunked_automatic_tiles(dtype, batch):
+    blob = synth.make_weights(REAL, 0)
+    ids = synth.make_tokens(REAL, batch, 100)
+    say(f"real {dtype} B={batch}: 4 chunks of 25 vs a state with chunk_tokens=100")
+    a = dc.Decoder(REAL, dtype, blob, batch=batch, chunk_tokens=25)
+    pa = decode_chunks(a, ids, [25] * 4)
+    assert a.stats()["replays"] == 4
+    a.close()
+    b = dc.Decoder(REAL, dtype, blob, batch=batch, chunk_tokens=100)
+    pb = decode_chunks(b, ids, [100])
+    assert b.stats()["replays"] == 1
+    b.close()
+    assert bits_equal(pa, pb)
+
+
+@pytest.mark.parametrize("dtype,big,small", [("f32", 3, 1), ("bf16", 3, 1), ("bf16", 16, 8)])
+def test_stream_bits_independent_of_batch_within_class(dtype, big, small):
+    blob = synth.make_weights(REAL, 0)
+    ids = synth.make_tokens(REAL, big, 8)
+    say(f"real {dtype}: batch {big} vs batch {small}, automatic tiles")
+    a = dc.Decoder(REAL, dtype, blob, batch=big, chunk_tokens=4)
+    pa = decode_chunks(a, ids, [4, 4])
+    a.close()
+    b = dc.Decoder(REAL, dtype, blob, batch=small, chunk_tokens=8)
+    pb = decode_chunks(b, ids[big - small:], [8])
+    b.close()
+    assert bits_equal(pa[big - small:], pb)
+
+
 def test_reset_and_reset_stream_equal_fresh_state():
     blob = synth.make_weights(TINY, 0)
     ids = synth.make_tokens(TINY, 2, 24)

@@ -139,6 +139,7 @@ typedef struct dc_stats {
     int32_t graph_classes;    /* captured shape classes: 0, 1 or chunk_tokens                   */
     int32_t reserved;
     int64_t staged_f0;        /* f0 copies into the fixed f0 buffer (caller not aliased)        */
+    int64_t direct_static;    /* direct launches of dc_decode_chunk_f0_static                   */
 } dc_stats;
 
 typedef struct dc_state dc_state;
@@ -199,6 +200,28 @@ dc_status dc_decode_chunk(dc_state* s, const int32_t* tokens, int32_t n, float* 
  * declared clock).  Errors as dc_decode_chunk, plus DC_EINVAL for a NULL f0.
  */
 dc_status dc_decode_chunk_f0(dc_state* s, const int32_t* tokens, const float* f0, int32_t n, float* audio_out);
+
+/*
+ * dc_decode_chunk_f0 for callers that cannot allocate device memory or must
+ * not have the library do so on their behalf (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): the call's one
+ * scratch buffer -- the harmonic source's table of phases at the start of
+ * every f0 frame, batch * n * frames_per_token * (n_harmonics + 1) doubles --
+ * lives in a file-scope device array of the library (4 MiB, one copy per
+ * device for the life of the process, its address resolved at the dc_init of
+ * the first decoder with a source on that device) instead of the state's
+ * arena.  The call allocates nothing, captures nothing and always launches
+ * the step's kernels directly (counted as direct_static); tokens, f0 and
+ * audio_out are as for dc_decode_chunk_f0, and the PCM is bit-identical to
+ * it.  The array keeps the last call's contents, which every call overwrites
+ * before reading; all calls on one device share it, so calls that overlap in
+ * time on one device (states on different streams) race and must be
+ * serialised by the caller.  Errors: as dc_decode_chunk_f0, plus DC_ERANGE
+ * (nothing launched, state unchanged) when the phase table would exceed
+ * 4 MiB, and DC_EINVAL for a decoder without a harmonic source.
+ */
+dc_status dc_decode_chunk_f0_static(dc_state* s, const int32_t* tokens, const float* f0, int32_t n,
+                                    float* audio_out);
 
 /* Return every stream to its start: zero every ring in place (addresses are
  * unchanged) and set the clock to 0.  Clears a poisoned state.  This is the

@@ -66,7 +66,7 @@ class DcStats(ctypes.Structure):
         ("arena_bytes", ctypes.c_int64), ("weight_bytes", ctypes.c_int64), ("carry_bytes", ctypes.c_int64),
         ("ring_bytes", ctypes.c_int64), ("kernels_per_step", ctypes.c_int32), ("graph_nodes", ctypes.c_int32),
         ("capture_ms", ctypes.c_double), ("replays_flush", ctypes.c_int64), ("graph_classes", ctypes.c_int32),
-        ("reserved", ctypes.c_int32), ("staged_f0", ctypes.c_int64),
+        ("reserved", ctypes.c_int32), ("staged_f0", ctypes.c_int64), ("direct_static", ctypes.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -85,6 +85,7 @@ SIGNATURES = {
     "dc_init": ([_P, ctypes.c_size_t, ctypes.POINTER(DcCfg), ctypes.POINTER(_P)], ctypes.c_int),
     "dc_decode_chunk": ([_P, _P, ctypes.c_int32, _P], ctypes.c_int),
     "dc_decode_chunk_f0": ([_P, _P, _P, ctypes.c_int32, _P], ctypes.c_int),
+    "dc_decode_chunk_f0_static": ([_P, _P, _P, ctypes.c_int32, _P], ctypes.c_int),
     "dc_reset": ([_P], ctypes.c_int),
     "dc_reset_stream": ([_P, ctypes.c_int32], ctypes.c_int),
     "dc_sync": ([_P], ctypes.c_int),
@@ -196,6 +197,13 @@ def dc_decode_chunk_f0(h, tokens, f0, n: int, audio_out) -> int:
     return lib().dc_decode_chunk_f0(h, _ptr(tokens) if tokens is not None else None,
                                     _ptr(f0) if f0 is not None else None, n,
                                     _ptr(audio_out) if audio_out is not None else None)
+
+
+def dc_decode_chunk_f0_static(h, tokens, f0, n: int, audio_out) -> int:
+    """Raw call: returns the status (no exception)."""
+    return lib().dc_decode_chunk_f0_static(h, _ptr(tokens) if tokens is not None else None,
+                                           _ptr(f0) if f0 is not None else None, n,
+                                           _ptr(audio_out) if audio_out is not None else None)
 
 
 def dc_reset(h) -> int:
@@ -388,13 +396,14 @@ class Decoder:
         except Exception:
             pass
 
-    def decode(self, tokens, f0=None, check: bool = True):
+    def decode(self, tokens, f0=None, check: bool = True, static_scratch: bool = False):
         """tokens [batch][n] int32 (numpy in host mode, else a device tensor or
         numpy copied to the device), and for a decoder with a harmonic source
         f0 [batch][n*frames_per_token] float32 likewise -> PCM [batch][n*spt]
         (numpy in host mode, else a device tensor).  Arguments that the C call
         would misread (another dtype, rank, row count or device) raise DcError
-        before anything is launched; see check_decode_args."""
+        before anything is launched; see check_decode_args.  static_scratch
+        (a decoder with a harmonic source) calls dc_decode_chunk_f0_static."""
         torch = self.torch
         n = check_decode_args(tokens, f0, self.batch, self.max_tokens, self.arch["frames_per_token"],
                               self.has_source, self.host, torch.cuda.current_device())
@@ -402,7 +411,8 @@ class Decoder:
             tok = np.ascontiguousarray(tokens, dtype=np.int32)
             out = np.empty((self.batch, n * self.spt), dtype=np.float32)
             if self.has_source:
-                st = dc_decode_chunk_f0(self.h, tok, np.ascontiguousarray(f0, dtype=np.float32), n, out)
+                call = dc_decode_chunk_f0_static if static_scratch else dc_decode_chunk_f0
+                st = call(self.h, tok, np.ascontiguousarray(f0, dtype=np.float32), n, out)
             else:
                 st = dc_decode_chunk(self.h, tok, n, out)
         else:
@@ -420,7 +430,8 @@ class Decoder:
                 out = torch.empty((self.batch, n * self.spt), dtype=torch.float32, device="cuda")
             self.stream.wait_stream(torch.cuda.current_stream())
             if self.has_source:
-                st = dc_decode_chunk_f0(self.h, tok, f0d, n, out)
+                call = dc_decode_chunk_f0_static if static_scratch else dc_decode_chunk_f0
+                st = call(self.h, tok, f0d, n, out)
             else:
                 st = dc_decode_chunk(self.h, tok, n, out)
             tok.record_stream(self.stream)

@@ -20,6 +20,7 @@
 #include <chrono>
 #include <cmath>
 #include <limits>
+#include <mutex>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -132,6 +133,8 @@ struct dc_state {
     std::vector<hipGraph_t> flush_graph;
     std::vector<hipGraphExec_t> flush_exec;
     dc_stats st{};
+    int device = 0;             // the device current at dc_init (the arena's)
+    double* static_ptab = nullptr;   // that device's static scratch (harmonic source only)
     int64_t clock_host = 0;
     bool poisoned = false;
     std::string msg;
@@ -750,14 +753,16 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
     return p;
 }
 
-static SourceParams source_params(const dc_state* s, int n)
+// ptab: the per-call phase table (the arena's, or the static scratch of
+// dc_decode_chunk_f0_static when non-null).
+static SourceParams source_params(const dc_state* s, int n, double* ptab = nullptr)
 {
     const dc_cfg& c = s->cfg;
     SourceParams p{};
     p.f0 = s->f0;
     p.carry = (double*)(s->arena + s->phase_off);
     p.tags = (int64_t*)(p.carry + (size_t)c.batch * 2 * (c.n_harmonics + 1));
-    p.ptab = (double*)(s->arena + s->ptab_off);
+    p.ptab = ptab ? ptab : (double*)(s->arena + s->ptab_off);
     p.src = (float*)s->rings[s->ring_src].ptr;
     p.src_R = s->rings[s->ring_src].R;
     p.mw = (const float*)(s->arena + s->src_w_off);
@@ -824,7 +829,7 @@ static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n
     return p;
 }
 
-static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
+static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st, double* ptab = nullptr)
 {
     const dc_cfg& c = s->cfg;
     const int L = c.n_stages;
@@ -848,9 +853,9 @@ static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
         return launch_pair(la.pair_variant, ps, cnt, st);
     }
     case L_PHASE:
-        return launch_phase(source_params(s, n), st);
+        return launch_phase(source_params(s, n, ptab), st);
     case L_SOURCE:
-        return launch_source(source_params(s, n), st);
+        return launch_source(source_params(s, n, ptab), st);
     case L_SPECTRUM:
         return launch_spectrum((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL,
                                s->table, s->rings[s->ring_G], s->clock, s->fpt[L], st);
@@ -861,10 +866,10 @@ static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st)
     }
 }
 
-static hipError_t enqueue_step(dc_state* s, int n, hipStream_t st)
+static hipError_t enqueue_step(dc_state* s, int n, hipStream_t st, double* ptab = nullptr)
 {
     for (int i = 0; i < layer_count(s); i++) {
-        const hipError_t e = launch_layer(s, i, n, st);
+        const hipError_t e = launch_layer(s, i, n, st, ptab);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -890,6 +895,8 @@ extern "C" {
 int64_t dc_samples_per_token(const dc_cfg* cfg) { return cfg ? samples_per_token(cfg) : 0; }
 
 int64_t dc_blob_floats(const dc_cfg* cfg) { return cfg ? blob_floats(cfg) : 0; }
+
+static hipError_t static_scratch(int dev, void** out);
 
 dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg, dc_state** out)
 {
@@ -1004,6 +1011,19 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
         }
         s->own_stream = true;
     }
+    // the device of the arena; a decoder with a harmonic source also resolves
+    // that device's static scratch address here (dc_decode_chunk_f0_static)
+    e = hipGetDevice(&s->device);
+    if (e == hipSuccess && c.n_harmonics > 0) {
+        void* p = nullptr;
+        e = static_scratch(s->device, &p);
+        s->static_ptab = (double*)p;
+    }
+    if (e != hipSuccess) {
+        const std::string m = std::string("static scratch: ") + hipGetErrorString(e);
+        dc_free(s);
+        return fail(nullptr, DC_EDEVICE, m);
+    }
 
     // ---- host-side packing of weights and device-resident constants
     std::vector<char> host(weights_end, 0);
@@ -1103,7 +1123,10 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
 
 // One call: admission, staging of tokens (and f0), replay or direct launch,
 // staging of the PCM.  f0 is non-null exactly for a decoder with a source.
-static dc_status decode_call(dc_state* s, const int32_t* tokens, const float* f0, int32_t n, float* audio_out)
+// static_ptab non-null: dc_decode_chunk_f0_static (direct launches whose phase
+// table is the device's static scratch; never a graph replay).
+static dc_status decode_call(dc_state* s, const int32_t* tokens, const float* f0, int32_t n, float* audio_out,
+                             double* static_ptab = nullptr)
 {
     if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned; call dc_reset");
     const dc_cfg& c = s->cfg;
@@ -1142,7 +1165,11 @@ static dc_status decode_call(dc_state* s, const int32_t* tokens, const float* f0
         if (e != hipSuccess) return device_fail(s, e, "f0 staging");
         s->st.staged_f0++;
     }
-    if (n == c.chunk_tokens && s->exec) {
+    if (static_ptab) {
+        e = enqueue_step(s, n, s->stream, static_ptab);
+        if (e != hipSuccess) return device_fail(s, e, "direct launch (static scratch)");
+        s->st.direct_static++;
+    } else if (n == c.chunk_tokens && s->exec) {
         e = hipGraphLaunch(s->exec, s->stream);
         if (e != hipSuccess) return device_fail(s, e, "hipGraphLaunch");
         s->st.replays++;
@@ -1187,6 +1214,63 @@ dc_status dc_decode_chunk_f0(dc_state* s, const int32_t* tokens, const float* f0
         return fail(s, DC_EINVAL, "this decoder has no harmonic source: call dc_decode_chunk");
     }
     return decode_call(s, tokens, f0, n, audio_out);
+}
+
+// ------------------------------------------- the static-scratch entry point
+//
+// The one per-call scratch buffer of the step is the harmonic source's phase
+// table: every sinusoid's phase at the start of each f0 frame of the call,
+// written by the phase kernel and read by the source kernel.
+// dc_decode_chunk_f0_static keeps it in this file-scope device array instead
+// of the state's arena.  Each device holds its own copy of the array for the
+// life of the process; its device address is resolved once per device (at
+// the dc_init of the first state with a source on that device), and host code
+// passes only that address to kernels, never the array's name.
+constexpr size_t kStaticScratchBytes = (size_t)4 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// Device address of `scratch` on device dev, which must be current.
+static hipError_t static_scratch(int dev, void** out)
+{
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress((void**)&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+dc_status dc_decode_chunk_f0_static(dc_state* s, const int32_t* tokens, const float* f0, int32_t n,
+                                    float* audio_out)
+{
+    if (!s) return DC_EINVAL;
+    const dc_cfg& c = s->cfg;
+    if (c.n_harmonics == 0) {
+        s->st.rejected++;
+        return fail(s, DC_EINVAL, "this decoder has no harmonic source: it has no per-call scratch to move");
+    }
+    if (n > 0 && n <= c.max_tokens) {
+        const size_t need = (size_t)c.batch * n * s->fpt[0] * (c.n_harmonics + 1) * sizeof(double);
+        if (need > kStaticScratchBytes) {
+            s->st.rejected++;
+            char m[160];
+            std::snprintf(m, sizeof m, "the call's phase table needs %zu bytes, more than the %zu-byte static scratch",
+                          need, kStaticScratchBytes);
+            return fail(s, DC_ERANGE, m);
+        }
+    }
+    if (!s->static_ptab) return fail(s, DC_EDEVICE, "static scratch address was not resolved at dc_init");
+    return decode_call(s, tokens, f0, n, audio_out, s->static_ptab);
 }
 
 dc_status dc_sync(dc_state* s)

@@ -42,8 +42,8 @@ def test_struct_sizes_match_header_layout():
     # dc_cfg: 34 int32 fields + float + uint32 (144 bytes), the source's int32
     # and four floats (164, padded to 168), the uint64 seed and the pointer
     assert ctypes.sizeof(dc.DcCfg) == 168 + 8 + 8
-    # dc_stats: 12 int64, 2 int32, a double, then replays_flush, two int32 and staged_f0
-    assert ctypes.sizeof(dc.DcStats) == 12 * 8 + 2 * 4 + 8 + 8 + 2 * 4 + 8
+    # dc_stats: 12 int64, 2 int32, a double, then replays_flush, two int32, staged_f0 and direct_static
+    assert ctypes.sizeof(dc.DcStats) == 12 * 8 + 2 * 4 + 8 + 8 + 2 * 4 + 8 + 8
 
 
 @pytest.mark.parametrize("name", list(synth.WORKLOADS))
@@ -108,6 +108,7 @@ def test_null_state_calls_fail_closed():
     L = dc.lib()
     assert L.dc_decode_chunk(None, None, 1, None) == dc.DC_EINVAL
     assert L.dc_decode_chunk_f0(None, None, None, 1, None) == dc.DC_EINVAL
+    assert L.dc_decode_chunk_f0_static(None, None, None, 1, None) == dc.DC_EINVAL
     assert L.dc_f0_buffer(None) is None
     assert L.dc_carry_bytes(None) == 0
     assert L.dc_carry_export(None, 0, None, 0) == dc.DC_EINVAL

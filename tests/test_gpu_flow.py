@@ -110,6 +110,8 @@ def _chunks_match_oracle(a, dtype, ncalls):
             want = s.carry(i, l, c, kv)
             assert got.shape == want.shape
             ok, e = _carry_ok(got, want, dtype)
+            e_r15, _ = err_stats(got, want)
+            say(f"  carry {(b, i, l, c, kv)}: audit {e:.3e} (max-abs/RMS {e_r15:.3e})")
             assert ok, f"carry {(b, i, l, c, kv)}: {e:.3e}"
     say(f"  worst max-abs/RMS {worst:.3e}")
     dec.close()
@@ -237,7 +239,39 @@ def test_real_shape_matches_oracle(dtype):
         assert e <= TOL[dtype], f"call {k}: {e:.3e}"
     for (i, l, c, kv) in [(9, 15, 0, 1), (0, 7, 1, 0)]:
         ok, e = _carry_ok(dec.carry(0, i, l, c, kv), s.carry(i, l, c, kv), dtype)
-        say(f"  carry {(i, l, c, kv)}: {e:.3e}")
+        e_r15, _ = err_stats(dec.carry(0, i, l, c, kv), s.carry(i, l, c, kv))
+        say(f"  carry {(i, l, c, kv)}: audit {e:.3e} (max-abs/RMS {e_r15:.3e})")
+        assert ok, f"carry {(i, l, c, kv)}: {e:.3e}"
+    dec.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_real_shape_at_the_papers_extents_matches_oracle(dtype):
+    """The paper-shaped decoder at the paper's operating point: a 302-frame
+    prompt, then four calls of f_call = 56 frames (50 retained plus 6 of
+    lookahead), so the attended extents run 302, 352, 402, 402 and the last two
+    calls cut the carry back to H[0:100] || H[ext - 302:ext] (Eq. carry).
+    Every call's mel against the oracle, and the carry after the last call
+    (the shadow audit) in both metrics."""
+    a = synth.REAL_FLOW_ARCH
+    blob = synth.make_flow_weights(a, 0)
+    P = a["f_prompt"]
+    calls = [a["f_call"]] * 4
+    say(f"flow real {dtype} B=1 P={P} calls={calls}")
+    dec, outs, mu, prompts = _run_gpu(a, dtype, blob, 1, P, calls)
+    assert dec.stats()["replays"] == 4
+    s, ref = _run_oracle(a, dtype, blob, 0, prompts[0], mu[0], calls)
+    assert s.extent == 402
+    for k, (g, r) in enumerate(zip(outs, ref)):
+        e, er = err_stats(g[0], r)
+        say(f"  call {k}: max-abs/RMS {e:.3e}, RMS err/RMS {er:.3e}")
+        assert e <= TOL[dtype], f"call {k}: {e:.3e}"
+    for (i, l, c, kv) in [(9, 15, 0, 1), (0, 7, 1, 0), (5, 3, 0, 0)]:
+        got, want = dec.carry(0, i, l, c, kv), s.carry(i, l, c, kv)
+        assert got.shape == want.shape == (402, a["dim"])
+        e_r15, _ = err_stats(got, want)
+        ok, e = _carry_ok(got, want, dtype)
+        say(f"  carry {(i, l, c, kv)}: audit {e:.3e} (max-abs/RMS {e_r15:.3e})")
         assert ok, f"carry {(i, l, c, kv)}: {e:.3e}"
     dec.close()
 

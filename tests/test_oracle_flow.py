@@ -274,3 +274,102 @@ def test_chunked_with_carry_equals_offline_masked_pass(retained):
     if retained < 1000:
         loose = _offline(a, blob, 6, 1, mu_p, cond_p, spk, mu_c, n_chunks, band=10 ** 6)
         assert np.abs(got - loose)[P + 3 * fc:].max() > 1e-6
+
+
+# ------------------------------------------- a lookahead call (n = f_call > f_chunk)
+
+def _call_torch(arch, W, x, mu, cond, spk, carry):
+    """One call of T frames written with torch primitives: every frame of the
+    call attends to the carry of its (step, block, branch) followed by the
+    call's own frames (no mask).  carry[i][l] is None or (K, V), each
+    [2][len][D] in Eq. carry order.  Returns x_N [T][M] and the call's own
+    keys and values kv[i][l] = (K, V), each [2][T][D]."""
+    D, M, NL, NS, Hh = arch["dim"], arch["n_mel"], arch["depth"], arch["n_steps"], arch["heads"]
+    T = x.shape[0]
+    w = arch["cfg_rate"]
+    t = [1 - math.cos(math.pi / 2 * i / NS) for i in range(NS + 1)]
+    half = arch["t_dim"] // 2
+    freqs = torch.exp(-math.log(10000.0) * torch.arange(half, dtype=torch.float64) / half)
+    sp = spk.expand(T, M)
+    z = torch.zeros_like(mu)
+    kv_out = [[None] * NL for _ in range(NS)]
+    for i in range(NS):
+        arg = 1000.0 * t[i] * freqs
+        emb = torch.cat([torch.cos(arg), torch.sin(arg)])
+        c = Fn.silu(Fn.linear(Fn.silu(Fn.linear(emb, W["t.W1"], W["t.b1"])), W["t.W2"], W["t.b2"]))
+        h = Fn.linear(torch.stack([torch.cat([x, mu, sp, cond], 1), torch.cat([x, z, z, z], 1)]),
+                      W["in.W"], W["in.b"])
+        for l in range(NL):
+            sh1, sc1, g1, sh2, sc2, g2 = Fn.linear(c, W[f"b{l}.ada.W"], W[f"b{l}.ada.b"]).chunk(6)
+            a = Fn.layer_norm(h, (D,), eps=1e-6) * (1 + sc1) + sh1
+            q, k, v = Fn.linear(a, W[f"b{l}.qkv.W"], W[f"b{l}.qkv.b"]).chunk(3, dim=-1)
+            kv_out[i][l] = (k, v)
+            if carry[i][l] is not None:
+                k = torch.cat([carry[i][l][0], k], 1)
+                v = torch.cat([carry[i][l][1], v], 1)
+            heads = lambda y: y.reshape(2, y.shape[1], Hh, D // Hh).transpose(1, 2)
+            o = Fn.scaled_dot_product_attention(heads(q), heads(k), heads(v)).transpose(1, 2).reshape(2, T, D)
+            h = h + g1 * Fn.linear(o, W[f"b{l}.o.W"], W[f"b{l}.o.b"])
+            a = Fn.layer_norm(h, (D,), eps=1e-6) * (1 + sc2) + sh2
+            h = h + g2 * Fn.linear(Fn.gelu(Fn.linear(a, W[f"b{l}.fc1.W"], W[f"b{l}.fc1.b"]), approximate="tanh"),
+                                   W[f"b{l}.fc2.W"], W[f"b{l}.fc2.b"])
+        sh, sc = Fn.linear(c, W["f.ada.W"], W["f.ada.b"]).chunk(2)
+        vel = Fn.linear(Fn.layer_norm(h, (D,), eps=1e-6) * (1 + sc) + sh, W["out.W"], W["out.b"])
+        x = x + (t[i + 1] - t[i]) * ((1 + w) * vel[0] - w * vel[1])
+    return x, kv_out
+
+
+def test_lookahead_calls_retain_their_first_f_chunk_frames():
+    """Calls of f_call = f_chunk + lookahead frames, recomputed with torch
+    primitives over carry || call frames: the lookahead frames enter the call's
+    attention (and are presented again, with the same noise, by the next
+    call), and only the call's first f_chunk frames enter the carry, in front
+    (Eq. carry; reading F5).  Every call's mel and, after every call, the
+    whole carry of every (step, block, branch) must match the oracle.  An
+    oracle that kept the call's last f_chunk frames, or left the lookahead
+    out of the attention, fails here."""
+    a = dict(TINY)
+    fc, fcall, fr, P = a["f_chunk"], a["f_call"], a["f_retained"], a["f_prompt"]
+    L = fr + P
+    NL, NS, M = a["depth"], a["n_steps"], a["n_mel"]
+    blob = synth.make_flow_weights(a, 3)
+    W = {k: torch.tensor(v, dtype=torch.float64) for k, v in synth.split_flow_weights(a, blob).items()}
+    seed, key = 7, 2
+    mu_p, cond_p, spk = synth.make_flow_prompt(a, P, seed=4)
+    n_calls = 4
+    mu_c = synth.make_flow_mu(a, 1, n_calls * fc + fcall, seed=4)[0]
+    s = _stream(a, blob, seed=seed, key=key)
+    s.prompt(mu_p, cond_p, spk)
+    sp = torch.tensor(spk, dtype=torch.float64)
+    x0 = torch.tensor(oracle.flow_noise(M, a["temperature"], seed, key, 0, P))
+    _, kv = _call_torch(a, W, x0, torch.tensor(mu_p), torch.tensor(cond_p), sp, [[None] * NL for _ in range(NS)])
+    carry = [[(kv[i][l][0].clone(), kv[i][l][1].clone()) for l in range(NL)] for i in range(NS)]
+    for k in range(n_calls):
+        tau0 = P + k * fc
+        m = mu_c[k * fc:k * fc + fcall]
+        got = s.chunk(m)
+        x0 = torch.tensor(oracle.flow_noise(M, a["temperature"], seed, key, tau0, fcall))
+        ref, kv = _call_torch(a, W, x0, torch.tensor(m, dtype=torch.float64),
+                              torch.zeros(fcall, M, dtype=torch.float64), sp, carry)
+        err = np.abs(got - ref.numpy()).max()
+        assert err < 1e-11, f"call {k}: mel differs by {err}"
+        # Eq. carry: H = (the first f_chunk frames' K, V) || C, cut back to
+        # H[0:f_retained] || H[ext - f_prompt:ext] when the extent exceeds L
+        for i in range(NS):
+            for l in range(NL):
+                new = []
+                for j in range(2):
+                    H = torch.cat([kv[i][l][j][:, :fc], carry[i][l][j]], 1)
+                    if H.shape[1] > L:
+                        H = torch.cat([H[:, :fr], H[:, H.shape[1] - P:]], 1)
+                    new.append(H)
+                carry[i][l] = tuple(new)
+                for c in range(2):
+                    for j in range(2):
+                        cur = s.carry(i, l, c, j)
+                        want = carry[i][l][j][c].numpy()
+                        assert cur.shape == want.shape, (k, i, l, c, j, cur.shape, want.shape)
+                        assert np.abs(cur - want).max() < 1e-11, (k, i, l, c, j)
+        # the front of the carry holds the keys of this call's first f_chunk frames
+        assert np.abs(s.carry(0, 0, 0, 0)[:fc] - kv[0][0][0][0, :fc].numpy()).max() < 1e-11
+    assert s.position == P + n_calls * fc

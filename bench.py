@@ -56,29 +56,41 @@ class _Addr:
         return self.addr
 
 
-def cpu_baseline(arch, dtype, blob, tokens, budget_s: float, f0=None):
-    """Time the oracle (as it stands) decoding a prefix of stream 0, growing the
-    prefix until one run takes budget_s or the workload's tokens run out."""
+def cpu_baseline(arch, dtype, blob, tokens, budget_s: float, f0=None, streams=(0,), max_tokens=None):
+    """Time the oracle (as it stands) decoding a prefix of each stream in
+    `streams` (budget_s split evenly between them), growing the prefix until
+    one run takes its share of the budget or the workload's tokens (or
+    max_tokens) run out.  Returns the baseline record and each stream's
+    oracle PCM of its prefix (the parity reference on the same subset)."""
     import oracle
     from paper_2609_35115_amd import synth
     spt = synth.samples_per_token(arch)
     fpt = arch["frames_per_token"]
-    T_full = tokens.shape[1]
-    T = min(T_full, 4)
-    while True:
-        t0 = time.perf_counter()
-        if f0 is None:
-            oracle.decode(arch, dtype, blob, tokens[0, :T])
-        else:
-            oracle.decode(arch, dtype, blob, tokens[0, :T], f0=f0[0, :T * fpt], seed=RNG_SEED, stream=0)
-        dt = time.perf_counter() - t0
-        if dt >= budget_s or T >= T_full:
-            break
-        T = min(T_full, max(2 * T, int(T * budget_s / max(dt, 1e-3) * 1.05)))
-    return {"value": T * spt / synth.SAMPLE_RATE / dt, "unit": "audio-s/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"stream 0, tokens [0,{T}) of the workload decoded offline in fp64"
-                      f"{' on bf16-rounded weights' if dtype == 'bf16' else ''}, {dt:.1f} s wall"}
+    T_full = tokens.shape[1] if max_tokens is None else min(tokens.shape[1], max_tokens)
+    share = budget_s / len(streams)
+    total_audio, total_wall, refs, parts = 0.0, 0.0, {}, []
+    for b in streams:
+        T = min(T_full, 4)
+        while True:
+            t0 = time.perf_counter()
+            if f0 is None:
+                ref = oracle.decode(arch, dtype, blob, tokens[b, :T])
+            else:
+                ref = oracle.decode(arch, dtype, blob, tokens[b, :T], f0=f0[b, :T * fpt], seed=RNG_SEED, stream=b)
+            dt = time.perf_counter() - t0
+            if dt >= share or T >= T_full:
+                break
+            T = min(T_full, max(2 * T, int(T * share / max(dt, 1e-3) * 1.05)))
+        total_audio += T * spt / synth.SAMPLE_RATE
+        total_wall += dt
+        refs[b] = ref
+        parts.append(f"{b}: [0,{T})")
+    rec = {"value": total_audio / total_wall, "unit": "audio-s/s", "cores": oracle.num_threads(),
+           "kind": "oracle",
+           "sample": f"stream{'s' if len(streams) > 1 else ''} {', '.join(parts)} of the workload's tokens decoded "
+                     f"offline in fp64{' on bf16-rounded weights' if dtype == 'bf16' else ''}, "
+                     f"{total_wall:.1f} s wall"}
+    return rec, refs
 
 
 FLOW_FRAME_RATE = 50.0   # frames per second of audio: 2 frames per 25 Hz token
@@ -503,6 +515,8 @@ def main():
     ap.add_argument("--tile-variant", type=int, default=0)
     ap.add_argument("--skip-peaks", action="store_true", help="skip the device copy and GEMM peak runs "
                     "(for profiler runs; the roofline then has no measured-peak fraction)")
+    ap.add_argument("--no-configs", action="store_true", help="time only the named workload (by default the "
+                    "headline workload is followed by the other configurations in a 'configs' object)")
     ap.add_argument("--only-steps", action="store_true", help="flow workloads: run the warmup and timed steps only "
                     "and print their timing (for hardware-counter runs, which serialise every dispatch)")
     args = ap.parse_args()
@@ -515,17 +529,43 @@ def main():
     if args.workload.startswith("flow_"):
         return bench_flow(args)
 
+    peaks = None if args.skip_peaks else measured_peaks()
+    out = bench_vocoder(args.workload, args.steps, args.warmup, args, peaks, headline=True)
+    if not args.no_configs and args.workload == DEFAULT_WORKLOAD:
+        out["configs"] = {}
+        for name, (steps, warmup, latency) in CONFIG_RUNS.items():
+            out["configs"][name] = bench_vocoder(name, steps, warmup, args, peaks, latency_chunks=latency)
+    print(json.dumps(out), flush=True)
+
+
+# The other configurations timed beside the headline (steps, warmup, latency
+# calls): the tiny decoder, batch 16, the 4-token chunk, batch 128.
+CONFIG_RUNS = {
+    "tiny_f32_b1_n8": (200, 8, 100),
+    "real_bf16_b16_n25": (100, 20, 50),
+    "real_bf16_b1_n4": (400, 50, 200),
+    "real_bf16_b128_n25": (40, 20, 20),
+}
+# Oracle subsets of the CPU baseline and the parity check (streams of each
+# workload): the batch-16 and batch-128 workloads on three and two streams.
+CPU_STREAMS = {"real_bf16_b16_n25": (0, 7, 15), "real_bf16_b128_n25": (0, 127), "real_bf16_b16_n25_nsf": (0, 7, 15)}
+
+
+def bench_vocoder(name, steps, warmup, args, peaks, headline=False, latency_chunks=None):
+    """Time one vocoder workload; returns its record (the headline fields, or
+    the per-configuration fields for a non-headline workload)."""
     import numpy as np
     import torch
 
     import paper_2609_35115_amd as dc
     from paper_2609_35115_amd import synth
 
-    w = synth.workload(args.workload)
+    w = synth.workload(name)
     arch, dtype, B, n, chunks = w["arch"], w["dtype"], w["batch"], w["chunk_tokens"], w["chunks"]
     spt = synth.samples_per_token(arch)
     fpt = arch["frames_per_token"]
     has_src = arch.get("n_harmonics", 0) > 0
+    latency_chunks = args.latency_chunks if latency_chunks is None else latency_chunks
     torch.cuda.set_device(0)
     blob = synth.make_weights(arch, 0)
     tokens = synth.make_tokens(arch, B, chunks * n)
@@ -546,28 +586,40 @@ def main():
         if st != dc.DC_OK:
             raise dc.DcError(st, dc.dc_last_error(dec.h))
 
-    print(f"# workload {args.workload}: batch {B}, chunk {n} tokens, {dtype}; warmup {args.warmup}, "
-          f"steps {args.steps}", file=sys.stderr, flush=True)
-    for i in range(args.warmup):
-        step(i)
+    print(f"# workload {name}: batch {B}, chunk {n} tokens, {dtype}; warmup {warmup}, steps {steps}",
+          file=sys.stderr, flush=True)
+    # warmup: the first chunks of every stream from the start, replayed like
+    # the timed steps; the PCM of the oracle subset's streams is kept for the
+    # parity check
+    cpu_streams = CPU_STREAMS.get(name, (0,))
+    sel = torch.tensor(cpu_streams, device="cuda")
+    kept = []
+    for i in range(warmup):
+        if has_src:
+            out_i = dec.decode(tok_dev[i % chunks], f0_dev[i % chunks])
+        else:
+            out_i = dec.decode(tok_dev[i % chunks])
+        if i < chunks:
+            kept.append(out_i.index_select(0, sel))
     dec.sync()
+    kept = torch.cat(kept, dim=1).cpu().numpy() if kept else None
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(args.warmup + i)
+    for i in range(steps):
+        step(warmup + i)
     dec.stream.synchronize()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     dec.sync()
-    ms_per_step = 1000.0 * wall / args.steps
+    ms_per_step = 1000.0 * wall / steps
     audio_s = B * n * spt / synth.SAMPLE_RATE
-    value = audio_s * args.steps / wall
-    print(f"# timed {args.steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
+    value = audio_s * steps / wall
+    print(f"# timed {steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
 
     # device-resident buffers: submit, then wait for the PCM on the device
     lat_dev, lat_ev = [], []
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    for i in range(args.latency_chunks):
+    for i in range(latency_chunks):
         t = time.perf_counter()
         ev[0].record(dec.stream)
         step(i)
@@ -580,9 +632,17 @@ def main():
     layers = dec.layers()
     us = dec.time_layers(args.layer_reps)
     roof = roofline(layers, us, dtype)
-    roof["traffic"] = traffic_from_profiles(args.workload, roof["kernel"])
+    roof["traffic"] = traffic_from_profiles(name, roof["kernel"])
+    flops_step = sum(l["flops"] for l in layers)
+    op = "bf16" if dtype == "bf16" else "f32"
+    # the whole step against the MFMA peak of its operand type: step FLOPs over
+    # the timed loop's wall time per step
+    roof["step"] = {"achieved": round(flops_step / (ms_per_step * 1e-3) / 1e12, 2), "peak": PEAK[op],
+                    "unit": "TFLOP/s", "frac": round(flops_step / (ms_per_step * 1e-3) / 1e12 / PEAK[op], 4)}
     stats = dec.stats()
     dec.close()
+    del tok_dev, f0_dev
+    torch.cuda.empty_cache()
 
     # host buffers: dc_decode_chunk uploads the tokens, replays the step and
     # returns once the PCM is in host memory
@@ -592,7 +652,7 @@ def main():
     host_tok = [np.ascontiguousarray(tokens[:, c * n:(c + 1) * n]) for c in range(chunks)]
     host_f0 = [np.ascontiguousarray(f0[:, c * n * fpt:(c + 1) * n * fpt]) for c in range(chunks)] if has_src else None
     lat = []
-    for i in range(args.warmup + args.latency_chunks):
+    for i in range(min(warmup, 20) + latency_chunks):
         t = time.perf_counter()
         if has_src:
             st = dc.dc_decode_chunk_f0(hdec.h, host_tok[i % chunks], host_f0[i % chunks], n, pcm)
@@ -601,45 +661,60 @@ def main():
         dt = 1000.0 * (time.perf_counter() - t)
         if st != dc.DC_OK:
             raise dc.DcError(st, dc.dc_last_error(hdec.h))
-        if i >= args.warmup:
+        if i >= min(warmup, 20):
             lat.append(dt)
     hdec.close()
 
-    if not args.skip_peaks:
-        peaks = measured_peaks()
+    if peaks is not None:
         key = "hbm_copy_GBs" if roof["bound"] == "hbm" else f"{roof['operand']}_gemm_TFLOPs"
         roof["measured_peak"] = peaks[key]
         roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
-        roof["measured_peaks"] = peaks
-    print(f"# roofline: {roof['kernel']} {roof['achieved']} {roof['unit']} ({roof['frac']:.1%})",
-          file=sys.stderr, flush=True)
+        if headline:
+            roof["measured_peaks"] = peaks
+    print(f"# roofline: {roof['kernel']} {roof['achieved']} {roof['unit']} ({roof['frac']:.1%}); "
+          f"step {roof['step']['achieved']} TFLOP/s ({roof['step']['frac']:.1%})", file=sys.stderr, flush=True)
 
-    cpu = None
+    cpu = parity = None
     if args.cpu_budget > 0:
-        cpu = cpu_baseline(arch, dtype, blob, tokens, args.cpu_budget, f0)
+        cpu, refs = cpu_baseline(arch, dtype, blob, tokens, args.cpu_budget, f0, streams=cpu_streams,
+                                 max_tokens=min(warmup, chunks) * n)
+        # the GPU's replayed warmup chunks against the oracle on the same subset
+        tol = 1e-4 if dtype == "f32" else 2e-2
+        worst = 0.0
+        for j, b in enumerate(cpu_streams):
+            ref = refs[b]
+            got = kept[j, :ref.size].astype(np.float64)
+            e = float(np.abs(got - ref).max() / np.sqrt(np.mean(ref ** 2)))
+            worst = max(worst, e)
+        parity = {"streams": list(cpu_streams), "samples_per_stream": [int(refs[b].size) for b in cpu_streams],
+                  "max_abs_err_over_rms": round(worst, 6), "tolerance": tol, "ok": worst <= tol}
 
-    out = {
-        "metric": METRIC, "value": round(value, 3), "unit": "audio-s/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
-        "data": "synthetic (seeded random-weight decoder and uniform token ids"
-                + (", synthetic f0 contours)" if has_src else ")"),
-        "config": {"workload": args.workload, "arch": "real" if arch["embed"] == 512 else "tiny",
-                   "batch": B, "chunk_tokens": n, "chunks_cycled": chunks,
-                   "audio_s_per_step": audio_s, "graph_replay": stats["replays"] > 0,
-                   "kernels_per_step": stats["kernels_per_step"],
-                   "flops_per_step": sum(l["flops"] for l in layers)},
+    lat_fields = {
         "p50_chunk_ms": round(float(np.percentile(lat, 50)), 4),
         "p99_chunk_ms": round(float(np.percentile(lat, 99)), 4),
         "latency_path": "host tokens in, host PCM out, synchronous dc_decode_chunk",
         "p50_chunk_ms_device_buffers": round(float(np.percentile(lat_dev, 50)), 4),
         "p99_chunk_ms_device_buffers": round(float(np.percentile(lat_dev, 99)), 4),
         "p50_replay_ms_hip_events": round(float(np.percentile(lat_ev, 50)), 4),
-        "capture_ms": round(stats["capture_ms"], 3),
-        "roofline": roof,
-        "cpu_baseline": cpu,
     }
-    print(json.dumps(out), flush=True)
+    config = {"workload": name, "arch": "real" if arch["embed"] == 512 else "tiny",
+              "batch": B, "chunk_tokens": n, "chunks_cycled": chunks,
+              "audio_s_per_step": audio_s, "graph_replay": stats["replays"] > 0,
+              "kernels_per_step": stats["kernels_per_step"], "flops_per_step": flops_step}
+    if not headline:
+        return {"value": round(value, 3), "unit": "audio-s/s" if arch["embed"] == 512 else "nominal audio-s/s",
+                "steps": steps, "warmup": warmup, "ms_per_step": round(ms_per_step, 4), "dtype": dtype,
+                "config": config, **lat_fields, "capture_ms": round(stats["capture_ms"], 3),
+                "roofline": roof, "cpu_baseline": cpu, "parity": parity}
+    return {
+        "metric": METRIC, "value": round(value, 3), "unit": "audio-s/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+        "data": "synthetic (seeded random-weight decoder and uniform token ids"
+                + (", synthetic f0 contours)" if has_src else ")"),
+        "config": config, **lat_fields, "capture_ms": round(stats["capture_ms"], 3),
+        "roofline": roof, "cpu_baseline": cpu, "parity": parity,
+    }
 
 
 if __name__ == "__main__":

@@ -313,7 +313,7 @@ dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32
  * kernel launches ("layers": embed, each conv / transposed conv -- the
  * convs at one position of the parallel resblock branches share a launch,
  * and a fused resblock pair is one launch --,
- * head, spectrum, overlap-add, clock).  dc_layer_info describes launch i at
+ * head, the iSTFT tail, clock).  dc_layer_info describes launch i at
  * n = chunk_tokens: its kernel (the demangled name a profiler shows), the
  * GEMM shape of a conv (rows = batch * frames, cols, depth = taps * input
  * channels, summed over the launch's convs), its algorithmic FLOPs (2 *

@@ -182,13 +182,11 @@ hipError_t launch_conv(int v, bool bf16, const ConvParams* ps, int count, hipStr
 hipError_t launch_embed(const int32_t* tokens, int n, int B, const void* table, int vocab, int C,
                         int elem, int fpt, Ring out, const int64_t* clock, int* err, hipStream_t st);
 
-// Head output [B][F][2*(N/2+1)] -> windowed inverse-DFT frames in the G ring.
-hipError_t launch_spectrum(const float* head, int64_t head_R, int B, int F, const float* table,
-                           Ring g, const int64_t* clock, int64_t fpt, hipStream_t st);
-
-// G ring -> PCM [B][F*hop] (row stride F*hop), overlap-added in ascending frame order.
-hipError_t launch_ola(Ring g, int B, int F, int hop, int n_fft, float* pcm, const int64_t* clock,
-                      int64_t fpt, hipStream_t st);
+// Head output -> PCM [B][F*hop] in one launch (spectrum, iDFT, window and
+// overlap-add; n_fft = 16, hop = 4); writes the call's last 3 windowed frames
+// to the G ring (the next call's left context) and reads the previous call's.
+hipError_t launch_istft(const float* head, int64_t head_R, int B, int F, const float* table, Ring g, float* pcm,
+                        const int64_t* clock, int64_t fpt, hipStream_t st);
 
 // Harmonic-plus-noise excitation source of one call.
 struct SourceParams {

@@ -1479,93 +1479,105 @@ hipError_t launch_embed(const int32_t* tokens, int n, int B, const void* table, 
 }
 
 // ------------------------------------------------ spectrum + iDFT + window
-
-// One thread per (stream, frame m): X_kk = exp(logmag_kk) (cos ph_kk + i sin ph_kk),
-// g[n] = sum_kk Tre[n][kk] Re X_kk + Tim[n][kk] Im X_kk, where the tables fold
-// the real inverse DFT, the periodic Hann window and the overlap-add
-// normaliser (computed in double on the host from their definitions).  The
-// windowed frame g goes to the G ring, whose zeroed slots stand for frames
-// before the start of the stream.
+//
+// The tables fold the real inverse DFT, the periodic Hann window and the
+// overlap-add normaliser (computed in double on the host from their
+// definitions): g[n] = sum_kk Tre[n][kk] Re X_kk + Tim[n][kk] Im X_kk with
+// X_kk = exp(logmag_kk) (cos ph_kk + i sin ph_kk).  A windowed frame's zeroed
+// ring slot stands for a frame before the start of the stream.
 constexpr int kNFFT = 16, kBins = 9;
 
-__global__ __launch_bounds__(256) void spectrum_kernel(const float* head, int64_t head_R, int B, int F,
-                                                       const float* table, Ring g, const int64_t* clock,
-                                                       int64_t fpt)
+// ----------------------------------------------- iSTFT tail, one kernel
+//
+// Spectrum, inverse DFT, window and overlap-add of one call in one launch.  A
+// block owns kTail consecutive frames [f0, f0 + kTail) of one stream: each
+// thread turns one frame's log-magnitude and phase into its windowed frame g
+// in LDS (exp and sincos per bin, then per output sample a chain of fmas over
+// the bins in ascending order, real part before imaginary), where the block
+// also holds the 3 frames before f0 -- recomputed from the head output when
+// they belong to this call, read from the G ring when they are the previous
+// call's.  Then each thread overlap-adds the hop = 4 samples of its frame
+// from the LDS rows of the 4 frames that cover them, in ascending frame order
+// starting from +0, and stores them as one vector.  Only the call's last 3
+// frames go to the G ring: they are the next call's left context.  Every
+// sample's arithmetic depends only on its frame index, so a frame gives the
+// same bits in any block, call or chunking.
+constexpr int kTail = 256;
+
+__global__ __launch_bounds__(256) void istft_kernel(const float* head, int64_t head_R, int B, int F,
+                                                    const float* table, Ring g, float* pcm,
+                                                    const int64_t* clock, int64_t fpt)
 {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)B * F) return;
-    const int b = (int)(i / F), m = (int)(i % F);
-    const int64_t tau = clock[0] * fpt + m;
-    const float* s = head + ((size_t)b * head_R + ring_slot(tau, head_R)) * (2 * kBins);
-    float re[kBins], im[kBins];
+    constexpr int W = kNFFT + 1;                 // LDS row stride (odd: no bank conflicts)
+    __shared__ float G[(kTail + 3) * W];
+    const int tiles = (F + kTail - 1) / kTail;
+    const int b = blockIdx.x / tiles, f0 = (blockIdx.x - b * tiles) * kTail;
+    const int64_t tau0 = clock[0] * fpt;          // absolute index of this call's frame 0
+    float* gb = (float*)g.ptr + (size_t)b * g.R * kNFFT;
+    for (int i = threadIdx.x; i < kTail + 3; i += blockDim.x) {
+        const int m = f0 - 3 + i;                 // frame of this call (negative: the previous call's)
+        if (m >= F) continue;
+        float* row = G + i * W;
+        const int64_t tau = tau0 + m;
+        if (m < 0) {
+            const float* src = gb + ring_slot(tau, g.R) * kNFFT;
 #pragma unroll
-    for (int kk = 0; kk < kBins; kk++) {
-        const float mag = expf(s[kk]);
-        float sn, cs;
-        sincosf(s[kBins + kk], &sn, &cs);
-        re[kk] = mag * cs;
-        im[kk] = mag * sn;
-    }
-    float* out = (float*)g.ptr + ((size_t)b * g.R + ring_slot(tau, g.R)) * kNFFT;
+            for (int k = 0; k < kNFFT; k++) row[k] = src[k];
+            continue;
+        }
+        const float* sp = head + ((size_t)b * head_R + ring_slot(tau, head_R)) * (2 * kBins);
+        float re[kBins], im[kBins];
 #pragma unroll
-    for (int n4 = 0; n4 < kNFFT; n4 += 4) {
-        f32x4 o;
+        for (int kk = 0; kk < kBins; kk++) {
+            const float mag = expf(sp[kk]);
+            float sn, cs;
+            sincosf(sp[kBins + kk], &sn, &cs);
+            re[kk] = mag * cs;
+            im[kk] = mag * sn;
+        }
 #pragma unroll
-        for (int e = 0; e < 4; e++) {
-            const float* tr = table + (n4 + e) * kBins;
-            const float* ti = table + kNFFT * kBins + (n4 + e) * kBins;
+        for (int n = 0; n < kNFFT; n++) {
+            const float* tr = table + n * kBins;
+            const float* ti = table + kNFFT * kBins + n * kBins;
             float v = 0.f;
 #pragma unroll
             for (int kk = 0; kk < kBins; kk++) {
                 v = fmaf(tr[kk], re[kk], v);
                 v = fmaf(ti[kk], im[kk], v);
             }
-            o[e] = v;
+            row[n] = v;
         }
-        *(f32x4*)(out + n4) = o;
+        if (m >= F - 3 && i >= 3) {               // the next call's left context
+            float* dst = gb + ring_slot(tau, g.R) * kNFFT;
+#pragma unroll
+            for (int n4 = 0; n4 < kNFFT; n4 += 4)
+                *(f32x4*)(dst + n4) = f32x4{row[n4], row[n4 + 1], row[n4 + 2], row[n4 + 3]};
+        }
+    }
+    __syncthreads();
+    const int t = threadIdx.x, m = f0 + t;
+    if (t < kTail && m < F) {
+        // samples 4m + r: frames m - 3 + q (q = 0..3) at offset 12 - 4q + r
+        f32x4 o;
+#pragma unroll
+        for (int r = 0; r < 4; r++) {
+            float acc = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; q++) acc = acc + G[(t + q) * W + 12 - 4 * q + r];
+            o[r] = acc;
+        }
+        *(f32x4*)(pcm + (size_t)b * F * 4 + 4 * (size_t)m) = o;
     }
 }
 
-hipError_t launch_spectrum(const float* head, int64_t head_R, int B, int F, const float* table, Ring g,
-                           const int64_t* clock, int64_t fpt, hipStream_t st)
+hipError_t launch_istft(const float* head, int64_t head_R, int B, int F, const float* table, Ring g, float* pcm,
+                        const int64_t* clock, int64_t fpt, hipStream_t st)
 {
-    const int64_t total = (int64_t)B * F;
-    hipLaunchKernelGGL(spectrum_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, head, head_R,
-                       B, F, table, g, clock, fpt);
-    return hipGetLastError();
-}
-
-// ------------------------------------------------------------ overlap-add
-
-// Sample T = hop*m0 + t: sum over the frames m = floor(T/hop) - (n_fft/hop - 1)
-// .. floor(T/hop) of g_m[T - hop*m], added in ascending m from +0.
-__global__ __launch_bounds__(256) void ola_kernel(Ring g, int B, int F, int hop, int n_fft, float* pcm,
-                                                  const int64_t* clock, int64_t fpt)
-{
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t per = (int64_t)F * hop;
-    if (i >= (int64_t)B * per) return;
-    const int b = (int)(i / per);
-    const int64_t t = i % per;
-    const int64_t m0 = clock[0] * fpt;
-    const int64_t T = m0 * hop + t;
-    const int64_t mu = m0 + t / hop;
-    const float* base = (const float*)g.ptr + (size_t)b * g.R * kNFFT;
-    float acc = 0.f;
-    for (int64_t m = mu - (n_fft / hop - 1); m <= mu; m++)
-        acc = acc + base[ring_slot(m, g.R) * kNFFT + (T - hop * m)];
-    pcm[(size_t)b * per + t] = acc;
-}
-
-hipError_t launch_ola(Ring g, int B, int F, int hop, int n_fft, float* pcm, const int64_t* clock, int64_t fpt,
-                      hipStream_t st)
-{
-    const int64_t total = (int64_t)B * F * hop;
-    hipLaunchKernelGGL(ola_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, g, B, F, hop, n_fft,
+    const int tiles = (F + kTail - 1) / kTail;
+    hipLaunchKernelGGL(istft_kernel, dim3((unsigned)(B * tiles)), dim3(256), 0, st, head, head_R, B, F, table, g,
                        pcm, clock, fpt);
     return hipGetLastError();
 }
-
 
 // ------------------------------------------------ harmonic-plus-noise source
 //

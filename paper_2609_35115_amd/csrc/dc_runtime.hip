@@ -54,7 +54,7 @@ struct ConvOp {
 };
 
 // One kernel launch of a chunk step.
-enum LaunchKind { L_EMBED, L_CONV, L_PAIR, L_SPECTRUM, L_OLA, L_CLOCK, L_PHASE, L_SOURCE };
+enum LaunchKind { L_EMBED, L_CONV, L_PAIR, L_ISTFT, L_CLOCK, L_PHASE, L_SOURCE };
 struct Launch {
     LaunchKind kind;
     std::vector<int> convs;   // members of a conv launch (same tile shape; parallel branches);
@@ -691,15 +691,15 @@ static void build_schedule(dc_state* s)
                 }
             }
     }
-    s->launches.push_back({L_SPECTRUM, {}, "spectrum"});
-    s->launches.push_back({L_OLA, {}, "ola"});
+    s->launches.push_back({L_ISTFT, {}, "istft"});
     s->launches.push_back({L_CLOCK, {}, "clock"});
 }
 
 // ------------------------------------------------------------ one chunk step
 //
 // A step is a fixed list of launches ("layers"): 0 embed, 1..C the convs in
-// network order, then spectrum, overlap-add and clock.
+// network order, then the iSTFT tail (spectrum, iDFT, window, overlap-add)
+// and the clock.
 
 static int layer_count(const dc_state* s) { return (int)s->launches.size(); }
 
@@ -856,11 +856,9 @@ static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st, double
         return launch_phase(source_params(s, n, ptab), st);
     case L_SOURCE:
         return launch_source(source_params(s, n, ptab), st);
-    case L_SPECTRUM:
-        return launch_spectrum((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL,
-                               s->table, s->rings[s->ring_G], s->clock, s->fpt[L], st);
-    case L_OLA:
-        return launch_ola(s->rings[s->ring_G], c.batch, FL, c.hop, c.n_fft, s->audio, s->clock, s->fpt[L], st);
+    case L_ISTFT:
+        return launch_istft((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL, s->table,
+                            s->rings[s->ring_G], s->audio, s->clock, s->fpt[L], st);
     default:
         return launch_clock(s->clock, n, st);
     }
@@ -1615,13 +1613,9 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
         out->bytes = B * F0 * 4 + B * F0 * H1 * 8 + B * FL * c.hop * 4;
         break;
     }
-    case L_SPECTRUM:
-        set("dc::spectrum_kernel");
-        out->bytes = B * FL * (2 * (c.n_fft / 2 + 1) + c.n_fft) * 4;
-        break;
-    case L_OLA:
-        set("dc::ola_kernel");
-        out->bytes = B * FL * c.n_fft * 4 + B * FL * c.hop * 4;
+    case L_ISTFT:   // head output in, PCM out, the 3-frame left context in and out
+        set("dc::istft_kernel");
+        out->bytes = B * FL * (2 * (c.n_fft / 2 + 1) + c.hop) * 4 + 2.0 * B * (c.n_fft / c.hop - 1) * c.n_fft * 4;
         break;
     default:
         set("dc::clock_kernel");

@@ -167,6 +167,19 @@ def calibrate_copy():
     print(f"copied {n} bytes 3 times", flush=True)
 
 
+def calibrate_read():
+    """A read-only pass over 256 MiB, three times (torch's sum of 64 Mi floats):
+    checks the FETCH_SIZE factor of the copy calibration on a kernel that
+    writes nothing but its partial sums."""
+    import torch
+    x = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    for _ in range(3):
+        s = x.sum()
+    torch.cuda.synchronize()
+    print(f"read {x.numel() * 4} bytes 3 times (sum {float(s)})", flush=True)
+
+
 def measured_peaks():
     """Achievable rates on this device: a 1 GiB device copy (read + write bytes)
     and 8192^3 library GEMMs in bf16 and fp32, best of several timed runs."""
@@ -500,6 +513,8 @@ def main():
         return summarize_mfma(*sys.argv[2:6])
     if len(sys.argv) > 1 and sys.argv[1] == "--calibrate-copy":
         return calibrate_copy()
+    if len(sys.argv) > 1 and sys.argv[1] == "--calibrate-read":
+        return calibrate_read()
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize-stats":
         return summarize_stats(sys.argv[2], sys.argv[3], sys.argv[4])
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize-traffic":

@@ -28,6 +28,17 @@ def build() -> str:
     return _LIB
 
 
+def build_sanitized(out: str) -> str:
+    """The same sources with AddressSanitizer and UndefinedBehaviorSanitizer
+    (host code, gcc; single-threaded, any sanitizer report aborts the
+    process).  Load it by setting DC_ORACLE_LIB to `out` in a process started
+    with the sanitizer runtime preloaded."""
+    subprocess.run(["gcc", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                    "-fno-sanitize-recover=all", "-fPIC", "-shared", "-Wall", "-Wno-unknown-pragmas",
+                    "-std=gnu11", "-o", out, *_SRCS, "-lm"], check=True)
+    return out
+
+
 class _Arch(ctypes.Structure):
     _fields_ = [
         ("vocab", ctypes.c_int), ("embed", ctypes.c_int), ("frames_per_token", ctypes.c_int),
@@ -46,9 +57,12 @@ class _Arch(ctypes.Structure):
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(f) for f in _SRCS):
-            build()
-        lib = ctypes.CDLL(_LIB)
+        path = os.environ.get("DC_ORACLE_LIB")   # a sanitized build (tests)
+        if path is None:
+            path = _LIB
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(f) for f in _SRCS):
+                build()
+        lib = ctypes.CDLL(path)
         D = ctypes.POINTER(ctypes.c_double)
         F = ctypes.POINTER(ctypes.c_float)
         I = ctypes.POINTER(ctypes.c_int32)

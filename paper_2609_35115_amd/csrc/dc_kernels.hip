@@ -17,10 +17,6 @@
 #include "dc_internal.h"
 #include "dc_philox.h"
 
-#ifndef DC_LOAD_BATCH
-#define DC_LOAD_BATCH 1
-#endif
-
 
 namespace dc {
 
@@ -928,6 +924,7 @@ static const TileShape kTiles[] = {
     {4, 4, 4, 1, 1, 4, 1}, // 24: 256x64
     {2, 4, 4, 1, 1, 4, 1}, // 25: 128x64
     {1, 4, 4, 1, 1, 4, 1}, // 26: 64x64
+    {2, 2, 1, 1, 4, 8},    // 27: 32x32, 4 partitions, 8-chunk channel block
 };
 
 int num_tile_variants() { return (int)(sizeof(kTiles) / sizeof(kTiles[0])); }
@@ -983,7 +980,7 @@ static hipError_t launch_w(const ConvGroup& g, int count, size_t lds, hipStream_
 template <bool BF16>
 static hipError_t launch_dt(int v, const ConvGroup& p, int count, size_t lds, hipStream_t st)
 {
-    if (v >= 20) {
+    if (v >= 20 && v <= 26) {
         if (!BF16) return hipErrorInvalidValue;
         switch (v) {
         case 20: return launch_w<4, 4, 2, 2, 4>(p, count, lds, st);
@@ -1017,6 +1014,7 @@ static hipError_t launch_dt(int v, const ConvGroup& p, int count, size_t lds, hi
     case 17: return launch_t<BF16, 1, 1, 1, 1, 4, 32>(p, count, lds, st);
     case 18: return launch_t<BF16, 1, 2, 1, 1, 4, 16>(p, count, lds, st);
     case 19: return launch_t<BF16, 1, 1, 2, 2, 1, 1>(p, count, lds, st);
+    case 27: return launch_t<BF16, 2, 2, 1, 1, 4, 8>(p, count, lds, st);
     default: return hipErrorInvalidValue;
     }
 }

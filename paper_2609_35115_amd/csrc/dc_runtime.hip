@@ -314,9 +314,9 @@ static const int kPreferRing[] = {20, 24, 22, 21, 25, 23};
 // streaming class (batch below DC_BATCHED_MIN), whose calls leave too few
 // output tiles to fill the machine, else 1.  Then the channel block:
 // as wide as the layer's channels (capped at 4 chunks for unsplit tiles),
-// so no K step is padding.  Then the tile: for split K the one that best
-// fills the machine, otherwise the first in preference order that keeps
-// enough blocks.
+// so no K step is padding.  Then the tile: for split K the largest that still
+// gives the launch about three waves per SIMD, otherwise the first in
+// preference order that keeps enough blocks.
 static int pick_variant(const dc_state* s, const ConvOp& op)
 {
     const int64_t B = s->cfg.batch;
@@ -387,8 +387,11 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
             if (t.WGK != wgk || t.KCH != kch || !variant_fits(op, v)) continue;
             double score;
             if (wgk == 4) {
-                const double waves = (double)blocks(t) * 4.0;
-                score = (waves < 2048.0 ? waves : 2048.0) * eff(t) * (t.MB * t.NB >= 2 ? 1.0 : 0.85);
+                // waves of the whole launch (all its members) up to three per
+                // SIMD, then larger tiles: each wave's operands then serve
+                // more MFMAs and the layer's weights are read by fewer blocks
+                const double waves = (double)(members * blocks(t)) * 4.0;
+                score = (waves < 3072.0 ? waves : 3072.0) * eff(t) * (1.0 + 0.1 * std::log2((double)(t.MB * t.NB)));
             } else {
                 // the first shape in preference order that keeps enough blocks
                 if (members * blocks(t) >= 512 && eff(t) >= 0.75) return v;

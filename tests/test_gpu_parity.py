@@ -109,20 +109,21 @@ def test_graph_replay_equals_direct_launch(arch_name, dtype):
 # partitions across waves and channel block -- and fit every layer of the
 # case: their results must be identical.
 TILE_GROUPS = {
-    ("tiny", "f32"): [7, 10, 13],      # 32x32, 64x64, 128x64; unsplit K, 32-channel blocks
-    ("real", "f32"): [1, 4, 6],        # 16x16, 16x32, 32x32; K in 4 partitions, 64-channel blocks
-    ("real", "bf16"): [8, 9, 11,       # 32x32, 32x64, 64x64; unsplit K, 128-channel blocks
-                       21, 22, 25, 26, 27],   # the same with weights through the LDS ring
+    ("tiny", "f32", "unsplit"): [7, 10, 13],     # 32x32, 64x64, 128x64; unsplit K, 32-channel blocks
+    ("real", "f32", "kch4"): [1, 4, 6],          # 16x16, 16x32, 32x32; K in 4 partitions, 64-channel blocks
+    ("real", "f32", "kch8"): [2, 5, 28],         # 16x16, 16x32, 32x32; K in 4 partitions, 128-channel blocks
+    ("real", "bf16", "unsplit"): [8, 9, 11,      # 32x32, 32x64, 64x64; unsplit K, 128-channel blocks
+                                  21, 22, 25, 26, 27],   # the same with weights through the LDS ring
 }
 
 
-@pytest.mark.parametrize("arch_name,dtype", list(TILE_GROUPS))
-def test_tile_shape_does_not_change_results(arch_name, dtype):
+@pytest.mark.parametrize("arch_name,dtype,group", list(TILE_GROUPS))
+def test_tile_shape_does_not_change_results(arch_name, dtype, group):
     arch = TINY if arch_name == "tiny" else REAL
     n = 8 if arch_name == "tiny" else 3
     blob = synth.make_weights(arch, 2)
     ids = synth.make_tokens(arch, 1, 2 * n)
-    variants = TILE_GROUPS[(arch_name, dtype)]
+    variants = TILE_GROUPS[(arch_name, dtype, group)]
     ref = None
     for v in variants:
         dec = dc.Decoder(arch, dtype, blob, batch=1, chunk_tokens=n, tile_variant=v)

@@ -1119,21 +1119,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     // ring slot of frame f of this chunk, for f0 - H <= f < f0 - H + z_R
     auto zslot = [&](int f) { return slot_add(zs0, f - (f0 - H), z_R); };
 
-    // z frames [fa, fa + n) -> Zs (LeakyReLU, bf16); frames at or past F are zeros
+    // z frames [fa, fa + n) -> Zs (LeakyReLU, bf16); frames at or past F are
+    // zeros.  A thread's vectors go SU at a time: their loads are all issued
+    // before the first is converted (a vector past the range, or of a frame
+    // at or past F, loads frame fa, which is in the ring).
     auto stage = [&](int fa, int n) {
-        for (int v = tid; v < n * VPR; v += 256) {
-            const int r = v / VPR, c8 = (v - r * VPR) * 8;
-            const int f = fa + r;
-            float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            if (f < p.F) {
-                const u32x4 a = *(const u32x4*)(zb + (size_t)zslot(f) * C + c8);
+        constexpr int SU = 8;
+        for (int v0 = tid; v0 < n * VPR; v0 += 256 * SU) {
+            u32x4 q[SU];
+#pragma unroll
+            for (int u = 0; u < SU; u++) {
+                const int v = v0 + 256 * u, r = v / VPR, c8 = (v - r * VPR) * 8;
+                const bool in = v < n * VPR && fa + r < p.F;
+                q[u] = *(const u32x4*)(zb + (size_t)zslot(in ? fa + r : fa) * C + (in ? c8 : 0));
+            }
+            __builtin_amdgcn_sched_barrier(0);   // all loads before the first use
+#pragma unroll
+            for (int u = 0; u < SU; u++) {
+                const int v = v0 + 256 * u, r = v / VPR, c8 = (v - r * VPR) * 8;
+                const int f = fa + r;
+                float x[8];
 #pragma unroll
                 for (int e = 0; e < 4; e++) {
-                    x[2 * e] = lrelu(h2f(a[e] & 0xffffu), p.slope);
-                    x[2 * e + 1] = lrelu(h2f(a[e] >> 16), p.slope);
+                    x[2 * e] = f < p.F ? lrelu(h2f(q[u][e] & 0xffffu), p.slope) : 0.f;
+                    x[2 * e + 1] = f < p.F ? lrelu(h2f(q[u][e] >> 16), p.slope) : 0.f;
                 }
+                if (v < n * VPR) store8_lds(Zs + (f & ZM) * LDW + c8, x);
             }
-            store8_lds(Zs + (f & ZM) * LDW + c8, x);
         }
     };
     // the same for the BM frames of the next sub-tile in two halves: fetch
@@ -1216,19 +1228,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
 #pragma unroll
             for (int nb = 0; nb < NB; nb++) acc[i][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
         const int row0 = fr + fl - H1;         // z frame of tap 0 for row block 0
+        // a row block's frame fragment of the next channel chunk is read
+        // right after that block's MFMAs of this chunk, into the same
+        // registers: the read has the other row blocks' MFMAs to arrive in
         auto tap1 = [&](int j, const Frag (&w)[KCH][NB]) {
             int ai[R];
 #pragma unroll
             for (int i = 0; i < R; i++) ai[i] = ((row0 + 16 * i + j * p.d) & ZM) * LDW + koff;
+            bf16x8_t a[R];
+#pragma unroll
+            for (int i = 0; i < R; i++) a[i] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(Zs + ai[i]));
 #pragma unroll
             for (int ki = 0; ki < KCH; ki++) {
 #pragma unroll
                 for (int i = 0; i < R; i++) {
-                    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(Zs + ai[i] + ki * KQ));
 #pragma unroll
                     for (int nb = 0; nb < NB; nb++)
                         acc[i][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w[ki][nb]),
-                                                                            a, acc[i][nb], 0, 0, 0);
+                                                                            a[i], acc[i][nb], 0, 0, 0);
+                    if (ki + 1 < KCH)
+                        a[i] = __builtin_bit_cast(bf16x8_t, *(const u32x4*)(Zs + ai[i] + (ki + 1) * KQ));
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
         };
@@ -1259,10 +1279,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         else
             conv1(std::integral_constant<int, MB>{}, t + wm * 16 * MB);
         __syncthreads();
-        // the next sub-tile's z frames, loaded while the second conv runs
+        // the epilogue's residual and branch-mean vectors: fp16, four channels
+        // of one frame, loaded raw and converted where used (rows past the
+        // run read its last frame and store nothing)
+        auto tl_of = [&](int mb) {
+            const int tl = wm * 16 * MB + mb * 16 + fl;
+            return t + tl < f1 ? tl : f1 - 1 - t;
+        };
+        auto h4 = [](u32x2 w) {
+            return f32x4{h2f(w[0] & 0xffffu), h2f(w[0] >> 16), h2f(w[1] & 0xffffu), h2f(w[1] >> 16)};
+        };
+        auto issue_z = [&](int mb, u32x2 (&q)[NB]) {
+            const uint16_t* zr = zb + (size_t)zslot(t + tl_of(mb)) * C + nblk0 * 16 + cg;
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++) q[nb] = *(const u32x2*)(zr + nb * 16);
+        };
+        // the next sub-tile's z frames (where registers allow) and, without a
+        // branch mean, the residual, loaded while the second conv runs
         u32x4 zq[PV];
+        u32x2 zpre[MB][NB];
         if constexpr (PF) {
             if (t + BM < f1) fetch(t + BM, zq);
+        }
+        if (p.n_mean == 0) {
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++) issue_z(mb, zpre[mb]);
         }
 
         // ---- second conv: output frames t + wm*16*MB + 16 mb + fl, h from Hs
@@ -1301,54 +1342,43 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         // ---- epilogue: bias, residual z, branch mean; fp16 through the output ring
         const int out_s = (int)ring_slot(tau0 + t, out_R);
         const int mean_s = p.n_mean ? (int)ring_slot(tau0 + t, p.mean_R) : 0;
-        // the residual loads of row block mb + 1 are issued before row block mb
-        // is finished (rows past the run read its last frame and store
-        // nothing); with a branch mean, each row block loads what it adds
-        auto tl_of = [&](int mb) {
-            const int tl = wm * 16 * MB + mb * 16 + fl;
-            return t + tl < f1 ? tl : f1 - 1 - t;
-        };
         auto store = [&](int mb, int nb, f32x4 v) {
             const int tl = wm * 16 * MB + mb * 16 + fl;
             if (t + tl < f1)
                 store4(out, kF16, ((size_t)b * out_R + slot_add(out_s, tl, out_R)) * C + (nblk0 + nb) * 16 + cg, v);
         };
         if (p.n_mean == 0) {
-            f32x4 ld[2][NB];
-            auto issue = [&](int mb, f32x4 (&q)[NB]) {
-                const uint16_t* zr = zb + (size_t)zslot(t + tl_of(mb)) * C + nblk0 * 16 + cg;
+            // the residual was loaded during the second conv
 #pragma unroll
-                for (int nb = 0; nb < NB; nb++) q[nb] = load4(zr, kF16, nb * 16);
-            };
-            issue(0, ld[0]);
+            for (int mb = 0; mb < MB; mb++)
 #pragma unroll
-            for (int mb = 0; mb < MB; mb++) {
-                if (mb + 1 < MB) issue(mb + 1, ld[(mb + 1) & 1]);
-#pragma unroll
-                for (int nb = 0; nb < NB; nb++) store(mb, nb, ld[mb & 1][nb] + (acc[mb][nb] + bias2[nb]));
-            }
+                for (int nb = 0; nb < NB; nb++) store(mb, nb, h4(zpre[mb][nb]) + (acc[mb][nb] + bias2[nb]));
         } else {
+            // with the branch means: every row block's residual and three mean
+            // vectors are issued before the first is used (a mean past n_mean
+            // reads the first and is not used, so the loads need no branch)
             const float J = (float)(p.n_mean + 1);
+            const uint16_t* mp[3];
+#pragma unroll
+            for (int i = 0; i < 3; i++) mp[i] = p.mean[i < p.n_mean ? i : 0];
+            u32x2 r[MB][NB], m[MB][3][NB];
 #pragma unroll
             for (int mb = 0; mb < MB; mb++) {
-                const int tl = tl_of(mb);
-                const uint16_t* zr = zb + (size_t)zslot(t + tl) * C + nblk0 * 16 + cg;
-                const size_t mo = ((size_t)b * mean_R + slot_add(mean_s, tl, mean_R)) * C + nblk0 * 16 + cg;
-                f32x4 r[NB], m[3][NB];
+                issue_z(mb, r[mb]);
+                const size_t mo = ((size_t)b * mean_R + slot_add(mean_s, tl_of(mb), mean_R)) * C + nblk0 * 16 + cg;
+#pragma unroll
+                for (int i = 0; i < 3; i++)
+#pragma unroll
+                    for (int nb = 0; nb < NB; nb++) m[mb][i][nb] = *(const u32x2*)(mp[i] + mo + nb * 16);
+            }
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++) {
 #pragma unroll
                 for (int nb = 0; nb < NB; nb++) {
-                    r[nb] = load4(zr, kF16, nb * 16);
-#pragma unroll
-                    for (int i = 0; i < 3; i++)
-                        if (i < p.n_mean) m[i][nb] = load4(p.mean[i], kF16, mo + nb * 16);
-                }
-#pragma unroll
-                for (int nb = 0; nb < NB; nb++) {
-                    const f32x4 v = r[nb] + (acc[mb][nb] + bias2[nb]);
-                    f32x4 x = m[0][nb];
-#pragma unroll
-                    for (int i = 1; i < 3; i++)
-                        if (i < p.n_mean) x = x + m[i][nb];
+                    const f32x4 v = h4(r[mb][nb]) + (acc[mb][nb] + bias2[nb]);
+                    f32x4 x = h4(m[mb][0][nb]);
+                    if (p.n_mean > 1) x = x + h4(m[mb][1][nb]);
+                    if (p.n_mean > 2) x = x + h4(m[mb][2][nb]);
                     x = x + v;
                     store(mb, nb, f32x4{x[0] / J, x[1] / J, x[2] / J, x[3] / J});
                 }

@@ -244,10 +244,12 @@ dc_status dc_reset_stream(dc_state* s, int32_t b);
  * placement", local fail-closed admission). */
 dc_status dc_sync(dc_state* s);
 
-/* frames_per_token * prod(up_rate) * hop for cfg (0 for a NULL cfg). */
+/* frames_per_token * prod(up_rate) * hop for cfg (0 for a NULL cfg or one
+ * that dc_init would reject as invalid). */
 int64_t dc_samples_per_token(const dc_cfg* cfg);
 
-/* Number of float32 values the weight blob of cfg must hold (0 for NULL). */
+/* Number of float32 values the weight blob of cfg must hold (0 for a NULL or
+ * invalid cfg). */
 int64_t dc_blob_floats(const dc_cfg* cfg);
 
 /* The fixed device buffers that dc_decode_chunk stages through:

@@ -893,9 +893,11 @@ static hipError_t zero_state(dc_state* s)
 
 extern "C" {
 
-int64_t dc_samples_per_token(const dc_cfg* cfg) { return cfg ? samples_per_token(cfg) : 0; }
+// Both sizes read the stage and branch tables only as far as a valid
+// configuration's counts reach: 0 for an invalid one.
+int64_t dc_samples_per_token(const dc_cfg* cfg) { return cfg && validate(cfg).empty() ? samples_per_token(cfg) : 0; }
 
-int64_t dc_blob_floats(const dc_cfg* cfg) { return cfg ? blob_floats(cfg) : 0; }
+int64_t dc_blob_floats(const dc_cfg* cfg) { return cfg && validate(cfg).empty() ? blob_floats(cfg) : 0; }
 
 static hipError_t static_scratch(int dev, void** out);
 

@@ -339,6 +339,18 @@ int32_t dc_layer_count(const dc_state* s);
 dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out);
 dc_status dc_time_layers(dc_state* s, int32_t reps, double* us_per_launch);
 
+/* Bounds checks of the checked build (libdc_debug.so, the same sources built
+ * with DC_DEBUG): every ring access of the kernels (operand, output,
+ * residual, branch-mean, source, z, head, iSTFT and embedding rings) and the
+ * row range of every staged operand tile is checked; a failed check sets its
+ * bit and the access is redirected to element 0 of its buffer.  Returns the
+ * OR of the bits set on the current device since the last clear (0: none),
+ * clearing them if clear != 0, after waiting for the device; -1 from the
+ * release build (checks compiled out), -2 on a HIP error.  Bits: 1 operand
+ * ring, 2 operand tile rows, 4 conv output/residual/mean/source rings, 8 fused
+ * pair z ring, 16 fused pair output/mean rings, 32 iSTFT tail, 64 embedding. */
+int32_t dc_debug_checks(int32_t clear);
+
 /* Human-readable reason for the last error on s (or on dc_init when s is NULL). */
 const char* dc_last_error(const dc_state* s);
 

@@ -104,6 +104,7 @@ SIGNATURES = {
     "dc_layer_count": ([_P], ctypes.c_int32),
     "dc_layer_info_get": ([_P, ctypes.c_int32, ctypes.POINTER(DcLayerInfo)], ctypes.c_int),
     "dc_time_layers": ([_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
+    "dc_debug_checks": ([ctypes.c_int32], ctypes.c_int32),
     "dc_last_error": ([_P], ctypes.c_char_p),
     "dc_free": ([_P], None),
 }
@@ -115,6 +116,9 @@ def lib() -> ctypes.CDLL:
     """The loaded libdc.so; raises if it has not been built."""
     global _lib
     if _lib is None:
+        # torch first: libdc.so then binds to the HIP runtime torch has
+        # loaded (the same soname), not a second copy of its own
+        import torch  # noqa: F401
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                                "(hipcc --offload-arch=gfx950); there is no fallback path")

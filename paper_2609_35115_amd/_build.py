@@ -33,22 +33,36 @@ def _run(cmd, verbose):
         raise RuntimeError(f"hipcc failed ({r.returncode}): {cmd[-1]}")
 
 
-def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+DEBUG_LIB = os.path.join(PKG, "libdc_debug.so")
+
+
+def build(verbose: bool = False, out: str = LIB, defines=(), debug: bool = True) -> str:
     """Compile every source to an object in parallel (they share no device
-    code), then link the shared library."""
+    code), then link the shared library; with `debug`, also the checked
+    library libdc_debug.so: the vocoder kernels built with DC_DEBUG (bounds
+    checks on every ring access) linked with the same other objects."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
     tag = os.path.basename(out).replace(".", "_")
     objs = [os.path.join(objdir, f"{tag}_{os.path.splitext(s)[0]}.o") for s in SOURCES]
-    cmds = [[hipcc, *HIPCC_FLAGS, *[f"-D{d}" for d in defines], "-I", os.path.join(ROOT, "include"),
+    inc = ["-I", os.path.join(ROOT, "include")]
+    cmds = [[hipcc, *HIPCC_FLAGS, *[f"-D{d}" for d in defines], *inc,
              "-c", "-o", o, os.path.join(CSRC, s)] for s, o in zip(SOURCES, objs)]
+    dbg_obj = os.path.join(objdir, "libdc_debug_dc_kernels.o")
+    if debug:
+        cmds.append([hipcc, *HIPCC_FLAGS, "-DDC_DEBUG", *inc, "-c", "-o", dbg_obj,
+                     os.path.join(CSRC, "dc_kernels.hip")])
     with ThreadPoolExecutor(max_workers=len(cmds)) as ex:
         for f in [ex.submit(_run, c, verbose) for c in cmds]:
             f.result()
-    tmp = out + ".tmp"
-    _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
-    os.replace(tmp, out)
+    links = [(out, objs)]
+    if debug:
+        links.append((DEBUG_LIB, [dbg_obj if s == "dc_kernels.hip" else o for s, o in zip(SOURCES, objs)]))
+    for lib, lobjs in links:
+        tmp = lib + ".tmp"
+        _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *lobjs], verbose)
+        os.replace(tmp, lib)
     return out
 
 

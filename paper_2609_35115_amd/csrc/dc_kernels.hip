@@ -104,6 +104,47 @@ __device__ __forceinline__ int64_t ring_slot(int64_t tau, int64_t R)
     return s < 0 ? s + R : s;
 }
 
+// ------------------------------------------------------- checked build
+//
+// Built with DC_DEBUG, ring accesses take their offsets from ring_at and the
+// fixed-size tiles check their row ranges: an index outside its buffer sets a
+// bit of dc_debug_bits (one word per lane, so the atomic has a per-lane
+// address) and the access goes to element 0 of the buffer instead, so a
+// checked run never leaves its buffers.  dc_debug_checks reads and clears
+// the bits.  The release build computes the same offsets with no checks.
+enum DebugBit : int {
+    kDbgOperand = 1,      // conv: operand rows read through the input ring
+    kDbgTile = 2,         // conv: operand rows of the LDS tile
+    kDbgOut = 4,          // conv: output, residual, branch-mean and source rings
+    kDbgPairZ = 8,        // fused pair: z ring
+    kDbgPairOut = 16,     // fused pair: output and branch-mean rings
+    kDbgTail = 32,        // iSTFT tail: head ring, G ring, PCM
+    kDbgEmbed = 64,       // embedding: output ring
+};
+#ifdef DC_DEBUG
+__device__ int dc_debug_bits[64];
+__device__ __forceinline__ void dbg_flag(int bit) { atomicOr(&dc_debug_bits[threadIdx.x & 63], bit); }
+#define DC_DBG_CHECK(cond, bit) \
+    do {                        \
+        if (!(cond)) dbg_flag(bit); \
+    } while (0)
+#else
+#define DC_DBG_CHECK(cond, bit) ((void)0)
+#endif
+
+// Offset of elements c .. c + w - 1 of slot `slot` of stream b in a ring of
+// B streams x R slots x C elements.
+__device__ __forceinline__ size_t ring_at(int b, int B, int64_t slot, int64_t R, int c, int w, int C, int bit)
+{
+#ifdef DC_DEBUG
+    if (b < 0 || b >= B || slot < 0 || slot >= R || c < 0 || c + w > C) {
+        dbg_flag(bit);
+        return 0;
+    }
+#endif
+    return ((size_t)b * R + slot) * C + c;
+}
+
 // ----------------------------------------------------- operand type traits
 
 template <bool BF16> struct OpT;
@@ -202,7 +243,7 @@ struct OutRef {
 //   sd_b[c] + sum_j sd_w[c][j] * src[j], j ascending.
 __device__ __forceinline__ f32x4 src_term4(const ConvParams& p, int b, int slot, int co)
 {
-    const f32x4 x = *(const f32x4*)(p.src + ((size_t)b * p.src_R + slot) * 4);
+    const f32x4 x = *(const f32x4*)(p.src + ring_at(b, p.B, slot, p.src_R, 0, 4, 4, kDbgOut));
     f32x4 v = *(const f32x4*)(p.sd_b + co);
 #pragma unroll
     for (int e = 0; e < 4; e++) {
@@ -217,7 +258,7 @@ __device__ __forceinline__ f32x4 src_term4(const ConvParams& p, int b, int slot,
 
 __device__ __forceinline__ float src_term1(const ConvParams& p, int b, int slot, int co)
 {
-    const f32x4 x = *(const f32x4*)(p.src + ((size_t)b * p.src_R + slot) * 4);
+    const f32x4 x = *(const f32x4*)(p.src + ring_at(b, p.B, slot, p.src_R, 0, 4, 4, kDbgOut));
     const f32x4 w = *(const f32x4*)(p.sd_w + (size_t)co * 4);
     float a = p.sd_b[co];
 #pragma unroll
@@ -238,16 +279,16 @@ __device__ __forceinline__ void store_out(const ConvParams& p, int b, const OutR
     // off: output frame offset from the block's base frame; co: output channel
     if (p.src) v = v + src_term1(p, b, slot_add(rs.src_s, off, (int)p.src_R), co);
     const int oe = p.out_elem;
-    if (rs.res) v = load1(rs.res, oe, ((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co) + v;
+    if (rs.res) v = load1(rs.res, oe, ring_at(b, p.B, slot_add(rs.res_s, off, rs.res_R), rs.res_R, co, 1, p.out_C, kDbgOut)) + v;
     if (p.n_mean) {
-        const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean_s, off, (int)p.mean_R)) * p.out_C + co;
+        const size_t mo = ring_at(b, p.B, slot_add(rs.mean_s, off, (int)p.mean_R), p.mean_R, co, 1, p.out_C, kDbgOut);
         float x = load1(p.mean[0], oe, mo);
         for (int i = 1; i < p.n_mean; i++) x = x + load1(p.mean[i], oe, mo);
         x = x + v;
         v = x / (float)(p.n_mean + 1);
     }
     if (p.out_act) v = lrelu(v, p.slope);
-    store1(rs.out, oe, ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co, v);
+    store1(rs.out, oe, ring_at(b, p.B, slot_add(rs.out_s, off, rs.out_R), rs.out_R, co, 1, p.out_C, kDbgOut), v);
 }
 
 // Four consecutive output channels co .. co+3 of one frame (nv < 4 at the
@@ -261,9 +302,9 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Out
     }
     if (p.src) v = v + src_term4(p, b, slot_add(rs.src_s, off, (int)p.src_R), co);
     const int oe = p.out_elem;
-    if (rs.res) v = load4(rs.res, oe, ((size_t)b * rs.res_R + slot_add(rs.res_s, off, rs.res_R)) * p.out_C + co) + v;
+    if (rs.res) v = load4(rs.res, oe, ring_at(b, p.B, slot_add(rs.res_s, off, rs.res_R), rs.res_R, co, 4, p.out_C, kDbgOut)) + v;
     if (p.n_mean) {
-        const size_t mo = ((size_t)b * p.mean_R + slot_add(rs.mean_s, off, (int)p.mean_R)) * p.out_C + co;
+        const size_t mo = ring_at(b, p.B, slot_add(rs.mean_s, off, (int)p.mean_R), p.mean_R, co, 4, p.out_C, kDbgOut);
         f32x4 x = load4(p.mean[0], oe, mo);
         for (int i = 1; i < p.n_mean; i++) x = x + load4(p.mean[i], oe, mo);
         x = x + v;
@@ -274,7 +315,7 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Out
 #pragma unroll
         for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
     }
-    store4(rs.out, oe, ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co, v);
+    store4(rs.out, oe, ring_at(b, p.B, slot_add(rs.out_s, off, rs.out_R), rs.out_R, co, 4, p.out_C, kDbgOut), v);
 }
 
 // Operand rows [t0 - halo, t0 - halo + rows) of channel block cb of stream b,
@@ -294,7 +335,7 @@ __device__ __forceinline__ void stage_operand(const ConvParams& p, const void* i
         const int ch = cb * CB + c8;
         float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
         if (t < p.F && ch < p.in_C) {
-            load8(in_ptr, p.in_elem, ((size_t)b * in_R + slot_add(base_in, r, in_R)) * p.in_C + ch, x);
+            load8(in_ptr, p.in_elem, ring_at(b, p.B, slot_add(base_in, r, in_R), in_R, ch, 8, p.in_C, kDbgOperand), x);
             if (p.in_act) {
 #pragma unroll
                 for (int e = 0; e < 8; e++) x[e] = lrelu(x[e], p.slope);
@@ -363,8 +404,8 @@ __device__ __forceinline__ void store_tile_e(const ConvParams& p, const OutRef& 
             const int off = off_of(mb);
 #pragma unroll
             for (int nb = 0; nb < NB; nb++)
-                q[nb] = load4(rs.res, OE, ((size_t)b * rs.res_R + slot_add(rs.res_s, off + rp[nb], rs.res_R)) *
-                                              p.out_C + co[nb]);
+                q[nb] = load4(rs.res, OE, ring_at(b, p.B, slot_add(rs.res_s, off + rp[nb], rs.res_R), rs.res_R, co[nb], 4,
+                                                  p.out_C, kDbgOut));
         };
         if (rs.res) issue(0, ld[0]);
 #pragma unroll
@@ -382,8 +423,8 @@ __device__ __forceinline__ void store_tile_e(const ConvParams& p, const OutRef& 
                     for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
                 }
                 if (!live) continue;
-                store4(rs.out, OE, ((size_t)b * rs.out_R + slot_add(rs.out_s, off + rp[nb], rs.out_R)) * p.out_C + co[nb],
-                       v);
+                store4(rs.out, OE, ring_at(b, p.B, slot_add(rs.out_s, off + rp[nb], rs.out_R), rs.out_R, co[nb], 4, p.out_C,
+                                           kDbgOut), v);
             }
         }
     } else {
@@ -483,8 +524,8 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
             if (e_pre && rs.res) {
                 const int rpn = p.u == 1 ? 0 : e_n4 / p.out_C;
                 const int res_s = (int)ring_slot((tau0 + t0) * p.u, rs.res_R);
-                e_res = load4(rs.res, p.out_elem, ((size_t)b * rs.res_R + slot_add(res_s, e_tl * p.u + rpn, rs.res_R)) *
-                                                      p.out_C + e_n4 - rpn * p.out_C);
+                e_res = load4(rs.res, p.out_elem, ring_at(b, p.B, slot_add(res_s, e_tl * p.u + rpn, rs.res_R), rs.res_R,
+                                                          e_n4 - rpn * p.out_C, 4, p.out_C, kDbgOut));
             }
         }
     }
@@ -521,6 +562,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
     };
     auto step_a = [&](int st) {   // this lane's frame fragment of step st, block row 0
         const int j = st / KPW, ki = st - (st / KPW) * KPW;
+        DC_DBG_CHECK(wm * 16 * MB + 16 * MB - 1 + j * p.d < rows, kDbgTile);
         return a_lane + j * p.d * LDW + ki * WGK * Tr::KQ;
     };
     auto load_a = [&](int st, AFrag (&a)[MB]) {
@@ -581,6 +623,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
         // MFMAs of tap j: this lane's fragment address is fixed; a tap adds a
         // row offset, a block / chunk an immediate
         auto compute_tap = [&](int j, const Frag (&w)[KPW][NB]) {
+            DC_DBG_CHECK(wm * 16 * MB + 16 * MB - 1 + j * p.d < rows, kDbgTile);
             const T* aj = a_lane + j * p.d * LDW;
 #pragma unroll
             for (int ki = 0; ki < KPW; ki++) {
@@ -715,7 +758,8 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
 #pragma unroll
                     for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
                 }
-                store4(rs.out, p.out_elem, ((size_t)b * rs.out_R + slot_add(rs.out_s, off, rs.out_R)) * p.out_C + co, v);
+                store4(rs.out, p.out_elem, ring_at(b, p.B, slot_add(rs.out_s, off, rs.out_R), rs.out_R, co, 4, p.out_C, kDbgOut),
+                       v);
             } else {
                 store_out4(p, b, rs, off, co, v, p.N - e_n4 < 4 ? p.N - e_n4 : 4);
             }
@@ -815,6 +859,7 @@ __global__ __launch_bounds__(256, 2) void wconv_kernel(const ConvGroup g)
     // fragments of K step st (local step sl within its channel block)
     auto readf = [&](int st, int sl, u32x4 (&a)[MB], u32x4 (&w)[NB]) {
         const int j = sl / KCH, kc = sl - (sl / KCH) * KCH;
+        DC_DBG_CHECK(wm * 16 * MB + 16 * MB - 1 + j * p.d < rows, kDbgTile);
         const u32x4* wr = ring + (st % kRing) * NFR * 64 + wn * NB * 64 + lane;
 #pragma unroll
         for (int nb = 0; nb < NB; nb++) w[nb] = wr[nb * 64];
@@ -1117,7 +1162,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     const uint16_t* zb = z + (size_t)b * z_R * C;
     const int zs0 = (int)ring_slot(tau0 + f0 - H, z_R);   // ring slot of frame f0 - H
     // ring slot of frame f of this chunk, for f0 - H <= f < f0 - H + z_R
-    auto zslot = [&](int f) { return slot_add(zs0, f - (f0 - H), z_R); };
+    auto zslot = [&](int f) {
+        DC_DBG_CHECK(b < p.B && f - (f0 - H) >= 0 && f - (f0 - H) < z_R, kDbgPairZ);
+        return slot_add(zs0, f - (f0 - H), z_R);
+    };
 
     // z frames [fa, fa + n) -> Zs (LeakyReLU, bf16); frames at or past F are
     // zeros.  A thread's vectors go SU at a time: their loads are all issued
@@ -1345,7 +1393,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         auto store = [&](int mb, int nb, f32x4 v) {
             const int tl = wm * 16 * MB + mb * 16 + fl;
             if (t + tl < f1)
-                store4(out, kF16, ((size_t)b * out_R + slot_add(out_s, tl, out_R)) * C + (nblk0 + nb) * 16 + cg, v);
+                store4(out, kF16, ring_at(b, p.B, slot_add(out_s, tl, out_R), out_R, (nblk0 + nb) * 16 + cg, 4, C, kDbgPairOut),
+                       v);
         };
         if (p.n_mean == 0) {
             // the residual was loaded during the second conv
@@ -1365,7 +1414,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
 #pragma unroll
             for (int mb = 0; mb < MB; mb++) {
                 issue_z(mb, r[mb]);
-                const size_t mo = ((size_t)b * mean_R + slot_add(mean_s, tl_of(mb), mean_R)) * C + nblk0 * 16 + cg;
+                const size_t mo = ring_at(b, p.B, slot_add(mean_s, tl_of(mb), mean_R), mean_R, nblk0 * 16 + cg,
+                                          (NB - 1) * 16 + 4, C, kDbgPairOut);
 #pragma unroll
                 for (int i = 0; i < 3; i++)
 #pragma unroll
@@ -1476,7 +1526,7 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* tokens, int n
     const int b = (int)(bf / (n * fpt));
     const int tok = tokens[(size_t)b * n + f / fpt];
     const int64_t slot = ring_slot(clock[0] * fpt + f, out.R);
-    const size_t dst = ((size_t)b * out.R + slot) * C + c8;
+    const size_t dst = ring_at(b, B, slot, out.R, c8, 8, C, kDbgEmbed);
     const bool ok = tok >= 0 && tok < vocab;
     if (!ok) *err = 1;
     if (elem == kF32) {
@@ -1541,19 +1591,18 @@ __global__ __launch_bounds__(256) void istft_kernel(const float* head, int64_t h
     const int tiles = (F + kTail - 1) / kTail;
     const int b = blockIdx.x / tiles, f0 = (blockIdx.x - b * tiles) * kTail;
     const int64_t tau0 = clock[0] * fpt;          // absolute index of this call's frame 0
-    float* gb = (float*)g.ptr + (size_t)b * g.R * kNFFT;
     for (int i = threadIdx.x; i < kTail + 3; i += blockDim.x) {
         const int m = f0 - 3 + i;                 // frame of this call (negative: the previous call's)
         if (m >= F) continue;
         float* row = G + i * W;
         const int64_t tau = tau0 + m;
         if (m < 0) {
-            const float* src = gb + ring_slot(tau, g.R) * kNFFT;
+            const float* src = (const float*)g.ptr + ring_at(b, B, ring_slot(tau, g.R), g.R, 0, kNFFT, kNFFT, kDbgTail);
 #pragma unroll
             for (int k = 0; k < kNFFT; k++) row[k] = src[k];
             continue;
         }
-        const float* sp = head + ((size_t)b * head_R + ring_slot(tau, head_R)) * (2 * kBins);
+        const float* sp = head + ring_at(b, B, ring_slot(tau, head_R), head_R, 0, 2 * kBins, 2 * kBins, kDbgTail);
         float re[kBins], im[kBins];
 #pragma unroll
         for (int kk = 0; kk < kBins; kk++) {
@@ -1576,7 +1625,7 @@ __global__ __launch_bounds__(256) void istft_kernel(const float* head, int64_t h
             row[n] = v;
         }
         if (m >= F - 3 && i >= 3) {               // the next call's left context
-            float* dst = gb + ring_slot(tau, g.R) * kNFFT;
+            float* dst = (float*)g.ptr + ring_at(b, B, ring_slot(tau, g.R), g.R, 0, kNFFT, kNFFT, kDbgTail);
 #pragma unroll
             for (int n4 = 0; n4 < kNFFT; n4 += 4)
                 *(f32x4*)(dst + n4) = f32x4{row[n4], row[n4 + 1], row[n4 + 2], row[n4 + 3]};
@@ -1594,7 +1643,7 @@ __global__ __launch_bounds__(256) void istft_kernel(const float* head, int64_t h
             for (int q = 0; q < 4; q++) acc = acc + G[(t + q) * W + 12 - 4 * q + r];
             o[r] = acc;
         }
-        *(f32x4*)(pcm + (size_t)b * F * 4 + 4 * (size_t)m) = o;
+        *(f32x4*)(pcm + ring_at(b, B, m, F, 0, 4, 4, kDbgTail)) = o;
     }
 }
 
@@ -1770,3 +1819,23 @@ hipError_t launch_init_keys(uint64_t* keys, int B, hipStream_t st)
 }
 
 }  // namespace dc
+
+// Bounds-check bits of a checked build (see ring_at); -1 in a release build.
+extern "C" int32_t dc_debug_checks(int32_t clear)
+{
+#ifdef DC_DEBUG
+    int bits[64];
+    if (hipDeviceSynchronize() != hipSuccess) return -2;
+    if (hipMemcpyFromSymbol(bits, HIP_SYMBOL(dc::dc_debug_bits), sizeof(bits)) != hipSuccess) return -2;
+    int all = 0;
+    for (int i = 0; i < 64; i++) all |= bits[i];
+    if (clear) {
+        const int zero[64] = {0};
+        if (hipMemcpyToSymbol(HIP_SYMBOL(dc::dc_debug_bits), zero, sizeof(zero)) != hipSuccess) return -2;
+    }
+    return all;
+#else
+    (void)clear;
+    return -1;
+#endif
+}

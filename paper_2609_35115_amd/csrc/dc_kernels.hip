@@ -935,6 +935,26 @@ __global__ __launch_bounds__(256, 2) void wconv_kernel(const ConvGroup g)
     store_tile<true, MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
 }
 
+// ------------------------------------------------- dynamic LDS over 64 KB
+//
+// A kernel launched with more than 64 KB of dynamic LDS needs its limit
+// raised first, on each device it runs on: `set` caches, per device, the
+// largest size already allowed for that kernel (a race between two threads
+// only repeats the call).
+constexpr int kMaxDevices = 64;
+static hipError_t allow_lds(const void* kernel, size_t lds, size_t (&set)[kMaxDevices])
+{
+    if (lds <= 64 * 1024) return hipSuccess;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const bool cached = dev >= 0 && dev < kMaxDevices;
+    if (cached && lds <= set[dev]) return hipSuccess;
+    e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess && cached) set[dev] = lds;
+    return e;
+}
+
 // ------------------------------------------------------------- tile table
 
 // Every shape exists for both operand types; KCH is the channel block in
@@ -993,14 +1013,10 @@ static hipError_t launch_t(const ConvGroup& g, int count, size_t lds, hipStream_
     constexpr int BN = 16 * NB * WGN;
     const ConvParams& p = g.p;   // members share B, F, N and the tiling
     dim3 grid((unsigned)(p.B * p.tiles_t), (unsigned)((p.N + BN - 1) / BN), (unsigned)count);
-    static size_t lds_set = 64 * 1024;   // the default dynamic LDS limit of a kernel
-    if (lds > lds_set) {
-        const hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&conv_kernel<BF16, MB, NB, WGM, WGN, WGK, KCH>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        lds_set = lds;
-    }
+    static size_t lds_set[kMaxDevices] = {};
+    const hipError_t e = allow_lds(reinterpret_cast<const void*>(&conv_kernel<BF16, MB, NB, WGM, WGN, WGK, KCH>), lds,
+                                   lds_set);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((conv_kernel<BF16, MB, NB, WGM, WGN, WGK, KCH>), grid, dim3(256), lds, st, g);
     return hipGetLastError();
 }
@@ -1011,13 +1027,9 @@ static hipError_t launch_w(const ConvGroup& g, int count, size_t lds, hipStream_
     constexpr int BN = 16 * NB * WGN;
     const ConvParams& p = g.p;
     dim3 grid((unsigned)(p.B * p.tiles_t), (unsigned)((p.N + BN - 1) / BN), (unsigned)count);
-    static size_t lds_set = 64 * 1024;
-    if (lds > lds_set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&wconv_kernel<MB, NB, WGM, WGN, KCH>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        lds_set = lds;
-    }
+    static size_t lds_set[kMaxDevices] = {};
+    const hipError_t e = allow_lds(reinterpret_cast<const void*>(&wconv_kernel<MB, NB, WGM, WGN, KCH>), lds, lds_set);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((wconv_kernel<MB, NB, WGM, WGN, KCH>), grid, dim3(256), lds, st, g);
     return hipGetLastError();
 }
@@ -1468,13 +1480,10 @@ static hipError_t launch_pair_t(const PairGroup& g, int count, size_t lds, hipSt
 {
     const PairParams& p = g.p;
     dim3 grid((unsigned)(p.B * p.segs), 1u, (unsigned)count);
-    static size_t lds_set = 64 * 1024;
-    if (lds > lds_set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&pair_kernel<MB, NB, WGM, WGN, KCH, LZ, LH>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        lds_set = lds;
-    }
+    static size_t lds_set[kMaxDevices] = {};
+    const hipError_t e = allow_lds(reinterpret_cast<const void*>(&pair_kernel<MB, NB, WGM, WGN, KCH, LZ, LH>), lds,
+                                   lds_set);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((pair_kernel<MB, NB, WGM, WGN, KCH, LZ, LH>), grid, dim3(256), lds, st, g);
     return hipGetLastError();
 }

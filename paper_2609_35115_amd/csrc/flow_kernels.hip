@@ -307,17 +307,31 @@ constexpr size_t tiled_lds_bytes()
     return (size_t)2 * (32 * MB + 32 * NB) * (KC + (BF16 ? 8 : 4)) * (BF16 ? 2 : 4);
 }
 
+// A kernel launched with more than 64 KB of dynamic LDS needs its limit
+// raised first, on each device it runs on: `set` caches, per device, the
+// largest size already allowed for that kernel (a race between two threads
+// only repeats the call).
+constexpr int kMaxDevices = 64;
+static hipError_t allow_lds(const void* kernel, size_t lds, size_t (&set)[kMaxDevices])
+{
+    if (lds <= 64 * 1024) return hipSuccess;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const bool cached = dev >= 0 && dev < kMaxDevices;
+    if (cached && lds <= set[dev]) return hipSuccess;
+    e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess && cached) set[dev] = lds;
+    return e;
+}
+
 template <bool BF16, int EPI, int MB, int NB>
 hipError_t launch_tiled(const GemmParams& p, hipStream_t st)
 {
     constexpr size_t lds = tiled_lds_bytes<BF16, MB, NB>();
-    static bool set = false;
-    if (lds > 65536 && !set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<BF16, EPI, MB, NB>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        set = true;
-    }
+    static size_t set[kMaxDevices] = {};
+    const hipError_t e = allow_lds(reinterpret_cast<const void*>(&gemm_kernel<BF16, EPI, MB, NB>), lds, set);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((gemm_kernel<BF16, EPI, MB, NB>), dim3((p.N + 32 * NB - 1) / (32 * NB), (p.M + 32 * MB - 1) / (32 * MB)),
                        dim3(256), lds, st, p);
     return hipGetLastError();
@@ -571,13 +585,9 @@ template <bool BF16, int EPI, bool LN, int NW, int NBLK, int RB>
 hipError_t launch_skinny(const GemmParams& p, hipStream_t st)
 {
     const size_t lds = skinny_lds_bytes(p, BF16, NW, NBLK, RB);
-    static size_t set = 0;
-    if (lds > 65536 && lds > set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<BF16, EPI, LN, NW, NBLK, RB>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        set = lds;
-    }
+    static size_t set[kMaxDevices] = {};
+    const hipError_t e = allow_lds(reinterpret_cast<const void*>(&skinny_kernel<BF16, EPI, LN, NW, NBLK, RB>), lds, set);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((skinny_kernel<BF16, EPI, LN, NW, NBLK, RB>),
                        dim3((p.N + 16 * NBLK - 1) / (16 * NBLK), (p.M + 16 * RB - 1) / (16 * RB)),
                        dim3(64 * NW), lds, st, p);
@@ -930,13 +940,9 @@ hipError_t launch_attn_shape(const AttnParams& p, int Bc, hipStream_t st)
 {
     const dim3 grid(Bc * 2 * p.heads, (p.n + 16 * QG - 1) / (16 * QG));
     const size_t lds = attn_lds_bytes(NW, QG);
-    static bool set = false;
-    if (!set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<BF16, QG, NW>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        set = true;
-    }
+    static size_t set[kMaxDevices] = {};
+    const hipError_t e = allow_lds(reinterpret_cast<const void*>(&attn_kernel<BF16, QG, NW>), lds, set);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_kernel<BF16, QG, NW>), grid, dim3(64 * NW), lds, st, p);
     return hipGetLastError();
 }

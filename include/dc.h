@@ -315,7 +315,8 @@ dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32
  * kernel launches ("layers": embed, each conv / transposed conv -- the
  * convs at one position of the parallel resblock branches share a launch,
  * and a fused resblock pair is one launch --,
- * head, the iSTFT tail, clock).  dc_layer_info describes launch i at
+ * head, the iSTFT tail, which also advances the clock).  dc_layer_info
+ * describes launch i at
  * n = chunk_tokens: its kernel (the demangled name a profiler shows), the
  * GEMM shape of a conv (rows = batch * frames, cols, depth = taps * input
  * channels, summed over the launch's convs), its algorithmic FLOPs (2 *
@@ -325,7 +326,8 @@ dc_status dc_tap_read(dc_state* s, int32_t tap, int32_t b, int64_t frame0, int32
  * every layer reps times in isolation on the state's stream, bracketed by HIP
  * events, and writes the mean microseconds per launch into us_per_launch
  * [dc_layer_count].  Re-running a layer rewrites only ring slots of frames the
- * next call overwrites anyway, so the stream state is unaffected.  Synchronous.
+ * next call overwrites anyway, and a re-run iSTFT tail leaves the clock where
+ * it is, so the stream state is unaffected.  Synchronous.
  */
 typedef struct dc_layer_info {
     char name[48];

@@ -185,8 +185,11 @@ hipError_t launch_embed(const int32_t* tokens, int n, int B, const void* table, 
 // Head output -> PCM [B][F*hop] in one launch (spectrum, iDFT, window and
 // overlap-add; n_fft = 16, hop = 4); writes the call's last 3 windowed frames
 // to the G ring (the next call's left context) and reads the previous call's.
+// With n_advance > 0 the launch also advances the clock by n_advance tokens
+// once every block has read it (arrivals: a zeroed counter it leaves zeroed);
+// 0 leaves the clock as it is (a launch re-run for timing).
 hipError_t launch_istft(const float* head, int64_t head_R, int B, int F, const float* table, Ring g, float* pcm,
-                        const int64_t* clock, int64_t fpt, hipStream_t st);
+                        int64_t* clock, int64_t fpt, int n_advance, unsigned* arrivals, hipStream_t st);
 
 // Harmonic-plus-noise excitation source of one call.
 struct SourceParams {
@@ -211,7 +214,6 @@ struct SourceParams {
 hipError_t launch_phase(const SourceParams& p, hipStream_t st);
 hipError_t launch_source(const SourceParams& p, hipStream_t st);
 
-hipError_t launch_clock(int64_t* clock, int n, hipStream_t st);
 hipError_t launch_mark_start(int64_t* start, uint64_t* keys, int b, const int64_t* clock, int64_t back, uint64_t key,
                              hipStream_t st);
 hipError_t launch_init_keys(uint64_t* keys, int B, hipStream_t st);

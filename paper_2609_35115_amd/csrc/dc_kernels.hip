@@ -1589,11 +1589,18 @@ constexpr int kNFFT = 16, kBins = 9;
 // frames go to the G ring: they are the next call's left context.  Every
 // sample's arithmetic depends only on its frame index, so a frame gives the
 // same bits in any block, call or chunking.
+//
+// The launch also ends the call: with `advance` set, the last block to finish
+// adds the call's tokens to the device clock.  Every block counts itself in
+// `arrivals` after its last read of the clock, so the block that counts last
+// knows that no block still reads the old value; it then re-arms the count
+// for the next call.
 constexpr int kTail = 256;
 
 __global__ __launch_bounds__(256) void istft_kernel(const float* head, int64_t head_R, int B, int F,
                                                     const float* table, Ring g, float* pcm,
-                                                    const int64_t* clock, int64_t fpt)
+                                                    int64_t* clock, int64_t fpt, int n_advance,
+                                                    unsigned* arrivals)
 {
     constexpr int W = kNFFT + 1;                 // LDS row stride (odd: no bank conflicts)
     __shared__ float G[(kTail + 3) * W];
@@ -1654,14 +1661,25 @@ __global__ __launch_bounds__(256) void istft_kernel(const float* head, int64_t h
         }
         *(f32x4*)(pcm + ring_at(b, B, m, F, 0, 4, 4, kDbgTail)) = o;
     }
+    if (n_advance > 0) {
+        __syncthreads();   // every thread of this block is past its use of the clock
+        if (threadIdx.x == 0) {
+            __threadfence();
+            const unsigned before = atomicAdd(arrivals, 1u);
+            if (before + 1 == gridDim.x) {
+                atomicAdd((unsigned long long*)clock, (unsigned long long)n_advance);
+                atomicExch(arrivals, 0u);
+            }
+        }
+    }
 }
 
 hipError_t launch_istft(const float* head, int64_t head_R, int B, int F, const float* table, Ring g, float* pcm,
-                        const int64_t* clock, int64_t fpt, hipStream_t st)
+                        int64_t* clock, int64_t fpt, int n_advance, unsigned* arrivals, hipStream_t st)
 {
     const int tiles = (F + kTail - 1) / kTail;
     hipLaunchKernelGGL(istft_kernel, dim3((unsigned)(B * tiles)), dim3(256), 0, st, head, head_R, B, F, table, g,
-                       pcm, clock, fpt);
+                       pcm, clock, fpt, n_advance, arrivals);
     return hipGetLastError();
 }
 
@@ -1782,18 +1800,7 @@ hipError_t launch_source(const SourceParams& p, hipStream_t st)
     return hipGetLastError();
 }
 
-// --------------------------------------------------------------- clock
-
-__global__ void clock_kernel(int64_t* clock, int n)
-{
-    if (threadIdx.x == 0) clock[0] = clock[0] + n;
-}
-
-hipError_t launch_clock(int64_t* clock, int n, hipStream_t st)
-{
-    hipLaunchKernelGGL(clock_kernel, dim3(1), dim3(64), 0, st, clock, n);
-    return hipGetLastError();
-}
+// --------------------------------------------------------- stream starts
 
 // start[b] = the clock minus `back` tokens (in stream order): stream b
 // restarted `back` tokens before the next call; keys[b] keys its source

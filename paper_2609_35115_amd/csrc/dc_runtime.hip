@@ -54,7 +54,7 @@ struct ConvOp {
 };
 
 // One kernel launch of a chunk step.
-enum LaunchKind { L_EMBED, L_CONV, L_PAIR, L_ISTFT, L_CLOCK, L_PHASE, L_SOURCE };
+enum LaunchKind { L_EMBED, L_CONV, L_PAIR, L_ISTFT, L_PHASE, L_SOURCE };
 struct Launch {
     LaunchKind kind;
     std::vector<int> convs;   // members of a conv launch (same tile shape; parallel branches);
@@ -113,6 +113,7 @@ struct dc_state {
     int64_t fpt[DC_MAX_STAGES + 2] = {};
     int64_t spt = 0;
     size_t emb_off = 0, table_off = 0, tok_off = 0, audio_off = 0, clock_off = 0, start_off = 0, err_off = 0;
+    size_t arrivals_off = 0;
     size_t keys_off = 0;
     // harmonic source: merge weights and bias, down-conv weights and bias,
     // the f0 buffer, the carried phases and the per-call phase table
@@ -125,6 +126,7 @@ struct dc_state {
     int64_t* start = nullptr;   // [B] tokens decoded when each stream last started
     uint64_t* keys = nullptr;   // [B] each stream's source-generator key
     int* err = nullptr;
+    unsigned* arrivals = nullptr;   // blocks of the running iSTFT launch that are done (zero between calls)
     void* emb = nullptr;
     float* table = nullptr;
     hipGraph_t graph = nullptr;
@@ -694,8 +696,7 @@ static void build_schedule(dc_state* s)
                 }
             }
     }
-    s->launches.push_back({L_ISTFT, {}, "istft"});
-    s->launches.push_back({L_CLOCK, {}, "clock"});
+    s->launches.push_back({L_ISTFT, {}, "istft"});   // also advances the clock
 }
 
 // ------------------------------------------------------------ one chunk step
@@ -832,7 +833,9 @@ static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n
     return p;
 }
 
-static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st, double* ptab = nullptr)
+// timing: a launch re-run on its own (dc_time_layers), which must leave the
+// clock where it is.
+static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st, double* ptab = nullptr, bool timing = false)
 {
     const dc_cfg& c = s->cfg;
     const int L = c.n_stages;
@@ -861,9 +864,9 @@ static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st, double
         return launch_source(source_params(s, n, ptab), st);
     case L_ISTFT:
         return launch_istft((const float*)s->rings[s->ring_S].ptr, s->rings[s->ring_S].R, c.batch, FL, s->table,
-                            s->rings[s->ring_G], s->audio, s->clock, s->fpt[L], st);
+                            s->rings[s->ring_G], s->audio, s->clock, s->fpt[L], timing ? 0 : n, s->arrivals, st);
     default:
-        return launch_clock(s->clock, n, st);
+        return hipErrorInvalidValue;
     }
 }
 
@@ -885,6 +888,8 @@ static hipError_t zero_state(dc_state* s)
     e = hipMemsetAsync(s->start, 0, (size_t)s->cfg.batch * sizeof(int64_t), s->stream);
     if (e != hipSuccess) return e;
     e = launch_init_keys(s->keys, s->cfg.batch, s->stream);
+    if (e != hipSuccess) return e;
+    e = hipMemsetAsync(s->arrivals, 0, sizeof(unsigned), s->stream);
     if (e != hipSuccess) return e;
     return hipMemsetAsync(s->err, 0, sizeof(int), s->stream);
 }
@@ -985,6 +990,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     s->start_off = take((size_t)c.batch * sizeof(int64_t));
     s->keys_off = take((size_t)c.batch * sizeof(uint64_t));
     s->err_off = take(sizeof(int));
+    s->arrivals_off = take(sizeof(unsigned));
     s->arena_bytes = off;
 
     hipError_t e = hipMalloc((void**)&s->arena, s->arena_bytes);
@@ -1001,6 +1007,7 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
     s->start = (int64_t*)(s->arena + s->start_off);
     s->keys = (uint64_t*)(s->arena + s->keys_off);
     s->err = (int*)(s->arena + s->err_off);
+    s->arrivals = (unsigned*)(s->arena + s->arrivals_off);
     if (c.n_harmonics > 0) s->f0 = (float*)(s->arena + s->f0_off);
 
     if (c.hip_stream) {
@@ -1618,13 +1625,9 @@ dc_status dc_layer_info_get(const dc_state* s, int32_t i, dc_layer_info* out)
         out->bytes = B * F0 * 4 + B * F0 * H1 * 8 + B * FL * c.hop * 4;
         break;
     }
-    case L_ISTFT:   // head output in, PCM out, the 3-frame left context in and out
+    default:   // the iSTFT tail: head output in, PCM out, the 3-frame left context in and out, the clock
         set("dc::istft_kernel");
-        out->bytes = B * FL * (2 * (c.n_fft / 2 + 1) + c.hop) * 4 + 2.0 * B * (c.n_fft / c.hop - 1) * c.n_fft * 4;
-        break;
-    default:
-        set("dc::clock_kernel");
-        out->bytes = 16;
+        out->bytes = B * FL * (2 * (c.n_fft / 2 + 1) + c.hop) * 4 + 2.0 * B * (c.n_fft / c.hop - 1) * c.n_fft * 4 + 16;
     }
     return DC_OK;
 }
@@ -1637,17 +1640,17 @@ dc_status dc_time_layers(dc_state* s, int32_t reps, double* us_per_launch)
     hipError_t e = hipEventCreate(&e0);
     if (e == hipSuccess) e = hipEventCreate(&e1);
     const int nl = layer_count(s);
-    for (int i = 0; i < nl - 1 && e == hipSuccess; i++) {   // the clock is not re-run
-        e = launch_layer(s, i, s->cfg.chunk_tokens, s->stream);   // warm
+    for (int i = 0; i < nl && e == hipSuccess; i++) {   // re-runs leave the clock where it is
+        e = launch_layer(s, i, s->cfg.chunk_tokens, s->stream, nullptr, true);   // warm
         if (e == hipSuccess) e = hipEventRecord(e0, s->stream);
-        for (int r = 0; r < reps && e == hipSuccess; r++) e = launch_layer(s, i, s->cfg.chunk_tokens, s->stream);
+        for (int r = 0; r < reps && e == hipSuccess; r++)
+            e = launch_layer(s, i, s->cfg.chunk_tokens, s->stream, nullptr, true);
         if (e == hipSuccess) e = hipEventRecord(e1, s->stream);
         if (e == hipSuccess) e = hipEventSynchronize(e1);
         float ms = 0.f;
         if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
         us_per_launch[i] = 1000.0 * ms / reps;
     }
-    us_per_launch[nl - 1] = 0.0;
     if (e0) (void)hipEventDestroy(e0);
     if (e1) (void)hipEventDestroy(e1);
     if (e != hipSuccess) return device_fail(s, e, "dc_time_layers");

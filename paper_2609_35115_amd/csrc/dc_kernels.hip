@@ -1595,7 +1595,10 @@ constexpr int kNFFT = 16, kBins = 9;
 // `arrivals` after its last read of the clock, so the block that counts last
 // knows that no block still reads the old value; it then re-arms the count
 // for the next call.
-constexpr int kTail = 256;
+//
+// kTail + 3 = 256: every thread builds exactly one LDS row, so no thread
+// runs the per-frame chain (head loads, exp and sincos, the fmas) twice.
+constexpr int kTail = 253;
 
 __global__ __launch_bounds__(256) void istft_kernel(const float* head, int64_t head_R, int B, int F,
                                                     const float* table, Ring g, float* pcm,
@@ -1618,7 +1621,17 @@ __global__ __launch_bounds__(256) void istft_kernel(const float* head, int64_t h
             for (int k = 0; k < kNFFT; k++) row[k] = src[k];
             continue;
         }
-        const float* sp = head + ring_at(b, B, ring_slot(tau, head_R), head_R, 0, 2 * kBins, 2 * kBins, kDbgTail);
+        // the frame's 2 * kBins values: 8-byte aligned, so loaded as pairs
+        typedef __attribute__((ext_vector_type(2))) float f32x2;
+        const f32x2* sp2 = (const f32x2*)(head + ring_at(b, B, ring_slot(tau, head_R), head_R, 0, 2 * kBins,
+                                                          2 * kBins, kDbgTail));
+        float sp[2 * kBins];
+#pragma unroll
+        for (int j = 0; j < kBins; j++) {
+            const f32x2 q = sp2[j];
+            sp[2 * j] = q[0];
+            sp[2 * j + 1] = q[1];
+        }
         float re[kBins], im[kBins];
 #pragma unroll
         for (int kk = 0; kk < kBins; kk++) {

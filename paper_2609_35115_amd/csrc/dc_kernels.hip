@@ -990,6 +990,7 @@ static const TileShape kTiles[] = {
     {2, 4, 4, 1, 1, 4, 1}, // 25: 128x64
     {1, 4, 4, 1, 1, 4, 1}, // 26: 64x64
     {2, 2, 1, 1, 4, 8},    // 27: 32x32, 4 partitions, 8-chunk channel block
+    {2, 2, 4, 1, 1, 2},    // 28: 128x32, for outputs of at most 32 columns
 };
 
 int num_tile_variants() { return (int)(sizeof(kTiles) / sizeof(kTiles[0])); }
@@ -1072,6 +1073,7 @@ static hipError_t launch_dt(int v, const ConvGroup& p, int count, size_t lds, hi
     case 18: return launch_t<BF16, 1, 2, 1, 1, 4, 16>(p, count, lds, st);
     case 19: return launch_t<BF16, 1, 1, 2, 2, 1, 1>(p, count, lds, st);
     case 27: return launch_t<BF16, 2, 2, 1, 1, 4, 8>(p, count, lds, st);
+    case 28: return launch_t<BF16, 2, 2, 4, 1, 1, 2>(p, count, lds, st);
     default: return hipErrorInvalidValue;
     }
 }

@@ -284,8 +284,8 @@ static void pack_weights(const ConvOp& op, const float* blob, bool round_bf16, c
 // tiles, whose lower register use keeps more waves (and loads) in flight;
 // the others favour 64x128 tiles (four waves per SIMD with the step
 // pipeline), then 128x128.
-static const int kPreferLarge[] = {11, 14, 12, 13, 9, 10, 15, 16, 8, 6, 7, 19};
-static const int kPrefer64[] = {9, 10, 11, 12, 13, 14, 15, 16, 8, 6, 7, 19};
+static const int kPreferLarge[] = {11, 14, 12, 13, 9, 10, 15, 16, 28, 8, 6, 7, 19};
+static const int kPrefer64[] = {9, 10, 11, 12, 13, 14, 15, 16, 28, 8, 6, 7, 19};
 
 // LDS budget of one block: at most 80 KB of the CU's 160 KB, so two blocks
 // stay resident.

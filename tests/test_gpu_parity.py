@@ -114,6 +114,7 @@ TILE_GROUPS = {
     ("real", "f32", "kch8"): [2, 5, 28],         # 16x16, 16x32, 32x32; K in 4 partitions, 128-channel blocks
     ("real", "bf16", "unsplit"): [8, 9, 11,      # 32x32, 32x64, 64x64; unsplit K, 128-channel blocks
                                   21, 22, 25, 26, 27],   # the same with weights through the LDS ring
+    ("real", "bf16", "kch2"): [7, 10, 13, 29],   # 32x32, 64x64, 128x64, 128x32; 64-channel blocks
 }
 
 

@@ -512,20 +512,33 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
     const int e_idx = tid * 4;
     const int e_tl = e_idx / BN, e_n4 = n0 + (e_idx - (e_idx / BN) * BN);
     const bool e_live = WGK > 1 && e_idx < BM * BN && t0 + e_tl < p.F && e_n4 < p.N;
-    f32x4 e_bias = {0.f, 0.f, 0.f, 0.f}, e_res = {0.f, 0.f, 0.f, 0.f};
+    // Both are kept as loaded (the residual as raw bits, converted in the
+    // epilogue, and bias elements past the layer's columns as whatever the
+    // clamped load returned, never stored), so that nothing reads these
+    // registers before the epilogue and the loads stay in flight through the
+    // operand staging instead of being waited for ahead of it.
+    f32x4 e_bias = {0.f, 0.f, 0.f, 0.f};
+    u32x4 e_raw = {0u, 0u, 0u, 0u};
     bool e_pre = false;
     if constexpr (WGK > 1) {
         static_assert(BM * BN <= 4 * 256, "one output vector per thread");
         if (e_live) {
             const int nv = p.N - e_n4 < 4 ? p.N - e_n4 : 4;
 #pragma unroll
-            for (int e = 0; e < 4; e++) e_bias[e] = e < nv ? bias_ptr[e_n4 + e] : 0.f;
+            for (int e = 0; e < 4; e++) e_bias[e] = bias_ptr[e_n4 + (e < nv ? e : 0)];
             e_pre = nv == 4 && (p.out_C & 3) == 0 && p.n_mean == 0;
             if (e_pre && rs.res) {
                 const int rpn = p.u == 1 ? 0 : e_n4 / p.out_C;
                 const int res_s = (int)ring_slot((tau0 + t0) * p.u, rs.res_R);
-                e_res = load4(rs.res, p.out_elem, ring_at(b, p.B, slot_add(res_s, e_tl * p.u + rpn, rs.res_R), rs.res_R,
-                                                          e_n4 - rpn * p.out_C, 4, p.out_C, kDbgOut));
+                const size_t ro = ring_at(b, p.B, slot_add(res_s, e_tl * p.u + rpn, rs.res_R), rs.res_R,
+                                          e_n4 - rpn * p.out_C, 4, p.out_C, kDbgOut);
+                if (p.out_elem == kF32) {
+                    e_raw = *(const u32x4*)((const float*)rs.res + ro);
+                } else {
+                    const u32x2 h = *(const u32x2*)((const uint16_t*)rs.res + ro);
+                    e_raw[0] = h[0];
+                    e_raw[1] = h[1];
+                }
             }
         }
     }
@@ -753,7 +766,15 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
             const int off = e_tl * p.u + rpn, co = e_n4 - rpn * p.out_C;
             if (e_pre) {   // the vector path of store_out4, with the residual loaded up front
                 if (p.src) v = v + src_term4(p, b, slot_add(rs.src_s, off, (int)p.src_R), co);
-                if (rs.res) v = e_res + v;
+                if (rs.res) {
+                    const f32x4 e_res =
+                        p.out_elem == kF32 ? __builtin_bit_cast(f32x4, e_raw)
+                        : p.out_elem == kF16
+                            ? f32x4{h2f(e_raw[0] & 0xffffu), h2f(e_raw[0] >> 16), h2f(e_raw[1] & 0xffffu), h2f(e_raw[1] >> 16)}
+                            : f32x4{bf2f(e_raw[0] & 0xffffu), bf2f(e_raw[0] >> 16), bf2f(e_raw[1] & 0xffffu),
+                                    bf2f(e_raw[1] >> 16)};
+                    v = e_res + v;
+                }
                 if (p.out_act) {
 #pragma unroll
                     for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);

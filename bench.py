@@ -118,9 +118,16 @@ def traffic_from_profiles(workload: str, kernel: str, files=("dc_kernels.hip", "
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             rec[k.strip()] = v.strip()
-    if rec.get("kernel_source_hash") != kernel_source_hash(files) or rec.get("kernel") != kernel:
+    if rec.get("kernel_source_hash") != kernel_source_hash(files):
         return None
-    return float(rec["hbm_bytes_per_launch"])
+    if rec.get("kernel") == kernel:
+        return float(rec["hbm_bytes_per_launch"])
+    # the other kernels of the same runs (which kernel dominates a step can
+    # change between runs when two take about the same time)
+    for line in open(path):
+        if line.startswith(f"hbm_bytes_per_launch[{kernel}]:"):
+            return float(line.rsplit(":", 1)[1])
+    return None
 
 
 def roofline(layers, us, dtype):
@@ -245,25 +252,35 @@ def summarize_stats(prof_dir: str, out: str, command: str):
 def summarize_traffic(fetch_dir: str, write_dir: str, workload: str, kernel: str, out: str, command: str):
     """Mean HBM bytes per dispatch of `kernel` from FETCH_SIZE and WRITE_SIZE runs."""
     import glob
-    def mean_kib(d, counter):
+    def per_kernel(d, counter):
         rows = _csv(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0])
         vals, grid = {}, {}
         for r in rows:
             name = r["Kernel_Name"].replace("void ", "")
             name = name[:name.index("(")] if "(" in name else name
-            if name == kernel and r["Counter_Name"] == counter:
+            if r["Counter_Name"] == counter and name.startswith(("dc::", "dcf::")):
                 i = int(r["Dispatch_Id"])
-                vals[i] = vals.get(i, 0.0) + float(r["Counter_Value"])
-                grid[i] = int(r["Grid_Size"])
+                vals.setdefault(name, {})
+                vals[name][i] = vals[name].get(i, 0.0) + float(r["Counter_Value"])
+                grid.setdefault(name, {})[i] = int(r["Grid_Size"])
+        return vals, grid
+    def mean_kib(tables, name):
+        vals, grid = tables[0][name], tables[1][name]
         if workload.startswith("flow_"):
             # the timed calls' launches only: the prompt passes that set up
             # the streams run the same kernels over other row counts
             g_last = grid[max(grid)]
             vals = {i: v for i, v in vals.items() if grid[i] == g_last}
         return sum(vals.values()) / len(vals), len(vals), grid[max(grid)]
-    f, nf, g = mean_kib(fetch_dir, "FETCH_SIZE")
-    w, nw, _ = mean_kib(write_dir, "WRITE_SIZE")
+    ft, wt = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+    f, nf, g = mean_kib(ft, kernel)
+    w, nw, _ = mean_kib(wt, kernel)
     hbm = (f * FETCH_SCALE + w * WRITE_SCALE) * 1024.0
+    others = []
+    for name in sorted(set(ft[0]) & set(wt[0])):
+        if name != kernel:
+            fo, wo = mean_kib(ft, name)[0], mean_kib(wt, name)[0]
+            others.append(f"hbm_bytes_per_launch[{name}]: {(fo * FETCH_SCALE + wo * WRITE_SCALE) * 1024.0:.0f}")
     lines = ["# HBM traffic per launch from rocprofv3 PMC counters", f"# command: {command}",
              f"# FETCH_SIZE x {FETCH_SCALE} + WRITE_SIZE x {WRITE_SCALE} (KiB per dispatch; scale factors from a "
              "plain 256 MiB device copy: python3 bench.py --calibrate-copy)",
@@ -271,6 +288,8 @@ def summarize_traffic(fetch_dir: str, write_dir: str, workload: str, kernel: str
              f"dispatches: {nf} / {nw}" + (f" (grid size {g}: the timed calls' launches)" if workload.startswith("flow_") else ""),
              f"fetch_kib_per_dispatch: {f:.1f}", f"write_kib_per_dispatch: {w:.1f}",
              f"hbm_bytes_per_launch: {hbm:.0f}"]
+    if others:
+        lines += ["# the run's other kernels, the same measure"] + others
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 

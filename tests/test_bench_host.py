@@ -50,6 +50,10 @@ def test_traffic_summary(tmp_path, workload, want_fetch):
     want = (want_fetch * bench.FETCH_SCALE + 1.0 * bench.WRITE_SCALE) * 1024.0
     assert float(s["hbm_bytes_per_launch"]) == pytest.approx(want)
     assert s["dispatches"].startswith("2 / 2" if workload.startswith("flow_") else "4 / 4")
+    # the run's other kernels are recorded too, and found by traffic_from_profiles
+    want_other = (999.0 * bench.FETCH_SCALE + 1.0 * bench.WRITE_SCALE) * 1024.0
+    line = [x for x in out.read_text().splitlines() if x.startswith(f"hbm_bytes_per_launch[{other}]:")]
+    assert len(line) == 1 and float(line[0].rsplit(":", 1)[1]) == pytest.approx(want_other)
 
 
 def test_flow_kernel_names_follow_the_launch_rules():

@@ -159,7 +159,9 @@ typedef struct dc_state dc_state;
  * freed on return.  A DC_BF16 state stores the stages' residual stream (the
  * "s<s>.y", "s<s>.rb<j>.z<i>" and "s<s>.x" intermediates) as IEEE binary16:
  * activations of order one keep 11 significant bits; magnitudes beyond
- * 65504 do not fit (a DC_F32 state has no such limit).  On success *out owns the state, reset to the start of
+ * 65504 do not fit (a DC_F32 state has no such limit): a value that would
+ * round to infinity (|v| >= 65520), or a NaN, raises the device flag, which
+ * the next dc_sync reports as DC_ERANGE (the state is poisoned until dc_reset).  On success *out owns the state, reset to the start of
  * every stream, with the chunk graph captured unless DC_NO_GRAPH.
  * Errors: DC_EVERSION, DC_EINVAL (cfg or blob size), DC_ENOMEM, DC_EDEVICE;
  * *out is NULL then.
@@ -238,7 +240,9 @@ dc_status dc_reset(dc_state* s);
 dc_status dc_reset_stream(dc_state* s, int32_t b);
 
 /* Wait for all work of the state; report DC_ERANGE for a bad token id seen on
- * the device, DC_EDEVICE for a HIP error (both poison the state).  A failure
+ * the device or, in a DC_BF16 state, a residual-stream value beyond the
+ * binary16 range, DC_EDEVICE for a HIP error (all poison the state; the
+ * message names which).  A failure
  * found here is the device side of the fail-closed admission: the call that
  * raised it produced no trusted output (Design, "Granularity and capture
  * placement", local fail-closed admission). */

@@ -12,6 +12,12 @@ namespace dc {
 // order one keep 11 significant bits at half the bytes of fp32.
 enum Elem : int { kF32 = 0, kBF16 = 1, kF16 = 2 };
 
+// Bits of a state's device error flag (dc_sync reports and clears none of
+// them; dc_reset clears them): a token id outside [0, vocab) reached the
+// embedding, or a value that binary16 cannot hold (|v| >= 65520, which rounds
+// to infinity, or NaN) was about to be stored in a bf16 state's residual stream.
+enum ErrBit : int { kErrTokenId = 1, kErrF16Range = 2 };
+
 inline int elem_bytes(int e) { return e == kF32 ? 4 : 2; }
 
 // A ring of frames for B streams: frame with absolute index tau of stream b
@@ -71,6 +77,7 @@ struct ConvParams {
     int64_t src_R;
     const float* sd_w;    // [out_C][4]
     const float* sd_b;    // [out_C]
+    int* err;             // the state's device error flag (kErrF16Range on a binary16 overflow)
 };
 
 // Block of 4 waves: WGM x WGN waves tile the output, each wave MB x NB MFMA
@@ -136,6 +143,7 @@ struct PairParams {
     const int64_t* start; // [B]: tokens decoded when each stream last started
     int64_t in_fpt;
     float slope;
+    int* err;             // the state's device error flag (kErrF16Range on a binary16 overflow)
 };
 struct PairMember {
     const uint16_t* z;

@@ -77,25 +77,44 @@ __device__ __forceinline__ float load1(const void* base, int elem, size_t off)
     return elem == kF16 ? h2f(h) : bf2f(h);
 }
 
-__device__ __forceinline__ void store4(void* base, int elem, size_t off, f32x4 v)
+// A binary16 ring is a bf16 state's residual stream: a value it cannot hold
+// (|v| >= 65520 rounds to infinity; NaN) must raise the state's error flag, so
+// that the overflow poisons the state instead of silently carrying infinities
+// forward.  The stores only keep, in one register per lane (`mag`, when
+// given), the largest magnitude's bits (|v| as an unsigned integer orders
+// finite values, infinity and NaN alike); each kernel raises the flag once,
+// after its last store (raise_f16_range), so the store loops keep their shape.
+constexpr uint32_t kF16Limit = 0x477ff000u;   // bits of 65520.0f
+
+__device__ __forceinline__ uint32_t mag_bits(float v) { return __float_as_uint(v) & 0x7fffffffu; }
+
+__device__ __forceinline__ void raise_f16_range(int* err, uint32_t mag)
+{
+    if (mag >= kF16Limit) atomicOr(err, kErrF16Range);
+}
+
+__device__ __forceinline__ void store4(void* base, int elem, size_t off, f32x4 v, uint32_t* mag = nullptr)
 {
     if (elem == kF32) {
         *(f32x4*)((float*)base + off) = v;
     } else if (elem == kF16) {
+        if (mag) *mag = max(*mag, max(max(mag_bits(v[0]), mag_bits(v[1])), max(mag_bits(v[2]), mag_bits(v[3]))));
         *(u32x2*)((uint16_t*)base + off) = u32x2{pack_f16x2(v[0], v[1]), pack_f16x2(v[2], v[3])};
     } else {
         *(u32x2*)((uint16_t*)base + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
     }
 }
 
-__device__ __forceinline__ void store1(void* base, int elem, size_t off, float v)
+__device__ __forceinline__ void store1(void* base, int elem, size_t off, float v, uint32_t* mag = nullptr)
 {
-    if (elem == kF32)
+    if (elem == kF32) {
         ((float*)base)[off] = v;
-    else if (elem == kF16)
+    } else if (elem == kF16) {
+        if (mag) *mag = max(*mag, mag_bits(v));
         ((uint16_t*)base)[off] = __builtin_bit_cast(uint16_t, (_Float16)v);
-    else
+    } else {
         ((uint16_t*)base)[off] = (uint16_t)f2bf(v);
+    }
 }
 
 __device__ __forceinline__ int64_t ring_slot(int64_t tau, int64_t R)
@@ -236,6 +255,7 @@ struct OutRef {
     int out_R, res_R;
     int out_s, res_s, mean_s;
     int src_s;   // ring slot of the source samples of that frame
+    mutable uint32_t f16_mag = 0;   // largest binary16 store magnitude's bits (checked once, at the end)
 };
 
 // The harmonic source's contribution to output channels co .. co+3 of the
@@ -288,7 +308,7 @@ __device__ __forceinline__ void store_out(const ConvParams& p, int b, const OutR
         v = x / (float)(p.n_mean + 1);
     }
     if (p.out_act) v = lrelu(v, p.slope);
-    store1(rs.out, oe, ring_at(b, p.B, slot_add(rs.out_s, off, rs.out_R), rs.out_R, co, 1, p.out_C, kDbgOut), v);
+    store1(rs.out, oe, ring_at(b, p.B, slot_add(rs.out_s, off, rs.out_R), rs.out_R, co, 1, p.out_C, kDbgOut), v, &rs.f16_mag);
 }
 
 // Four consecutive output channels co .. co+3 of one frame (nv < 4 at the
@@ -315,7 +335,7 @@ __device__ __forceinline__ void store_out4(const ConvParams& p, int b, const Out
 #pragma unroll
         for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
     }
-    store4(rs.out, oe, ring_at(b, p.B, slot_add(rs.out_s, off, rs.out_R), rs.out_R, co, 4, p.out_C, kDbgOut), v);
+    store4(rs.out, oe, ring_at(b, p.B, slot_add(rs.out_s, off, rs.out_R), rs.out_R, co, 4, p.out_C, kDbgOut), v, &rs.f16_mag);
 }
 
 // Operand rows [t0 - halo, t0 - halo + rows) of channel block cb of stream b,
@@ -424,7 +444,7 @@ __device__ __forceinline__ void store_tile_e(const ConvParams& p, const OutRef& 
                 }
                 if (!live) continue;
                 store4(rs.out, OE, ring_at(b, p.B, slot_add(rs.out_s, off + rp[nb], rs.out_R), rs.out_R, co[nb], 4, p.out_C,
-                                           kDbgOut), v);
+                                           kDbgOut), v, &rs.f16_mag);
             }
         }
     } else {
@@ -780,12 +800,13 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvGroup g)
                     for (int e = 0; e < 4; e++) v[e] = lrelu(v[e], p.slope);
                 }
                 store4(rs.out, p.out_elem, ring_at(b, p.B, slot_add(rs.out_s, off, rs.out_R), rs.out_R, co, 4, p.out_C, kDbgOut),
-                       v);
+                       v, &rs.f16_mag);
             } else {
                 store_out4(p, b, rs, off, co, v, p.N - e_n4 < 4 ? p.N - e_n4 : 4);
             }
         }
     }
+    raise_f16_range(p.err, rs.f16_mag);
 }
 
 // ------------------------------------------- conv with an LDS weight ring
@@ -954,6 +975,7 @@ __global__ __launch_bounds__(256, 2) void wconv_kernel(const ConvGroup g)
     rs.mean_s = p.n_mean ? (int)ring_slot(tau_out0, p.mean_R) : 0;
     rs.src_s = p.src ? (int)ring_slot(tau_out0, p.src_R) : 0;
     store_tile<true, MB, NB>(p, rs, acc, bias, b, t0, n0, wm * 16 * MB, wn * NB, lane);
+    raise_f16_range(p.err, rs.f16_mag);
 }
 
 // ------------------------------------------------- dynamic LDS over 64 KB
@@ -1353,6 +1375,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     };
 
     const int mean_R = (int)p.mean_R;
+    uint32_t f16_mag = 0;   // largest output magnitude's bits (checked once, at the end)
     stage(f0 - H, BM + H);
     __syncthreads();
     for (int t = f0; t < f1; t += BM) {
@@ -1429,7 +1452,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             const int tl = wm * 16 * MB + mb * 16 + fl;
             if (t + tl < f1)
                 store4(out, kF16, ring_at(b, p.B, slot_add(out_s, tl, out_R), out_R, (nblk0 + nb) * 16 + cg, 4, C, kDbgPairOut),
-                       v);
+                       v, &f16_mag);
         };
         if (p.n_mean == 0) {
             // the residual was loaded during the second conv
@@ -1479,6 +1502,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         }
         __syncthreads();
     }
+    raise_f16_range(p.err, f16_mag);
 }
 
 // Fused-pair shapes (ids of this table).
@@ -1560,7 +1584,7 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* tokens, int n
     const int64_t slot = ring_slot(clock[0] * fpt + f, out.R);
     const size_t dst = ring_at(b, B, slot, out.R, c8, 8, C, kDbgEmbed);
     const bool ok = tok >= 0 && tok < vocab;
-    if (!ok) *err = 1;
+    if (!ok) *err = kErrTokenId;
     if (elem == kF32) {
         f32x4 a = {0.f, 0.f, 0.f, 0.f}, c = a;
         if (ok) {

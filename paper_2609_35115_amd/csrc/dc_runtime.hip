@@ -748,6 +748,7 @@ static ConvParams conv_params(const dc_state* s, const ConvOp& op, int n)
     p.clock = s->clock;
     p.in_fpt = s->fpt[op.level_in];
     p.slope = c.lrelu_slope;
+    p.err = s->err;
     if (op.src_ring >= 0) {
         p.src = (const float*)s->rings[op.src_ring].ptr;
         p.src_R = s->rings[op.src_ring].R;
@@ -830,6 +831,7 @@ static PairParams pair_params(const dc_state* s, const ConvOp& c1, int pv, int n
     p.start = s->start;
     p.in_fpt = s->fpt[c1.level_in];
     p.slope = c.lrelu_slope;
+    p.err = s->err;
     return p;
 }
 
@@ -1293,7 +1295,8 @@ dc_status dc_sync(dc_state* s)
     if (e != hipSuccess) return device_fail(s, e, "error flag read");
     if (flag) {
         s->poisoned = true;
-        return fail(s, DC_ERANGE, "token id outside [0, vocab) reached the device; call dc_reset");
+        if (flag & kErrTokenId) return fail(s, DC_ERANGE, "token id outside [0, vocab) reached the device; call dc_reset");
+        return fail(s, DC_ERANGE, "a value beyond the binary16 range reached the residual stream; call dc_reset");
     }
     if (s->poisoned) return fail(s, DC_ESTATE, "state is poisoned; call dc_reset");
     return DC_OK;

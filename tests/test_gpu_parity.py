@@ -274,6 +274,34 @@ def test_out_of_range_ids():
     d.close()
 
 
+def test_binary16_overflow_raises_the_flag():
+    """A bf16 state keeps its residual stream in binary16: with the embedding
+    scaled far past that range, the stores raise the device flag (dc_sync:
+    DC_ERANGE naming the overflow, the state poisoned until dc_reset), where a
+    normal decode raises nothing; an fp32 state has no such limit."""
+    blob = synth.make_weights(TINY, 0)
+    big = blob.copy()
+    synth.split_weights(TINY, big)["emb"][...] *= 1.0e6
+    ids = synth.make_tokens(TINY, 1, 8)
+    ok = dc.Decoder(TINY, "bf16", blob, batch=1, chunk_tokens=8)
+    ok.decode(ids)
+    assert dc.dc_sync(ok.h) == dc.DC_OK
+    ok.close()
+    d = dc.Decoder(TINY, "bf16", big, batch=1, chunk_tokens=8)
+    d.decode(ids)
+    assert dc.dc_sync(d.h) == dc.DC_ERANGE
+    assert "binary16" in dc.dc_last_error(d.h)
+    out = torch.empty((1, 8 * 64), device="cuda")
+    assert dc.dc_decode_chunk(d.h, torch.from_numpy(ids).cuda(), 8, out) == dc.DC_ESTATE
+    d.reset()
+    assert dc.dc_sync(d.h) == dc.DC_OK
+    d.close()
+    f = dc.Decoder(TINY, "f32", big, batch=1, chunk_tokens=8)
+    f.decode(ids)
+    assert dc.dc_sync(f.h) == dc.DC_OK
+    f.close()
+
+
 def test_fixed_addresses_and_aliasing():
     """Buffers keep their addresses across calls and resets; passing them
     aliases the call (no staging copy) with identical output."""

@@ -1794,8 +1794,8 @@ hipError_t launch_phase(const SourceParams& p, hipStream_t st)
     return hipGetLastError();
 }
 
-// One thread per (stream, last-stage frame of this call): the frame's 4
-// samples.  Sample t of the call lies in f0 frame t / S at offset r; its
+// One thread per (stream, sample of this call).  Sample t of the call lies
+// in f0 frame t / S at offset r; its
 // sinusoid h has phase frac(P_h[frame] + (r+1) (h+1) f0 / sr).  Noise of
 // sinusoids 4g .. 4g+3 comes from Philox4x64-10 with key (seed, stream) and
 // counter (sample since the stream's start, g, 0, 0), by Box-Muller on its
@@ -1806,56 +1806,53 @@ constexpr int kMaxSinusoids = 32;
 
 __global__ __launch_bounds__(256) void source_kernel(const SourceParams p)
 {
+    // (a sample's draws and sinusoids are independent of its neighbours';
+    // four consecutive lanes write one last-stage frame's four samples)
     const int FL = p.F0 / (int)p.fpt0 * (int)p.fptL;   // last-stage frames of this call
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)p.B * FL) return;
-    const int b = (int)(i / FL), tau = (int)(i - (i / FL) * FL);
+    if (i >= (int64_t)p.B * FL * 4) return;
+    const int b = (int)(i / (4 * FL)), t = (int)(i - (i / (4 * FL)) * (4 * FL));   // sample of this call
+    const int tau = t >> 2, j = t & 3;
     const int64_t tauL = p.clock[0] * p.fptL + tau;                  // absolute last-stage frame
-    const int64_t t_rel0 = (tauL - p.start[b] * p.fptL) * 4;        // sample index since the stream's start
+    const int64_t t_rel = (tauL - p.start[b] * p.fptL) * 4 + j;     // sample index since the stream's start
     const float* f0 = p.f0 + (size_t)b * p.F0;
     const double* ptab = p.ptab + (size_t)b * p.F0 * p.H1;
     const int groups = (p.H1 + 3) / 4;
     const uint64_t key = p.keys[b];
-    f32x4 out;
+    const int f = t / p.S, r = t - (t / p.S) * p.S;
+    const float fv = f0[f];
+    const bool voiced = fv > p.thr;
+    const float nscale = voiced ? p.noise : p.amp / 3.0f;
+    float acc = 0.f;
+    for (int g = 0; g < groups; g++) {
+        const Philox4 x = philox4x64_10((uint64_t)t_rel, (uint64_t)g, 0, 0, p.seed, key);
+        float nz[4];
 #pragma unroll
-    for (int j = 0; j < 4; j++) {
-        const int t = tau * 4 + j;                 // sample of this call
-        const int f = t / p.S, r = t - (t / p.S) * p.S;
-        const float fv = f0[f];
-        const bool voiced = fv > p.thr;
-        const float nscale = voiced ? p.noise : p.amp / 3.0f;
-        float acc = 0.f;
-        for (int g = 0; g < groups; g++) {
-            const Philox4 x = philox4x64_10((uint64_t)(t_rel0 + j), (uint64_t)g, 0, 0, p.seed, key);
-            float nz[4];
-#pragma unroll
-            for (int q = 0; q < 2; q++) {
-                const float rad = (float)sqrt(-2.0 * log(to_u01(x.v[2 * q])));
-                const float ang = (float)(2.0 * M_PI * to_u01(x.v[2 * q + 1]));
-                float sn, cs;
-                sincosf(ang, &sn, &cs);
-                nz[2 * q] = rad * cs;
-                nz[2 * q + 1] = rad * sn;
-            }
-#pragma unroll
-            for (int q = 0; q < 4; q++) {
-                const int h = 4 * g + q;
-                if (h >= p.H1) break;
-                const double inc = (double)(h + 1) * (double)fv / p.sr;
-                const double ph = ptab[(size_t)f * p.H1 + h] + (double)(r + 1) * inc;
-                const float frac = (float)(ph - floor(ph));
-                const float sine = voiced ? p.amp * sinf(6.28318530717958647692f * frac) : 0.f;
-                acc = acc + p.mw[h] * (sine + nz[q] * nscale);
-            }
+        for (int q = 0; q < 2; q++) {
+            const float rad = (float)sqrt(-2.0 * log(to_u01(x.v[2 * q])));
+            const float ang = (float)(2.0 * M_PI * to_u01(x.v[2 * q + 1]));
+            float sn, cs;
+            sincosf(ang, &sn, &cs);
+            nz[2 * q] = rad * cs;
+            nz[2 * q + 1] = rad * sn;
         }
-        out[j] = tanhf(p.mb[0] + acc);
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            const int h = 4 * g + q;
+            if (h >= p.H1) break;
+            const double inc = (double)(h + 1) * (double)fv / p.sr;
+            const double ph = ptab[(size_t)f * p.H1 + h] + (double)(r + 1) * inc;
+            const float frac = (float)(ph - floor(ph));
+            const float sine = voiced ? p.amp * sinf(6.28318530717958647692f * frac) : 0.f;
+            acc = acc + p.mw[h] * (sine + nz[q] * nscale);
+        }
     }
-    *(f32x4*)(p.src + ((size_t)b * p.src_R + ring_slot(tauL, p.src_R)) * 4) = out;
+    p.src[((size_t)b * p.src_R + ring_slot(tauL, p.src_R)) * 4 + j] = tanhf(p.mb[0] + acc);
 }
 
 hipError_t launch_source(const SourceParams& p, hipStream_t st)
 {
-    const int64_t n = (int64_t)p.B * (p.F0 / p.fpt0 * p.fptL);
+    const int64_t n = (int64_t)p.B * (p.F0 / p.fpt0 * p.fptL) * 4;
     hipLaunchKernelGGL(source_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p);
     return hipGetLastError();
 }

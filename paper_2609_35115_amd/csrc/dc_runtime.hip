@@ -100,6 +100,11 @@ struct dc_state {
     dc_cfg cfg{};
     hipStream_t stream = nullptr;
     bool own_stream = false;
+    // harmonic source: its two launches run on a side stream, forked at the
+    // step's start and joined before the launch that adds the source
+    hipStream_t side = nullptr;
+    hipEvent_t fork_ev = nullptr, join_ev = nullptr;
+    int src_join = -1;          // index of the launch that reads the source ring
     char* arena = nullptr;
     size_t arena_bytes = 0;
     std::vector<Ring> rings;
@@ -872,13 +877,26 @@ static hipError_t launch_layer(dc_state* s, int i, int n, hipStream_t st, double
     }
 }
 
+// With a harmonic source, its phase and source launches depend only on the
+// call's f0, the clock and their own carry: they run on the side stream
+// beside the pre-stack and the first stages, and the main stream waits for
+// them just before the launch that adds the source (in a captured graph the
+// fork and the join become two parallel branches).
 static hipError_t enqueue_step(dc_state* s, int n, hipStream_t st, double* ptab = nullptr)
 {
-    for (int i = 0; i < layer_count(s); i++) {
-        const hipError_t e = launch_layer(s, i, n, st, ptab);
-        if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
+    if (s->side) {
+        e = hipEventRecord(s->fork_ev, st);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s->side, s->fork_ev, 0);
     }
-    return hipSuccess;
+    for (int i = 0; i < layer_count(s) && e == hipSuccess; i++) {
+        const LaunchKind k = s->launches[i].kind;
+        const bool on_side = s->side && (k == L_PHASE || k == L_SOURCE);
+        if (s->side && i == s->src_join) e = hipStreamWaitEvent(st, s->join_ev, 0);
+        if (e == hipSuccess) e = launch_layer(s, i, n, on_side ? s->side : st, ptab);
+        if (e == hipSuccess && on_side && k == L_SOURCE) e = hipEventRecord(s->join_ev, s->side);
+    }
+    return e;
 }
 
 static hipError_t zero_state(dc_state* s)
@@ -1022,6 +1040,19 @@ dc_status dc_init(const void* weights_blob, size_t blob_bytes, const dc_cfg* cfg
             return fail(nullptr, DC_EDEVICE, std::string("hipStreamCreate: ") + hipGetErrorString(e));
         }
         s->own_stream = true;
+    }
+    if (c.n_harmonics > 0) {
+        for (int i = 0; i < (int)s->launches.size(); i++)
+            if (s->launches[i].kind == L_CONV && s->convs[s->launches[i].convs[0]].src_ring >= 0) s->src_join = i;
+        e = hipStreamCreateWithFlags(&s->side, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&s->fork_ev, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&s->join_ev, hipEventDisableTiming);
+        if (e == hipSuccess && s->src_join < 0) e = hipErrorInvalidValue;
+        if (e != hipSuccess) {
+            const std::string m = std::string("dc_init: side stream: ") + hipGetErrorString(e);
+            dc_free(s);
+            return fail(nullptr, DC_EDEVICE, m);
+        }
     }
     // the device of the arena; a decoder with a harmonic source also resolves
     // that device's static scratch address here (dc_decode_chunk_f0_static)
@@ -1672,7 +1703,11 @@ void dc_free(dc_state* s)
         if (x) (void)hipGraphExecDestroy(x);
     for (hipGraph_t g : s->flush_graph)
         if (g) (void)hipGraphDestroy(g);
+    if (s->side) (void)hipStreamSynchronize(s->side);
     if (s->arena) (void)hipFree(s->arena);
+    if (s->fork_ev) (void)hipEventDestroy(s->fork_ev);
+    if (s->join_ev) (void)hipEventDestroy(s->join_ev);
+    if (s->side) (void)hipStreamDestroy(s->side);
     if (s->own_stream && s->stream) (void)hipStreamDestroy(s->stream);
     delete s;
 }

@@ -311,6 +311,9 @@ static bool variant_fits(const ConvOp& op, int v)
 // measured slower than the register-weight kernel and is not chosen.)
 static const int kPreferRing[] = {20, 24, 22, 21, 25, 23};
 
+// 128x128 register-weight tiles, 4-chunk channel blocks.
+static const int kWideHaloTile = 14;
+
 // Tile shape of a conv for this state.  Deterministic: it depends on the
 // layer, the batch and the chunk size only (never on a call's n), so every
 // call of a state -- replayed or direct, chunked or offline -- runs the same
@@ -361,6 +364,15 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
     for (int kch = 32; kch >= 1; kch /= 2) {
         if (kch > kch_all && kch > 1) continue;
         if (wgk == 1 && kch > 4) continue;
+        // a wide left context ((k-1)*d >= 30 rows): 128x128 tiles, whose
+        // 128 output rows dilute the halo every block stages (a 64-row tile
+        // stages 1.8x its rows at k = 11, d = 5), as long as the launch keeps
+        // at least 1024 of them
+        if (wgk == 1 && (op.k - 1) * op.d >= 30) {
+            const TileShape t = tile_variant(kWideHaloTile);
+            if (t.KCH == kch && variant_fits(op, kWideHaloTile) && members * blocks(t) >= 1024 && eff(t) >= 0.75)
+                return kWideHaloTile;
+        }
         if (wgk == 1 && op.bf16 && !op.split && !(s->cfg.flags & DC_NO_RING)) {
             // the ring shapes first, for unsplit operands (split ones read their
             // low halves unprefetched there) and launches that keep the machine

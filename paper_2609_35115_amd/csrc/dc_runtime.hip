@@ -350,8 +350,13 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
     };
     // a resblock conv shares its launch with the parallel branches' convs:
     // the launch has that many times the blocks (the K-partition choice
-    // below still looks at one conv)
+    // below still looks at one conv); at the branch-mean position the other
+    // branches' last convs share one launch and the mean conv runs alone
     const int64_t members = op.stage >= 0 ? s->cfg.n_rb : 1;
+    // the branch-mean position: the other branches' last convs share one
+    // launch and the mean conv runs alone, so those launches have fewer blocks
+    // than `members` counts (the shapes it picks for them measured best anyway)
+    const bool mean_pos = op.stage >= 0 && op.half == 2 && op.dil_i == s->cfg.n_dil - 1 && s->cfg.n_rb > 1;
     auto eff = [&](const TileShape& t) {
         const int bm = t.BM();
         return (double)F / (double)(((F + bm - 1) / bm) * bm);
@@ -377,13 +382,18 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
             // the ring shapes first, for unsplit operands (split ones read their
             // low halves unprefetched there) and launches that keep the machine
             // busy for at least two rounds of blocks (two resident per CU; with
-            // fewer the register-weight kernel measured faster): of those, the
-            // one with the least padding in rows and columns (then the largest)
+            // fewer the register-weight kernel measured faster), or one round
+            // for a narrow left context (below 30 rows, where the ring's
+            // staging is short: the B=16 256-channel convs at dilation 1, not
+            // counting the branch-mean position's smaller launches): of those,
+            // the one with the least padding in rows and columns (then the
+            // largest)
+            const int64_t min_ring = (op.k - 1) * op.d < 30 && !mean_pos ? 512 : 1024;
             int bestr = -1;
             double bestr_score = -1.0;
             for (int v : kPreferRing) {
                 const TileShape t = tile_variant(v);
-                if (t.KCH != kch || !variant_fits(op, v) || members * blocks(t) < 1024) continue;
+                if (t.KCH != kch || !variant_fits(op, v) || members * blocks(t) < min_ring) continue;
                 const int bn = t.BN();
                 const double col = (double)op.N / (double)(((op.N + bn - 1) / bn) * bn);
                 const double score = eff(t) * col;

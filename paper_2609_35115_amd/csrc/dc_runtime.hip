@@ -369,6 +369,11 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
     for (int kch = 32; kch >= 1; kch /= 2) {
         if (kch > kch_all && kch > 1) continue;
         if (wgk == 1 && kch > 4) continue;
+        // fp32 resblock convs of the streaming class: channel blocks of at
+        // most 128 channels.  The 256-channel stage's widest tile then stages
+        // 34 KB instead of 68 KB, four blocks fit a CU instead of two, and its
+        // grouped launches run in about one round of blocks instead of two.
+        if (wgk == 4 && !op.bf16 && op.stage >= 0 && kch > 8) continue;
         // a wide left context ((k-1)*d >= 30 rows): 128x128 tiles, whose
         // 128 output rows dilute the halo every block stages (a 64-row tile
         // stages 1.8x its rows at k = 11, d = 5), as long as the launch keeps

@@ -350,8 +350,7 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
     };
     // a resblock conv shares its launch with the parallel branches' convs:
     // the launch has that many times the blocks (the K-partition choice
-    // below still looks at one conv); at the branch-mean position the other
-    // branches' last convs share one launch and the mean conv runs alone
+    // below still looks at one conv)
     const int64_t members = op.stage >= 0 ? s->cfg.n_rb : 1;
     // the branch-mean position: the other branches' last convs share one
     // launch and the mean conv runs alone, so those launches have fewer blocks

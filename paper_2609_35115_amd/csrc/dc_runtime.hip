@@ -373,6 +373,18 @@ static int pick_variant(const dc_state* s, const ConvOp& op)
         // 34 KB instead of 68 KB, four blocks fit a CU instead of two, and its
         // grouped launches run in about one round of blocks instead of two.
         if (wgk == 4 && !op.bf16 && op.stage >= 0 && kch > 8) continue;
+        // fp32 K-split convs of 256 channels or more with a 50-row left
+        // context (the 256-channel stage at dilation 5): 16x32 tiles, so the
+        // 66 staged rows serve 32 columns per block instead of 16 (the
+        // grouped launch measured 24.9 -> 21.7 us; the 128-channel stage's
+        // 32x32 tiles stay, where 16x32 measured slower)
+        if (wgk == 4 && !op.bf16 && op.Ci >= 256 && (op.k - 1) * op.d >= 50) {
+            for (int v = 0; v < nv; v++) {
+                const TileShape t = tile_variant(v);
+                if (t.WGK == 4 && t.KCH == kch && t.MB == 1 && t.NB == 2 && t.WGM == 1 && t.WGN == 1 && variant_fits(op, v))
+                    return v;
+            }
+        }
         // a wide left context ((k-1)*d >= 30 rows): 128x128 tiles, whose
         // 128 output rows dilute the halo every block stages (a 64-row tile
         // stages 1.8x its rows at k = 11, d = 5), as long as the launch keeps

@@ -302,6 +302,40 @@ def test_binary16_overflow_raises_the_flag():
     f.close()
 
 
+# The last branch's last conv of the last stage writes the stage output x, the
+# last binary16 store before the head (whose outputs are fp32): planted there,
+# only that launch can raise the flag.
+@pytest.mark.parametrize("planted,flags", [
+    ("s2.rb2.d2.W2", 0),                 # the fused branch-mean pair
+    ("s2.rb2.d2.W2", dc.DC_NO_FUSE),     # the same conv unfused (batched conv tiles)
+    ("s2.up.W", 0),                      # the transposed conv's y (and what follows it)
+])
+def test_binary16_overflow_raises_the_flag_in_the_batched_kernels(planted, flags):
+    """The batched class (batch >= 8) stores the residual stream through other
+    kernels than batch 1 does: a weight scaled far past binary16's range makes
+    the stores of its layer raise the flag, and the unplanted weights raise
+    nothing."""
+    B, n = 8, 4
+    blob = synth.make_weights(REAL, 0)
+    ids = synth.make_tokens(REAL, B, n)
+    ok = dc.Decoder(REAL, "bf16", blob, batch=B, chunk_tokens=n, flags=flags)
+    ok.decode(ids)
+    assert dc.dc_sync(ok.h) == dc.DC_OK
+    ok.close()
+    big = blob.copy()
+    synth.split_weights(REAL, big)[planted][...] *= 1.0e6
+    d = dc.Decoder(REAL, "bf16", big, batch=B, chunk_tokens=n, flags=flags)
+    named = [f"{l['name']}: {l['kernel']}" for l in d.layers()
+             if l['name'].startswith("s2.") and ("mean" in l['name'] or ".up" in l['name'])]
+    say(f"binary16 flag: {planted} x 1e6, flags {flags}; {named}")
+    d.decode(ids)
+    assert dc.dc_sync(d.h) == dc.DC_ERANGE
+    assert "binary16" in dc.dc_last_error(d.h)
+    d.reset()
+    assert dc.dc_sync(d.h) == dc.DC_OK
+    d.close()
+
+
 def test_fixed_addresses_and_aliasing():
     """Buffers keep their addresses across calls and resets; passing them
     aliases the call (no staging copy) with identical output."""

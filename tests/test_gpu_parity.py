@@ -189,7 +189,10 @@ def test_whole_utterance_state_equals_chunked_automatic_tiles(dtype, batch):
     assert bits_equal(pa, pb)
 
 
-@pytest.mark.parametrize("dtype,big,small", [("f32", 3, 1), ("bf16", 3, 1), ("bf16", 16, 8)])
+# (batch 7 is the largest of the streaming class, batch 8 the smallest of the
+# batched one)
+@pytest.mark.parametrize("dtype,big,small", [("f32", 3, 1), ("bf16", 3, 1), ("bf16", 7, 1), ("bf16", 16, 8),
+                                             ("f32", 12, 8)])
 def test_stream_bits_independent_of_batch_within_class(dtype, big, small):
     blob = synth.make_weights(REAL, 0)
     ids = synth.make_tokens(REAL, big, 8)
@@ -305,12 +308,13 @@ def test_binary16_overflow_raises_the_flag():
 # The last branch's last conv of the last stage writes the stage output x, the
 # last binary16 store before the head (whose outputs are fp32): planted there,
 # only that launch can raise the flag.
-@pytest.mark.parametrize("planted,flags", [
-    ("s2.rb2.d2.W2", 0),                 # the fused branch-mean pair
-    ("s2.rb2.d2.W2", dc.DC_NO_FUSE),     # the same conv unfused (batched conv tiles)
-    ("s2.up.W", 0),                      # the transposed conv's y (and what follows it)
+@pytest.mark.parametrize("planted,flags,tv,kernel", [
+    ("s2.rb2.d2.W2", 0, 0, "pair_kernel"),                 # the fused branch-mean pair
+    ("s2.rb2.d2.W2", dc.DC_NO_FUSE, 0, "conv_kernel"),     # the same conv unfused
+    ("s2.rb2.d2.W2", dc.DC_NO_FUSE, 27, "wconv_kernel"),   # unfused, 64x64 tiles, weights through the LDS ring
+    ("s2.up.W", 0, 0, None),                               # the transposed conv's y (and what follows it)
 ])
-def test_binary16_overflow_raises_the_flag_in_the_batched_kernels(planted, flags):
+def test_binary16_overflow_raises_the_flag_in_the_batched_kernels(planted, flags, tv, kernel):
     """The batched class (batch >= 8) stores the residual stream through other
     kernels than batch 1 does: a weight scaled far past binary16's range makes
     the stores of its layer raise the flag, and the unplanted weights raise
@@ -318,16 +322,18 @@ def test_binary16_overflow_raises_the_flag_in_the_batched_kernels(planted, flags
     B, n = 8, 4
     blob = synth.make_weights(REAL, 0)
     ids = synth.make_tokens(REAL, B, n)
-    ok = dc.Decoder(REAL, "bf16", blob, batch=B, chunk_tokens=n, flags=flags)
+    ok = dc.Decoder(REAL, "bf16", blob, batch=B, chunk_tokens=n, flags=flags, tile_variant=tv)
     ok.decode(ids)
     assert dc.dc_sync(ok.h) == dc.DC_OK
     ok.close()
     big = blob.copy()
     synth.split_weights(REAL, big)[planted][...] *= 1.0e6
-    d = dc.Decoder(REAL, "bf16", big, batch=B, chunk_tokens=n, flags=flags)
+    d = dc.Decoder(REAL, "bf16", big, batch=B, chunk_tokens=n, flags=flags, tile_variant=tv)
     named = [f"{l['name']}: {l['kernel']}" for l in d.layers()
              if l['name'].startswith("s2.") and ("mean" in l['name'] or ".up" in l['name'])]
-    say(f"binary16 flag: {planted} x 1e6, flags {flags}; {named}")
+    say(f"binary16 flag: {planted} x 1e6, flags {flags}, tile variant {tv}; {named}")
+    if kernel:   # the planted conv runs in the kernel this case is for
+        assert any(".mean" in x and f"dc::{kernel}<" in x for x in named), named
     d.decode(ids)
     assert dc.dc_sync(d.h) == dc.DC_ERANGE
     assert "binary16" in dc.dc_last_error(d.h)
